@@ -1,0 +1,28 @@
+"""Plain, slow, float64 CPU oracle for the orthogonal-parametrization path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports this package:
+only the test suite, the smoke check of ``__graft_entry__`` and the CPU
+baseline leg of ``bench.py`` may call it.  It shares no code, constants or
+helpers with the HIP library; both sides receive the same seeded inputs from
+``paper_2601_13776_amd.workloads`` (which holds no arithmetic of the method).
+
+Modules
+-------
+bjorck   Frobenius pre-scaling and the Björck–Bowie iteration
+         (Appendix A.5, "Björck–Bowie Iterative Projection").
+aoc      RKO reshape, BCOP projector blocks, the block-convolution operator
+         and the AOC kernel composition (Appendix B.1, eq. AOC = RKO ⊛ K_BCOP;
+         stride / groups / dilation paragraphs of Appendix B.1).
+conv     Circular convolution with stride, dilation and groups, its adjoint,
+         the impulse-response Toeplitz matrix and the per-frequency FFT
+         singular values (Section 4 and Appendix C, unit-testing scheme).
+checks   Orthogonality deviation and norm ratios used as gates.
+
+Every function is pinned by ``tests/test_oracle_pins.py`` against closed
+forms, library routines (torch CPU conv2d, numpy SVD) or brute force; see the
+docstrings for which pin covers which function.
+"""
+
+from . import bjorck, aoc, conv, checks  # noqa: F401
+
+__all__ = ["bjorck", "aoc", "conv", "checks"]
