@@ -1,0 +1,211 @@
+/*
+ * orth.h — C ABI of liborth, the MI355X (gfx950) library that turns free
+ * parameters into orthogonal matrices and explicit orthogonal convolution
+ * kernels, as used by the orthogonal layers of "Orthogonium" (arXiv 2601.13776).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Matrices are row-major with a leading dimension in ELEMENTS.
+ * - Data pointers (matrices, kernels, conv inputs, outputs, workspace,
+ *   status arrays) are DEVICE pointers owned by the caller.  Descriptor
+ *   arrays (orth_mat, orth_conv_desc, orth_check_args) are HOST memory,
+ *   read only during the call.
+ * - The library never allocates device memory: each entry point that needs
+ *   scratch space has a *_workspace_size query; pass at least that many
+ *   bytes, 256-byte aligned.  The workspace must not be used by anything
+ *   else until the work enqueued by the call has finished.
+ * - Every argument is validated on the host before anything is enqueued;
+ *   a non-zero return means nothing was launched.  ORTH_EHIP reports a HIP
+ *   runtime error at launch time.  Errors inside kernels on well-formed
+ *   input cannot occur; degenerate matrices are reported per matrix (see
+ *   orth_orthogonalize_batched).
+ * - Work is asynchronous on `stream` (a hipStream_t, NULL = the legacy
+ *   default stream).  Nothing synchronizes inside a call.
+ * - bfloat16 is the raw 16-bit pattern (same layout as torch.bfloat16);
+ *   conversions to bfloat16 round to nearest, ties to even.
+ * - orth_last_error() returns a thread-local message for the last failing
+ *   call of the calling thread.
+ */
+#ifndef ORTH_H_
+#define ORTH_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ORTH_OK = 0,
+  ORTH_EINVAL = 1,        /* malformed argument */
+  ORTH_EUNSUPPORTED = 2,  /* well-formed but impossible or not implemented */
+  ORTH_EWORKSPACE = 3,    /* workspace missing, too small or misaligned */
+  ORTH_EHIP = 4           /* HIP runtime error */
+} orth_status;
+
+typedef enum { ORTH_F32 = 0, ORTH_BF16 = 1 } orth_dtype;
+
+/* Arithmetic of the Björck products: fp32 operands on fp32 MFMA, or
+ * bfloat16 operands with fp32 accumulation (the iterate itself is always
+ * kept in fp32). */
+typedef enum { ORTH_COMPUTE_F32 = 0, ORTH_COMPUTE_BF16 = 1 } orth_compute;
+
+typedef enum { ORTH_PRESCALE_NONE = 0, ORTH_PRESCALE_FROBENIUS = 1 } orth_prescale;
+
+/* Per-matrix status written to status_dev. */
+typedef enum {
+  ORTH_MAT_OK = 0,
+  ORTH_MAT_ZERO = 1,       /* Frobenius norm 0: output is all zeros */
+  ORTH_MAT_NONFINITE = 2   /* NaN/Inf in the input: output is all NaN */
+} orth_mat_status;
+
+/* One matrix to orthogonalize. */
+typedef struct {
+  const void* in;   /* device, rows x cols, leading dim ld_in, opts.in_dtype */
+  void* out;        /* device, rows x cols, leading dim ld_out, opts.out_dtype.
+                       May equal `in` (in-place) when dtypes and leading
+                       dims agree; otherwise the two must not overlap. */
+  int32_t rows, cols;   /* >= 1 */
+  int64_t ld_in, ld_out;
+} orth_mat;
+
+typedef struct {
+  int32_t iters;      /* number of Björck steps T >= 0 (no early exit) */
+  float beta;         /* step size in (0, 0.5]; 0.5 is the usual choice */
+  int32_t prescale;   /* orth_prescale */
+  int32_t in_dtype;   /* orth_dtype of every mats[i].in */
+  int32_t out_dtype;  /* orth_dtype of every mats[i].out */
+  int32_t compute;    /* orth_compute */
+} orth_bjorck_opts;
+
+/*
+ * Björck–Bowie orthogonalization of a batch of independent matrices
+ * (Appendix A.5 of the paper: W <- (1+beta) W - beta W W^T W, after an
+ * optional Frobenius pre-scaling W_0 = W / ||W||_F), exactly opts->iters
+ * steps per matrix.  Tall matrices (rows >= cols) get orthonormal columns
+ * in the limit, wide ones orthonormal rows.  All matrices of the batch are
+ * processed by the same few launches per step, whatever their shapes.
+ *
+ * status_dev: optional device array of n int32 (orth_mat_status).  A zero
+ * or non-finite matrix does not fail the call.
+ * Returns ORTH_EINVAL for n < 0, a NULL pointer, rows or cols < 1,
+ * ld < cols, iters < 0, beta outside (0, 0.5], an unknown dtype, compute or
+ * prescale mode, or in == out with differing dtype/leading dim.
+ */
+int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n,
+                                      const orth_bjorck_opts* opts, size_t* bytes);
+int orth_orthogonalize_batched(const orth_mat* mats, int32_t n,
+                               const orth_bjorck_opts* opts, void* workspace,
+                               size_t workspace_bytes, int32_t* status_dev,
+                               void* stream);
+
+/* Geometry of one orthogonal convolution (groups g, stride s, dilation d). */
+typedef struct {
+  int32_t cin, cout, k, stride, dilation, groups;
+} orth_conv_geom;
+
+/*
+ * Shapes of the free parameters of one AOC layer (Appendix B.1: the kernel
+ * is RKO composed with BCOP blocks; valid iff k >= stride).  Per group:
+ * one RKO matrix of rko_rows x rko_cols = (cout/g) x (cin/g * s^2) and
+ * n_proj = 2 (k - s) projector factors of proj_rows x proj_cols =
+ * (cin/g) x floor(cin/g / 2).  Host only; launches nothing.
+ * Returns ORTH_EINVAL for non-positive sizes or groups not dividing cin and
+ * cout, ORTH_EUNSUPPORTED for k < s, s > 1 with gcd(s, d) != 1, or fewer
+ * than 2 channels per group when k > s.
+ */
+int orth_aoc_param_shapes(const orth_conv_geom* geom, int32_t* rko_rows,
+                          int32_t* rko_cols, int32_t* n_proj,
+                          int32_t* proj_rows, int32_t* proj_cols);
+
+/* One conv layer to build. */
+typedef struct {
+  orth_conv_geom geom;
+  const void* rko;   /* device: g x rko_rows x rko_cols, contiguous, orthogonalized */
+  const void* proj;  /* device: g x n_proj x proj_rows x proj_cols, contiguous,
+                        orthogonalized; horizontal 1x2 blocks first, then the
+                        vertical 2x1 blocks.  Ignored (may be NULL) if n_proj == 0. */
+  void* kernel;      /* device: cout x (cin/g) x k x k (OIHW), contiguous */
+} orth_conv_desc;
+
+/*
+ * Explicit AOC kernels (Appendix B.1, AOC = RKO ⊛ K_BCOP, with native
+ * stride, groups and dilation).  For every group, the s x s RKO kernel
+ * R[o, i, a, b] = M[o, i s^2 + a s + b] is composed with k - s horizontal
+ * blocks (taps P, I - P) and k - s vertical blocks (taps Q, I - Q), where
+ * P = V V^T for each projector factor V, by the block-convolution operator
+ * (the kernel of the composition of two convolutions).  Group j fills
+ * output channels [j cout/g, (j+1) cout/g).  Dilation does not change the
+ * kernel; it is only validated.  `dtype` is the storage type of rko, proj
+ * and kernel; arithmetic is fp32.  Errors as orth_aoc_param_shapes, plus
+ * ORTH_EINVAL for NULL pointers or n < 0.
+ */
+int orth_build_conv_kernels_workspace_size(const orth_conv_desc* descs, int32_t n,
+                                           int32_t dtype, size_t* bytes);
+int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n,
+                                    int32_t dtype, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+/* Single-layer convenience form of orth_build_conv_kernels_batched. */
+int orth_build_conv_kernel(const void* rko, const void* proj, int32_t cin,
+                           int32_t cout, int32_t k, int32_t stride,
+                           int32_t dilation, int32_t groups, int32_t dtype,
+                           void* kernel_out, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+typedef enum {
+  ORTH_CHECK_GRAM = 0,          /* out[i] = max |G_i - I|, G the smaller Gram of mats[i].in */
+  ORTH_CHECK_CONV = 1,          /* out[b] = ||conv(K, x_b)|| / ||x_b|| */
+  ORTH_CHECK_CONV_ADJOINT = 2   /* out[b] = ||conv^T(K, x_b)|| / ||x_b|| */
+} orth_check_mode;
+
+/*
+ * Verification quantities (Section 4 and Appendix C: orthogonality of
+ * matrices, norm preservation of the circular-padded convolution).
+ * CONV: x is batch x cin x height x width fp32; the convolution is the
+ * circular-padded cross-correlation with stride s and dilation d, total
+ * padding d (k - 1) + 1 - s split floor/ceil, output (height/s, width/s).
+ * CONV_ADJOINT: x is batch x cout x height x width on the OUTPUT grid and
+ * the transpose maps it to cin x (height s) x (width s).
+ * height and width must be divisible by s (CONV).
+ */
+typedef struct {
+  int32_t mode;             /* orth_check_mode */
+  /* GRAM */
+  const orth_mat* mats;     /* reads mats[i].in, rows, cols, ld_in */
+  int32_t n_mats;
+  int32_t mat_dtype;
+  /* CONV / CONV_ADJOINT */
+  const void* kernel;       /* cout x (cin/g) x k x k */
+  int32_t kernel_dtype;
+  orth_conv_geom geom;
+  const float* x;
+  int32_t batch, height, width;
+} orth_check_args;
+
+int orth_check_workspace_size(const orth_check_args* args, size_t* bytes);
+int orth_check_norm(const orth_check_args* args, float* out_dev, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Diagnostics. */
+const char* orth_status_string(int status);
+const char* orth_last_error(void);
+int32_t orth_version(void);
+
+/*
+ * Per-kernel timing with HIP events recorded around every launch on the
+ * launch stream (off by default; process-wide; not for concurrent callers).
+ * orth_timing_read synchronizes the recorded events and returns the total
+ * milliseconds and launch count of the named kernel since the last reset.
+ * orth_timing_names writes a ';'-separated list of the kernel names seen.
+ */
+int orth_timing_enable(int32_t on);
+int orth_timing_reset(void);
+int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launches);
+int orth_timing_names(char* buf, size_t buf_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ORTH_H_ */

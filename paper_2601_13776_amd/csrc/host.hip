@@ -1,0 +1,956 @@
+// Host side of liborth: argument validation, planning of the batched
+// launches, workspace layout, descriptor upload and the C ABI of
+// include/orth.h.  Every entry point validates everything before it
+// enqueues anything; the library allocates no device memory.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace orth {
+
+// ------------------------------------------------------------ errors ----
+static thread_local std::string g_last_error;
+
+static int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+#define ORTH_HIP(call)                                                                  \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess) return fail(ORTH_EHIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+// ------------------------------------------------------------ timing ----
+namespace {
+struct TimingRec {
+  std::string name;
+  hipEvent_t a, b;
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+std::map<std::string, std::pair<double, int64_t>> g_totals;
+
+hipEvent_t pool_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+int drain_timing_locked() {
+  int rc = ORTH_OK;
+  for (auto& r : g_pending) {
+    float ms = 0.f;
+    if (r.a && r.b && hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      auto& t = g_totals[r.name];
+      t.first += ms;
+      t.second += 1;
+    } else {
+      rc = ORTH_EHIP;
+    }
+    if (r.a) g_event_pool.push_back(r.a);
+    if (r.b) g_event_pool.push_back(r.b);
+  }
+  g_pending.clear();
+  return rc;
+}
+}  // namespace
+
+void timing_begin(const char* name, hipStream_t s) {
+  if (!g_timing) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  TimingRec r{name, pool_event(), nullptr};
+  if (r.a) hipEventRecord(r.a, s);
+  g_pending.push_back(r);
+}
+
+void timing_end(const char* name, hipStream_t s) {
+  if (!g_timing) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  for (auto it = g_pending.rbegin(); it != g_pending.rend(); ++it) {
+    if (it->b == nullptr && it->name == name) {
+      it->b = pool_event();
+      if (it->b) hipEventRecord(it->b, s);
+      break;
+    }
+  }
+}
+
+// ------------------------------------------------- descriptor staging ----
+// Descriptor tables are built on the host and copied into the head of the
+// caller's workspace.  The copy source is a pinned staging buffer from a
+// small ring; an event recorded after each copy guards reuse of the buffer.
+namespace {
+struct StageSlot {
+  void* buf = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+};
+std::mutex g_smu;
+StageSlot g_stage[4];
+int g_stage_next = 0;
+}  // namespace
+
+static int upload_tables(const std::vector<unsigned char>& img, void* dst, hipStream_t s) {
+  if (img.empty()) return ORTH_OK;
+  std::lock_guard<std::mutex> lk(g_smu);
+  StageSlot& sl = g_stage[g_stage_next];
+  g_stage_next = (g_stage_next + 1) % 4;
+  if (sl.done) ORTH_HIP(hipEventSynchronize(sl.done));
+  if (sl.cap < img.size()) {
+    if (sl.buf) ORTH_HIP(hipHostFree(sl.buf));
+    sl.buf = nullptr;
+    size_t cap = std::max<size_t>(img.size(), 1 << 16);
+    cap = (cap + 4095) & ~size_t(4095);
+    ORTH_HIP(hipHostMalloc(&sl.buf, cap, hipHostMallocDefault));
+    sl.cap = cap;
+  }
+  if (!sl.done) ORTH_HIP(hipEventCreateWithFlags(&sl.done, hipEventDisableTiming));
+  std::memcpy(sl.buf, img.data(), img.size());
+  ORTH_HIP(hipMemcpyAsync(dst, sl.buf, img.size(), hipMemcpyHostToDevice, s));
+  ORTH_HIP(hipEventRecord(sl.done, s));
+  return ORTH_OK;
+}
+
+// ------------------------------------------------------------ layout ----
+namespace {
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+struct Arena {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    off = align_up(off);
+    const size_t o = off;
+    off += bytes;
+    return o;
+  }
+};
+
+// Reorders a logical work list so that physical block p (dispatched to XCD
+// p % 8) gets consecutive logical items: XCD x owns one contiguous chunk.
+template <typename T>
+std::vector<T> xcd_order(const std::vector<T>& logical) {
+  const size_t n = logical.size();
+  std::vector<T> phys(n);
+  size_t start = 0;
+  for (size_t x = 0; x < 8; ++x) {
+    const size_t cnt = n > x ? (n - x + 7) / 8 : 0;
+    for (size_t slot = 0; slot < cnt; ++slot) phys[x + 8 * slot] = logical[start + slot];
+    start += cnt;
+  }
+  return phys;
+}
+
+// Tiles of a tr x tc grid in groups of `gm` tile rows (column-major inside a
+// group), so concurrently running tiles share operand panels.
+void grouped_tiles(int mat, int tr, int tc, int gm, bool upper_only, std::vector<TileItem>& out) {
+  for (int r0 = 0; r0 < tr; r0 += gm) {
+    const int r1 = std::min(tr, r0 + gm);
+    for (int j = 0; j < tc; ++j)
+      for (int i = r0; i < r1; ++i)
+        if (!upper_only || i <= j) out.push_back(TileItem{mat, i, j, 0});
+  }
+}
+}  // namespace
+
+// ---------------------------------------------------- orthogonalize plan --
+namespace {
+enum Bucket { SMALL32 = 0, SMALL64 = 1, TILED_F32 = 2, TILED_BF16_128 = 3, TILED_BF16_256 = 4 };
+
+struct MatPlan {
+  int bucket;
+  int32_t M, N, Mp, Np, transposed;
+};
+
+struct OrthoPlan {
+  std::vector<MatPlan> mp;
+  std::vector<SmallMat> small[2];
+  std::vector<TiledMat> tiled;                  // host copy with device pointers
+  std::vector<TileItem> partial_items, scale_items, writeout_items;
+  std::vector<TileItem> gram_items[2], update_items[2];  // bf16: [0] = 128 tiles, [1] = 256 tiles
+  std::vector<GemmItem> f32_gram, f32_update[2];
+  int max_mp[2] = {32, 32};
+  int total_partials = 0;
+  // offsets in the workspace
+  size_t off_small[2] = {0, 0}, off_tiled = 0, off_partial_items = 0, off_scale_items = 0, off_writeout_items = 0;
+  size_t off_gram_items[2] = {0, 0}, off_update_items[2] = {0, 0};
+  size_t off_f32_gram = 0, off_f32_update[2] = {0, 0};
+  size_t off_partials = 0, off_inv = 0, off_status = 0;
+  size_t table_bytes = 0, total_bytes = 0;
+};
+
+int validate_ortho(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !mats) return fail(ORTH_EINVAL, "mats is NULL");
+  if (!o) return fail(ORTH_EINVAL, "opts is NULL");
+  if (o->iters < 0) return fail(ORTH_EINVAL, "iters must be >= 0");
+  if (!(o->beta > 0.f && o->beta <= 0.5f)) return fail(ORTH_EINVAL, "beta must lie in (0, 0.5]");
+  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS)
+    return fail(ORTH_EINVAL, "unknown prescale mode");
+  if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
+    return fail(ORTH_EINVAL, "unknown dtype");
+  if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    char buf[160];
+    if (!m.in || !m.out) {
+      snprintf(buf, sizeof buf, "matrix %d: NULL data pointer", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.rows < 1 || m.cols < 1 || m.rows > (1 << 20) || m.cols > (1 << 20)) {
+      snprintf(buf, sizeof buf, "matrix %d: rows and cols must be in [1, 2^20]", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.ld_in < m.cols || m.ld_out < m.cols) {
+      snprintf(buf, sizeof buf, "matrix %d: leading dimension smaller than cols", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.in == m.out && (o->in_dtype != o->out_dtype || m.ld_in != m.ld_out)) {
+      snprintf(buf, sizeof buf, "matrix %d: in-place needs equal dtypes and leading dims", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+  }
+  return ORTH_OK;
+}
+
+// Builds the whole plan; device pointers are derived from `ws` (may be
+// nullptr when only sizing).
+void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o, OrthoPlan& P,
+                      unsigned char* ws, bool want_status_scratch) {
+  const bool bf16 = o->compute == ORTH_COMPUTE_BF16;
+  P.mp.resize(n);
+  int n_tiled = 0;
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    MatPlan& q = P.mp[i];
+    q.transposed = m.rows < m.cols;
+    q.M = std::max(m.rows, m.cols);
+    q.N = std::min(m.rows, m.cols);
+    if (q.N <= 64 && q.M <= 128) {
+      q.bucket = q.N <= 32 ? SMALL32 : SMALL64;
+      q.Mp = (int32_t)round_up(q.M, 32);
+      q.Np = q.N <= 32 ? 32 : 64;
+    } else if (!bf16) {
+      q.bucket = TILED_F32;
+      q.Mp = (int32_t)round_up(q.M, 64);
+      q.Np = (int32_t)round_up(q.N, 64);
+    } else if (q.N >= 1024) {
+      q.bucket = TILED_BF16_256;
+      q.Mp = (int32_t)round_up(q.M, 256);
+      q.Np = (int32_t)round_up(q.N, 256);
+    } else {
+      q.bucket = TILED_BF16_128;
+      q.Mp = (int32_t)round_up(q.M, 128);
+      q.Np = (int32_t)round_up(q.N, 128);
+    }
+    if (q.bucket >= TILED_F32) ++n_tiled;
+  }
+
+  // table region
+  Arena A;
+  int n_small[2] = {0, 0};
+  for (auto& q : P.mp)
+    if (q.bucket <= SMALL64) ++n_small[q.bucket];
+  P.off_small[0] = A.take(sizeof(SmallMat) * n_small[0]);
+  P.off_small[1] = A.take(sizeof(SmallMat) * n_small[1]);
+  P.off_tiled = A.take(sizeof(TiledMat) * n_tiled);
+
+  // count work items first (sizes of the tables)
+  int64_t n_part = 0, n_scale = 0, n_wo = 0, n_g[2] = {0, 0}, n_u[2] = {0, 0}, n_fg = 0, n_fu = 0;
+  for (int i = 0; i < n; ++i) {
+    const MatPlan& q = P.mp[i];
+    if (q.bucket <= SMALL64) continue;
+    const int64_t pr = (mats[i].rows + 63) / 64, pc = (mats[i].cols + 63) / 64;
+    n_part += pr * pc;
+    n_wo += pr * pc;
+    n_scale += (int64_t)(q.Mp / 64) * (q.Np / 64);
+    if (q.bucket == TILED_F32) {
+      const int64_t tn = q.Np / 64, tm = q.Mp / 64;
+      n_fg += tn * (tn + 1) / 2;
+      n_fu += tm * tn;
+    } else {
+      const int b = q.bucket == TILED_BF16_256 ? 1 : 0;
+      const int t = b ? 256 : 128;
+      const int64_t tn = q.Np / t, tm = q.Mp / t;
+      n_g[b] += tn * (tn + 1) / 2;
+      n_u[b] += tm * tn;
+    }
+  }
+  P.off_partial_items = A.take(sizeof(TileItem) * n_part);
+  P.off_scale_items = A.take(sizeof(TileItem) * n_scale);
+  P.off_writeout_items = A.take(sizeof(TileItem) * n_wo);
+  for (int b = 0; b < 2; ++b) {
+    P.off_gram_items[b] = A.take(sizeof(TileItem) * n_g[b]);
+    P.off_update_items[b] = A.take(sizeof(TileItem) * n_u[b]);
+  }
+  P.off_f32_gram = A.take(sizeof(GemmItem) * n_fg);
+  P.off_f32_update[0] = A.take(sizeof(GemmItem) * n_fu);
+  P.off_f32_update[1] = A.take(sizeof(GemmItem) * n_fu);
+  P.table_bytes = align_up(A.off);
+  P.off_partials = A.take(sizeof(double) * n_part);
+  P.off_inv = A.take(sizeof(float) * n_tiled);
+  P.off_status = A.take(want_status_scratch ? sizeof(int32_t) * n : 0);
+
+  auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
+
+  // per-matrix buffers and descriptors
+  int part_base = 0, tiled_idx = 0;
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    const MatPlan& q = P.mp[i];
+    if (q.bucket <= SMALL64) {
+      SmallMat s{};
+      s.in = m.in;
+      s.out = m.out;
+      s.ld_in = m.ld_in;
+      s.ld_out = m.ld_out;
+      s.rows = m.rows;
+      s.cols = m.cols;
+      s.M = q.M;
+      s.N = q.N;
+      s.Mp = q.Mp;
+      s.transposed = q.transposed;
+      s.status_index = i;
+      P.small[q.bucket].push_back(s);
+      P.max_mp[q.bucket] = std::max(P.max_mp[q.bucket], q.Mp);
+      continue;
+    }
+    TiledMat t{};
+    t.in = m.in;
+    t.out = m.out;
+    t.ld_in = m.ld_in;
+    t.ld_out = m.ld_out;
+    t.rows = m.rows;
+    t.cols = m.cols;
+    t.M = q.M;
+    t.N = q.N;
+    t.Mp = q.Mp;
+    t.Np = q.Np;
+    t.transposed = q.transposed;
+    t.status_index = i;
+    const int pr = (m.rows + 63) / 64, pc = (m.cols + 63) / 64;
+    t.partial_base = part_base;
+    t.n_partials = pr * pc;
+    part_base += pr * pc;
+    const size_t elems = (size_t)q.Mp * q.Np;
+    const size_t csz = bf16 ? 2 : 4;
+    t.master[0] = reinterpret_cast<float*>(dev(A.take(elems * 4)));
+    t.master[1] = bf16 ? nullptr : reinterpret_cast<float*>(dev(A.take(elems * 4)));
+    t.xc[0] = bf16 ? dev(A.take(elems * 2)) : nullptr;
+    t.xc[1] = bf16 ? dev(A.take(elems * 2)) : nullptr;
+    t.xt = dev(A.take(elems * csz));
+    t.e = dev(A.take((size_t)q.Np * q.Np * csz));
+    t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + tiled_idx;
+    P.tiled.push_back(t);
+
+    for (int a = 0; a < pr; ++a)
+      for (int b = 0; b < pc; ++b) {
+        P.partial_items.push_back(TileItem{tiled_idx, a, b, 0});
+        P.writeout_items.push_back(TileItem{tiled_idx, a, b, 0});
+      }
+    for (int a = 0; a < q.Mp / 64; ++a)
+      for (int b = 0; b < q.Np / 64; ++b) P.scale_items.push_back(TileItem{tiled_idx, a, b, 0});
+
+    if (q.bucket == TILED_F32) {
+      const int tn = q.Np / 64, tm = q.Mp / 64;
+      std::vector<TileItem> gt, ut;
+      grouped_tiles(tiled_idx, tn, tn, 4, true, gt);
+      grouped_tiles(tiled_idx, tm, tn, 4, false, ut);
+      for (auto& g : gt) {
+        GemmItem gi{};
+        gi.A = t.xt;
+        gi.B = t.xt;
+        gi.C = t.e;
+        gi.lda = gi.ldb = q.Mp;
+        gi.ldc = q.Np;
+        gi.M = gi.N = q.Np;
+        gi.K = q.Mp;
+        gi.ti = g.ti;
+        gi.tj = g.tj;
+        gi.a_dtype = gi.b_dtype = ORTH_F32;
+        gi.epi = EPI_GRAM_E;
+        gi.mirror = g.ti != g.tj;
+        P.f32_gram.push_back(gi);
+      }
+      for (int par = 0; par < 2; ++par)
+        for (auto& u : ut) {
+          GemmItem gi{};
+          gi.A = t.master[par];
+          gi.B = t.e;
+          gi.C = t.master[par ^ 1];
+          gi.src = t.master[par];
+          gi.dst2 = static_cast<float*>(t.xt);
+          gi.lda = q.Np;
+          gi.ldb = q.Np;
+          gi.ldc = q.Np;
+          gi.ld_src = q.Np;
+          gi.ld2 = q.Mp;
+          gi.M = q.Mp;
+          gi.N = q.Np;
+          gi.K = q.Np;
+          gi.ti = u.ti;
+          gi.tj = u.tj;
+          gi.a_dtype = gi.b_dtype = ORTH_F32;
+          gi.epi = EPI_UPDATE;
+          gi.beta = o->beta;
+          P.f32_update[par].push_back(gi);
+        }
+    } else {
+      const int b = q.bucket == TILED_BF16_256 ? 1 : 0;
+      const int tsz = b ? 256 : 128;
+      const int tn = q.Np / tsz, tm = q.Mp / tsz;
+      grouped_tiles(tiled_idx, tn, tn, 4, true, P.gram_items[b]);
+      grouped_tiles(tiled_idx, tm, tn, 4, false, P.update_items[b]);
+    }
+    ++tiled_idx;
+  }
+  P.total_partials = part_base;
+  P.total_bytes = align_up(A.off);
+
+  // XCD-aware physical order of the GEMM work lists
+  for (int b = 0; b < 2; ++b) {
+    P.gram_items[b] = xcd_order(P.gram_items[b]);
+    P.update_items[b] = xcd_order(P.update_items[b]);
+  }
+  P.f32_gram = xcd_order(P.f32_gram);
+  P.f32_update[0] = xcd_order(P.f32_update[0]);
+  P.f32_update[1] = xcd_order(P.f32_update[1]);
+}
+
+template <typename T>
+void put(std::vector<unsigned char>& img, size_t off, const std::vector<T>& v) {
+  if (v.empty()) return;
+  std::memcpy(img.data() + off, v.data(), sizeof(T) * v.size());
+}
+
+int check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return ORTH_OK;
+  if (!ws) return fail(ORTH_EWORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(ORTH_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need) {
+    char buf[128];
+    snprintf(buf, sizeof buf, "workspace too small: %zu bytes given, %zu needed", have, need);
+    return fail(ORTH_EWORKSPACE, buf);
+  }
+  return ORTH_OK;
+}
+}  // namespace
+
+// ------------------------------------------------------- conv planning ---
+namespace {
+int validate_geom(const orth_conv_geom* g) {
+  if (!g) return fail(ORTH_EINVAL, "geometry is NULL");
+  if (g->cin < 1 || g->cout < 1 || g->k < 1 || g->stride < 1 || g->dilation < 1 || g->groups < 1)
+    return fail(ORTH_EINVAL, "all conv sizes must be >= 1");
+  if (g->cin > (1 << 20) || g->cout > (1 << 20) || g->k > 64 || g->stride > 64 || g->dilation > 1024)
+    return fail(ORTH_EINVAL, "conv sizes out of range");
+  if (g->cin % g->groups || g->cout % g->groups) return fail(ORTH_EINVAL, "groups must divide cin and cout");
+  if (g->k < g->stride) return fail(ORTH_EUNSUPPORTED, "kernel size must be >= stride");
+  int a = g->stride, b = g->dilation;
+  while (b) {
+    const int t = a % b;
+    a = b;
+    b = t;
+  }
+  if (g->stride > 1 && a != 1) return fail(ORTH_EUNSUPPORTED, "stride > 1 needs gcd(stride, dilation) == 1");
+  if (g->k > g->stride && g->cin / g->groups < 2)
+    return fail(ORTH_EUNSUPPORTED, "BCOP blocks need at least 2 channels per group");
+  return ORTH_OK;
+}
+
+struct ConvPlan {
+  std::vector<ComposeGroup> groups;
+  std::vector<GemmItem> proj_items;
+  std::vector<std::vector<GemmItem>> phase_gemm;
+  std::vector<std::vector<CombineItem>> phase_comb;
+  std::vector<int64_t> phase_max_elems;
+  int64_t init_max = 0, scatter_max = 0;
+  size_t off_groups = 0, off_proj_items = 0;
+  std::vector<size_t> off_phase_gemm, off_phase_comb;
+  size_t table_bytes = 0, total_bytes = 0;
+};
+
+int validate_conv_descs(const orth_conv_desc* d, int32_t n, int32_t dtype) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !d) return fail(ORTH_EINVAL, "descs is NULL");
+  if (dtype != ORTH_F32 && dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+  for (int i = 0; i < n; ++i) {
+    const int rc = validate_geom(&d[i].geom);
+    if (rc) return rc;
+    const int nproj = 2 * (d[i].geom.k - d[i].geom.stride);
+    if (!d[i].rko || !d[i].kernel || (nproj > 0 && !d[i].proj)) return fail(ORTH_EINVAL, "NULL conv data pointer");
+  }
+  return ORTH_OK;
+}
+
+void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan& P, unsigned char* ws) {
+  const size_t esz = dtype == ORTH_BF16 ? 2 : 4;
+  int max_kp = 1;
+  for (int i = 0; i < n; ++i) max_kp = std::max(max_kp, d[i].geom.k - d[i].geom.stride + 1);
+  const int n_phase = 2 * (max_kp - 1);
+  // count
+  int n_groups = 0;
+  for (int i = 0; i < n; ++i) n_groups += d[i].geom.groups;
+  Arena A;
+  P.off_groups = A.take(sizeof(ComposeGroup) * n_groups);
+
+  auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
+  // item lists (pointers filled after buffer layout, so lay out buffers in a
+  // second arena that starts after the tables; sizes of tables are counted first)
+  P.phase_gemm.assign(n_phase, {});
+  P.phase_comb.assign(n_phase, {});
+  P.phase_max_elems.assign(n_phase, 0);
+
+  struct Tmp {
+    int layer, group;
+  };
+  std::vector<Tmp> tmp;
+  for (int i = 0; i < n; ++i)
+    for (int g = 0; g < d[i].geom.groups; ++g) tmp.push_back(Tmp{i, g});
+
+  // counts of items to size the table region
+  size_t n_proj_items = 0;
+  std::vector<size_t> n_pg(n_phase, 0), n_pc(n_phase, 0);
+  for (auto& t : tmp) {
+    const orth_conv_geom& g = d[t.layer].geom;
+    const int c = g.cin / g.groups, og = g.cout / g.groups, s = g.stride, k = g.k, kp = k - s + 1;
+    const int nproj = 2 * (kp - 1);
+    const size_t ct = (c + 63) / 64, ot = (og + 63) / 64;
+    n_proj_items += nproj * ct * ct;
+    for (int ph = 0; ph < n_phase; ++ph) {
+      const bool vert = ph >= max_kp - 1;
+      const int j = vert ? ph - (max_kp - 1) : ph;
+      if (j >= kp - 1) continue;
+      const int in_h = vert ? s + j : s, in_w = vert ? k : s + j;
+      n_pg[ph] += (size_t)in_h * in_w * ot * ct;
+      n_pc[ph] += 1;
+    }
+  }
+  P.off_proj_items = A.take(sizeof(GemmItem) * n_proj_items);
+  P.off_phase_gemm.resize(n_phase);
+  P.off_phase_comb.resize(n_phase);
+  for (int ph = 0; ph < n_phase; ++ph) {
+    P.off_phase_gemm[ph] = A.take(sizeof(GemmItem) * n_pg[ph]);
+    P.off_phase_comb[ph] = A.take(sizeof(CombineItem) * n_pc[ph]);
+  }
+  P.table_bytes = align_up(A.off);
+
+  for (auto& t : tmp) {
+    const orth_conv_desc& L = d[t.layer];
+    const orth_conv_geom& g = L.geom;
+    const int c = g.cin / g.groups, og = g.cout / g.groups, s = g.stride, k = g.k, kp = k - s + 1;
+    const int h = c / 2, nproj = 2 * (kp - 1);
+    ComposeGroup G{};
+    G.rko = static_cast<const unsigned char*>(L.rko) + (size_t)t.group * og * c * s * s * esz;
+    G.proj = nproj ? static_cast<const unsigned char*>(L.proj) + (size_t)t.group * nproj * c * h * esz : nullptr;
+    G.kernel = L.kernel;
+    const size_t tapbytes = (size_t)k * k * og * c * sizeof(float);
+    G.taps[0] = reinterpret_cast<float*>(dev(A.take(tapbytes)));
+    G.taps[1] = kp > 1 ? reinterpret_cast<float*>(dev(A.take(tapbytes))) : nullptr;
+    G.y = kp > 1 ? reinterpret_cast<float*>(dev(A.take(tapbytes))) : nullptr;
+    G.p = nproj ? reinterpret_cast<float*>(dev(A.take((size_t)nproj * c * c * sizeof(float)))) : nullptr;
+    G.cout_g = og;
+    G.c = c;
+    G.h = h;
+    G.k = k;
+    G.s = s;
+    G.group = t.group;
+    G.nproj = nproj;
+    const int gidx = (int)P.groups.size();
+    P.init_max = std::max<int64_t>(P.init_max, (int64_t)s * s * og * c);
+    P.scatter_max = std::max<int64_t>(P.scatter_max, (int64_t)k * k * og * c);
+
+    const int ct = (c + 63) / 64, ot = (og + 63) / 64;
+    for (int j = 0; j < nproj; ++j)
+      for (int a = 0; a < ct; ++a)
+        for (int b = 0; b < ct; ++b) {
+          GemmItem gi{};
+          gi.A = static_cast<const unsigned char*>(G.proj) + (size_t)j * c * h * esz;
+          gi.B = gi.A;
+          gi.C = G.p + (size_t)j * c * c;
+          gi.lda = gi.ldb = h;
+          gi.ldc = c;
+          gi.M = gi.N = c;
+          gi.K = h;
+          gi.ti = a;
+          gi.tj = b;
+          gi.a_dtype = gi.b_dtype = dtype;
+          gi.epi = EPI_STORE;
+          P.proj_items.push_back(gi);
+        }
+    int cur = 0;
+    for (int ph = 0; ph < n_phase; ++ph) {
+      const bool vert = ph >= max_kp - 1;
+      const int j = vert ? ph - (max_kp - 1) : ph;
+      if (j >= kp - 1) continue;
+      const int in_h = vert ? s + j : s, in_w = vert ? k : s + j;
+      const int pj = vert ? (kp - 1) + j : j;  // projector index: h blocks first
+      const size_t tap = (size_t)og * c;
+      for (int a = 0; a < in_h; ++a)
+        for (int b = 0; b < in_w; ++b)
+          for (int ti = 0; ti < ot; ++ti)
+            for (int tj = 0; tj < ct; ++tj) {
+              GemmItem gi{};
+              gi.A = G.taps[cur] + (size_t)(a * k + b) * tap;
+              gi.B = G.p + (size_t)pj * c * c;
+              gi.C = G.y + (size_t)(a * k + b) * tap;
+              gi.lda = c;
+              gi.ldb = c;
+              gi.ldc = c;
+              gi.M = og;
+              gi.N = c;
+              gi.K = c;
+              gi.ti = ti;
+              gi.tj = tj;
+              gi.a_dtype = gi.b_dtype = ORTH_F32;
+              gi.epi = EPI_STORE;
+              P.phase_gemm[ph].push_back(gi);
+            }
+      P.phase_comb[ph].push_back(CombineItem{gidx, vert ? 1 : 0, in_h, in_w, cur, 0});
+      const int out_taps = (in_h + (vert ? 1 : 0)) * (in_w + (vert ? 0 : 1));
+      P.phase_max_elems[ph] = std::max<int64_t>(P.phase_max_elems[ph], (int64_t)out_taps * og * c);
+      cur ^= 1;
+    }
+    G.cur = cur;
+    P.groups.push_back(G);
+  }
+  P.total_bytes = align_up(A.off);
+  for (int ph = 0; ph < n_phase; ++ph) P.phase_gemm[ph] = xcd_order(P.phase_gemm[ph]);
+}
+}  // namespace
+
+}  // namespace orth
+
+using namespace orth;
+
+// ================================================================== C ABI =
+extern "C" {
+
+const char* orth_status_string(int status) {
+  switch (status) {
+    case ORTH_OK: return "ok";
+    case ORTH_EINVAL: return "invalid argument";
+    case ORTH_EUNSUPPORTED: return "unsupported configuration";
+    case ORTH_EWORKSPACE: return "workspace missing, too small or misaligned";
+    case ORTH_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* orth_last_error(void) { return g_last_error.c_str(); }
+
+int32_t orth_version(void) { return 100; }
+
+int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
+                                      size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  int rc = validate_ortho(mats, n, opts);
+  if (rc) return rc;
+  OrthoPlan P;
+  build_ortho_plan(mats, n, opts, P, nullptr, true);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
+                               size_t workspace_bytes, int32_t* status_dev, void* stream) {
+  int rc = validate_ortho(mats, n, opts);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  OrthoPlan P;
+  build_ortho_plan(mats, n, opts, P, nullptr, true);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = OrthoPlan();
+  build_ortho_plan(mats, n, opts, P, ws, true);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
+
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_small[0], P.small[0]);
+  put(img, P.off_small[1], P.small[1]);
+  put(img, P.off_tiled, P.tiled);
+  put(img, P.off_partial_items, P.partial_items);
+  put(img, P.off_scale_items, P.scale_items);
+  put(img, P.off_writeout_items, P.writeout_items);
+  for (int b = 0; b < 2; ++b) {
+    put(img, P.off_gram_items[b], P.gram_items[b]);
+    put(img, P.off_update_items[b], P.update_items[b]);
+  }
+  put(img, P.off_f32_gram, P.f32_gram);
+  put(img, P.off_f32_update[0], P.f32_update[0]);
+  put(img, P.off_f32_update[1], P.f32_update[1]);
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+
+  auto T = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
+  const TiledMat* tm = reinterpret_cast<const TiledMat*>(ws + P.off_tiled);
+  const int nt = (int)P.tiled.size();
+  const bool bf16 = opts->compute == ORTH_COMPUTE_BF16;
+  const int iters = opts->iters;
+  if (nt > 0) {
+    double* partials = reinterpret_cast<double*>(ws + P.off_partials);
+    ORTH_HIP(launch_prescale_partial(tm, T(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
+                                     partials, s));
+    ORTH_HIP(launch_prescale_finish(tm, nt, partials, opts->prescale, status, s));
+    ORTH_HIP(launch_prescale_scale(tm, T(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
+                                   opts->compute, s));
+    for (int t = 0; t < iters; ++t) {
+      if (bf16) {
+        for (int b = 1; b >= 0; --b)
+          ORTH_HIP(launch_bf16_gram(b, tm, T(P.off_gram_items[b]), (int)P.gram_items[b].size(), s));
+        for (int b = 1; b >= 0; --b)
+          ORTH_HIP(launch_bf16_update(b, tm, T(P.off_update_items[b]), (int)P.update_items[b].size(), t & 1,
+                                      opts->beta, s));
+      } else {
+        ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_gram), (int)P.f32_gram.size(),
+                                 "bjorck_gram_f32", s));
+        ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_update[t & 1]),
+                                 (int)P.f32_update[t & 1].size(), "bjorck_update_f32", s));
+      }
+    }
+    ORTH_HIP(launch_writeout(tm, T(P.off_writeout_items), (int)P.writeout_items.size(), bf16 ? 0 : (iters & 1),
+                             opts->out_dtype, s));
+  }
+  for (int b = 0; b < 2; ++b)
+    ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
+                                 b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale, opts->in_dtype,
+                                 opts->out_dtype, status, s));
+  return ORTH_OK;
+}
+
+int orth_aoc_param_shapes(const orth_conv_geom* geom, int32_t* rko_rows, int32_t* rko_cols, int32_t* n_proj,
+                          int32_t* proj_rows, int32_t* proj_cols) {
+  const int rc = validate_geom(geom);
+  if (rc) return rc;
+  const int c = geom->cin / geom->groups, s = geom->stride;
+  if (rko_rows) *rko_rows = geom->cout / geom->groups;
+  if (rko_cols) *rko_cols = c * s * s;
+  if (n_proj) *n_proj = 2 * (geom->k - s);
+  if (proj_rows) *proj_rows = c;
+  if (proj_cols) *proj_cols = c / 2;
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernels_workspace_size(const orth_conv_desc* descs, int32_t n, int32_t dtype, size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  int rc = validate_conv_descs(descs, n, dtype);
+  if (rc) return rc;
+  ConvPlan P;
+  build_conv_plan(descs, n, dtype, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  int rc = validate_conv_descs(descs, n, dtype);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  ConvPlan P;
+  build_conv_plan(descs, n, dtype, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = ConvPlan();
+  build_conv_plan(descs, n, dtype, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_groups, P.groups);
+  put(img, P.off_proj_items, P.proj_items);
+  for (size_t ph = 0; ph < P.phase_gemm.size(); ++ph) {
+    put(img, P.off_phase_gemm[ph], P.phase_gemm[ph]);
+    put(img, P.off_phase_comb[ph], P.phase_comb[ph]);
+  }
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+  const ComposeGroup* G = reinterpret_cast<const ComposeGroup*>(ws + P.off_groups);
+  const int ng = (int)P.groups.size();
+  ORTH_HIP(launch_compose_init(G, ng, dtype, P.init_max, s));
+  ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_proj_items), (int)P.proj_items.size(),
+                           "compose_projector", s));
+  for (size_t ph = 0; ph < P.phase_gemm.size(); ++ph) {
+    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_phase_gemm[ph]),
+                             (int)P.phase_gemm[ph].size(), "compose_tap_gemm", s));
+    ORTH_HIP(launch_compose_combine(G, reinterpret_cast<const CombineItem*>(ws + P.off_phase_comb[ph]),
+                                    (int)P.phase_comb[ph].size(), P.phase_max_elems[ph], s));
+  }
+  ORTH_HIP(launch_compose_scatter(G, ng, dtype, P.scatter_max, s));
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernel(const void* rko, const void* proj, int32_t cin, int32_t cout, int32_t k, int32_t stride,
+                           int32_t dilation, int32_t groups, int32_t dtype, void* kernel_out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  orth_conv_desc d;
+  d.geom = orth_conv_geom{cin, cout, k, stride, dilation, groups};
+  d.rko = rko;
+  d.proj = proj;
+  d.kernel = kernel_out;
+  return orth_build_conv_kernels_batched(&d, 1, dtype, workspace, workspace_bytes, stream);
+}
+
+// --------------------------------------------------------------- checks --
+namespace {
+int validate_check(const orth_check_args* a) {
+  if (!a) return fail(ORTH_EINVAL, "args is NULL");
+  if (a->mode == ORTH_CHECK_GRAM) {
+    if (a->n_mats < 0 || (a->n_mats > 0 && !a->mats)) return fail(ORTH_EINVAL, "bad matrix list");
+    if (a->mat_dtype != ORTH_F32 && a->mat_dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+    for (int i = 0; i < a->n_mats; ++i) {
+      const orth_mat& m = a->mats[i];
+      if (!m.in || m.rows < 1 || m.cols < 1 || m.ld_in < m.cols || m.rows > (1 << 20) || m.cols > (1 << 20))
+        return fail(ORTH_EINVAL, "bad matrix in check list");
+    }
+    return ORTH_OK;
+  }
+  if (a->mode != ORTH_CHECK_CONV && a->mode != ORTH_CHECK_CONV_ADJOINT) return fail(ORTH_EINVAL, "unknown check mode");
+  int rc = validate_geom(&a->geom);
+  if (rc) return rc;
+  if (a->kernel_dtype != ORTH_F32 && a->kernel_dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+  if (!a->kernel || !a->x) return fail(ORTH_EINVAL, "NULL kernel or input");
+  if (a->batch < 1 || a->height < 1 || a->width < 1) return fail(ORTH_EINVAL, "batch, height, width must be >= 1");
+  if (a->mode == ORTH_CHECK_CONV && (a->height % a->geom.stride || a->width % a->geom.stride))
+    return fail(ORTH_EINVAL, "height and width must be divisible by the stride");
+  if ((int64_t)a->geom.cout * a->height * a->width * a->geom.stride * a->geom.stride > (int64_t)1 << 31 ||
+      (int64_t)a->geom.cin * a->height * a->width * a->geom.stride * a->geom.stride > (int64_t)1 << 31)
+    return fail(ORTH_EINVAL, "conv check input too large");
+  return ORTH_OK;
+}
+
+void gram_check_items(const orth_check_args* a, float* out, std::vector<GemmItem>& items) {
+  for (int i = 0; i < a->n_mats; ++i) {
+    const orth_mat& m = a->mats[i];
+    const bool tall = m.rows >= m.cols;
+    const int nsz = tall ? m.cols : m.rows, ksz = tall ? m.rows : m.cols;
+    const int t = (nsz + 63) / 64;
+    for (int ti = 0; ti < t; ++ti)
+      for (int tj = 0; tj < t; ++tj) {
+        GemmItem g{};
+        g.A = g.B = m.in;
+        g.lda = g.ldb = m.ld_in;
+        g.M = g.N = nsz;
+        g.K = ksz;
+        g.ti = ti;
+        g.tj = tj;
+        g.a_dtype = g.b_dtype = a->mat_dtype;
+        g.a_trans = g.b_trans = tall ? 1 : 0;
+        g.epi = EPI_MAXDEV;
+        g.red = out + i;
+        items.push_back(g);
+      }
+  }
+}
+
+size_t conv_partial_doubles(const orth_check_args* a) {
+  const int s = a->geom.stride;
+  int64_t in_ps, out_ps;
+  if (a->mode == ORTH_CHECK_CONV) {
+    in_ps = (int64_t)a->geom.cin * a->height * a->width;
+    out_ps = (int64_t)a->geom.cout * (a->height / s) * (a->width / s);
+  } else {
+    in_ps = (int64_t)a->geom.cout * a->height * a->width;
+    out_ps = (int64_t)a->geom.cin * a->height * s * a->width * s;
+  }
+  return (size_t)a->batch * (size_t)((in_ps + 255) / 256 + (out_ps + 255) / 256);
+}
+}  // namespace
+
+int orth_check_workspace_size(const orth_check_args* args, size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  int rc = validate_check(args);
+  if (rc) return rc;
+  if (args->mode == ORTH_CHECK_GRAM) {
+    std::vector<GemmItem> items;
+    gram_check_items(args, nullptr, items);
+    *bytes = align_up(sizeof(GemmItem) * items.size());
+  } else {
+    *bytes = align_up(sizeof(double) * conv_partial_doubles(args));
+  }
+  return ORTH_OK;
+}
+
+int orth_check_norm(const orth_check_args* args, float* out_dev, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  int rc = validate_check(args);
+  if (rc) return rc;
+  if (!out_dev) return fail(ORTH_EINVAL, "out_dev is NULL");
+  size_t need = 0;
+  orth_check_workspace_size(args, &need);
+  rc = check_workspace(workspace, workspace_bytes, need);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (args->mode == ORTH_CHECK_GRAM) {
+    if (args->n_mats == 0) return ORTH_OK;
+    std::vector<GemmItem> items;
+    gram_check_items(args, out_dev, items);
+    std::vector<unsigned char> img(sizeof(GemmItem) * items.size());
+    std::memcpy(img.data(), items.data(), img.size());
+    ORTH_HIP(launch_fill_f32(out_dev, args->n_mats, 0.f, s));
+    rc = upload_tables(img, workspace, s);
+    if (rc) return rc;
+    ORTH_HIP(launch_gemm_f32(static_cast<const GemmItem*>(workspace), (int)items.size(), "check_gram", s));
+    return ORTH_OK;
+  }
+  ORTH_HIP(launch_conv_check(args, args->kernel, args->x, static_cast<double*>(workspace), out_dev,
+                             args->mode == ORTH_CHECK_CONV_ADJOINT, s));
+  return ORTH_OK;
+}
+
+// --------------------------------------------------------------- timing --
+int orth_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+  return ORTH_OK;
+}
+
+int orth_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  const int rc = drain_timing_locked();
+  g_totals.clear();
+  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+}
+
+int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launches) {
+  if (!kernel_name || !total_ms || !launches) return fail(ORTH_EINVAL, "NULL argument");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  const int rc = drain_timing_locked();
+  auto it = g_totals.find(kernel_name);
+  *total_ms = it == g_totals.end() ? 0.0 : it->second.first;
+  *launches = it == g_totals.end() ? 0 : it->second.second;
+  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+}
+
+int orth_timing_names(char* buf, size_t buf_bytes) {
+  if (!buf || buf_bytes == 0) return fail(ORTH_EINVAL, "NULL buffer");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  drain_timing_locked();
+  std::string all;
+  for (auto& kv : g_totals) {
+    if (!all.empty()) all += ";";
+    all += kv.first;
+  }
+  if (all.size() + 1 > buf_bytes) return fail(ORTH_EINVAL, "buffer too small");
+  std::memcpy(buf, all.c_str(), all.size() + 1);
+  return ORTH_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,163 @@
+// Internal declarations shared by the HIP kernels and the host side of
+// liborth.  Not part of the public ABI (include/orth.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/orth.h"
+
+namespace orth {
+
+// ---------------------------------------------------------------------------
+// bfloat16 <-> fp32.  Round to nearest, ties to even; NaN stays a quiet NaN.
+// ---------------------------------------------------------------------------
+__host__ __device__ inline float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+__device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+__device__ inline float load_as_f32(const void* p, int64_t idx, int dtype) {
+  return dtype == ORTH_BF16 ? bf16_to_f32(static_cast<const uint16_t*>(p)[idx])
+                            : static_cast<const float*>(p)[idx];
+}
+__device__ inline void store_from_f32(void* p, int64_t idx, int dtype, float v) {
+  if (dtype == ORTH_BF16)
+    static_cast<uint16_t*>(p)[idx] = f32_to_bf16(v);
+  else
+    static_cast<float*>(p)[idx] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Björck batch descriptors (device-resident tables built by the host).
+// Every matrix is processed in its tall orientation M x N (M >= N); a wide
+// input (rows < cols) is transposed on the way in and out.
+// ---------------------------------------------------------------------------
+struct TiledMat {
+  const void* in;
+  void* out;
+  int64_t ld_in, ld_out;
+  int32_t rows, cols;        // as given by the caller
+  int32_t M, N;              // tall orientation
+  int32_t Mp, Np;            // padded to the tile grid (zero padding is exact)
+  int32_t transposed;        // rows < cols
+  int32_t status_index;      // index in the batch (status array slot)
+  int32_t partial_base;      // first slot of this matrix's partial sums
+  int32_t n_partials;
+  float* master[2];          // fp32 iterate, Mp x Np (bf16 mode uses [0] only)
+  void* xc[2];               // bf16 mode: bf16 copies of the iterate, Mp x Np
+  void* xt;                  // transposed iterate in compute dtype, Np x Mp
+  void* e;                   // I - X^T X in compute dtype, Np x Np
+  float* inv_norm;           // this matrix's pre-scale factor
+};
+
+struct TileItem {
+  int32_t mat;
+  int32_t ti, tj;
+  int32_t pad;
+};
+
+struct SmallMat {
+  const void* in;
+  void* out;
+  int64_t ld_in, ld_out;
+  int32_t rows, cols;
+  int32_t M, N;              // tall orientation
+  int32_t Mp;                // M rounded up to 32
+  int32_t transposed;
+  int32_t status_index;
+  int32_t pad;
+};
+
+// Generic bounds-checked fp32 GEMM work item: C = A * B^T over one
+// 64 x 64 output tile, A logically M x K, B logically N x K.
+enum GemmEpi : int32_t {
+  EPI_STORE = 0,     // C[i][j] = acc
+  EPI_GRAM_E = 1,    // C[i][j] = delta_ij - acc  (and C[j][i] if mirror)
+  EPI_UPDATE = 2,    // v = src[i][j] + beta acc; C[i][j] = v; dst2[j][i] = v
+  EPI_MAXDEV = 3     // red[0] = max(red[0], |delta_ij - acc|)
+};
+
+struct GemmItem {
+  const void* A;
+  const void* B;
+  void* C;
+  const float* src;
+  float* dst2;
+  float* red;
+  int64_t lda, ldb, ldc, ld_src, ld2;
+  int32_t M, N, K;
+  int32_t ti, tj;
+  int32_t a_dtype, b_dtype;  // storage of A and B
+  int32_t a_trans, b_trans;  // 0: row-major [M][K]; 1: stored [K][M]
+  int32_t epi;
+  int32_t mirror;
+  float beta;
+};
+
+// Compose (AOC) descriptors: one entry per (layer, group).
+struct ComposeGroup {
+  const void* rko;           // this group's RKO matrix, cout_g x (c s^2)
+  const void* proj;          // this group's projector factors, nproj x c x h
+  void* kernel;              // whole layer kernel (OIHW); group offset applied in-kernel
+  float* taps[2];            // ping-pong tap buffers, k*k taps of cout_g x c
+  float* y;                  // tap products, k*k taps of cout_g x c
+  float* p;                  // projectors, nproj x c x c
+  int32_t cout_g, c, h;      // h = floor(c / 2)
+  int32_t k, s, group, nproj;
+  int32_t cur;               // which taps[] holds the current kernel
+  int32_t pad;
+};
+
+// One tap-combination work item of a block step.
+struct CombineItem {
+  int32_t grp;               // ComposeGroup index
+  int32_t vertical;          // 0: horizontal block, 1: vertical block
+  int32_t in_h, in_w;        // tap grid before the step
+  int32_t src;               // taps[src] is read, taps[src ^ 1] written
+  int32_t pad;
+};
+
+// ---------------------------------------------------------------------------
+// Launch helpers (host).
+// ---------------------------------------------------------------------------
+struct LaunchCtx {
+  hipStream_t stream;
+};
+
+// Timing hooks around every launch (no-ops unless timing is enabled).
+void timing_begin(const char* name, hipStream_t s);
+void timing_end(const char* name, hipStream_t s);
+
+// Kernel launchers (defined next to their kernels).
+hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
+                               int prescale, int in_dtype, int out_dtype, int32_t* status,
+                               hipStream_t s);
+hipError_t launch_prescale_partial(const TiledMat* mats, const TileItem* items, int n_items,
+                                   int in_dtype, double* partials, hipStream_t s);
+hipError_t launch_prescale_finish(const TiledMat* mats, int n_mats, const double* partials,
+                                  int prescale, int32_t* status, hipStream_t s);
+hipError_t launch_prescale_scale(const TiledMat* mats, const TileItem* items, int n_items,
+                                 int in_dtype, int compute, hipStream_t s);
+hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_items,
+                           int master_index, int out_dtype, hipStream_t s);
+hipError_t launch_bf16_gram(int big, const TiledMat* mats, const TileItem* items, int n_items,
+                            hipStream_t s);
+hipError_t launch_bf16_update(int big, const TiledMat* mats, const TileItem* items, int n_items,
+                              int parity, float beta, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s);
+hipError_t launch_compose_init(const ComposeGroup* groups, int n_groups, int dtype, int64_t max_elems,
+                               hipStream_t s);
+hipError_t launch_compose_combine(const ComposeGroup* groups, const CombineItem* items, int n_items,
+                                  int64_t max_elems, hipStream_t s);
+hipError_t launch_compose_scatter(const ComposeGroup* groups, int n_groups, int dtype,
+                                  int64_t max_elems, hipStream_t s);
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+hipError_t launch_conv_check(const orth_check_args* a, const void* kernel, const float* x,
+                             double* partial, float* out, int adjoint, hipStream_t s);
+
+}  // namespace orth

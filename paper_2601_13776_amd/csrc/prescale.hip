@@ -1,0 +1,214 @@
+// Frobenius pre-scaling and layout kernels of the tiled Björck path.
+//
+//   partial  : squared norm of every 64x64 tile of every input (fp64 sums,
+//              NaN when the tile holds a non-finite value)
+//   finish   : per matrix, fixed-order sum of its partials -> 1/||W||_F and
+//              the per-matrix status (deterministic: no atomics)
+//   scale    : W_0 = W / ||W||_F in the tall orientation, zero padded to the
+//              tile grid, written as the fp32 iterate, its compute-dtype
+//              copy and its transpose (the Gram operand)
+//   writeout : the fp32 iterate back to the caller's orientation and dtype
+//
+// All four are HBM-bound; tiles go through LDS so that both the row-major
+// and the transposed sides are read and written with coalesced accesses.
+#include "internal.h"
+
+namespace orth {
+namespace {
+
+constexpr int TB = 64;  // tile edge
+
+__device__ inline double block_sum_256(double v, double* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0) t = ((red[0] + red[1]) + red[2]) + red[3];
+  return t;  // valid in thread 0
+}
+
+__global__ __launch_bounds__(256) void prescale_partial_kernel(const TiledMat* __restrict__ mats,
+                                                               const TileItem* __restrict__ items,
+                                                               int in_dtype, double* __restrict__ partials) {
+  __shared__ double red[4];
+  __shared__ int bad_any;
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  if (threadIdx.x == 0) bad_any = 0;
+  __syncthreads();
+  double ss = 0.0;
+  int bad = 0;
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int r = it.ti * TB + e / TB, c = it.tj * TB + (e % TB);
+    if (r < d.rows && c < d.cols) {
+      const float v = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+      bad |= !isfinite(v);
+      ss += (double)v * (double)v;
+    }
+  }
+  if (bad) atomicOr(&bad_any, 1);
+  const double tot = block_sum_256(ss, red);
+  if (threadIdx.x == 0) {
+    const int tiles_c = (d.cols + TB - 1) / TB;
+    partials[d.partial_base + it.ti * tiles_c + it.tj] = bad_any ? __builtin_nan("") : tot;
+  }
+}
+
+__global__ __launch_bounds__(256) void prescale_finish_kernel(const TiledMat* __restrict__ mats,
+                                                              const double* __restrict__ partials,
+                                                              int prescale, int32_t* __restrict__ status) {
+  __shared__ double red[4];
+  const TiledMat& d = mats[blockIdx.x];
+  double ss = 0.0;
+  for (int i = threadIdx.x; i < d.n_partials; i += 256) ss += partials[d.partial_base + i];
+  const double tot = block_sum_256(ss, red);
+  if (threadIdx.x == 0) {
+    int st = ORTH_MAT_OK;
+    float inv = 1.f;
+    if (isnan(tot)) {
+      st = ORTH_MAT_NONFINITE;
+      inv = __builtin_nanf("");
+    } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
+      if (tot == 0.0) {
+        st = ORTH_MAT_ZERO;
+        inv = 0.f;
+      } else {
+        inv = (float)(1.0 / sqrt(tot));
+      }
+    }
+    *d.inv_norm = inv;
+    if (status) status[d.status_index] = st;
+  }
+}
+
+__global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __restrict__ mats,
+                                                             const TileItem* __restrict__ items,
+                                                             int in_dtype, int compute) {
+  __shared__ float tile[TB][TB + 1];
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the tall padded layout
+  const float inv = *d.inv_norm;
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    if (!d.transposed) {
+      const int r = R + a, c = C + b;   // tall == original
+      float v = 0.f;
+      if (r < d.M && c < d.N) v = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+      tile[a][b] = v * inv;
+    } else {
+      // original element (C + a, R + b) is tall element (R + b, C + a)
+      const int orow = C + a, ocol = R + b;
+      float v = 0.f;
+      if (orow < d.N && ocol < d.M) v = load_as_f32(d.in, (int64_t)orow * d.ld_in + ocol, in_dtype);
+      tile[b][a] = v * inv;
+    }
+  }
+  __syncthreads();
+  float* master = d.master[0];
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    const int64_t off = (int64_t)(R + a) * d.Np + C + b;
+    const float v = tile[a][b];
+    master[off] = v;
+    if (compute == ORTH_COMPUTE_BF16) {
+      static_cast<uint16_t*>(d.xc[0])[off] = f32_to_bf16(v);
+    }
+    // transpose: xt[(C + a)][(R + b)] = tile[b][a]
+    const int64_t toff = (int64_t)(C + a) * d.Mp + R + b;
+    const float tv = tile[b][a];
+    if (compute == ORTH_COMPUTE_BF16)
+      static_cast<uint16_t*>(d.xt)[toff] = f32_to_bf16(tv);
+    else
+      static_cast<float*>(d.xt)[toff] = tv;
+  }
+}
+
+__global__ __launch_bounds__(256) void writeout_kernel(const TiledMat* __restrict__ mats,
+                                                       const TileItem* __restrict__ items,
+                                                       int master_index, int out_dtype) {
+  __shared__ float tile[TB][TB + 1];
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const float* master = d.master[master_index];
+  const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the ORIGINAL layout
+  if (!d.transposed) {
+    for (int e = threadIdx.x; e < TB * TB; e += 256) {
+      const int r = R + e / TB, c = C + e % TB;
+      if (r < d.rows && c < d.cols)
+        store_from_f32(d.out, (int64_t)r * d.ld_out + c, out_dtype, master[(int64_t)r * d.Np + c]);
+    }
+    return;
+  }
+  // original (R + x, C + y) is tall (C + y, R + x)
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    const int tr = C + a, tc = R + b;  // tall row / col
+    tile[a][b] = (tr < d.Mp && tc < d.Np) ? master[(int64_t)tr * d.Np + tc] : 0.f;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int x = e / TB, y = e % TB;
+    const int r = R + x, c = C + y;
+    if (r < d.rows && c < d.cols) store_from_f32(d.out, (int64_t)r * d.ld_out + c, out_dtype, tile[y][x]);
+  }
+}
+
+__global__ void fill_f32_kernel(float* p, int64_t n, float v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+}  // namespace
+
+hipError_t launch_prescale_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                                   double* partials, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("prescale_partial", s);
+  hipLaunchKernelGGL(prescale_partial_kernel, dim3(n_items), dim3(256), 0, s, mats, items, in_dtype, partials);
+  hipError_t e = hipGetLastError();
+  timing_end("prescale_partial", s);
+  return e;
+}
+
+hipError_t launch_prescale_finish(const TiledMat* mats, int n_mats, const double* partials, int prescale,
+                                  int32_t* status, hipStream_t s) {
+  if (n_mats <= 0) return hipSuccess;
+  timing_begin("prescale_finish", s);
+  hipLaunchKernelGGL(prescale_finish_kernel, dim3(n_mats), dim3(256), 0, s, mats, partials, prescale, status);
+  hipError_t e = hipGetLastError();
+  timing_end("prescale_finish", s);
+  return e;
+}
+
+hipError_t launch_prescale_scale(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                                 int compute, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("prescale_scale", s);
+  hipLaunchKernelGGL(prescale_scale_kernel, dim3(n_items), dim3(256), 0, s, mats, items, in_dtype, compute);
+  hipError_t e = hipGetLastError();
+  timing_end("prescale_scale", s);
+  return e;
+}
+
+hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_items, int master_index,
+                           int out_dtype, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("writeout", s);
+  hipLaunchKernelGGL(writeout_kernel, dim3(n_items), dim3(256), 0, s, mats, items, master_index, out_dtype);
+  hipError_t e = hipGetLastError();
+  timing_end("writeout", s);
+  return e;
+}
+
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+}  // namespace orth

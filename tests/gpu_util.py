@@ -1,0 +1,35 @@
+"""Helpers shared by the GPU tests: moving seeded inputs to the device and
+calling the library through its binding.  No arithmetic of the method."""
+
+import numpy as np
+import torch
+
+from paper_2601_13776_amd import orth
+from paper_2601_13776_amd import workloads as wl
+
+DEV = "cuda:0"
+
+
+def to_dev(stored):
+    """Stored matrix (float32 array or uint16 bf16 bits) -> device tensor."""
+    if stored.dtype == np.uint16:
+        return torch.from_numpy(stored.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(stored)).to(DEV)
+
+
+def to_f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def gpu_orthogonalize(stored_list, iters, compute="f32", out_dtype=torch.float32, beta=0.5, prescale="frobenius"):
+    ins = [to_dev(s) for s in stored_list]
+    outs = [torch.empty(t.shape, dtype=out_dtype, device=DEV) for t in ins]
+    status = torch.full((len(ins),), -1, dtype=torch.int32, device=DEV)
+    orth.orth_orthogonalize_batched(ins, outs, iters, beta=beta, prescale=prescale, compute=compute,
+                                    status=status)
+    torch.cuda.synchronize()
+    return outs, status.cpu().numpy()
+
+
+def oracle_inputs(stored_list):
+    return [wl.as_f64(s) for s in stored_list]

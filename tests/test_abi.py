@@ -1,0 +1,165 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry
+point the header declares, and its host-side validation and planning agree
+with the oracle's geometry rules.  No compute call is made here."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import aoc
+from paper_2601_13776_amd import orth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "orth.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(orth._LIB_PATH):
+        from paper_2601_13776_amd import build
+        build.build(verbose=False)
+    return orth.lib()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(orth_\w+)\s*\(", text, flags=re.M))
+
+
+def test_header_symbols_exported(L):
+    names = header_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(L, name), f"{name} declared in orth.h but not exported"
+    assert names == set(orth.EXPORTED)
+
+
+def test_status_strings(L):
+    assert L.orth_status_string(0) == b"ok"
+    assert b"workspace" in L.orth_status_string(3)
+    assert L.orth_version() >= 100
+
+
+GEOMS = [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (128, 512, 2, 2, 1, 1), (256, 256, 3, 1, 1, 4),
+         (256, 256, 3, 1, 2, 1), (8, 8, 1, 1, 1, 1), (6, 6, 5, 2, 3, 3), (4, 4, 1, 2, 1, 1),
+         (4, 4, 3, 2, 2, 1), (4, 4, 3, 1, 1, 3), (0, 4, 3, 1, 1, 1), (2, 4, 3, 1, 1, 2), (4, 4, 3, 1, 0, 1)]
+
+
+@pytest.mark.parametrize("geom", GEOMS)
+def test_param_shapes_agree_with_oracle(L, geom):
+    try:
+        want = aoc.param_shapes(*geom)
+        kind = None
+    except aoc.GeometryError as e:
+        want, kind = None, e.kind
+    g = orth.orth_conv_geom(*geom)
+    out = [ctypes.c_int32() for _ in range(5)]
+    rc = L.orth_aoc_param_shapes(ctypes.byref(g), *[ctypes.byref(o) for o in out])
+    if kind is None:
+        assert rc == orth.ORTH_OK
+        assert tuple(o.value for o in out) == want
+    else:
+        assert rc == {"invalid": orth.ORTH_EINVAL, "unsupported": orth.ORTH_EUNSUPPORTED}[kind]
+        assert L.orth_last_error()
+
+
+def _mats(shapes, base=0x10000):
+    arr = (orth.orth_mat * len(shapes))()
+    for i, (r, c) in enumerate(shapes):
+        arr[i] = orth.orth_mat(base + 0x100000 * i, base + 0x100000 * i + 0x80000, r, c, c, c)
+    return arr
+
+
+def _ws_size(L, shapes, **kw):
+    opts = orth.orth_bjorck_opts(kw.get("iters", 5), kw.get("beta", 0.5), 1, kw.get("dt", 0), kw.get("dt", 0),
+                                 kw.get("compute", 0))
+    n = ctypes.c_size_t()
+    rc = L.orth_orthogonalize_workspace_size(_mats(shapes), len(shapes), ctypes.byref(opts), ctypes.byref(n))
+    return rc, n.value
+
+
+def test_workspace_sizes(L):
+    rc, small = _ws_size(L, [(16, 16), (16, 8), (8, 16)])
+    assert rc == 0 and 0 < small < 1 << 16        # tables only
+    rc, big = _ws_size(L, [(4096, 4096)], compute=1, dt=1)
+    # fp32 iterate + two bf16 copies + bf16 transpose + bf16 E
+    assert rc == 0 and big >= 4096 * 4096 * (4 + 2 + 2 + 2 + 2)
+    rc, f32 = _ws_size(L, [(512, 256)])
+    assert rc == 0 and f32 >= 512 * 256 * (4 + 4 + 4) + 256 * 256 * 4
+
+
+@pytest.mark.parametrize("kw,shapes,code", [
+    (dict(beta=0.75), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(beta=0.0), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(iters=-1), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(compute=7), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(dt=3), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(), [(0, 4)], orth.ORTH_EINVAL),
+    (dict(), [(4, 0)], orth.ORTH_EINVAL),
+])
+def test_invalid_orthogonalize_args(L, kw, shapes, code):
+    rc, _ = _ws_size(L, shapes, **kw)
+    assert rc == code
+    opts = orth.orth_bjorck_opts(kw.get("iters", 5), kw.get("beta", 0.5), 1, kw.get("dt", 0), kw.get("dt", 0),
+                                 kw.get("compute", 0))
+    rc = L.orth_orthogonalize_batched(_mats(shapes), len(shapes), ctypes.byref(opts), None, 0, None, None)
+    assert rc == code
+
+
+def test_bad_leading_dim_and_inplace(L):
+    arr = (orth.orth_mat * 1)()
+    arr[0] = orth.orth_mat(0x1000, 0x2000, 8, 8, 4, 8)
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0)
+    n = ctypes.c_size_t()
+    assert L.orth_orthogonalize_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
+    arr[0] = orth.orth_mat(0x1000, 0x1000, 8, 8, 8, 8)
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 1, 0, 0)          # bf16 in, fp32 out, in place
+    assert L.orth_orthogonalize_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
+
+
+def test_workspace_errors_before_launch(L):
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0)
+    shapes = [(256, 128)]
+    rc, need = _ws_size(L, shapes)
+    assert rc == 0
+    assert L.orth_orthogonalize_batched(_mats(shapes), 1, ctypes.byref(opts), None, need, None, None) \
+        == orth.ORTH_EWORKSPACE
+    assert L.orth_orthogonalize_batched(_mats(shapes), 1, ctypes.byref(opts), 0x100000, need - 1, None, None) \
+        == orth.ORTH_EWORKSPACE
+    assert L.orth_orthogonalize_batched(_mats(shapes), 1, ctypes.byref(opts), 0x100010, need, None, None) \
+        == orth.ORTH_EWORKSPACE
+    assert b"aligned" in L.orth_last_error()
+    # an empty batch is a no-op
+    assert L.orth_orthogonalize_batched(None, 0, ctypes.byref(opts), None, 0, None, None) == orth.ORTH_OK
+
+
+def test_conv_validation(L):
+    d = (orth.orth_conv_desc * 1)()
+    d[0] = orth.orth_conv_desc(orth.orth_conv_geom(4, 4, 3, 2, 2, 1), 0x1000, 0x2000, 0x3000)
+    n = ctypes.c_size_t()
+    assert L.orth_build_conv_kernels_workspace_size(d, 1, 0, ctypes.byref(n)) == orth.ORTH_EUNSUPPORTED
+    d[0] = orth.orth_conv_desc(orth.orth_conv_geom(16, 16, 3, 1, 1, 1), 0x1000, None, 0x3000)
+    assert L.orth_build_conv_kernels_workspace_size(d, 1, 0, ctypes.byref(n)) == orth.ORTH_EINVAL
+    d[0] = orth.orth_conv_desc(orth.orth_conv_geom(16, 16, 3, 1, 1, 1), 0x1000, 0x2000, 0x3000)
+    assert L.orth_build_conv_kernels_workspace_size(d, 1, 0, ctypes.byref(n)) == orth.ORTH_OK
+    # two tap buffers + products (9 taps of 16x16) + 4 projectors 16x16, fp32
+    assert n.value >= (3 * 9 * 256 + 4 * 256) * 4
+    d[0] = orth.orth_conv_desc(orth.orth_conv_geom(128, 512, 2, 2, 1, 1), 0x1000, None, 0x3000)
+    assert L.orth_build_conv_kernels_workspace_size(d, 1, 0, ctypes.byref(n)) == orth.ORTH_OK
+
+
+def test_check_validation(L):
+    a = orth.orth_check_args()
+    a.mode = 9
+    n = ctypes.c_size_t()
+    assert L.orth_check_workspace_size(ctypes.byref(a), ctypes.byref(n)) == orth.ORTH_EINVAL
+    a.mode = orth.ORTH_CHECK_CONV
+    a.geom = orth.orth_conv_geom(16, 16, 3, 2, 1, 1)
+    a.kernel, a.x, a.kernel_dtype = 0x1000, 0x2000, 0
+    a.batch, a.height, a.width = 2, 15, 16
+    assert L.orth_check_workspace_size(ctypes.byref(a), ctypes.byref(n)) == orth.ORTH_EINVAL  # 15 % 2
+    a.height = 16
+    assert L.orth_check_workspace_size(ctypes.byref(a), ctypes.byref(n)) == orth.ORTH_OK
