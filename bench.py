@@ -1,0 +1,252 @@
+"""Benchmark of one parametrization step on one MI355X.
+
+A step orthogonalizes every free matrix of a workload in one batched call
+(orth_orthogonalize_batched) and builds every conv kernel in one batched call
+(orth_build_conv_kernels_batched).  Inputs are seeded synthetic parameters
+already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--no-cpu-baseline] [--copy-calibration]
+"""
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2601_13776_amd import workloads as wl  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 MFMA
+PEAK_HBM_GBS = 8000.0
+METRIC = "orthogonalized layers/sec per param step; Björck TFLOP/s as % MFMA peak"
+DEFAULT_WORKLOAD = "stress_4096x64_32x4096"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def make_inputs(w, torch, dev):
+    shapes = w.matrix_shapes()
+
+    def one(i):
+        return wl.stored_matrix(w, i, *shapes[i])
+
+    tensors = [None] * len(shapes)
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        for i, s in zip(range(len(shapes)), ex.map(one, range(len(shapes)))):
+            if s.dtype == np.uint16:
+                t = torch.from_numpy(s.view(np.int16)).view(torch.bfloat16)
+            else:
+                t = torch.from_numpy(s)
+            tensors[i] = t.to(dev, non_blocking=False)
+    return tensors
+
+
+def allocate_outputs(w, ins, torch, dev, out_dtype):
+    """Output tensors for every matrix.  The factors of a conv layer are views
+    into that layer's contiguous RKO / projector buffers, so the batched
+    orthogonalization writes them exactly where the kernel build reads them."""
+    outs = [None] * len(ins)
+    layers = []
+    for layer, (a, b) in zip(w.layers, wl.layer_matrix_ranges(w)):
+        if not isinstance(layer, wl.ConvLayer):
+            for i in range(a, b):
+                outs[i] = torch.empty(ins[i].shape, dtype=out_dtype, device=dev)
+            continue
+        g, npj = layer.groups, layer.n_proj
+        per = 1 + npj
+        rr, rc = ins[a].shape
+        rko = torch.empty(g, rr, rc, device=dev, dtype=out_dtype)
+        proj = torch.empty(g, npj, layer.c, layer.c // 2, device=dev, dtype=out_dtype) if npj else None
+        for j in range(g):
+            outs[a + j * per] = rko[j]
+            for t in range(npj):
+                outs[a + j * per + 1 + t] = proj[j, t]
+        kern = torch.empty(layer.cout, layer.c, layer.k, layer.k, device=dev, dtype=out_dtype)
+        layers.append(dict(geom=(layer.cin, layer.cout, layer.k, layer.stride, layer.dilation, layer.groups),
+                           rko=rko, proj=proj, kernel=kern))
+    return outs, layers
+
+
+def kernel_flops(w, kernel_name):
+    """Algorithmic flops of one launch of a Björck product kernel: every
+    matrix of its class contributes 2 m n min(m, n) (Gram and update alike)."""
+    out = 0
+    for r, c in w.matrix_shapes():
+        m, n = max(r, c), min(r, c)
+        small = n <= 64 and m <= 128
+        if small:
+            continue
+        if w.dtype == "bf16":
+            cls = "256" if n >= 1024 else "128"
+            if not kernel_name.endswith(cls):
+                continue
+        out += 2 * m * n * n
+    return out
+
+
+def cpu_baseline(w, budget_s=25.0):
+    """Time the float64 oracle on a bounded sample of the workload and scale
+    to the whole workload."""
+    from oracle import bjorck
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    shapes = w.matrix_shapes()
+    # group matrices by shape; time one matrix of each big shape and a batch of
+    # each small shape, until the time budget is used
+    by_shape = {}
+    for i, s in enumerate(shapes):
+        by_shape.setdefault(s, []).append(i)
+    per_shape = {}
+    t_start = time.perf_counter()
+    sample_desc = []
+    for s, idx in sorted(by_shape.items(), key=lambda kv: kv[0][0] * kv[0][1]):
+        n_take = 1 if s[0] * s[1] >= 512 * 512 else min(len(idx), 64)
+        t0 = time.perf_counter()
+        for i in idx[:n_take]:
+            bjorck.bjorck(wl.as_f64(wl.stored_matrix(w, i, *s)), w.iters)
+        dt = (time.perf_counter() - t0) / n_take
+        per_shape[s] = dt
+        sample_desc.append(f"{n_take}x{s[0]}x{s[1]}")
+        if time.perf_counter() - t_start > budget_s:
+            break
+    # shapes not sampled (budget exhausted): scale by flops from the largest sampled shape
+    ref_s = max(per_shape, key=lambda s: s[0] * s[1] * min(s))
+    ref_f = ref_s[0] * ref_s[1] * min(ref_s)
+    total = 0.0
+    for s, idx in by_shape.items():
+        t = per_shape.get(s, per_shape[ref_s] * s[0] * s[1] * min(s) / ref_f)
+        total += t * len(idx)
+    value = w.n_layers / total
+    return {"value": value, "unit": "layers/s", "cores": threads, "kind": "oracle",
+            "sample": f"float64 numpy oracle, T={w.iters}, timed {'+'.join(sample_desc)} and scaled by matrix "
+                      f"count to all {len(shapes)} matrices (estimated full-step {total:.1f} s; "
+                      f"{platform.processor() or platform.machine()})",
+            "est_step_s": total}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=wl.WORKLOAD_ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (for HBM counter scaling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(matrices would be distributed across GPUs by size; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2601_13776_amd import orth
+
+    if not os.path.exists(orth._LIB_PATH):
+        from paper_2601_13776_amd import build
+        build.build()
+    dev = torch.device("cuda:0")
+    w = wl.WORKLOADS[args.workload]
+    log(f"[bench] generating {w.name}: {len(w.matrix_shapes())} matrices")
+    ins = make_inputs(w, torch, dev)
+    out_dtype = torch.float32
+    outs, layers = allocate_outputs(w, ins, torch, dev, out_dtype)
+    status = torch.zeros(len(ins), dtype=torch.int32, device=dev)
+    compute = "bf16" if w.dtype == "bf16" else "f32"
+    ws = orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status)
+    conv_ws = None
+    torch.cuda.synchronize()
+    log(f"[bench] workspace {ws.numel() / 2**30:.2f} GiB")
+
+    def step():
+        nonlocal conv_ws
+        orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status, workspace=ws)
+        if layers:
+            conv_ws = orth.orth_build_conv_kernels_batched(layers, workspace=conv_ws)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup}")
+    assert int(status.max().item()) == 0, "a matrix was reported degenerate"
+
+    orth.orth_timing_enable(True)
+    orth.orth_timing_reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"[bench] timed {args.steps} steps")
+    names = orth.orth_timing_names()
+    ktimes = {n: orth.orth_timing_read(n) for n in names}
+    orth.orth_timing_enable(False)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = w.n_layers / (ms_per_step / 1e3)
+    shapes = w.matrix_shapes()
+    bjorck_flops = wl.algorithmic_bjorck_flops(shapes, w.iters)
+    gemm_names = [n for n in names if n.startswith("bjorck_gram") or n.startswith("bjorck_update")
+                  or n == "bjorck_small"]
+    t_bjorck_ms = sum(ktimes[n][0] for n in gemm_names) / args.steps
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    bjorck_tflops = bjorck_flops / (t_bjorck_ms / 1e3) / 1e12 if t_bjorck_ms > 0 else None
+    step_tflops = bjorck_flops / (ms_per_step / 1e3) / 1e12
+
+    # dominant kernel roofline
+    big = [n for n in names if n.startswith("bjorck_gram") or n.startswith("bjorck_update")]
+    roof = None
+    if big:
+        dom = max(big, key=lambda n: ktimes[n][0])
+        tot_ms, launches = ktimes[dom]
+        avg_ms = tot_ms / launches
+        flops = kernel_flops(w, dom)
+        achieved = flops / (avg_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": None, "avg_launch_ms": round(avg_ms, 4),
+                "algorithmic_flops_per_launch": flops}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample")
+        cpu = cpu_baseline(w)
+
+    if args.copy_calibration:
+        a = torch.empty(2**28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    rec = {
+        "metric": METRIC, "value": round(value, 3), "unit": "layers/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1/fan_in) parameters)",
+        "config": {"workload": w.name, "matrices": len(shapes), "layers": w.n_layers, "iters": w.iters,
+                   "compute": "bf16 operands, fp32 accumulate" if w.dtype == "bf16" else "fp32"},
+        "bjorck_tflops_algorithmic": round(bjorck_tflops, 1) if bjorck_tflops else None,
+        "bjorck_pct_peak": round(100 * bjorck_tflops / peak, 2) if bjorck_tflops else None,
+        "step_tflops_algorithmic": round(step_tflops, 1),
+        "kernel_ms_per_step": {n: round(ktimes[n][0] / args.steps, 4) for n in names},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -37,67 +37,101 @@ __device__ inline uint2 pack4_bf16(float a, float b, float c, float d) {
   return p;
 }
 
-template <int BM, int BN, int MODE>
-__global__ __launch_bounds__(256, 1) void bjorck_bf16_kernel(const TiledMat* __restrict__ mats,
-                                                             const TileItem* __restrict__ items, int parity,
-                                                             float beta) {
-  constexpr int BK = 64;
-  constexpr int PITCH = BK + 8;  // bf16 elements per LDS row (144 bytes)
-  constexpr int WTM = BM / 2, WTN = BN / 2;
-  constexpr int MI = WTM / 32, NI = WTN / 32;
-  constexpr int ACH = BM * BK / 8 / 256;  // 16-byte chunks per thread
-  constexpr int BCH = BN * BK / 8 / 256;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * PITCH];
+// 16-byte chunk swizzle of a 128-byte LDS row: chunk c of row r lives at
+// position c ^ swz(r).  Eight consecutive rows get eight distinct positions,
+// and so do the even (odd) rows among sixteen consecutive ones, so the
+// fragment reads below (one row per lane, same chunk) are bank-conflict
+// free whether the LDS serves 8 or 16 lanes of a 16-byte read per cycle.
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
+
+// 16-byte direct global -> LDS load of every lane (gfx950
+// global_load_lds_dwordx4): lane l's bytes land at lds + 16 l.  Kept in a
+// plain device function: used directly in a kernel template, the builtin
+// stops the host pass from emitting the kernel's launch stub.
+__device__ __forceinline__ void dma16(const void* g, void* lds) { __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0); }
+
+template <int BM, int BN, int WM, int WN, int MODE>
+__global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const TiledMat* __restrict__ mats,
+                                                                      const TileItem* __restrict__ items,
+                                                                      int parity, float beta) {
+  constexpr int BK = 64;                  // bf16 elements per LDS row (128 bytes)
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int MI = TM / 32, NI = TN / 32;
+  constexpr int ABLK = BM / (8 * NW);     // 1 KB direct-to-LDS blocks per wave and k-step
+  constexpr int BBLK = BN / (8 * NW);
+  // Two LDS stages held in distinct arrays and selected at compile time, so
+  // that the compiler can tell the reads of one stage from the asynchronous
+  // direct-to-LDS writes into the other.
+  __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB0[BN * BK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB1[BN * BK];
 
   const TileItem it = items[blockIdx.x];
   const TiledMat* d = mats + it.mat;
   const int Mp = d->Mp, Np = d->Np;
   const uint16_t* A;
   const uint16_t* B;
-  int64_t lda, ldb;
+  int lda;
   int K;
   if (MODE == 0) {
     const uint16_t* xt = static_cast<const uint16_t*>(d->xt);
     A = xt + (int64_t)it.ti * BM * Mp;
     B = xt + (int64_t)it.tj * BN * Mp;
-    lda = ldb = Mp;
+    lda = Mp;
     K = Mp;
   } else {
     A = static_cast<const uint16_t*>(d->xc[parity]) + (int64_t)it.ti * BM * Np;
     B = static_cast<const uint16_t*>(d->e) + (int64_t)it.tj * BN * Np;
-    lda = ldb = Np;
+    lda = Np;
     K = Np;
   }
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / WN, wn = wave % WN;
 
-  uint4 ra[ACH], rb[BCH];
-  auto gload = [&](int k0) {
+  // Direct-to-LDS operand loads: one instruction moves 64 lanes x 16 bytes
+  // = 8 rows of a tile into a contiguous 1 KB LDS block; lane l fills row
+  // l / 8 of the block at chunk position l % 8, so it fetches the global
+  // chunk that the swizzle maps there.  Byte offsets stay below 2^29.
+  uint32_t aoff[ABLK], boff[BBLK];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + 256 * i;
-      ra[i] = *reinterpret_cast<const uint4*>(A + (int64_t)(c >> 3) * lda + k0 + (c & 7) * 8);
-    }
+  for (int i = 0; i < ABLK; ++i) {
+    const int r = (i * NW + wave) * 8 + (lane >> 3);
+    aoff[i] = ((uint32_t)r * lda + ((lane & 7) ^ swz(r)) * 8) * 2;
+  }
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + 256 * i;
-      rb[i] = *reinterpret_cast<const uint4*>(B + (int64_t)(c >> 3) * ldb + k0 + (c & 7) * 8);
-    }
+  for (int i = 0; i < BBLK; ++i) {
+    const int r = (i * NW + wave) * 8 + (lane >> 3);
+    boff[i] = ((uint32_t)r * lda + ((lane & 7) ^ swz(r)) * 8) * 2;
+  }
+  auto issue = [&](uint16_t* la, uint16_t* lb, int k0) {
+    const char* ab = reinterpret_cast<const char*>(A) + (int64_t)k0 * 2;
+    const char* bb = reinterpret_cast<const char*>(B) + (int64_t)k0 * 2;
+#pragma unroll
+    for (int i = 0; i < ABLK; ++i)
+      dma16(ab + aoff[i], la + (i * NW + wave) * 512);
+#pragma unroll
+    for (int i = 0; i < BBLK; ++i)
+      dma16(bb + boff[i], lb + (i * NW + wave) * 512);
   };
-  auto sstore = [&](int buf) {
+
+  // fragment addressing: row R of the wave tile, chunk (2 kk + lane / 32)
+  int arow[MI], axor[MI], brow[NI], bxor[NI];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + 256 * i;
-      *reinterpret_cast<uint4*>(&As[buf][(c >> 3) * PITCH + (c & 7) * 8]) = ra[i];
-    }
+  for (int mi = 0; mi < MI; ++mi) {
+    const int R = wm * TM + mi * 32 + (lane & 31);
+    arow[mi] = R * BK;
+    axor[mi] = swz(R) ^ (lane >> 5);
+  }
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + 256 * i;
-      *reinterpret_cast<uint4*>(&Bs[buf][(c >> 3) * PITCH + (c & 7) * 8]) = rb[i];
-    }
-  };
+  for (int ni = 0; ni < NI; ++ni) {
+    const int R = wn * TN + ni * 32 + (lane & 31);
+    brow[ni] = R * BK;
+    bxor[ni] = swz(R) ^ (lane >> 5);
+  }
 
   f32x16 acc[MI][NI];
 #pragma unroll
@@ -105,31 +139,55 @@ __global__ __launch_bounds__(256, 1) void bjorck_bf16_kernel(const TiledMat* __r
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x16{};
 
-  const int nk = K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int arow = (wm * WTM + (lane & 31)) * PITCH + (lane >> 5) * 8;
-  const int brow = (wn * WTN + (lane & 31)) * PITCH + (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+  // MFMAs over one LDS stage.  Each 16-deep sub-step is fenced into its own
+  // scheduling region holding the LDS reads of the next sub-step's
+  // fragments and the current sub-step's independent MFMAs, so the reads
+  // are always in flight behind a full set of MFMAs.
+  auto compute = [&](const uint16_t* pa, const uint16_t* pb) {
+    bf16x8 a[2][MI], b[2][NI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      a[0][mi] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(pa + arow[mi] + (axor[mi] << 3)));
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+      b[0][ni] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(pb + brow[ni] + (bxor[ni] << 3)));
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 a[MI], b[NI];
+      const int cur = kk & 1;
+      if (kk + 1 < BK / 16) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-        a[mi] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&As[buf][arow + mi * 32 * PITCH + kk * 16]));
+        for (int mi = 0; mi < MI; ++mi)
+          a[cur ^ 1][mi] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const uint4*>(pa + arow[mi] + (((2 * (kk + 1)) ^ axor[mi]) << 3)));
 #pragma unroll
-      for (int ni = 0; ni < NI; ++ni)
-        b[ni] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(&Bs[buf][brow + ni * 32 * PITCH + kk * 16]));
+        for (int ni = 0; ni < NI; ++ni)
+          b[cur ^ 1][ni] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const uint4*>(pb + brow[ni] + (((2 * (kk + 1)) ^ bxor[ni]) << 3)));
+      }
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][mi], b[cur][ni], acc[mi][ni], 0, 0, 0);
+      if (kk + 1 < BK / 16) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI, 0);  // LDS reads first
+      __builtin_amdgcn_sched_group_barrier(0x008, MI * NI, 0);                       // then the MFMAs
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+  };
+
+  const int nk = K / BK;  // even: K is a multiple of 128
+  issue(sA0, sB0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    issue(sA1, sB1, (kt + 1) * BK);
+    compute(sA0, sB0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kt + 2 < nk) issue(sA0, sB0, (kt + 2) * BK);
+    compute(sA1, sB1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
@@ -142,10 +200,10 @@ __global__ __launch_bounds__(256, 1) void bjorck_bf16_kernel(const TiledMat* __r
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < NI; ++ni) {
-        const int j = it.tj * BN + wn * WTN + ni * 32 + col;
+        const int j = it.tj * BN + wn * TN + ni * 32 + col;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int i0 = it.ti * BM + wm * WTM + mi * 32 + acc_row(rg * 4, lane);
+          const int i0 = it.ti * BM + wm * TM + mi * 32 + acc_row(rg * 4, lane);
           float v[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -163,10 +221,10 @@ __global__ __launch_bounds__(256, 1) void bjorck_bf16_kernel(const TiledMat* __r
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
       for (int ni = 0; ni < NI; ++ni) {
-        const int j = it.tj * BN + wn * WTN + ni * 32 + col;
+        const int j = it.tj * BN + wn * TN + ni * 32 + col;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int i0 = it.ti * BM + wm * WTM + mi * 32 + acc_row(rg * 4, lane);
+          const int i0 = it.ti * BM + wm * TM + mi * 32 + acc_row(rg * 4, lane);
           float v[4];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -188,9 +246,9 @@ hipError_t launch_bf16_gram(int big, const TiledMat* mats, const TileItem* items
   const char* name = big ? "bjorck_gram_bf16_256" : "bjorck_gram_bf16_128";
   timing_begin(name, s);
   if (big)
-    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 0>), dim3(n_items), dim3(256), 0, s, mats, items, 0, 0.f);
+    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 2, 2, 0>), dim3(n_items), dim3(256), 0, s, mats, items, 0, 0.f);
   else
-    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 0>), dim3(n_items), dim3(256), 0, s, mats, items, 0, 0.f);
+    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 2, 2, 0>), dim3(n_items), dim3(256), 0, s, mats, items, 0, 0.f);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
   return e;
@@ -202,10 +260,10 @@ hipError_t launch_bf16_update(int big, const TiledMat* mats, const TileItem* ite
   const char* name = big ? "bjorck_update_bf16_256" : "bjorck_update_bf16_128";
   timing_begin(name, s);
   if (big)
-    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 1>), dim3(n_items), dim3(256), 0, s, mats, items, parity,
+    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 2, 2, 1>), dim3(n_items), dim3(256), 0, s, mats, items, parity,
                        beta);
   else
-    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 1>), dim3(n_items), dim3(256), 0, s, mats, items, parity,
+    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 2, 2, 1>), dim3(n_items), dim3(256), 0, s, mats, items, parity,
                        beta);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
