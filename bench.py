@@ -78,20 +78,20 @@ def allocate_outputs(w, ins, torch, dev, out_dtype):
     return outs, layers
 
 
-def kernel_flops(w, kernel_name):
-    """Algorithmic flops of one launch of a Björck product kernel: every
-    matrix of its class contributes 2 m n min(m, n) (Gram and update alike)."""
+def class_flops(w, kernel_name):
+    """Algorithmic Björck flops of one parametrization step that run in the
+    named tiled kernel: every matrix of its size class contributes
+    4 m n min(m, n) T (a Gram and an update product per iteration)."""
     out = 0
     for r, c in w.matrix_shapes():
         m, n = max(r, c), min(r, c)
-        small = n <= 64 and m <= 128
-        if small:
+        if n <= 64 and m <= 128:          # fused small-matrix kernel
             continue
         if w.dtype == "bf16":
             cls = "256" if n >= 1024 else "128"
             if not kernel_name.endswith(cls):
                 continue
-        out += 2 * m * n * n
+        out += 4 * m * n * n * w.iters
     return out
 
 
@@ -201,25 +201,28 @@ def main():
     value = w.n_layers / (ms_per_step / 1e3)
     shapes = w.matrix_shapes()
     bjorck_flops = wl.algorithmic_bjorck_flops(shapes, w.iters)
-    gemm_names = [n for n in names if n.startswith("bjorck_gram") or n.startswith("bjorck_update")
-                  or n == "bjorck_small"]
+    gemm_names = [n for n in names if n.startswith("bjorck_")]
     t_bjorck_ms = sum(ktimes[n][0] for n in gemm_names) / args.steps
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     bjorck_tflops = bjorck_flops / (t_bjorck_ms / 1e3) / 1e12 if t_bjorck_ms > 0 else None
     step_tflops = bjorck_flops / (ms_per_step / 1e3) / 1e12
 
-    # dominant kernel roofline
-    big = [n for n in names if n.startswith("bjorck_gram") or n.startswith("bjorck_update")]
+    # roofline of the dominant kernel: algorithmic flops of its launches in
+    # the timed region over its measured time (= per-launch average / average
+    # launch duration)
+    tiled = [n for n in names if n.startswith("bjorck_bf16") or n in ("bjorck_gram_f32", "bjorck_update_f32")]
     roof = None
-    if big:
-        dom = max(big, key=lambda n: ktimes[n][0])
+    if tiled:
+        dom = max(tiled, key=lambda n: ktimes[n][0])
         tot_ms, launches = ktimes[dom]
-        avg_ms = tot_ms / launches
-        flops = kernel_flops(w, dom)
-        achieved = flops / (avg_ms / 1e3) / 1e12
+        if dom.startswith("bjorck_bf16"):
+            flops = class_flops(w, dom) * args.steps
+        else:   # fp32 path: Gram and update launches are timed separately, each half of the flops
+            flops = class_flops(w, "") * args.steps / 2
+        achieved = flops / (tot_ms / 1e3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None, "avg_launch_ms": round(avg_ms, 4),
-                "algorithmic_flops_per_launch": flops}
+                "frac": round(achieved / peak, 4), "traffic": None, "avg_launch_ms": round(tot_ms / launches, 4),
+                "algorithmic_flops_per_launch": int(flops / launches)}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -167,6 +167,22 @@ void grouped_tiles(int mat, int tr, int tc, int gm, bool upper_only, std::vector
         if (!upper_only || i <= j) out.push_back(TileItem{mat, i, j, 0});
   }
 }
+// Interleaves two work lists in proportion to their lengths, in runs of a
+// few items, so every XCD chunk of the result holds both kinds of work.
+std::vector<TileItem> interleave(const std::vector<TileItem>& a, const std::vector<TileItem>& b) {
+  std::vector<TileItem> out;
+  out.reserve(a.size() + b.size());
+  constexpr size_t run = 8;
+  size_t ia = 0, ib = 0;
+  while (ia < a.size() || ib < b.size()) {
+    // take from the list that is behind its share
+    const bool take_a = ib >= b.size() || (ia < a.size() && ia * b.size() <= ib * a.size());
+    const std::vector<TileItem>& src = take_a ? a : b;
+    size_t& i = take_a ? ia : ib;
+    for (size_t k = 0; k < run && i < src.size(); ++k) out.push_back(src[i++]);
+  }
+  return out;
+}
 }  // namespace
 
 // ---------------------------------------------------- orthogonalize plan --
@@ -178,18 +194,23 @@ struct MatPlan {
   int32_t M, N, Mp, Np, transposed;
 };
 
+// bf16 tile tables of one size class, pipelining two groups of matrices
+// (A and B): Gram(A); then per step t, [update(A, t) + Gram(B, t)] and
+// [update(B, t) + Gram(A, t + 1)], the last step ending with update(B).
+enum { TAB_GA = 0, TAB_UA_GB = 1, TAB_UB_GA = 3, TAB_UB = 5, N_TABS = 7 };  // +parity for 1, 3, 5
+
 struct OrthoPlan {
   std::vector<MatPlan> mp;
   std::vector<SmallMat> small[2];
   std::vector<TiledMat> tiled;                  // host copy with device pointers
   std::vector<TileItem> partial_items, scale_items, writeout_items;
-  std::vector<TileItem> gram_items[2], update_items[2];  // bf16: [0] = 128 tiles, [1] = 256 tiles
+  std::vector<TileItem> tabs[2][N_TABS];        // bf16: [0] = 128 tiles, [1] = 256 tiles
   std::vector<GemmItem> f32_gram, f32_update[2];
   int max_mp[2] = {32, 32};
   int total_partials = 0;
   // offsets in the workspace
   size_t off_small[2] = {0, 0}, off_tiled = 0, off_partial_items = 0, off_scale_items = 0, off_writeout_items = 0;
-  size_t off_gram_items[2] = {0, 0}, off_update_items[2] = {0, 0};
+  size_t off_tabs[2][N_TABS] = {};
   size_t off_f32_gram = 0, off_f32_update[2] = {0, 0};
   size_t off_partials = 0, off_inv = 0, off_status = 0;
   size_t table_bytes = 0, total_bytes = 0;
@@ -235,6 +256,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
                       unsigned char* ws, bool want_status_scratch) {
   const bool bf16 = o->compute == ORTH_COMPUTE_BF16;
   P.mp.resize(n);
+  std::vector<int> tiled_of(n, -1);
   int n_tiled = 0;
   for (int i = 0; i < n; ++i) {
     const orth_mat& m = mats[i];
@@ -259,7 +281,43 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
       q.Mp = (int32_t)round_up(q.M, 128);
       q.Np = (int32_t)round_up(q.N, 128);
     }
-    if (q.bucket >= TILED_F32) ++n_tiled;
+    if (q.bucket >= TILED_F32) tiled_of[i] = n_tiled++;
+  }
+
+  // bf16 tile tables (matrix indices only; no device pointers needed)
+  for (int cls = 0; cls < 2; ++cls) {
+    const int bucket = cls ? TILED_BF16_256 : TILED_BF16_128;
+    const int tsz = cls ? 256 : 128;
+    std::vector<int> members;
+    for (int i = 0; i < n; ++i)
+      if (P.mp[i].bucket == bucket) members.push_back(i);
+    // flop-balanced split into groups A and B (largest first, to the lighter group)
+    std::sort(members.begin(), members.end(), [&](int x, int y) {
+      const double fx = (double)P.mp[x].Mp * P.mp[x].Np * P.mp[x].Np, fy = (double)P.mp[y].Mp * P.mp[y].Np * P.mp[y].Np;
+      return fx != fy ? fx > fy : x < y;
+    });
+    std::vector<TileItem> g[2], u[2][2];
+    double load[2] = {0, 0};
+    for (int i : members) {
+      const MatPlan& q = P.mp[i];
+      const int grp = load[0] <= load[1] ? 0 : 1;
+      load[grp] += (double)q.Mp * q.Np * q.Np;
+      const int tn = q.Np / tsz, tm = q.Mp / tsz;
+      grouped_tiles(tiled_of[i], tn, tn, 4, true, g[grp]);
+      std::vector<TileItem> ut;
+      grouped_tiles(tiled_of[i], tm, tn, 4, false, ut);
+      for (int par = 0; par < 2; ++par)
+        for (TileItem t : ut) {
+          t.flags = TILE_UPDATE | (par ? TILE_PARITY : 0);
+          u[grp][par].push_back(t);
+        }
+    }
+    P.tabs[cls][TAB_GA] = xcd_order(g[0]);
+    for (int par = 0; par < 2; ++par) {
+      P.tabs[cls][TAB_UA_GB + par] = xcd_order(interleave(u[0][par], g[1]));
+      P.tabs[cls][TAB_UB_GA + par] = xcd_order(interleave(u[1][par], g[0]));
+      P.tabs[cls][TAB_UB + par] = xcd_order(u[1][par]);
+    }
   }
 
   // table region
@@ -270,35 +328,23 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   P.off_small[0] = A.take(sizeof(SmallMat) * n_small[0]);
   P.off_small[1] = A.take(sizeof(SmallMat) * n_small[1]);
   P.off_tiled = A.take(sizeof(TiledMat) * n_tiled);
-
-  // count work items first (sizes of the tables)
-  int64_t n_part = 0, n_scale = 0, n_wo = 0, n_g[2] = {0, 0}, n_u[2] = {0, 0}, n_fg = 0, n_fu = 0;
+  int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
   for (int i = 0; i < n; ++i) {
     const MatPlan& q = P.mp[i];
     if (q.bucket <= SMALL64) continue;
-    const int64_t pr = (mats[i].rows + 63) / 64, pc = (mats[i].cols + 63) / 64;
-    n_part += pr * pc;
-    n_wo += pr * pc;
+    n_part += (int64_t)((mats[i].rows + 63) / 64) * ((mats[i].cols + 63) / 64);
     n_scale += (int64_t)(q.Mp / 64) * (q.Np / 64);
     if (q.bucket == TILED_F32) {
       const int64_t tn = q.Np / 64, tm = q.Mp / 64;
       n_fg += tn * (tn + 1) / 2;
       n_fu += tm * tn;
-    } else {
-      const int b = q.bucket == TILED_BF16_256 ? 1 : 0;
-      const int t = b ? 256 : 128;
-      const int64_t tn = q.Np / t, tm = q.Mp / t;
-      n_g[b] += tn * (tn + 1) / 2;
-      n_u[b] += tm * tn;
     }
   }
   P.off_partial_items = A.take(sizeof(TileItem) * n_part);
   P.off_scale_items = A.take(sizeof(TileItem) * n_scale);
-  P.off_writeout_items = A.take(sizeof(TileItem) * n_wo);
-  for (int b = 0; b < 2; ++b) {
-    P.off_gram_items[b] = A.take(sizeof(TileItem) * n_g[b]);
-    P.off_update_items[b] = A.take(sizeof(TileItem) * n_u[b]);
-  }
+  P.off_writeout_items = A.take(sizeof(TileItem) * n_part);
+  for (int cls = 0; cls < 2; ++cls)
+    for (int t = 0; t < N_TABS; ++t) P.off_tabs[cls][t] = A.take(sizeof(TileItem) * P.tabs[cls][t].size());
   P.off_f32_gram = A.take(sizeof(GemmItem) * n_fg);
   P.off_f32_update[0] = A.take(sizeof(GemmItem) * n_fu);
   P.off_f32_update[1] = A.take(sizeof(GemmItem) * n_fu);
@@ -310,7 +356,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
 
   // per-matrix buffers and descriptors
-  int part_base = 0, tiled_idx = 0;
+  int part_base = 0;
   for (int i = 0; i < n; ++i) {
     const orth_mat& m = mats[i];
     const MatPlan& q = P.mp[i];
@@ -331,6 +377,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
       P.max_mp[q.bucket] = std::max(P.max_mp[q.bucket], q.Mp);
       continue;
     }
+    const int tiled_idx = tiled_of[i];
     TiledMat t{};
     t.in = m.in;
     t.out = m.out;
@@ -411,23 +458,12 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
           gi.beta = o->beta;
           P.f32_update[par].push_back(gi);
         }
-    } else {
-      const int b = q.bucket == TILED_BF16_256 ? 1 : 0;
-      const int tsz = b ? 256 : 128;
-      const int tn = q.Np / tsz, tm = q.Mp / tsz;
-      grouped_tiles(tiled_idx, tn, tn, 4, true, P.gram_items[b]);
-      grouped_tiles(tiled_idx, tm, tn, 4, false, P.update_items[b]);
     }
-    ++tiled_idx;
   }
   P.total_partials = part_base;
   P.total_bytes = align_up(A.off);
 
-  // XCD-aware physical order of the GEMM work lists
-  for (int b = 0; b < 2; ++b) {
-    P.gram_items[b] = xcd_order(P.gram_items[b]);
-    P.update_items[b] = xcd_order(P.update_items[b]);
-  }
+  // XCD-aware physical order of the fp32 GEMM work lists
   P.f32_gram = xcd_order(P.f32_gram);
   P.f32_update[0] = xcd_order(P.f32_update[0]);
   P.f32_update[1] = xcd_order(P.f32_update[1]);
@@ -690,10 +726,8 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   put(img, P.off_partial_items, P.partial_items);
   put(img, P.off_scale_items, P.scale_items);
   put(img, P.off_writeout_items, P.writeout_items);
-  for (int b = 0; b < 2; ++b) {
-    put(img, P.off_gram_items[b], P.gram_items[b]);
-    put(img, P.off_update_items[b], P.update_items[b]);
-  }
+  for (int cls = 0; cls < 2; ++cls)
+    for (int t = 0; t < N_TABS; ++t) put(img, P.off_tabs[cls][t], P.tabs[cls][t]);
   put(img, P.off_f32_gram, P.f32_gram);
   put(img, P.off_f32_update[0], P.f32_update[0]);
   put(img, P.off_f32_update[1], P.f32_update[1]);
@@ -712,14 +746,21 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
     ORTH_HIP(launch_prescale_finish(tm, nt, partials, opts->prescale, status, s));
     ORTH_HIP(launch_prescale_scale(tm, T(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
                                    opts->compute, s));
-    for (int t = 0; t < iters; ++t) {
-      if (bf16) {
-        for (int b = 1; b >= 0; --b)
-          ORTH_HIP(launch_bf16_gram(b, tm, T(P.off_gram_items[b]), (int)P.gram_items[b].size(), s));
-        for (int b = 1; b >= 0; --b)
-          ORTH_HIP(launch_bf16_update(b, tm, T(P.off_update_items[b]), (int)P.update_items[b].size(), t & 1,
-                                      opts->beta, s));
-      } else {
+    if (bf16) {
+      // per size class: Gram(A); then [update(A, t) + Gram(B, t)], [update(B, t) + Gram(A, t + 1)]
+      auto run = [&](int tab) -> int {
+        for (int cls = 1; cls >= 0; --cls)
+          ORTH_HIP(launch_bf16_tiles(cls, tm, T(P.off_tabs[cls][tab]), (int)P.tabs[cls][tab].size(), opts->beta, s));
+        return ORTH_OK;
+      };
+      if (iters > 0 && (rc = run(TAB_GA))) return rc;
+      for (int t = 0; t < iters; ++t) {
+        const int par = t & 1;
+        if ((rc = run(TAB_UA_GB + par))) return rc;
+        if ((rc = run(t + 1 < iters ? TAB_UB_GA + par : TAB_UB + par))) return rc;
+      }
+    } else {
+      for (int t = 0; t < iters; ++t) {
         ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_gram), (int)P.f32_gram.size(),
                                  "bjorck_gram_f32", s));
         ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_update[t & 1]),

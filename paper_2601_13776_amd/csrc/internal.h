@@ -58,7 +58,11 @@ struct TiledMat {
 struct TileItem {
   int32_t mat;
   int32_t ti, tj;
-  int32_t pad;
+  int32_t flags;             // TILE_* bits
+};
+enum : int32_t {
+  TILE_UPDATE = 1,           // bf16 Björck: update tile (else Gram tile)
+  TILE_PARITY = 2            // bf16 Björck: the update reads xc[1] and writes xc[0]
 };
 
 struct SmallMat {
@@ -145,10 +149,8 @@ hipError_t launch_prescale_scale(const TiledMat* mats, const TileItem* items, in
                                  int in_dtype, int compute, hipStream_t s);
 hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_items,
                            int master_index, int out_dtype, hipStream_t s);
-hipError_t launch_bf16_gram(int big, const TiledMat* mats, const TileItem* items, int n_items,
-                            hipStream_t s);
-hipError_t launch_bf16_update(int big, const TiledMat* mats, const TileItem* items, int n_items,
-                              int parity, float beta, hipStream_t s);
+hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
+                             hipStream_t s);
 hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s);
 hipError_t launch_compose_init(const ComposeGroup* groups, int n_groups, int dtype, int64_t max_elems,
                                hipStream_t s);
