@@ -167,22 +167,6 @@ void grouped_tiles(int mat, int tr, int tc, int gm, bool upper_only, std::vector
         if (!upper_only || i <= j) out.push_back(TileItem{mat, i, j, 0});
   }
 }
-// Interleaves two work lists in proportion to their lengths, in runs of a
-// few items, so every XCD chunk of the result holds both kinds of work.
-std::vector<TileItem> interleave(const std::vector<TileItem>& a, const std::vector<TileItem>& b) {
-  std::vector<TileItem> out;
-  out.reserve(a.size() + b.size());
-  constexpr size_t run = 8;
-  size_t ia = 0, ib = 0;
-  while (ia < a.size() || ib < b.size()) {
-    // take from the list that is behind its share
-    const bool take_a = ib >= b.size() || (ia < a.size() && ia * b.size() <= ib * a.size());
-    const std::vector<TileItem>& src = take_a ? a : b;
-    size_t& i = take_a ? ia : ib;
-    for (size_t k = 0; k < run && i < src.size(); ++k) out.push_back(src[i++]);
-  }
-  return out;
-}
 }  // namespace
 
 // ---------------------------------------------------- orthogonalize plan --
@@ -194,10 +178,9 @@ struct MatPlan {
   int32_t M, N, Mp, Np, transposed;
 };
 
-// bf16 tile tables of one size class, pipelining two groups of matrices
-// (A and B): Gram(A); then per step t, [update(A, t) + Gram(B, t)] and
-// [update(B, t) + Gram(A, t + 1)], the last step ending with update(B).
-enum { TAB_GA = 0, TAB_UA_GB = 1, TAB_UB_GA = 3, TAB_UB = 5, N_TABS = 7 };  // +parity for 1, 3, 5
+// bf16 tile tables of one size class: the Gram and the update tiles of all
+// its matrices, for both ping-pong parities (step t uses parity t & 1).
+enum { TAB_GRAM = 0, TAB_UPDATE = 2, N_TABS = 4 };  // + parity
 
 struct OrthoPlan {
   std::vector<MatPlan> mp;
@@ -291,32 +274,27 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     std::vector<int> members;
     for (int i = 0; i < n; ++i)
       if (P.mp[i].bucket == bucket) members.push_back(i);
-    // flop-balanced split into groups A and B (largest first, to the lighter group)
-    std::sort(members.begin(), members.end(), [&](int x, int y) {
-      const double fx = (double)P.mp[x].Mp * P.mp[x].Np * P.mp[x].Np, fy = (double)P.mp[y].Mp * P.mp[y].Np * P.mp[y].Np;
-      return fx != fy ? fx > fy : x < y;
-    });
-    std::vector<TileItem> g[2], u[2][2];
-    double load[2] = {0, 0};
+    std::vector<TileItem> g[2], u[2];
     for (int i : members) {
       const MatPlan& q = P.mp[i];
-      const int grp = load[0] <= load[1] ? 0 : 1;
-      load[grp] += (double)q.Mp * q.Np * q.Np;
       const int tn = q.Np / tsz, tm = q.Mp / tsz;
-      grouped_tiles(tiled_of[i], tn, tn, 4, true, g[grp]);
-      std::vector<TileItem> ut;
+      std::vector<TileItem> gt, ut;
+      grouped_tiles(tiled_of[i], tn, tn, 4, true, gt);
       grouped_tiles(tiled_of[i], tm, tn, 4, false, ut);
-      for (int par = 0; par < 2; ++par)
+      for (int par = 0; par < 2; ++par) {
+        for (TileItem t : gt) {
+          t.flags = par ? TILE_PARITY : 0;
+          g[par].push_back(t);
+        }
         for (TileItem t : ut) {
           t.flags = TILE_UPDATE | (par ? TILE_PARITY : 0);
-          u[grp][par].push_back(t);
+          u[par].push_back(t);
         }
+      }
     }
-    P.tabs[cls][TAB_GA] = xcd_order(g[0]);
     for (int par = 0; par < 2; ++par) {
-      P.tabs[cls][TAB_UA_GB + par] = xcd_order(interleave(u[0][par], g[1]));
-      P.tabs[cls][TAB_UB_GA + par] = xcd_order(interleave(u[1][par], g[0]));
-      P.tabs[cls][TAB_UB + par] = xcd_order(u[1][par]);
+      P.tabs[cls][TAB_GRAM + par] = xcd_order(g[par]);
+      P.tabs[cls][TAB_UPDATE + par] = xcd_order(u[par]);
     }
   }
 
@@ -401,7 +379,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     t.master[1] = bf16 ? nullptr : reinterpret_cast<float*>(dev(A.take(elems * 4)));
     t.xc[0] = bf16 ? dev(A.take(elems * 2)) : nullptr;
     t.xc[1] = bf16 ? dev(A.take(elems * 2)) : nullptr;
-    t.xt = dev(A.take(elems * csz));
+    t.xt = bf16 ? nullptr : dev(A.take(elems * csz));   // the bf16 Gram reads X itself
     t.e = dev(A.take((size_t)q.Np * q.Np * csz));
     t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + tiled_idx;
     P.tiled.push_back(t);
@@ -747,18 +725,12 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
     ORTH_HIP(launch_prescale_scale(tm, T(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
                                    opts->compute, s));
     if (bf16) {
-      // per size class: Gram(A); then [update(A, t) + Gram(B, t)], [update(B, t) + Gram(A, t + 1)]
-      auto run = [&](int tab) -> int {
-        for (int cls = 1; cls >= 0; --cls)
-          ORTH_HIP(launch_bf16_tiles(cls, tm, T(P.off_tabs[cls][tab]), (int)P.tabs[cls][tab].size(), opts->beta, s));
-        return ORTH_OK;
-      };
-      if (iters > 0 && (rc = run(TAB_GA))) return rc;
-      for (int t = 0; t < iters; ++t) {
-        const int par = t & 1;
-        if ((rc = run(TAB_UA_GB + par))) return rc;
-        if ((rc = run(t + 1 < iters ? TAB_UB_GA + par : TAB_UB + par))) return rc;
-      }
+      // per step: all Gram tiles, then all update tiles (large class first)
+      for (int t = 0; t < iters; ++t)
+        for (int tab : {TAB_GRAM + (t & 1), TAB_UPDATE + (t & 1)})
+          for (int cls = 1; cls >= 0; --cls)
+            ORTH_HIP(launch_bf16_tiles(cls, tm, T(P.off_tabs[cls][tab]), (int)P.tabs[cls][tab].size(), opts->beta,
+                                       s));
     } else {
       for (int t = 0; t < iters; ++t) {
         ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_gram), (int)P.f32_gram.size(),

@@ -50,8 +50,8 @@ struct TiledMat {
   int32_t n_partials;
   float* master[2];          // fp32 iterate, Mp x Np (bf16 mode uses [0] only)
   void* xc[2];               // bf16 mode: bf16 copies of the iterate, Mp x Np
-  void* xt;                  // transposed iterate in compute dtype, Np x Mp
-  void* e;                   // I - X^T X in compute dtype, Np x Np
+  void* xt;                  // fp32 products only: transposed iterate, Np x Mp
+  void* e;                   // I - X^T X in compute dtype, Np x Np (bf16: upper tiles only)
   float* inv_norm;           // this matrix's pre-scale factor
 };
 

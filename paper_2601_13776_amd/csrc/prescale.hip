@@ -5,8 +5,8 @@
 //   finish   : per matrix, fixed-order sum of its partials -> 1/||W||_F and
 //              the per-matrix status (deterministic: no atomics)
 //   scale    : W_0 = W / ||W||_F in the tall orientation, zero padded to the
-//              tile grid, written as the fp32 iterate, its compute-dtype
-//              copy and its transpose (the Gram operand)
+//              tile grid, written as the fp32 iterate plus its bf16 copy
+//              (bf16 products) or its transpose (fp32 products)
 //   writeout : the fp32 iterate back to the caller's orientation and dtype
 //
 // All four are HBM-bound; tiles go through LDS so that both the row-major
@@ -116,13 +116,9 @@ __global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __r
     if (compute == ORTH_COMPUTE_BF16) {
       static_cast<uint16_t*>(d.xc[0])[off] = f32_to_bf16(v);
     }
-    // transpose: xt[(C + a)][(R + b)] = tile[b][a]
-    const int64_t toff = (int64_t)(C + a) * d.Mp + R + b;
-    const float tv = tile[b][a];
-    if (compute == ORTH_COMPUTE_BF16)
-      static_cast<uint16_t*>(d.xt)[toff] = f32_to_bf16(tv);
-    else
-      static_cast<float*>(d.xt)[toff] = tv;
+    // fp32 path: the transposed iterate xt[(C + a)][(R + b)] = tile[b][a]
+    if (compute != ORTH_COMPUTE_BF16)
+      static_cast<float*>(d.xt)[(int64_t)(C + a) * d.Mp + R + b] = tile[b][a];
   }
 }
 

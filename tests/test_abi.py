@@ -85,8 +85,8 @@ def test_workspace_sizes(L):
     rc, small = _ws_size(L, [(16, 16), (16, 8), (8, 16)])
     assert rc == 0 and 0 < small < 1 << 16        # tables only
     rc, big = _ws_size(L, [(4096, 4096)], compute=1, dt=1)
-    # fp32 iterate + two bf16 copies + bf16 transpose + bf16 E
-    assert rc == 0 and big >= 4096 * 4096 * (4 + 2 + 2 + 2 + 2)
+    # fp32 iterate + two bf16 copies (ping-pong) + bf16 E
+    assert rc == 0 and 4096 * 4096 * (4 + 2 + 2 + 2) <= big < 4096 * 4096 * 11
     rc, f32 = _ws_size(L, [(512, 256)])
     assert rc == 0 and f32 >= 512 * 256 * (4 + 4 + 4) + 256 * 256 * 4
 
