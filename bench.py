@@ -78,6 +78,30 @@ def allocate_outputs(w, ins, torch, dev, out_dtype):
     return outs, layers
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bjorck_bf16_256_stress_4096x64_32x4096.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2601_13776_amd", "csrc", "bjorck_bf16.hip")
+
+
+def measured_traffic(kernel_name, workload):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE measurement, or None when there is none
+    for this kernel and workload or the kernel source changed since."""
+    import hashlib
+    import re
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    fields = dict(re.findall(r"^- (\w+): (\S+)$", text, flags=re.M))
+    try:
+        src_hash = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        if fields.get("kernel") != kernel_name or fields.get("workload") != workload \
+                or fields.get("source_sha256") != src_hash:
+            return None
+        return int(fields["bytes_per_launch"])
+    except (KeyError, ValueError, OSError):
+        return None
+
+
 def class_flops(w, kernel_name):
     """Algorithmic Björck flops of one parametrization step that run in the
     named tiled kernel: every matrix of its size class contributes
@@ -221,7 +245,8 @@ def main():
             flops = class_flops(w, "") * args.steps / 2
         achieved = flops / (tot_ms / 1e3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None, "avg_launch_ms": round(tot_ms / launches, 4),
+                "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name),
+                "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(flops / launches)}
 
     cpu = None
@@ -230,9 +255,11 @@ def main():
         cpu = cpu_baseline(w)
 
     if args.copy_calibration:
-        a = torch.empty(2**28, dtype=torch.float32, device=dev)
+        # a plain streaming kernel of known traffic: reads 1 GiB, writes 1 GiB
+        a = torch.ones(2**28, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
-        b.copy_(a)
+        torch.cuda.synchronize()
+        torch.neg(a, out=b)
         torch.cuda.synchronize()
 
     rec = {

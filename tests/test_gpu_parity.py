@@ -5,8 +5,10 @@ Tolerances (stated by the target):
   fp32 compute : relative Frobenius difference to the oracle <= 1e-5;
                  max |W^T W - I| <= 1e-5 for matrices that have converged.
   bf16 operands, fp32 accumulation : max |W^T W - I| <= 3e-3 for converged
-                 matrices; the element-wise bound BF16_REL is derived from the
-                 arithmetic and checked too.
+                 matrices.  Element-wise, rounding the product operands to
+                 bf16 (unit roundoff u = 2^-9) moves the iterate by a few u in
+                 relative Frobenius norm: BF16_REL = 1e-2 (about 5 u) for
+                 every matrix, converged or not.
 """
 
 import math
@@ -26,7 +28,7 @@ pytestmark = pytest.mark.gpu
 REL_F32 = 1e-5
 ORTH_F32 = 1e-5
 ORTH_BF16 = 3e-3
-BF16_REL = 3e-2
+BF16_REL = 1e-2
 
 
 def stored(seed, shapes, dtype="f32"):
@@ -104,9 +106,12 @@ def test_bf16_mixed_batch():
         ref = bjorck.bjorck(s, iters)
         got = to_f64(o)
         rel = checks.relative_difference(got, ref)
+        assert rel <= BF16_REL, (shape, rel)
         if converged_at(s, iters):
             assert checks.gram_deviation(got) <= ORTH_BF16, shape
-            assert rel <= BF16_REL, (shape, rel)
+        else:
+            # not converged: the deviation from orthogonality is the oracle's
+            assert abs(checks.gram_deviation(got) - checks.gram_deviation(ref)) <= ORTH_BF16, shape
 
 
 def test_bf16_converged_all():
