@@ -79,13 +79,15 @@ def allocate_outputs(w, ins, torch, dev, out_dtype):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bjorck_bf16_256_stress_4096x64_32x4096.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2601_13776_amd", "csrc", "bjorck_bf16.hip")
+# the traffic depends on the kernel and on the tile order the host planner builds
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2601_13776_amd", "csrc", f) for f in ("bjorck_bf16.hip", "host.hip")]
 
 
 def measured_traffic(kernel_name, workload):
     """HBM bytes per launch of the dominant kernel from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE measurement, or None when there is none
-    for this kernel and workload or the kernel source changed since."""
+    for this kernel and workload or the kernel or planner source changed
+    since."""
     import hashlib
     import re
     if not os.path.exists(TRAFFIC_FILE):
@@ -93,7 +95,10 @@ def measured_traffic(kernel_name, workload):
     text = open(TRAFFIC_FILE).read()
     fields = dict(re.findall(r"^- (\w+): (\S+)$", text, flags=re.M))
     try:
-        src_hash = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        h = hashlib.sha256()
+        for f in KERNEL_SOURCES:
+            h.update(open(f, "rb").read())
+        src_hash = h.hexdigest()
         if fields.get("kernel") != kernel_name or fields.get("workload") != workload \
                 or fields.get("source_sha256") != src_hash:
             return None
