@@ -1,4 +1,4 @@
-// Fused Björck for small matrices: one wavefront owns one matrix and keeps
+// Fused Björck for small matrices: one workgroup owns one matrix and keeps
 // it in LDS for the whole run — load (transposing wide inputs to the tall
 // orientation), Frobenius pre-scaling, T steps of
 //     E = I - X^T X,   X <- X + beta X E      (Appendix A.5, E-form of
@@ -29,23 +29,29 @@ __device__ inline int wave_or(int v) {
 // row 8 (r / 4) + 4 (l / 32) + (r % 4), column l % 32.
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-template <int NP>
-__global__ __launch_bounds__(64) void bjorck_small_kernel(const SmallMat* __restrict__ mats, int iters,
-                                                          float beta, int prescale, int in_dtype,
-                                                          int out_dtype, int32_t* __restrict__ status) {
+template <int NP, int NWAVES>
+__global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMat* __restrict__ mats, int iters,
+                                                                  float beta, int prescale, int in_dtype,
+                                                                  int out_dtype, int32_t* __restrict__ status) {
   constexpr int NT = NP / 32;
-  constexpr int XP = NP + 1;  // row pitch of X and E in LDS (floats)
+  constexpr int XP = NP + 1;                      // row pitch of X and E in LDS (floats)
+  constexpr int MAXT = (4 * NT + NWAVES - 1) / NWAVES;  // update tiles per wave (Mp <= 128)
+  constexpr int NTHR = 64 * NWAVES;
   extern __shared__ float smem[];
+  __shared__ double red[NWAVES];
+  __shared__ int bad_any;
   const SmallMat d = mats[blockIdx.x];
   float* X = smem;
   float* E = smem + d.Mp * XP;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int M = d.M, N = d.N, Mp = d.Mp;
 
   // -- load, checking finiteness and accumulating the squared norm in fp64
+  if (tid == 0) bad_any = 0;
+  __syncthreads();
   double ss = 0.0;
   int bad = 0;
-  for (int idx = lane; idx < Mp * NP; idx += 64) {
+  for (int idx = tid; idx < Mp * NP; idx += NTHR) {
     const int r = idx / NP, c = idx - (idx / NP) * NP;
     float v = 0.f;
     if (r < M && c < N) {
@@ -57,23 +63,27 @@ __global__ __launch_bounds__(64) void bjorck_small_kernel(const SmallMat* __rest
     X[r * XP + c] = v;
   }
   ss = wave_sum(ss);
-  bad = wave_or(bad);
+  if (wave_or(bad) && lane == 0) bad_any = 1;
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  double tot = 0.0;
+#pragma unroll
+  for (int w = 0; w < NWAVES; ++w) tot += red[w];   // fixed order: deterministic
   int st = ORTH_MAT_OK;
   float scale = 1.f;
-  if (bad) {
+  if (bad_any) {
     st = ORTH_MAT_NONFINITE;
     scale = __builtin_nanf("");
   } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
-    if (ss == 0.0) {
+    if (tot == 0.0) {
       st = ORTH_MAT_ZERO;
       scale = 0.f;
     } else {
-      scale = (float)(1.0 / sqrt(ss));
+      scale = (float)(1.0 / sqrt(tot));
     }
   }
-  if (lane == 0 && status) status[d.status_index] = st;
-  __syncthreads();
-  for (int idx = lane; idx < Mp * NP; idx += 64) {
+  if (tid == 0 && status) status[d.status_index] = st;
+  for (int idx = tid; idx < Mp * NP; idx += NTHR) {
     const int r = idx / NP, c = idx - (idx / NP) * NP;
     X[r * XP + c] *= scale;   // NaN scale turns the whole matrix into NaN
   }
@@ -82,52 +92,54 @@ __global__ __launch_bounds__(64) void bjorck_small_kernel(const SmallMat* __rest
   const int half = lane >> 5, col = lane & 31;
   const int MT = Mp / 32;
   for (int t = 0; t < iters; ++t) {
-    // E = I - X^T X   (NT x NT tiles, contraction over the Mp rows)
+    // E = I - X^T X: the NT x NT output tiles are shared out over the waves
+    for (int tile = wave; tile < NT * NT; tile += NWAVES) {
+      const int gi = tile / NT, gj = tile % NT;
+      f32x16 acc = {};
+      for (int kk = 0; kk < Mp; kk += 2) {
+        const float* row = X + (kk + half) * XP;
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(row[gi * 32 + col], row[gj * 32 + col], acc, 0, 0, 0);
+      }
 #pragma unroll
-    for (int gi = 0; gi < NT; ++gi) {
+      for (int r = 0; r < 16; ++r) {
+        const int i = gi * 32 + acc_row(r, lane), j = gj * 32 + col;
+        E[i * XP + j] = (i == j ? 1.f : 0.f) - acc[r];
+      }
+    }
+    __syncthreads();
+    // X <- X + beta X E: every wave computes its tiles from the old X, then
+    // all write after a barrier
+    f32x16 acc[MAXT];
 #pragma unroll
-      for (int gj = 0; gj < NT; ++gj) {
-        f32x16 acc = {};
-        for (int kk = 0; kk < Mp; kk += 2) {
-          const float* row = X + (kk + half) * XP;
-          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(row[gi * 32 + col], row[gj * 32 + col], acc, 0, 0, 0);
-        }
+    for (int q = 0; q < MAXT; ++q) {
+      acc[q] = f32x16{};
+      const int tile = wave + q * NWAVES;
+      if (tile < MT * NT) {
+        const int ri = tile / NT, cj = tile % NT;
+        const float* xrow = X + (ri * 32 + col) * XP;
+        for (int kk = 0; kk < NP; kk += 2)
+          acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(xrow[kk + half], E[(kk + half) * XP + cj * 32 + col], acc[q],
+                                                        0, 0, 0);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < MAXT; ++q) {
+      const int tile = wave + q * NWAVES;
+      if (tile < MT * NT) {
+        const int ri = tile / NT, cj = tile % NT;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int i = gi * 32 + acc_row(r, lane), j = gj * 32 + col;
-          E[i * XP + j] = (i == j ? 1.f : 0.f) - acc[r];
+          const int i = ri * 32 + acc_row(r, lane), j = cj * 32 + col;
+          X[i * XP + j] += beta * acc[q][r];
         }
       }
     }
     __syncthreads();
-    // X <- X + beta X E, one 32-row block at a time (a block only reads its
-    // own rows of X, so it can be overwritten right after)
-    for (int ri = 0; ri < MT; ++ri) {
-      f32x16 acc[NT];
-#pragma unroll
-      for (int cj = 0; cj < NT; ++cj) acc[cj] = f32x16{};
-      const float* xrow = X + (ri * 32 + col) * XP;
-      for (int kk = 0; kk < NP; kk += 2) {
-        const float a = xrow[kk + half];
-        const float* erow = E + (kk + half) * XP;
-#pragma unroll
-        for (int cj = 0; cj < NT; ++cj)
-          acc[cj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, erow[cj * 32 + col], acc[cj], 0, 0, 0);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int cj = 0; cj < NT; ++cj)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = ri * 32 + acc_row(r, lane), j = cj * 32 + col;
-          X[i * XP + j] += beta * acc[cj][r];
-        }
-      __syncthreads();
-    }
   }
 
   // -- store in the caller's orientation and dtype
-  for (int idx = lane; idx < M * N; idx += 64) {
+  for (int idx = tid; idx < M * N; idx += NTHR) {
     const int r = idx / N, c = idx - (idx / N) * N;
     const int64_t dst = d.transposed ? (int64_t)c * d.ld_out + r : (int64_t)r * d.ld_out + c;
     store_from_f32(d.out, dst, out_dtype, X[r * XP + c]);
@@ -141,15 +153,15 @@ hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, 
   if (n <= 0) return hipSuccess;
   // dynamic LDS sized for the tallest matrix of this launch (max_mp <= 128)
   const size_t lds = (size_t)(max_mp + np) * (np + 1) * sizeof(float);
-  if (np == 32) {
-    timing_begin("bjorck_small", s);
-    hipLaunchKernelGGL(bjorck_small_kernel<32>, dim3(n), dim3(64), lds, s, mats, iters, beta, prescale,
+  timing_begin("bjorck_small", s);
+  // 32-wide matrices: one wavefront each (a single Gram tile); 64-wide: four
+  // wavefronts share the 4 Gram tiles and up to 8 update tiles
+  if (np == 32)
+    hipLaunchKernelGGL((bjorck_small_kernel<32, 1>), dim3(n), dim3(64), lds, s, mats, iters, beta, prescale, in_dtype,
+                       out_dtype, status);
+  else
+    hipLaunchKernelGGL((bjorck_small_kernel<64, 4>), dim3(n), dim3(256), lds, s, mats, iters, beta, prescale,
                        in_dtype, out_dtype, status);
-  } else {
-    timing_begin("bjorck_small", s);
-    hipLaunchKernelGGL(bjorck_small_kernel<64>, dim3(n), dim3(64), lds, s, mats, iters, beta, prescale,
-                       in_dtype, out_dtype, status);
-  }
   hipError_t e = hipGetLastError();
   timing_end("bjorck_small", s);
   return e;
