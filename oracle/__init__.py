@@ -17,12 +17,16 @@ conv     Circular convolution with stride, dilation and groups, its adjoint,
          the impulse-response Toeplitz matrix and the per-frequency FFT
          singular values (Section 4 and Appendix C, unit-testing scheme).
 checks   Orthogonality deviation and norm ratios used as gates.
+bjorck_grad  Vector-Jacobian product of pre-scaling + Björck (the
+         derivative of the Appendix A.5 step, chained backwards).
+aoc_grad Vector-Jacobian product of the composition (adjoint of each ⊛
+         step, of the projector blocks and of P = V V^T).
 
 Every function is pinned by ``tests/test_oracle_pins.py`` against closed
 forms, library routines (torch CPU conv2d, numpy SVD) or brute force; see the
 docstrings for which pin covers which function.
 """
 
-from . import bjorck, aoc, conv, checks  # noqa: F401
+from . import bjorck, aoc, conv, checks, bjorck_grad, aoc_grad  # noqa: F401
 
-__all__ = ["bjorck", "aoc", "conv", "checks"]
+__all__ = ["bjorck", "aoc", "conv", "checks", "bjorck_grad", "aoc_grad"]
