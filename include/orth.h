@@ -100,6 +100,47 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n,
                                size_t workspace_bytes, int32_t* status_dev,
                                void* stream);
 
+/* One matrix of a Björck vector-Jacobian product. */
+typedef struct {
+  const void* w;         /* device, the raw parameter W the forward call was
+                            given: rows x cols, leading dim ld_w, opts.in_dtype */
+  const void* grad_out;  /* device, dL/d(output of the forward call), rows x
+                            cols, leading dim ld_grad_out, opts.out_dtype */
+  void* grad_in;         /* device, dL/dW, rows x cols, leading dim ld_grad_in,
+                            opts.in_dtype.  May equal grad_out (equal dtypes
+                            and leading dims) or w (equal leading dims);
+                            otherwise it must not overlap either. */
+  int32_t rows, cols;    /* >= 1 */
+  int64_t ld_w, ld_grad_out, ld_grad_in;
+} orth_vjp_mat;
+
+/*
+ * Vector-Jacobian product of orth_orthogonalize_batched: for every matrix,
+ * dL/dW given dL/d(output), for the same opts (iters, beta, prescale,
+ * compute).  Derivative of the Appendix A.5 step for tall X with upstream
+ * gradient Y:
+ *   dL/dX = Y + beta (Y E - X S),  E = I - X^T X,  S = X^T Y + Y^T X
+ * (wide matrices through their transpose), chained from the last step to
+ * the first, then through the pre-scaling W_0 = W / ||W||_F:
+ *   dL/dW = (dL/dW_0 - <dL/dW_0, W_0> W_0) / ||W||_F.
+ * The forward iterates are recomputed inside the call and every X_t and E_t
+ * is kept in the workspace (about T (M N + N^2) elements per M x N matrix,
+ * in fp32 or bf16 per opts.compute), so the workspace query grows with T.
+ * Matrices with N <= 64 and M <= 128 (tall orientation) use fp32 products
+ * whatever opts.compute says, as the forward does.
+ *
+ * status_dev: optional, as for the forward (1: zero matrix -> zero gradient;
+ * 2: non-finite input -> NaN gradient).
+ * Returns ORTH_EINVAL for the argument errors of the forward call, iters >
+ * 4096, or aliasing other than the two allowed above.
+ */
+int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n,
+                                          const orth_bjorck_opts* opts, size_t* bytes);
+int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n,
+                                   const orth_bjorck_opts* opts, void* workspace,
+                                   size_t workspace_bytes, int32_t* status_dev,
+                                   void* stream);
+
 /* Geometry of one orthogonal convolution (groups g, stride s, dilation d). */
 typedef struct {
   int32_t cin, cout, k, stride, dilation, groups;

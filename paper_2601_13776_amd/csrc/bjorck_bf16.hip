@@ -17,6 +17,14 @@
 // Every work item names its matrix, tile, mode (Gram or update) and
 // ping-pong parity, so one launch can cover any mix of tiles.
 //
+// Vector-Jacobian product (second instantiation): with X_t and E_t the saved
+// bf16 iterate and E of step t and Y the gradient with respect to X_{t+1},
+// the derivative of the update gives
+//   dL/dX_t = Y + beta (Y E_t + X_t S'),   S' = -(X_t^T Y + Y^T X_t),
+// computed as S' tiles (two transposed-panel products, upper tiles only, no
+// identity) and then update-like tiles with two panel-times-symmetric
+// products, the fp32 gradient iterate updated in place.
+//
 // One workgroup of 4 waves (2 x 2) computes a BM x BN tile; each wave holds
 // a (BM/2) x (BN/2) block of 32x32 accumulators.  K advances in steps of 64
 // through a 2-stage LDS ring filled by direct global->LDS loads; 16-byte
@@ -224,10 +232,10 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
   __syncthreads();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, bool VJP>
 __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const TiledMat* __restrict__ mats,
                                                                       const TileItem* __restrict__ items,
-                                                                      float beta) {
+                                                                      float beta, int step) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int BK = T::BK, TM = T::TM, TN = T::TN, MI = T::MI, NI = T::NI;
   static_assert(MI * NI >= MI + NI, "a sub-step needs at least as many MFMAs as fragment reads");
@@ -244,8 +252,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   const int Mp = d->Mp, Np = d->Np;
   const int MODE = it.flags & TILE_UPDATE ? 1 : 0;   // uniform per workgroup
   const int parity = it.flags & TILE_PARITY ? 1 : 0;
-  const uint16_t* X = static_cast<const uint16_t*>(d->xc[parity]);
-  const uint16_t* Ep = static_cast<const uint16_t*>(d->e);
+  // saved-iterate mode: step t reads the t-th saved iterate and E
+  const int64_t xoff = (int64_t)step * d->xstep, eoff = (int64_t)step * d->estep;
+  const uint16_t* X = static_cast<const uint16_t*>(d->xc[VJP ? 0 : parity]) + xoff;
+  const uint16_t* Ep = static_cast<const uint16_t*>(d->e) + eoff;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -257,18 +267,38 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
 #pragma unroll
     for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = f32x16{};
 
-  if (MODE == 0) {
-    // Gram tile: column panels I and J of X, k over all Mp rows
-    kloop<BM, BN, WM, WN, true, true>(acc, X + (int64_t)it.ti * BM, Np, X + (int64_t)it.tj * BN, Np, 0, Mp, sA0,
-                                      sB0, sA1, sB1, wave, lane, wm, wn);
-  } else {
-    // update tile: row panel I of X times E[:, J]; below tile J the stored
-    // upper tiles E[k-block, J] are read transposed
+  // row panel I of P times the symmetric matrix Q (upper tiles stored) at
+  // column panel J: below tile J the stored tiles Q[k-block, J] are read
+  // transposed, from tile J on the stored rows Q[J, k] directly
+  auto panel_times_sym = [&](const uint16_t* P, const uint16_t* Q) {
     const int ksplit = it.tj * BN;
-    kloop<BM, BN, WM, WN, false, true>(acc, X + (int64_t)it.ti * BM * Np, Np, Ep + (int64_t)it.tj * BN, Np, 0,
+    kloop<BM, BN, WM, WN, false, true>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN, Np, 0,
                                        ksplit, sA0, sB0, sA1, sB1, wave, lane, wm, wn);
-    kloop<BM, BN, WM, WN, false, false>(acc, X + (int64_t)it.ti * BM * Np, Np, Ep + (int64_t)it.tj * BN * Np, Np,
+    kloop<BM, BN, WM, WN, false, false>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN * Np, Np,
                                         ksplit, Np, sA0, sB0, sA1, sB1, wave, lane, wm, wn);
+  };
+  // column panels I of P and J of Q, k over all Mp rows: P[:, I]^T Q[:, J]
+  auto cols_t_cols = [&](const uint16_t* P, const uint16_t* Q) {
+    kloop<BM, BN, WM, WN, true, true>(acc, P + (int64_t)it.ti * BM, Np, Q + (int64_t)it.tj * BN, Np, 0, Mp, sA0,
+                                      sB0, sA1, sB1, wave, lane, wm, wn);
+  };
+
+  const uint16_t* Y = nullptr;
+  if constexpr (!VJP) {
+    if (MODE == 0)
+      cols_t_cols(X, X);            // Gram tile of I - X^T X
+    else
+      panel_times_sym(X, Ep);       // update tile of X E
+  } else {
+    Y = static_cast<const uint16_t*>(d->yc[parity]);
+    const uint16_t* S = static_cast<const uint16_t*>(d->s);
+    if (MODE == 0) {
+      cols_t_cols(X, Y);            // S tile: X^T Y + Y^T X
+      cols_t_cols(Y, X);
+    } else {
+      panel_times_sym(Y, Ep);       // Y E + X S' with S' = -(X^T Y + Y^T X)
+      panel_times_sym(X, S);
+    }
   }
 
   // ------------------------------------------------------------ epilogue --
@@ -287,9 +317,13 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   const int col = lane & 31;
   const int gi0 = it.ti * BM + wm * TM;  // first global row of this wave
   const int gj0 = it.tj * BN + wn * TN;  // first global column
-  uint16_t* E = static_cast<uint16_t*>(d->e);
-  float* Xm = d->master[0];
-  uint16_t* Xo = static_cast<uint16_t*>(d->xc[parity ^ 1]);
+  // Gram-like tiles write E (or S' in VJP mode) with the identity (or
+  // none) subtracted from; update-like tiles advance the fp32 iterate (or
+  // gradient iterate) in place and emit its next bf16 copy
+  uint16_t* E = static_cast<uint16_t*>(VJP ? d->s : d->e) + (VJP ? 0 : eoff);
+  float* Xm = VJP ? d->gy[0] : d->master[0];
+  uint16_t* Xo = static_cast<uint16_t*>(VJP ? d->yc[parity ^ 1] : d->xc[parity ^ 1]) + (VJP ? 0 : xoff);
+  constexpr float DELTA = VJP ? 0.f : 1.f;
   constexpr int NQ = 32 * TN / 256;        // 4-column groups per lane and chunk
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
@@ -318,10 +352,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
       const int64_t off = (int64_t)(gi + r) * Np + gj0 + c;
       if (MODE == 0) {
         const int dg = (gi + r) - (gj0 + c);   // the diagonal hits column c + dg
-        v.x = (dg == 0 ? 1.f : 0.f) - v.x;
-        v.y = (dg == 1 ? 1.f : 0.f) - v.y;
-        v.z = (dg == 2 ? 1.f : 0.f) - v.z;
-        v.w = (dg == 3 ? 1.f : 0.f) - v.w;
+        v.x = (dg == 0 ? DELTA : 0.f) - v.x;
+        v.y = (dg == 1 ? DELTA : 0.f) - v.y;
+        v.z = (dg == 2 ? DELTA : 0.f) - v.z;
+        v.w = (dg == 3 ? DELTA : 0.f) - v.w;
         *reinterpret_cast<uint2*>(E + off) = pack4_bf16(v.x, v.y, v.z, v.w);
       } else {
         const float4 m = mpre[q];
@@ -339,16 +373,26 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
 }  // namespace
 
 // One launch over a table of Gram and/or update tiles (each item carries its
-// own mode and ping-pong parity).
+// own mode and ping-pong parity); vjp selects the gradient modes, step the
+// saved iterate.
 hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
-                             hipStream_t s) {
+                             hipStream_t s, int vjp, int step) {
   if (n_items <= 0) return hipSuccess;
-  const char* name = big ? "bjorck_bf16_256" : "bjorck_bf16_128";
+  const char* name = vjp ? (big ? "bjorck_vjp_bf16_256" : "bjorck_vjp_bf16_128")
+                         : (big ? "bjorck_bf16_256" : "bjorck_bf16_128");
   timing_begin(name, s);
-  if (big)
-    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 2, 2>), dim3(n_items), dim3(256), 0, s, mats, items, beta);
+  if (big && !vjp)
+    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 2, 2, false>), dim3(n_items), dim3(256), 0, s, mats, items,
+                       beta, step);
+  else if (!vjp)
+    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 2, 2, false>), dim3(n_items), dim3(256), 0, s, mats, items,
+                       beta, step);
+  else if (big)
+    hipLaunchKernelGGL((bjorck_bf16_kernel<256, 256, 2, 2, true>), dim3(n_items), dim3(256), 0, s, mats, items,
+                       beta, step);
   else
-    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 2, 2>), dim3(n_items), dim3(256), 0, s, mats, items, beta);
+    hipLaunchKernelGGL((bjorck_bf16_kernel<128, 128, 2, 2, true>), dim3(n_items), dim3(256), 0, s, mats, items,
+                       beta, step);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
   return e;

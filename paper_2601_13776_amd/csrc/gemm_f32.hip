@@ -1,11 +1,14 @@
 // Table-driven fp32 "NT" GEMM on gfx950 fp32 MFMA (v_mfma_f32_32x32x2f32):
-// every work item is one 64 x 64 tile of C = A B^T with its own operands,
+// every work item is one 64 x 64 tile of C = A B^T (+ A2 B2^T, a second
+// operand pair accumulated into the same tile) with its own operands,
 // shapes and epilogue, so a single launch covers a whole ragged batch
 // (all matrices of a Björck step, all tap products of a composition step,
 // all Gram checks).  Operands may be fp32 or bf16 and stored either
 // K-contiguous ([M][K]) or transposed ([K][M]); loads are bounds-checked
 // with zero fill, with a vectorized fast path for aligned in-bounds fp32
-// K-contiguous tiles.
+// K-contiguous tiles.  A launch's step argument moves each operand by its
+// item's per-step offset, so one table serves every step of a recurrence
+// whose buffers are laid out step after step.
 //
 // Four waves (2 x 2) each own one 32x32 accumulator.  The K loop steps by
 // 32 through a 2-stage LDS ring; the next step's loads are in flight while
@@ -22,88 +25,95 @@ namespace {
 
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items) {
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items, int step) {
   constexpr int BM = 64, BN = 64, BK = 32, PITCH = BK + 4;
   __shared__ __attribute__((aligned(16))) float As[2][BM * PITCH];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * PITCH];
   const GemmItem* g = items + blockIdx.x;
-  const int M = g->M, N = g->N, K = g->K;
+  const int M = g->M, N = g->N;
   const int row0 = g->ti * BM, col0 = g->tj * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-
-  const void* A = g->A;
-  const void* B = g->B;
-  const int64_t lda = g->lda, ldb = g->ldb;
-  const int adt = g->a_dtype, bdt = g->b_dtype, atr = g->a_trans, btr = g->b_trans;
-
-  // thread -> (row, first k of 8) for each operand
-  const int ar = atr ? (tid & 63) : (tid >> 2);
-  const int ak = atr ? (tid >> 6) * 8 : (tid & 3) * 8;
-  const int br = btr ? (tid & 63) : (tid >> 2);
-  const int bk = btr ? (tid >> 6) * 8 : (tid & 3) * 8;
-
-  float ra[8], rb[8];
-  auto load_op = [&](const void* P, int64_t ld, int dt, int tr, int r, int kq, int rows_lim, int rbase, int k0,
-                     float* dst) {
-    const int gr = rbase + r;
-    const int gk = k0 + kq;
-    if (!tr && dt == ORTH_F32 && gr < rows_lim && gk + 8 <= K) {
-      const float* p = static_cast<const float*>(P) + (int64_t)gr * ld + gk;
-      if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-        const float4 x = reinterpret_cast<const float4*>(p)[0];
-        const float4 y = reinterpret_cast<const float4*>(p)[1];
-        dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
-        dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
-        return;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      float v = 0.f;
-      if (gr < rows_lim && gk + q < K) {
-        const int64_t idx = tr ? (int64_t)(gk + q) * ld + gr : (int64_t)gr * ld + gk + q;
-        v = load_as_f32(P, idx, dt);
-      }
-      dst[q] = v;
-    }
-  };
-  auto gload = [&](int k0) {
-    load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra);
-    load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb);
-  };
-  auto sstore = [&](int buf) {
-    float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
-    pa[0] = make_float4(ra[0], ra[1], ra[2], ra[3]);
-    pa[1] = make_float4(ra[4], ra[5], ra[6], ra[7]);
-    float4* pb = reinterpret_cast<float4*>(&Bs[buf][br * PITCH + bk]);
-    pb[0] = make_float4(rb[0], rb[1], rb[2], rb[3]);
-    pb[1] = make_float4(rb[4], rb[5], rb[6], rb[7]);
-  };
+  const int64_t st = step;
 
   f32x16 acc = {};
-  const int nk = (K + BK - 1) / BK;
-  if (nk > 0) {
-    gload(0);
-    sstore(0);
-  }
-  __syncthreads();
   const int aoff = (wm * 32 + (lane & 31)) * PITCH + (lane >> 5) * 4;
   const int boff = (wn * 32 + (lane & 31)) * PITCH + (lane >> 5) * 4;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+  for (int pair = 0; pair < 2; ++pair) {
+    const int K = pair ? g->K2 : g->K;
+    if (K <= 0) continue;
+    const int adt = pair ? ORTH_F32 : g->a_dtype, bdt = pair ? ORTH_F32 : g->b_dtype;
+    const int atr = pair ? g->a2_trans : g->a_trans, btr = pair ? g->b2_trans : g->b_trans;
+    const int64_t lda = pair ? g->lda2 : g->lda, ldb = pair ? g->ldb2 : g->ldb;
+    const int esz_a = adt == ORTH_BF16 ? 2 : 4, esz_b = bdt == ORTH_BF16 ? 2 : 4;
+    const void* A = static_cast<const char*>(pair ? g->A2 : g->A) + (pair ? g->a2_step : g->a_step) * st * esz_a;
+    const void* B = static_cast<const char*>(pair ? g->B2 : g->B) + (pair ? g->b2_step : g->b_step) * st * esz_b;
+
+    // thread -> (row, first k of 8) for each operand
+    const int ar = atr ? (tid & 63) : (tid >> 2);
+    const int ak = atr ? (tid >> 6) * 8 : (tid & 3) * 8;
+    const int br = btr ? (tid & 63) : (tid >> 2);
+    const int bk = btr ? (tid >> 6) * 8 : (tid & 3) * 8;
+
+    float ra[8], rb[8];
+    auto load_op = [&](const void* P, int64_t ld, int dt, int tr, int r, int kq, int rows_lim, int rbase, int k0,
+                       float* dst) {
+      const int gr = rbase + r;
+      const int gk = k0 + kq;
+      if (!tr && dt == ORTH_F32 && gr < rows_lim && gk + 8 <= K) {
+        const float* p = static_cast<const float*>(P) + (int64_t)gr * ld + gk;
+        if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+          const float4 x = reinterpret_cast<const float4*>(p)[0];
+          const float4 y = reinterpret_cast<const float4*>(p)[1];
+          dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
+          dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
+          return;
+        }
+      }
 #pragma unroll
-    for (int gq = 0; gq < BK / 8; ++gq) {
-      const float4 a4 = *reinterpret_cast<const float4*>(&As[buf][aoff + gq * 8]);
-      const float4 b4 = *reinterpret_cast<const float4*>(&Bs[buf][boff + gq * 8]);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, b4.x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, b4.y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, b4.z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, b4.w, acc, 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+      for (int q = 0; q < 8; ++q) {
+        float v = 0.f;
+        if (gr < rows_lim && gk + q < K) {
+          const int64_t idx = tr ? (int64_t)(gk + q) * ld + gr : (int64_t)gr * ld + gk + q;
+          v = load_as_f32(P, idx, dt);
+        }
+        dst[q] = v;
+      }
+    };
+    auto gload = [&](int k0) {
+      load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra);
+      load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb);
+    };
+    auto sstore = [&](int buf) {
+      float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
+      pa[0] = make_float4(ra[0], ra[1], ra[2], ra[3]);
+      pa[1] = make_float4(ra[4], ra[5], ra[6], ra[7]);
+      float4* pb = reinterpret_cast<float4*>(&Bs[buf][br * PITCH + bk]);
+      pb[0] = make_float4(rb[0], rb[1], rb[2], rb[3]);
+      pb[1] = make_float4(rb[4], rb[5], rb[6], rb[7]);
+    };
+
+    // stage 0 is free here: every wave passed the last barrier of the
+    // previous pair after its final reads
+    const int nk = (K + BK - 1) / BK;
+    gload(0);
+    sstore(0);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+      for (int gq = 0; gq < BK / 8; ++gq) {
+        const float4 a4 = *reinterpret_cast<const float4*>(&As[buf][aoff + gq * 8]);
+        const float4 b4 = *reinterpret_cast<const float4*>(&Bs[buf][boff + gq * 8]);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, b4.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, b4.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, b4.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, b4.w, acc, 0, 0, 0);
+      }
+      if (kt + 1 < nk) sstore(buf ^ 1);
+      __syncthreads();
+    }
   }
 
   // ------------------------------------------------------------ epilogue --
@@ -129,7 +139,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     return;
   }
   if (j >= N) return;
-  float* C = static_cast<float*>(g->C);
+  float* C = static_cast<float*>(g->C) + g->c_step * st;
   const int64_t ldc = g->ldc;
   if (epi == EPI_STORE) {
 #pragma unroll
@@ -148,8 +158,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         if (mirror) C[(int64_t)j * ldc + i] = v;
       }
     }
+  } else if (epi == EPI_NEG) {
+    const bool mirror = g->mirror != 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = ibase + acc_row(r, lane);
+      if (i < M) {
+        C[(int64_t)i * ldc + j] = -acc[r];
+        if (mirror) C[(int64_t)j * ldc + i] = -acc[r];
+      }
+    }
   } else {  // EPI_UPDATE
-    const float* src = g->src;
+    const float* src = g->src + g->src_step * st;
     float* dst2 = g->dst2;
     const int64_t lds_ = g->ld_src, ld2 = g->ld2;
     const float beta = g->beta;
@@ -159,7 +179,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       if (i < M) {
         const float v = src[(int64_t)i * lds_ + j] + beta * acc[r];
         C[(int64_t)i * ldc + j] = v;
-        dst2[(int64_t)j * ld2 + i] = v;
+        if (dst2) dst2[(int64_t)j * ld2 + i] = v;
       }
     }
   }
@@ -167,10 +187,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
 
 }  // namespace
 
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s) {
+hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step) {
   if (n_items <= 0) return hipSuccess;
   timing_begin(name, s);
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_items), dim3(256), 0, s, items);
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_items), dim3(256), 0, s, items, step);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
   return e;

@@ -653,6 +653,302 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
 }
 }  // namespace
 
+// ------------------------------------------------ Björck VJP planning ---
+// The vector-Jacobian product recomputes the forward iterates, saving every
+// X_t and E_t = I - X_t^T X_t (step after step in the workspace), then runs
+// the gradient recurrence from t = T-1 down to 0 and finally the derivative
+// of the pre-scaling.  Matrices the forward would run in fp32 (fp32 products,
+// or the small fused bucket) use the fp32 tile GEMM; the others use the
+// bf16 tile kernel in its saved-iterate and gradient modes.
+namespace {
+enum VBucket { V_F32 = 0, V_BF16_128 = 1, V_BF16_256 = 2 };
+
+struct VjpPlan {
+  std::vector<int> bucket;
+  std::vector<TiledMat> mats;
+  std::vector<TileItem> partial_items, scale_items;
+  std::vector<GemmItem> f_gram, f_upd, b_s[2], b_upd[2];
+  std::vector<TileItem> t_gram[2], t_upd[2], t_s[2][2], t_yu[2][2];  // [class][parity]
+  size_t off_mats = 0, off_partial_items = 0, off_scale_items = 0;
+  size_t off_f_gram = 0, off_f_upd = 0, off_b_s[2] = {}, off_b_upd[2] = {};
+  size_t off_t_gram[2] = {}, off_t_upd[2] = {}, off_t_s[2][2] = {}, off_t_yu[2][2] = {};
+  size_t off_partials = 0, off_inv = 0, off_dot = 0, off_status = 0;
+  size_t table_bytes = 0, total_bytes = 0;
+};
+
+int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !mats) return fail(ORTH_EINVAL, "mats is NULL");
+  if (!o) return fail(ORTH_EINVAL, "opts is NULL");
+  if (o->iters < 0) return fail(ORTH_EINVAL, "iters must be >= 0");
+  if (o->iters > 4096) return fail(ORTH_EINVAL, "iters must be <= 4096");
+  if (!(o->beta > 0.f && o->beta <= 0.5f)) return fail(ORTH_EINVAL, "beta must lie in (0, 0.5]");
+  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS)
+    return fail(ORTH_EINVAL, "unknown prescale mode");
+  if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
+    return fail(ORTH_EINVAL, "unknown dtype");
+  if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
+  for (int i = 0; i < n; ++i) {
+    const orth_vjp_mat& m = mats[i];
+    char buf[160];
+    if (!m.w || !m.grad_out || !m.grad_in) {
+      snprintf(buf, sizeof buf, "matrix %d: NULL data pointer", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.rows < 1 || m.cols < 1 || m.rows > (1 << 20) || m.cols > (1 << 20)) {
+      snprintf(buf, sizeof buf, "matrix %d: rows and cols must be in [1, 2^20]", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.ld_w < m.cols || m.ld_grad_out < m.cols || m.ld_grad_in < m.cols) {
+      snprintf(buf, sizeof buf, "matrix %d: leading dimension smaller than cols", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.grad_in == m.grad_out && (o->in_dtype != o->out_dtype || m.ld_grad_in != m.ld_grad_out)) {
+      snprintf(buf, sizeof buf, "matrix %d: grad_in aliasing grad_out needs equal dtypes and leading dims", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.grad_in == m.w && m.ld_grad_in != m.ld_w) {
+      snprintf(buf, sizeof buf, "matrix %d: grad_in aliasing w needs equal leading dims", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+  }
+  return ORTH_OK;
+}
+
+void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o, VjpPlan& P,
+                    unsigned char* ws) {
+  const bool bf16 = o->compute == ORTH_COMPUTE_BF16;
+  const int T = o->iters;
+  const int slots = std::max(T, 1);
+  P.bucket.resize(n);
+  P.mats.resize(n);
+  int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
+  std::vector<TileItem> tg[2], tu[2];
+  for (int i = 0; i < n; ++i) {
+    const orth_vjp_mat& m = mats[i];
+    TiledMat& t = P.mats[i];
+    t = TiledMat{};
+    t.in = m.w;
+    t.out = m.grad_in;
+    t.gout = m.grad_out;
+    t.ld_in = m.ld_w;
+    t.ld_out = m.ld_grad_in;
+    t.ld_gout = m.ld_grad_out;
+    t.rows = m.rows;
+    t.cols = m.cols;
+    t.transposed = m.rows < m.cols;
+    t.M = std::max(m.rows, m.cols);
+    t.N = std::min(m.rows, m.cols);
+    t.status_index = i;
+    int b = V_F32, pad = 64;
+    if (bf16 && !(t.N <= 64 && t.M <= 128)) {
+      b = t.N >= 1024 ? V_BF16_256 : V_BF16_128;
+      pad = t.N >= 1024 ? 256 : 128;
+    }
+    P.bucket[i] = b;
+    t.Mp = (int32_t)round_up(t.M, pad);
+    t.Np = (int32_t)round_up(t.N, pad);
+    const int pr = (m.rows + 63) / 64, pc = (m.cols + 63) / 64;
+    t.partial_base = (int32_t)n_part;
+    t.n_partials = pr * pc;
+    n_part += pr * pc;
+    n_scale += (int64_t)(t.Mp / 64) * (t.Np / 64);
+    if (b == V_F32) {
+      const int64_t tn = t.Np / 64, tm = t.Mp / 64;
+      n_fg += tn * (tn + 1) / 2;
+      n_fu += tm * tn;
+    } else {
+      const int cls = b == V_BF16_256 ? 1 : 0, tsz = cls ? 256 : 128;
+      grouped_tiles(i, t.Np / tsz, t.Np / tsz, 4, true, tg[cls]);
+      grouped_tiles(i, t.Mp / tsz, t.Np / tsz, 4, false, tu[cls]);
+    }
+  }
+  for (int cls = 0; cls < 2; ++cls) {
+    P.t_gram[cls] = tg[cls];
+    P.t_upd[cls] = tu[cls];
+    for (auto& it : P.t_upd[cls]) it.flags = TILE_UPDATE;
+    for (int par = 0; par < 2; ++par) {
+      P.t_s[cls][par] = tg[cls];
+      for (auto& it : P.t_s[cls][par]) it.flags = TILE_VJP | (par ? TILE_PARITY : 0);
+      P.t_yu[cls][par] = tu[cls];
+      for (auto& it : P.t_yu[cls][par]) it.flags = TILE_VJP | TILE_UPDATE | (par ? TILE_PARITY : 0);
+    }
+  }
+
+  Arena A;
+  P.off_mats = A.take(sizeof(TiledMat) * n);
+  P.off_partial_items = A.take(sizeof(TileItem) * n_part);
+  P.off_scale_items = A.take(sizeof(TileItem) * n_scale);
+  P.off_f_gram = A.take(sizeof(GemmItem) * n_fg);
+  P.off_f_upd = A.take(sizeof(GemmItem) * n_fu);
+  for (int par = 0; par < 2; ++par) {
+    P.off_b_s[par] = A.take(sizeof(GemmItem) * n_fg);
+    P.off_b_upd[par] = A.take(sizeof(GemmItem) * n_fu);
+  }
+  for (int cls = 0; cls < 2; ++cls) {
+    P.off_t_gram[cls] = A.take(sizeof(TileItem) * P.t_gram[cls].size());
+    P.off_t_upd[cls] = A.take(sizeof(TileItem) * P.t_upd[cls].size());
+    for (int par = 0; par < 2; ++par) {
+      P.off_t_s[cls][par] = A.take(sizeof(TileItem) * P.t_s[cls][par].size());
+      P.off_t_yu[cls][par] = A.take(sizeof(TileItem) * P.t_yu[cls][par].size());
+    }
+  }
+  P.table_bytes = align_up(A.off);
+  P.off_partials = A.take(sizeof(double) * n_part);
+  P.off_inv = A.take(sizeof(float) * n);
+  P.off_dot = A.take(sizeof(double) * n);
+  P.off_status = A.take(sizeof(int32_t) * n);
+
+  auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
+  for (int i = 0; i < n; ++i) {
+    TiledMat& t = P.mats[i];
+    const int64_t xe = (int64_t)t.Mp * t.Np, ee = (int64_t)t.Np * t.Np;
+    t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + i;
+    t.dot = reinterpret_cast<double*>(dev(P.off_dot)) + i;
+    for (int a = 0; a < (t.rows + 63) / 64; ++a)
+      for (int b = 0; b < (t.cols + 63) / 64; ++b) P.partial_items.push_back(TileItem{i, a, b, 0});
+    for (int a = 0; a < t.Mp / 64; ++a)
+      for (int b = 0; b < t.Np / 64; ++b) P.scale_items.push_back(TileItem{i, a, b, 0});
+    if (P.bucket[i] != V_F32) {
+      t.master[0] = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+      unsigned char* xs = dev(A.take((size_t)slots * xe * 2));
+      t.xc[0] = xs;
+      t.xc[1] = xs ? xs + xe * 2 : nullptr;
+      t.xstep = xe;
+      t.e = dev(A.take((size_t)T * ee * 2));
+      t.estep = ee;
+      t.gy[0] = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+      t.yc[0] = dev(A.take(xe * 2));
+      t.yc[1] = dev(A.take(xe * 2));
+      t.s = dev(A.take(ee * 2));
+      t.gy_final = 0;
+      continue;
+    }
+    float* xs = reinterpret_cast<float*>(dev(A.take((size_t)slots * xe * 4)));
+    float* es = reinterpret_cast<float*>(dev(A.take((size_t)T * ee * 4)));
+    float* gy0 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+    float* gy1 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+    float* sb = reinterpret_cast<float*>(dev(A.take(ee * 4)));
+    t.master[0] = xs;
+    t.e = es;
+    t.gy[0] = gy0;
+    t.gy[1] = gy1;
+    t.s = sb;
+    t.gy_final = T & 1;
+    const int tn = t.Np / 64, tm = t.Mp / 64;
+    for (int a = 0; a < tn; ++a)
+      for (int b = a; b < tn; ++b) {
+        GemmItem g{};
+        g.A = xs;
+        g.B = xs;
+        g.a_trans = g.b_trans = 1;
+        g.lda = g.ldb = t.Np;
+        g.a_step = g.b_step = xe;
+        g.K = t.Mp;
+        g.M = g.N = t.Np;
+        g.C = es;
+        g.ldc = t.Np;
+        g.c_step = ee;
+        g.ti = a;
+        g.tj = b;
+        g.a_dtype = g.b_dtype = ORTH_F32;
+        g.epi = EPI_GRAM_E;
+        g.mirror = a != b;
+        P.f_gram.push_back(g);
+        for (int par = 0; par < 2; ++par) {
+          GemmItem h{};
+          h.A = xs;
+          h.a_trans = 1;
+          h.lda = t.Np;
+          h.a_step = xe;
+          h.B = par ? gy1 : gy0;
+          h.b_trans = 1;
+          h.ldb = t.Np;
+          h.K = t.Mp;
+          h.A2 = par ? gy1 : gy0;
+          h.a2_trans = 1;
+          h.lda2 = t.Np;
+          h.B2 = xs;
+          h.b2_trans = 1;
+          h.ldb2 = t.Np;
+          h.b2_step = xe;
+          h.K2 = t.Mp;
+          h.M = h.N = t.Np;
+          h.C = sb;
+          h.ldc = t.Np;
+          h.ti = a;
+          h.tj = b;
+          h.a_dtype = h.b_dtype = ORTH_F32;
+          h.epi = EPI_NEG;
+          h.mirror = a != b;
+          P.b_s[par].push_back(h);
+        }
+      }
+    for (int a = 0; a < tm; ++a)
+      for (int b = 0; b < tn; ++b) {
+        GemmItem g{};
+        g.A = xs;
+        g.lda = t.Np;
+        g.a_step = xe;
+        g.B = es;
+        g.ldb = t.Np;
+        g.b_step = ee;
+        g.K = t.Np;
+        g.M = t.Mp;
+        g.N = t.Np;
+        g.src = xs;
+        g.ld_src = t.Np;
+        g.src_step = xe;
+        g.C = xs + xe;
+        g.ldc = t.Np;
+        g.c_step = xe;
+        g.ti = a;
+        g.tj = b;
+        g.a_dtype = g.b_dtype = ORTH_F32;
+        g.epi = EPI_UPDATE;
+        g.beta = o->beta;
+        P.f_upd.push_back(g);
+        for (int par = 0; par < 2; ++par) {
+          float* y = par ? gy1 : gy0;
+          float* yn = par ? gy0 : gy1;
+          GemmItem h{};
+          h.A = y;
+          h.lda = t.Np;
+          h.B = es;
+          h.ldb = t.Np;
+          h.b_step = ee;
+          h.K = t.Np;
+          h.A2 = xs;
+          h.lda2 = t.Np;
+          h.a2_step = xe;
+          h.B2 = sb;
+          h.ldb2 = t.Np;
+          h.K2 = t.Np;
+          h.M = t.Mp;
+          h.N = t.Np;
+          h.src = y;
+          h.ld_src = t.Np;
+          h.C = yn;
+          h.ldc = t.Np;
+          h.ti = a;
+          h.tj = b;
+          h.a_dtype = h.b_dtype = ORTH_F32;
+          h.epi = EPI_UPDATE;
+          h.beta = o->beta;
+          P.b_upd[par].push_back(h);
+        }
+      }
+  }
+  P.total_bytes = align_up(A.off);
+  P.f_gram = xcd_order(P.f_gram);
+  P.f_upd = xcd_order(P.f_upd);
+  for (int par = 0; par < 2; ++par) {
+    P.b_s[par] = xcd_order(P.b_s[par]);
+    P.b_upd[par] = xcd_order(P.b_upd[par]);
+  }
+}
+}  // namespace
+
 }  // namespace orth
 
 using namespace orth;
@@ -750,6 +1046,96 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
     ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
                                  b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale, opts->in_dtype,
                                  opts->out_dtype, status, s));
+  return ORTH_OK;
+}
+
+int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* opts,
+                                          size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  int rc = validate_vjp(mats, n, opts);
+  if (rc) return rc;
+  VjpPlan P;
+  build_vjp_plan(mats, n, opts, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* opts,
+                                   void* workspace, size_t workspace_bytes, int32_t* status_dev, void* stream) {
+  int rc = validate_vjp(mats, n, opts);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  VjpPlan P;
+  build_vjp_plan(mats, n, opts, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = VjpPlan();
+  build_vjp_plan(mats, n, opts, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
+
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_mats, P.mats);
+  put(img, P.off_partial_items, P.partial_items);
+  put(img, P.off_scale_items, P.scale_items);
+  put(img, P.off_f_gram, P.f_gram);
+  put(img, P.off_f_upd, P.f_upd);
+  for (int par = 0; par < 2; ++par) {
+    put(img, P.off_b_s[par], P.b_s[par]);
+    put(img, P.off_b_upd[par], P.b_upd[par]);
+  }
+  for (int cls = 0; cls < 2; ++cls) {
+    put(img, P.off_t_gram[cls], P.t_gram[cls]);
+    put(img, P.off_t_upd[cls], P.t_upd[cls]);
+    for (int par = 0; par < 2; ++par) {
+      put(img, P.off_t_s[cls][par], P.t_s[cls][par]);
+      put(img, P.off_t_yu[cls][par], P.t_yu[cls][par]);
+    }
+  }
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+
+  auto TI = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
+  auto GI = [&](size_t off) { return reinterpret_cast<const GemmItem*>(ws + off); };
+  const TiledMat* tm = reinterpret_cast<const TiledMat*>(ws + P.off_mats);
+  const int T = opts->iters;
+  const float beta = opts->beta;
+  double* partials = reinterpret_cast<double*>(ws + P.off_partials);
+  ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
+                                   partials, s));
+  ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s));
+  ORTH_HIP(launch_prescale_scale(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
+                                 opts->compute, s));
+  // forward recomputation, saving X_t and E_t (X_T itself is never needed)
+  for (int t = 0; t < T; ++t) {
+    ORTH_HIP(launch_gemm_f32(GI(P.off_f_gram), (int)P.f_gram.size(), "vjp_fwd_gram_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_gram[cls]), (int)P.t_gram[cls].size(), beta, s, 0, t));
+    if (t + 1 == T) break;
+    ORTH_HIP(launch_gemm_f32(GI(P.off_f_upd), (int)P.f_upd.size(), "vjp_fwd_update_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_upd[cls]), (int)P.t_upd[cls].size(), beta, s, 0, t));
+  }
+  // gradient recurrence, last step first
+  ORTH_HIP(launch_vjp_load_grad(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->out_dtype, s));
+  for (int b = 0; b < T; ++b) {
+    const int t = T - 1 - b, par = b & 1;
+    ORTH_HIP(launch_gemm_f32(GI(P.off_b_s[par]), (int)P.b_s[par].size(), "vjp_s_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_s[cls][par]), (int)P.t_s[cls][par].size(), beta, s, 1, t));
+    ORTH_HIP(launch_gemm_f32(GI(P.off_b_upd[par]), (int)P.b_upd[par].size(), "vjp_update_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_yu[cls][par]), (int)P.t_yu[cls][par].size(), beta, s, 1, t));
+  }
+  // derivative of the pre-scaling, in the caller's layout
+  if (opts->prescale == ORTH_PRESCALE_FROBENIUS) {
+    ORTH_HIP(launch_vjp_dot_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
+                                    partials, s));
+    ORTH_HIP(launch_vjp_dot_finish(tm, n, partials, s));
+  }
+  ORTH_HIP(launch_vjp_writeout(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
+                               opts->prescale, status, s));
   return ORTH_OK;
 }
 

@@ -53,6 +53,18 @@ struct TiledMat {
   void* xt;                  // fp32 products only: transposed iterate, Np x Mp
   void* e;                   // I - X^T X in compute dtype, Np x Np (bf16: upper tiles only)
   float* inv_norm;           // this matrix's pre-scale factor
+  // Saved-iterate mode (vector-Jacobian product): step t of a launch reads
+  // xc[p] + t xstep and e + t estep (both 0 outside that mode).
+  int64_t xstep, estep;
+  // Vector-Jacobian product only.
+  const void* gout;          // dL/d(output) in the caller's layout
+  int64_t ld_gout;
+  float* gy[2];              // fp32 gradient iterate, Mp x Np (bf16 mode: [0], in place)
+  void* yc[2];               // bf16 copies of the gradient iterate (bf16 mode)
+  void* s;                   // -(X^T Y + Y^T X), Np x Np (bf16: upper tiles only)
+  double* dot;               // <Y_0, W_0>, one per matrix
+  int32_t gy_final;          // gy[] index holding dL/dW_0 after the last step
+  int32_t pad;
 };
 
 struct TileItem {
@@ -62,7 +74,8 @@ struct TileItem {
 };
 enum : int32_t {
   TILE_UPDATE = 1,           // bf16 Björck: update tile (else Gram tile)
-  TILE_PARITY = 2            // bf16 Björck: the update reads xc[1] and writes xc[0]
+  TILE_PARITY = 2,           // bf16 Björck: the update reads xc[1] and writes xc[0]
+  TILE_VJP = 4               // with TILE_UPDATE: Y <- Y + beta (Y E + X S), else S tile
 };
 
 struct SmallMat {
@@ -77,30 +90,38 @@ struct SmallMat {
   int32_t pad;
 };
 
-// Generic bounds-checked fp32 GEMM work item: C = A * B^T over one
-// 64 x 64 output tile, A logically M x K, B logically N x K.
+// Generic bounds-checked fp32 GEMM work item: C = A * B^T (+ A2 * B2^T)
+// over one 64 x 64 output tile, A logically M x K, B logically N x K, A2
+// M x K2, B2 N x K2 (K2 = 0: no second pair).
 enum GemmEpi : int32_t {
   EPI_STORE = 0,     // C[i][j] = acc
   EPI_GRAM_E = 1,    // C[i][j] = delta_ij - acc  (and C[j][i] if mirror)
-  EPI_UPDATE = 2,    // v = src[i][j] + beta acc; C[i][j] = v; dst2[j][i] = v
-  EPI_MAXDEV = 3     // red[0] = max(red[0], |delta_ij - acc|)
+  EPI_UPDATE = 2,    // v = src[i][j] + beta acc; C[i][j] = v; dst2[j][i] = v if dst2
+  EPI_MAXDEV = 3,    // red[0] = max(red[0], |delta_ij - acc|)
+  EPI_NEG = 4        // C[i][j] = -acc  (and C[j][i] if mirror)
 };
 
 struct GemmItem {
   const void* A;
   const void* B;
+  const void* A2;
+  const void* B2;
   void* C;
   const float* src;
   float* dst2;
   float* red;
-  int64_t lda, ldb, ldc, ld_src, ld2;
-  int32_t M, N, K;
+  int64_t lda, ldb, lda2, ldb2, ldc, ld_src, ld2;
+  // element offsets added per unit of the launch's step argument
+  int64_t a_step, b_step, a2_step, b2_step, c_step, src_step;
+  int32_t M, N, K, K2;
   int32_t ti, tj;
-  int32_t a_dtype, b_dtype;  // storage of A and B
+  int32_t a_dtype, b_dtype;  // storage of A and B (A2 and B2 are fp32)
   int32_t a_trans, b_trans;  // 0: row-major [M][K]; 1: stored [K][M]
+  int32_t a2_trans, b2_trans;
   int32_t epi;
   int32_t mirror;
   float beta;
+  int32_t pad;
 };
 
 // Compose (AOC) descriptors: one entry per (layer, group).
@@ -150,8 +171,15 @@ hipError_t launch_prescale_scale(const TiledMat* mats, const TileItem* items, in
 hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_items,
                            int master_index, int out_dtype, hipStream_t s);
 hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
-                             hipStream_t s);
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s);
+                             hipStream_t s, int vjp = 0, int step = 0);
+hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step = 0);
+hipError_t launch_vjp_load_grad(const TiledMat* mats, const TileItem* items, int n_items, int gout_dtype,
+                                hipStream_t s);
+hipError_t launch_vjp_dot_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                                  double* partials, hipStream_t s);
+hipError_t launch_vjp_dot_finish(const TiledMat* mats, int n_mats, const double* partials, hipStream_t s);
+hipError_t launch_vjp_writeout(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                               int prescale, const int32_t* status, hipStream_t s);
 hipError_t launch_compose_init(const ComposeGroup* groups, int n_groups, int dtype, int64_t max_elems,
                                hipStream_t s);
 hipError_t launch_compose_combine(const ComposeGroup* groups, const CombineItem* items, int n_items,

@@ -113,11 +113,10 @@ __global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __r
     const int64_t off = (int64_t)(R + a) * d.Np + C + b;
     const float v = tile[a][b];
     master[off] = v;
-    if (compute == ORTH_COMPUTE_BF16) {
-      static_cast<uint16_t*>(d.xc[0])[off] = f32_to_bf16(v);
-    }
-    // fp32 path: the transposed iterate xt[(C + a)][(R + b)] = tile[b][a]
-    if (compute != ORTH_COMPUTE_BF16)
+    // bf16 products: the bf16 copy; fp32 products: the transposed iterate
+    // xt[(C + a)][(R + b)] = tile[b][a] (each only where the plan has one)
+    if (compute == ORTH_COMPUTE_BF16 && d.xc[0]) static_cast<uint16_t*>(d.xc[0])[off] = f32_to_bf16(v);
+    if (compute != ORTH_COMPUTE_BF16 && d.xt)
       static_cast<float*>(d.xt)[(int64_t)(C + a) * d.Mp + R + b] = tile[b][a];
   }
 }

@@ -1,0 +1,186 @@
+// Layout and pre-scaling kernels of the Björck vector-Jacobian product.
+//
+//   load_grad   : dL/d(output) from the caller's layout and dtype into the
+//                 tall, zero-padded fp32 gradient iterate (plus its bf16
+//                 copy for bf16 products)
+//   dot_partial : per 64x64 tile of the caller's layout, sum of
+//                 dL/dW_0 * W in fp64 (fixed order inside the tile)
+//   dot_finish  : per matrix, <dL/dW_0, W_0> = inv * (fixed-order sum)
+//   writeout    : the derivative of W_0 = W / ||W||_F,
+//                   dL/dW = inv (Y_0 - <Y_0, W_0> W_0),  W_0 = inv W,
+//                 (Y_0 itself without pre-scaling), in the caller's layout;
+//                 zero for a zero matrix and NaN for a non-finite one
+//
+// HBM-bound; the transposed (wide) case goes through an LDS tile so that
+// both sides are accessed with coalesced rows.
+#include "internal.h"
+
+namespace orth {
+namespace {
+
+constexpr int TB = 64;
+
+// tile[x][y] = dL/dW_0 at caller element (R + x, C + y), 0 outside the
+// padded tall grid
+__device__ inline void caller_tile(const TiledMat& d, const float* y, int R, int C, float (*tile)[TB + 1]) {
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    if (!d.transposed) {
+      const int r = R + a, c = C + b;
+      tile[a][b] = (r < d.Mp && c < d.Np) ? y[(int64_t)r * d.Np + c] : 0.f;
+    } else {
+      // caller (R + b, C + a) is tall (C + a, R + b): rows of the tall
+      // buffer are read along b
+      const int tr = C + a, tc = R + b;
+      tile[b][a] = (tr < d.Mp && tc < d.Np) ? y[(int64_t)tr * d.Np + tc] : 0.f;
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __restrict__ mats,
+                                                            const TileItem* __restrict__ items, int gout_dtype) {
+  __shared__ float tile[TB][TB + 1];
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the tall padded layout
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    if (!d.transposed) {
+      const int r = R + a, c = C + b;
+      tile[a][b] = (r < d.M && c < d.N) ? load_as_f32(d.gout, (int64_t)r * d.ld_gout + c, gout_dtype) : 0.f;
+    } else {
+      // caller element (C + a, R + b) is tall element (R + b, C + a)
+      const int orow = C + a, ocol = R + b;
+      tile[b][a] =
+          (orow < d.N && ocol < d.M) ? load_as_f32(d.gout, (int64_t)orow * d.ld_gout + ocol, gout_dtype) : 0.f;
+    }
+  }
+  __syncthreads();
+  float* y = d.gy[0];
+  uint16_t* yc = static_cast<uint16_t*>(d.yc[0]);
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int a = e / TB, b = e % TB;
+    const int64_t off = (int64_t)(R + a) * d.Np + C + b;
+    y[off] = tile[a][b];
+    if (yc) yc[off] = f32_to_bf16(tile[a][b]);
+  }
+}
+
+__device__ inline double block_sum_256(double v, double* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0) t = ((red[0] + red[1]) + red[2]) + red[3];
+  return t;  // valid in thread 0
+}
+
+__global__ __launch_bounds__(256) void vjp_dot_partial_kernel(const TiledMat* __restrict__ mats,
+                                                              const TileItem* __restrict__ items, int in_dtype,
+                                                              double* __restrict__ partials) {
+  __shared__ float tile[TB][TB + 1];
+  __shared__ double red[4];
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const int R = it.ti * TB, C = it.tj * TB;  // caller layout
+  caller_tile(d, d.gy[d.gy_final], R, C, tile);
+  double acc = 0.0;
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int x = e / TB, y = e % TB;
+    const int r = R + x, c = C + y;
+    if (r < d.rows && c < d.cols)
+      acc += (double)tile[x][y] * (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+  }
+  const double tot = block_sum_256(acc, red);
+  if (threadIdx.x == 0) {
+    const int tiles_c = (d.cols + TB - 1) / TB;
+    partials[d.partial_base + it.ti * tiles_c + it.tj] = tot;
+  }
+}
+
+__global__ __launch_bounds__(256) void vjp_dot_finish_kernel(const TiledMat* __restrict__ mats,
+                                                             const double* __restrict__ partials) {
+  __shared__ double red[4];
+  const TiledMat& d = mats[blockIdx.x];
+  double ss = 0.0;
+  for (int i = threadIdx.x; i < d.n_partials; i += 256) ss += partials[d.partial_base + i];
+  const double tot = block_sum_256(ss, red);
+  if (threadIdx.x == 0) *d.dot = tot * (double)*d.inv_norm;
+}
+
+__global__ __launch_bounds__(256) void vjp_writeout_kernel(const TiledMat* __restrict__ mats,
+                                                           const TileItem* __restrict__ items, int in_dtype,
+                                                           int prescale, const int32_t* __restrict__ status) {
+  __shared__ float tile[TB][TB + 1];
+  const TileItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const int R = it.ti * TB, C = it.tj * TB;  // caller layout
+  caller_tile(d, d.gy[d.gy_final], R, C, tile);
+  const int st = status[d.status_index];
+  const float inv = *d.inv_norm;
+  const bool frob = prescale == ORTH_PRESCALE_FROBENIUS;
+  const float dscale = frob && st == ORTH_MAT_OK ? (float)(*d.dot) * inv : 0.f;
+  for (int e = threadIdx.x; e < TB * TB; e += 256) {
+    const int x = e / TB, y = e % TB;
+    const int r = R + x, c = C + y;
+    if (r >= d.rows || c >= d.cols) continue;
+    float v;
+    if (st == ORTH_MAT_NONFINITE) {
+      v = __builtin_nanf("");
+    } else if (st == ORTH_MAT_ZERO) {
+      v = 0.f;
+    } else if (frob) {
+      const float w = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+      v = inv * (tile[x][y] - dscale * w);
+    } else {
+      v = tile[x][y];
+    }
+    store_from_f32(d.out, (int64_t)r * d.ld_out + c, in_dtype, v);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_vjp_load_grad(const TiledMat* mats, const TileItem* items, int n_items, int gout_dtype,
+                                hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("vjp_load_grad", s);
+  hipLaunchKernelGGL(vjp_load_grad_kernel, dim3(n_items), dim3(256), 0, s, mats, items, gout_dtype);
+  hipError_t e = hipGetLastError();
+  timing_end("vjp_load_grad", s);
+  return e;
+}
+
+hipError_t launch_vjp_dot_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                                  double* partials, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("vjp_dot_partial", s);
+  hipLaunchKernelGGL(vjp_dot_partial_kernel, dim3(n_items), dim3(256), 0, s, mats, items, in_dtype, partials);
+  hipError_t e = hipGetLastError();
+  timing_end("vjp_dot_partial", s);
+  return e;
+}
+
+hipError_t launch_vjp_dot_finish(const TiledMat* mats, int n_mats, const double* partials, hipStream_t s) {
+  if (n_mats <= 0) return hipSuccess;
+  timing_begin("vjp_dot_finish", s);
+  hipLaunchKernelGGL(vjp_dot_finish_kernel, dim3(n_mats), dim3(256), 0, s, mats, partials);
+  hipError_t e = hipGetLastError();
+  timing_end("vjp_dot_finish", s);
+  return e;
+}
+
+hipError_t launch_vjp_writeout(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
+                               int prescale, const int32_t* status, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("vjp_writeout", s);
+  hipLaunchKernelGGL(vjp_writeout_kernel, dim3(n_items), dim3(256), 0, s, mats, items, in_dtype, prescale, status);
+  hipError_t e = hipGetLastError();
+  timing_end("vjp_writeout", s);
+  return e;
+}
+
+}  // namespace orth

@@ -21,7 +21,8 @@ ORTH_PRESCALE_NONE, ORTH_PRESCALE_FROBENIUS = 0, 1
 ORTH_CHECK_GRAM, ORTH_CHECK_CONV, ORTH_CHECK_CONV_ADJOINT = 0, 1, 2
 
 EXPORTED = [
-    "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched", "orth_aoc_param_shapes",
+    "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched",
+    "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
     "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
@@ -43,6 +44,12 @@ class orth_mat(ctypes.Structure):
 class orth_bjorck_opts(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("beta", ctypes.c_float), ("prescale", ctypes.c_int32),
                 ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("compute", ctypes.c_int32)]
+
+
+class orth_vjp_mat(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("grad_out", ctypes.c_void_p), ("grad_in", ctypes.c_void_p),
+                ("rows", ctypes.c_int32), ("cols", ctypes.c_int32), ("ld_w", ctypes.c_int64),
+                ("ld_grad_out", ctypes.c_int64), ("ld_grad_in", ctypes.c_int64)]
 
 
 class orth_conv_geom(ctypes.Structure):
@@ -73,6 +80,8 @@ def lib():
         P = ctypes.POINTER
         L.orth_orthogonalize_workspace_size.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), P(sz)]
         L.orth_orthogonalize_batched.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
+        L.orth_orthogonalize_vjp_workspace_size.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), P(sz)]
+        L.orth_orthogonalize_vjp_batched.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
         L.orth_aoc_param_shapes.argtypes = [P(orth_conv_geom)] + [P(i32)] * 5
         L.orth_build_conv_kernels_workspace_size.argtypes = [P(orth_conv_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_batched.argtypes = [P(orth_conv_desc), i32, i32, vp, sz, vp]
@@ -174,6 +183,54 @@ def orth_orthogonalize_batched(ins, outs, iters, beta=0.5, prescale="frobenius",
                                           status.data_ptr() if status is not None else None, _stream(stream))
     _check(rc, "orth_orthogonalize_batched")
     return ws
+
+
+def _vjp_mats(ws, gouts, gins):
+    arr = (orth_vjp_mat * len(ws))()
+    for i, (w, go, gi) in enumerate(zip(ws, gouts, gins)):
+        if not (w.shape == go.shape == gi.shape):
+            raise ValueError("w, grad_out and grad_in shapes differ")
+        arr[i] = orth_vjp_mat(w.data_ptr(), go.data_ptr(), gi.data_ptr(), w.shape[0], w.shape[1], _ld(w), _ld(go),
+                              _ld(gi))
+    return arr
+
+
+def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, prescale="frobenius", compute="f32",
+                                   status=None, workspace=None, stream=None):
+    """dL/dW into grads_in[i] for L depending on ws[i] through
+    orth_orthogonalize_batched with the same options, given grads_out[i] =
+    dL/d(output) (see include/orth.h).  grads_in share the dtype of ws,
+    grads_out that of the forward outputs.  Returns the workspace tensor."""
+    if len(ws) != len(grads_out) or len(ws) != len(grads_in):
+        raise ValueError("ws, grads_out and grads_in must have the same length")
+    for w, gi in zip(ws, grads_in):
+        if w.dtype != gi.dtype:
+            raise TypeError("grads_in must have the dtype of ws")
+    mats = _vjp_mats(ws, grads_out, grads_in)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute)
+    n = ctypes.c_size_t()
+    _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
+           "orth_orthogonalize_vjp_workspace_size")
+    device = ws[0].device if ws else torch.device("cuda")
+    wsp, nbytes = _workspace(n.value, device, workspace)
+    if status is not None and (status.dtype != torch.int32 or status.numel() < len(ws)):
+        raise ValueError("status must be an int32 tensor with one slot per matrix")
+    rc = lib().orth_orthogonalize_vjp_batched(mats, len(ws), ctypes.byref(opts),
+                                              wsp.data_ptr() if wsp is not None else None, nbytes,
+                                              status.data_ptr() if status is not None else None, _stream(stream))
+    _check(rc, "orth_orthogonalize_vjp_batched")
+    return wsp
+
+
+def orth_orthogonalize_vjp_workspace_size(ws, iters, beta=0.5, prescale="frobenius", compute="f32",
+                                          grads_out=None):
+    grads_out = ws if grads_out is None else grads_out
+    mats = _vjp_mats(ws, grads_out, ws)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute)
+    n = ctypes.c_size_t()
+    _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
+           "orth_orthogonalize_vjp_workspace_size")
+    return n.value
 
 
 def orth_aoc_param_shapes(cin, cout, k, stride=1, dilation=1, groups=1):

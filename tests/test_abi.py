@@ -163,3 +163,66 @@ def test_check_validation(L):
     assert L.orth_check_workspace_size(ctypes.byref(a), ctypes.byref(n)) == orth.ORTH_EINVAL  # 15 % 2
     a.height = 16
     assert L.orth_check_workspace_size(ctypes.byref(a), ctypes.byref(n)) == orth.ORTH_OK
+
+
+def _vjp_mats(shapes, alias=None):
+    arr = (orth.orth_vjp_mat * len(shapes))()
+    for i, (r, c) in enumerate(shapes):
+        w = 0x10000 + 0x1000000 * i
+        go = w + 0x400000
+        gi = {"grad_out": go, "w": w}.get(alias, w + 0x800000)
+        arr[i] = orth.orth_vjp_mat(w, go, gi, r, c, c, c, c)
+    return arr
+
+
+def _vjp_ws(L, shapes, iters=5, compute=0, dt=0, prescale=1, beta=0.5, alias=None):
+    opts = orth.orth_bjorck_opts(iters, beta, prescale, dt, dt, compute)
+    n = ctypes.c_size_t()
+    rc = L.orth_orthogonalize_vjp_workspace_size(_vjp_mats(shapes, alias), len(shapes), ctypes.byref(opts),
+                                                 ctypes.byref(n))
+    return rc, n.value
+
+
+def test_vjp_workspace_grows_with_saved_steps(L):
+    """The VJP keeps X_t and E_t of every step: fp32 products hold
+    T (M N + N^2) fp32 values beside a few fixed buffers, bf16 products
+    T (M N + N^2) bf16 values."""
+    rc, w5 = _vjp_ws(L, [(256, 128)], iters=5)
+    rc2, w10 = _vjp_ws(L, [(256, 128)], iters=10)
+    assert rc == rc2 == orth.ORTH_OK
+    assert w10 - w5 == pytest.approx(5 * (256 * 128 + 128 * 128) * 4, rel=0.01)
+    rc, b5 = _vjp_ws(L, [(2048, 1024)], iters=5, compute=1, dt=1)
+    rc2, b10 = _vjp_ws(L, [(2048, 1024)], iters=10, compute=1, dt=1)
+    assert rc == rc2 == orth.ORTH_OK
+    assert b10 - b5 == pytest.approx(5 * (2048 * 1024 + 1024 * 1024) * 2, rel=0.01)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(iters=-1), orth.ORTH_EINVAL),
+    (dict(iters=5000), orth.ORTH_EINVAL),
+    (dict(beta=0.7), orth.ORTH_EINVAL),
+    (dict(prescale=3), orth.ORTH_EINVAL),
+    (dict(compute=2), orth.ORTH_EINVAL),
+    (dict(alias="grad_out"), orth.ORTH_OK),
+    (dict(alias="w"), orth.ORTH_OK),
+    (dict(iters=0), orth.ORTH_OK),
+])
+def test_vjp_validation(L, kw, code):
+    rc, _ = _vjp_ws(L, [(64, 32), (16, 48)], **kw)
+    assert rc == code
+
+
+def test_vjp_rejects_bad_matrices(L):
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0)
+    n = ctypes.c_size_t()
+    arr = _vjp_mats([(8, 4)])
+    arr[0].grad_in = None
+    assert L.orth_orthogonalize_vjp_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
+    arr = _vjp_mats([(8, 4)])
+    arr[0].ld_grad_out = 3
+    assert L.orth_orthogonalize_vjp_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
+    # aliasing grad_out with a different dtype
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 1, 0, 0)
+    arr = _vjp_mats([(8, 4)], alias="grad_out")
+    assert L.orth_orthogonalize_vjp_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
+    assert b"alias" in L.orth_last_error()
