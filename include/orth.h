@@ -187,6 +187,37 @@ int orth_build_conv_kernels_workspace_size(const orth_conv_desc* descs, int32_t 
 int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n,
                                     int32_t dtype, void* workspace,
                                     size_t workspace_bytes, void* stream);
+/* One conv layer of a composition vector-Jacobian product. */
+typedef struct {
+  orth_conv_geom geom;
+  const void* rko;          /* device: the forward call's rko (orthogonalized factors) */
+  const void* proj;         /* device: the forward call's proj (may be NULL if n_proj == 0) */
+  const void* grad_kernel;  /* device: dL/dK, cout x (cin/g) x k x k (OIHW), contiguous */
+  void* grad_rko;           /* device: dL/d rko, g x rko_rows x rko_cols, contiguous */
+  void* grad_proj;          /* device: dL/d proj, g x n_proj x proj_rows x proj_cols,
+                               contiguous (ignored, may be NULL, if n_proj == 0) */
+} orth_conv_vjp_desc;
+
+/*
+ * Vector-Jacobian product of orth_build_conv_kernels_batched with respect to
+ * the factors: given dL/dK, the gradients with respect to the (already
+ * orthogonalized) RKO matrix and projector factors of every group.  Each ⊛
+ * step with a block of taps P, I - P is bilinear, so its adjoint sends the
+ * kernel gradient G to dT[a][b] = G[a][b] P + G[next] (I - P) and gives
+ * dP = sum_taps T^T (G[a][b] - G[next]), with "next" the neighbouring tap
+ * along the block's direction; P = V V^T gives dV = (dP + dP^T) V.  The
+ * forward taps are recomputed inside the call.  Chain with
+ * orth_orthogonalize_vjp_batched for the gradient with respect to the raw
+ * parameters.  dtype is the storage type of every tensor; arithmetic is fp32.
+ * Errors as orth_build_conv_kernels_batched.  grad_* must not overlap the
+ * inputs.
+ */
+int orth_build_conv_kernels_vjp_workspace_size(const orth_conv_vjp_desc* descs, int32_t n,
+                                               int32_t dtype, size_t* bytes);
+int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t n,
+                                        int32_t dtype, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
 /* Single-layer convenience form of orth_build_conv_kernels_batched. */
 int orth_build_conv_kernel(const void* rko, const void* proj, int32_t cin,
                            int32_t cout, int32_t k, int32_t stride,

@@ -42,7 +42,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
   for (int pair = 0; pair < 2; ++pair) {
     const int K = pair ? g->K2 : g->K;
     if (K <= 0) continue;
-    const int adt = pair ? ORTH_F32 : g->a_dtype, bdt = pair ? ORTH_F32 : g->b_dtype;
+    const int adt = g->a_dtype, bdt = g->b_dtype;   // the second pair is stored like the first
     const int atr = pair ? g->a2_trans : g->a_trans, btr = pair ? g->b2_trans : g->b_trans;
     const int64_t lda = pair ? g->lda2 : g->lda, ldb = pair ? g->ldb2 : g->ldb;
     const int esz_a = adt == ORTH_BF16 ? 2 : 4, esz_b = bdt == ORTH_BF16 ? 2 : 4;
@@ -142,10 +142,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
   float* C = static_cast<float*>(g->C) + g->c_step * st;
   const int64_t ldc = g->ldc;
   if (epi == EPI_STORE) {
+    const int cdt = g->c_dtype;
+    void* Cv = static_cast<char*>(g->C) + g->c_step * st * (cdt == ORTH_BF16 ? 2 : 4);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = ibase + acc_row(r, lane);
-      if (i < M) C[(int64_t)i * ldc + j] = acc[r];
+      if (i < M) store_from_f32(Cv, (int64_t)i * ldc + j, cdt, acc[r]);
     }
   } else if (epi == EPI_GRAM_E) {
     const bool mirror = g->mirror != 0;

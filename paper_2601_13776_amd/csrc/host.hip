@@ -653,6 +653,254 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
 }
 }  // namespace
 
+// ----------------------------------------------- composition VJP plan ---
+// Per group: the forward taps T_q (input of block step q) are recomputed in
+// compact grids and kept; the gradient G runs back through the steps with
+// Z = G P_q, the adjoint combine (dT and D) and dP_q = sum T_q^T D; finally
+// dV_q = (dP_q + dP_q^T) V_q and the RKO gradient is read off the s x s taps.
+// Steps are aligned across groups as in the forward plan (horizontal blocks
+// at global steps 0.., vertical ones after the longest horizontal run).
+namespace {
+struct ConvVjpPlan {
+  std::vector<GemmItem> proj_items, last_dp, dv_items;
+  std::vector<std::vector<GemmItem>> fwd_gemm, bwd_gemm;
+  std::vector<std::vector<TapItem>> fwd_comb, bwd_comb;
+  std::vector<TapItem> rko_taps, grad_taps, rko_grad;
+  std::vector<int64_t> fwd_max, bwd_max;
+  int64_t rko_max = 0, grad_max = 0;
+  size_t off_proj = 0, off_last_dp = 0, off_dv = 0, off_rko_taps = 0, off_grad_taps = 0, off_rko_grad = 0;
+  std::vector<size_t> off_fwd_gemm, off_bwd_gemm, off_fwd_comb, off_bwd_comb;
+  size_t table_bytes = 0, total_bytes = 0;
+};
+
+int validate_conv_vjp_descs(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !d) return fail(ORTH_EINVAL, "descs is NULL");
+  if (dtype != ORTH_F32 && dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+  for (int i = 0; i < n; ++i) {
+    const int rc = validate_geom(&d[i].geom);
+    if (rc) return rc;
+    const int nproj = 2 * (d[i].geom.k - d[i].geom.stride);
+    if (!d[i].rko || !d[i].grad_kernel || !d[i].grad_rko || (nproj > 0 && (!d[i].proj || !d[i].grad_proj)))
+      return fail(ORTH_EINVAL, "NULL conv data pointer");
+  }
+  return ORTH_OK;
+}
+
+// tiles of an M x N output for the fp32 tile GEMM
+void gemm_tiles(const GemmItem& proto, std::vector<GemmItem>& out) {
+  for (int a = 0; a < (proto.M + 63) / 64; ++a)
+    for (int b = 0; b < (proto.N + 63) / 64; ++b) {
+      GemmItem g = proto;
+      g.ti = a;
+      g.tj = b;
+      out.push_back(g);
+    }
+}
+
+void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, ConvVjpPlan& P,
+                         unsigned char* ws) {
+  const size_t esz = dtype == ORTH_BF16 ? 2 : 4;
+  int max_kp = 1;
+  for (int i = 0; i < n; ++i) max_kp = std::max(max_kp, d[i].geom.k - d[i].geom.stride + 1);
+  const int n_phase = 2 * (max_kp - 1);
+  P.fwd_gemm.assign(n_phase, {});
+  P.bwd_gemm.assign(n_phase, {});
+  P.fwd_comb.assign(n_phase, {});
+  P.bwd_comb.assign(n_phase, {});
+  P.fwd_max.assign(n_phase, 0);
+  P.bwd_max.assign(n_phase, 0);
+
+  // Two passes: the first (ws == nullptr inside) only counts table entries;
+  // buffers follow the tables, so table sizes must be known first.
+  for (int pass = 0; pass < 2; ++pass) {
+    Arena A;
+    if (pass == 1) {
+      P.off_proj = A.take(sizeof(GemmItem) * P.proj_items.size());
+      P.off_last_dp = A.take(sizeof(GemmItem) * P.last_dp.size());
+      P.off_dv = A.take(sizeof(GemmItem) * P.dv_items.size());
+      P.off_rko_taps = A.take(sizeof(TapItem) * P.rko_taps.size());
+      P.off_grad_taps = A.take(sizeof(TapItem) * P.grad_taps.size());
+      P.off_rko_grad = A.take(sizeof(TapItem) * P.rko_grad.size());
+      P.off_fwd_gemm.resize(n_phase);
+      P.off_bwd_gemm.resize(n_phase);
+      P.off_fwd_comb.resize(n_phase);
+      P.off_bwd_comb.resize(n_phase);
+      for (int ph = 0; ph < n_phase; ++ph) {
+        P.off_fwd_gemm[ph] = A.take(sizeof(GemmItem) * P.fwd_gemm[ph].size());
+        P.off_bwd_gemm[ph] = A.take(sizeof(GemmItem) * P.bwd_gemm[ph].size());
+        P.off_fwd_comb[ph] = A.take(sizeof(TapItem) * P.fwd_comb[ph].size());
+        P.off_bwd_comb[ph] = A.take(sizeof(TapItem) * P.bwd_comb[ph].size());
+      }
+      P.table_bytes = align_up(A.off);
+      P.proj_items.clear();
+      P.last_dp.clear();
+      P.dv_items.clear();
+      P.rko_taps.clear();
+      P.grad_taps.clear();
+      P.rko_grad.clear();
+      for (int ph = 0; ph < n_phase; ++ph) {
+        P.fwd_gemm[ph].clear();
+        P.bwd_gemm[ph].clear();
+        P.fwd_comb[ph].clear();
+        P.bwd_comb[ph].clear();
+      }
+    }
+    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 && ws) ? ws + off : nullptr; };
+    auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
+
+    for (int li = 0; li < n; ++li) {
+      const orth_conv_vjp_desc& L = d[li];
+      const orth_conv_geom& g = L.geom;
+      const int c = g.cin / g.groups, og = g.cout / g.groups, s = g.stride, k = g.k, kp = k - s + 1;
+      const int h = c / 2, nq = 2 * (kp - 1);
+      const int64_t tap = (int64_t)og * c;
+      auto in_grid = [&](int q, int& gh, int& gw, int& v) {
+        v = q >= kp - 1;
+        gh = v ? s + (q - (kp - 1)) : s;
+        gw = v ? k : s + q;
+      };
+      auto gphase = [&](int q) { return q < kp - 1 ? q : (max_kp - 1) + (q - (kp - 1)); };
+      for (int grp = 0; grp < g.groups; ++grp) {
+        const unsigned char* rko = static_cast<const unsigned char*>(L.rko) + (size_t)grp * og * c * s * s * esz;
+        const unsigned char* proj =
+            nq ? static_cast<const unsigned char*>(L.proj) + (size_t)grp * nq * c * h * esz : nullptr;
+        const unsigned char* gk =
+            static_cast<const unsigned char*>(L.grad_kernel) + (size_t)grp * og * c * k * k * esz;
+        unsigned char* grko = static_cast<unsigned char*>(L.grad_rko) + (size_t)grp * og * c * s * s * esz;
+        unsigned char* gproj = nq ? static_cast<unsigned char*>(L.grad_proj) + (size_t)grp * nq * c * h * esz : nullptr;
+        // buffers
+        std::vector<float*> Ts(std::max(nq, 1));
+        int64_t max_in = s * s;
+        for (int q = 0; q < std::max(nq, 1); ++q) {
+          int gh = s, gw = s, v = 0;
+          if (nq) in_grid(q, gh, gw, v);
+          Ts[q] = fbuf((int64_t)gh * gw * tap);
+          max_in = std::max<int64_t>(max_in, (int64_t)gh * gw);
+        }
+        float* Y = nq > 1 ? fbuf(max_in * tap) : nullptr;
+        float* G[2] = {fbuf((int64_t)k * k * tap), fbuf((int64_t)k * k * tap)};
+        float* Z = nq ? fbuf((int64_t)k * k * tap) : nullptr;
+        float* D = nq ? fbuf(max_in * tap) : nullptr;
+        float* Pm = nq ? fbuf((int64_t)nq * c * c) : nullptr;
+        float* dP = nq ? fbuf((int64_t)nq * c * c) : nullptr;
+
+        // forward recomputation
+        P.rko_taps.push_back(TapItem{rko, nullptr, Ts[0], nullptr, og, c, s, s, 0, 0});
+        P.rko_max = std::max<int64_t>(P.rko_max, (int64_t)s * s * tap);
+        for (int j = 0; j < nq; ++j) {
+          GemmItem gi{};
+          gi.A = proj + (size_t)j * c * h * esz;
+          gi.B = gi.A;
+          gi.C = Pm + (size_t)j * c * c;
+          gi.lda = gi.ldb = h;
+          gi.ldc = c;
+          gi.M = gi.N = c;
+          gi.K = h;
+          gi.a_dtype = gi.b_dtype = dtype;
+          gi.epi = EPI_STORE;
+          gemm_tiles(gi, P.proj_items);
+        }
+        for (int q = 0; q + 1 < nq; ++q) {
+          int gh, gw, v;
+          in_grid(q, gh, gw, v);
+          const int ph = gphase(q);
+          GemmItem gi{};
+          gi.A = Ts[q];
+          gi.B = Pm + (size_t)q * c * c;
+          gi.C = Y;
+          gi.lda = gi.ldb = gi.ldc = c;
+          gi.M = gh * gw * og;
+          gi.N = c;
+          gi.K = c;
+          gi.epi = EPI_STORE;
+          gemm_tiles(gi, P.fwd_gemm[ph]);
+          P.fwd_comb[ph].push_back(TapItem{Ts[q], Y, Ts[q + 1], nullptr, og, c, gh, gw, v, 0});
+          P.fwd_max[ph] = std::max<int64_t>(P.fwd_max[ph], (int64_t)(gh + v) * (gw + 1 - v) * tap);
+        }
+        // gradient, last step first
+        int cur = 0;
+        P.grad_taps.push_back(TapItem{gk, nullptr, G[0], nullptr, og, c, k, k, 0, 0});
+        P.grad_max = std::max<int64_t>(P.grad_max, (int64_t)k * k * tap);
+        for (int q = nq - 1; q >= 0; --q) {
+          int gh, gw, v;
+          in_grid(q, gh, gw, v);
+          const int ph = gphase(q);
+          GemmItem gi{};
+          gi.A = G[cur];
+          gi.B = Pm + (size_t)q * c * c;
+          gi.C = Z;
+          gi.lda = gi.ldb = gi.ldc = c;
+          gi.M = (gh + v) * (gw + 1 - v) * og;
+          gi.N = c;
+          gi.K = c;
+          gi.epi = EPI_STORE;
+          gemm_tiles(gi, P.bwd_gemm[ph]);
+          if (q + 1 < nq) {   // dP of the step above, whose D is still in place
+            int h1, w1, v1;
+            in_grid(q + 1, h1, w1, v1);
+            GemmItem gd{};
+            gd.A = Ts[q + 1];
+            gd.B = D;
+            gd.a_trans = gd.b_trans = 1;
+            gd.lda = gd.ldb = c;
+            gd.K = h1 * w1 * og;
+            gd.M = gd.N = c;
+            gd.C = dP + (size_t)(q + 1) * c * c;
+            gd.ldc = c;
+            gd.epi = EPI_STORE;
+            gemm_tiles(gd, P.bwd_gemm[ph]);
+          }
+          P.bwd_comb[ph].push_back(TapItem{G[cur], Z, G[cur ^ 1], D, og, c, gh, gw, v, 0});
+          P.bwd_max[ph] = std::max<int64_t>(P.bwd_max[ph], (int64_t)gh * gw * tap);
+          cur ^= 1;
+        }
+        if (nq) {
+          GemmItem gd{};
+          gd.A = Ts[0];
+          gd.B = D;
+          gd.a_trans = gd.b_trans = 1;
+          gd.lda = gd.ldb = c;
+          gd.K = s * s * og;
+          gd.M = gd.N = c;
+          gd.C = dP;
+          gd.ldc = c;
+          gd.epi = EPI_STORE;
+          gemm_tiles(gd, P.last_dp);
+        }
+        for (int j = 0; j < nq; ++j) {
+          GemmItem gv{};
+          gv.A = dP + (size_t)j * c * c;
+          gv.lda = c;
+          gv.B = proj + (size_t)j * c * h * esz;
+          gv.b_trans = 1;
+          gv.ldb = h;
+          gv.K = c;
+          gv.A2 = gv.A;
+          gv.a2_trans = 1;
+          gv.lda2 = c;
+          gv.B2 = gv.B;
+          gv.b2_trans = 1;
+          gv.ldb2 = h;
+          gv.K2 = c;
+          gv.M = c;
+          gv.N = h;
+          gv.a_dtype = ORTH_F32;
+          gv.b_dtype = dtype;
+          gv.C = gproj + (size_t)j * c * h * esz;
+          gv.ldc = h;
+          gv.c_dtype = dtype;
+          gv.epi = EPI_STORE;
+          gemm_tiles(gv, P.dv_items);
+        }
+        P.rko_grad.push_back(TapItem{G[cur], nullptr, grko, nullptr, og, c, s, s, 0, 0});
+      }
+    }
+    P.total_bytes = align_up(A.off);
+  }
+}
+}  // namespace
+
 // ------------------------------------------------ Björck VJP planning ---
 // The vector-Jacobian product recomputes the forward iterates, saving every
 // X_t and E_t = I - X_t^T X_t (step after step in the workspace), then runs
@@ -1197,6 +1445,66 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
                                     (int)P.phase_comb[ph].size(), P.phase_max_elems[ph], s));
   }
   ORTH_HIP(launch_compose_scatter(G, ng, dtype, P.scatter_max, s));
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernels_vjp_workspace_size(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype,
+                                               size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  const int rc = validate_conv_vjp_descs(descs, n, dtype);
+  if (rc) return rc;
+  ConvVjpPlan P;
+  build_conv_vjp_plan(descs, n, dtype, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  int rc = validate_conv_vjp_descs(descs, n, dtype);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  ConvVjpPlan P;
+  build_conv_vjp_plan(descs, n, dtype, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = ConvVjpPlan();
+  build_conv_vjp_plan(descs, n, dtype, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n_phase = (int)P.fwd_gemm.size();
+
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_proj, P.proj_items);
+  put(img, P.off_last_dp, P.last_dp);
+  put(img, P.off_dv, P.dv_items);
+  put(img, P.off_rko_taps, P.rko_taps);
+  put(img, P.off_grad_taps, P.grad_taps);
+  put(img, P.off_rko_grad, P.rko_grad);
+  for (int ph = 0; ph < n_phase; ++ph) {
+    put(img, P.off_fwd_gemm[ph], P.fwd_gemm[ph]);
+    put(img, P.off_bwd_gemm[ph], P.bwd_gemm[ph]);
+    put(img, P.off_fwd_comb[ph], P.fwd_comb[ph]);
+    put(img, P.off_bwd_comb[ph], P.bwd_comb[ph]);
+  }
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+  auto GI = [&](size_t off) { return reinterpret_cast<const GemmItem*>(ws + off); };
+  auto TI = [&](size_t off) { return reinterpret_cast<const TapItem*>(ws + off); };
+  ORTH_HIP(launch_tap_items(0, TI(P.off_rko_taps), (int)P.rko_taps.size(), dtype, P.rko_max, s));
+  ORTH_HIP(launch_gemm_f32(GI(P.off_proj), (int)P.proj_items.size(), "conv_vjp_projector", s));
+  for (int ph = 0; ph < n_phase; ++ph) {
+    ORTH_HIP(launch_gemm_f32(GI(P.off_fwd_gemm[ph]), (int)P.fwd_gemm[ph].size(), "conv_vjp_tap_gemm", s));
+    ORTH_HIP(launch_tap_items(3, TI(P.off_fwd_comb[ph]), (int)P.fwd_comb[ph].size(), dtype, P.fwd_max[ph], s));
+  }
+  ORTH_HIP(launch_tap_items(1, TI(P.off_grad_taps), (int)P.grad_taps.size(), dtype, P.grad_max, s));
+  for (int ph = n_phase - 1; ph >= 0; --ph) {
+    ORTH_HIP(launch_gemm_f32(GI(P.off_bwd_gemm[ph]), (int)P.bwd_gemm[ph].size(), "conv_vjp_tap_gemm", s));
+    ORTH_HIP(launch_tap_items(4, TI(P.off_bwd_comb[ph]), (int)P.bwd_comb[ph].size(), dtype, P.bwd_max[ph], s));
+  }
+  ORTH_HIP(launch_gemm_f32(GI(P.off_last_dp), (int)P.last_dp.size(), "conv_vjp_tap_gemm", s));
+  ORTH_HIP(launch_gemm_f32(GI(P.off_dv), (int)P.dv_items.size(), "conv_vjp_factor_grad", s));
+  ORTH_HIP(launch_tap_items(2, TI(P.off_rko_grad), (int)P.rko_grad.size(), dtype, P.rko_max, s));
   return ORTH_OK;
 }
 

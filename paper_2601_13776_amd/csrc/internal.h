@@ -115,13 +115,13 @@ struct GemmItem {
   int64_t a_step, b_step, a2_step, b2_step, c_step, src_step;
   int32_t M, N, K, K2;
   int32_t ti, tj;
-  int32_t a_dtype, b_dtype;  // storage of A and B (A2 and B2 are fp32)
+  int32_t a_dtype, b_dtype;  // storage of A and A2, of B and B2
   int32_t a_trans, b_trans;  // 0: row-major [M][K]; 1: stored [K][M]
   int32_t a2_trans, b2_trans;
   int32_t epi;
   int32_t mirror;
   float beta;
-  int32_t pad;
+  int32_t c_dtype;           // EPI_STORE: storage of C
 };
 
 // Compose (AOC) descriptors: one entry per (layer, group).
@@ -144,6 +144,20 @@ struct CombineItem {
   int32_t vertical;          // 0: horizontal block, 1: vertical block
   int32_t in_h, in_w;        // tap grid before the step
   int32_t src;               // taps[src] is read, taps[src ^ 1] written
+  int32_t pad;
+};
+
+// One elementwise work item of the composition's vector-Jacobian product.
+// Tap grids are compact: tap (a, b) of an h x w grid is the og x c matrix at
+// element offset (a w + b) og c.
+struct TapItem {
+  const void* a;             // first source (see the kernel using the item)
+  const void* b;             // second source
+  void* out;
+  void* out2;
+  int32_t og, c;             // tap matrix shape
+  int32_t h, w;              // grid of the tap buffer the item is defined on
+  int32_t vertical;          // block direction of a combine step
   int32_t pad;
 };
 
@@ -187,6 +201,10 @@ hipError_t launch_compose_combine(const ComposeGroup* groups, const CombineItem*
 hipError_t launch_compose_scatter(const ComposeGroup* groups, int n_groups, int dtype,
                                   int64_t max_elems, hipStream_t s);
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+// kind: 0 taps from the RKO matrix, 1 taps from an OIHW kernel gradient,
+// 2 RKO gradient from taps, 3 forward combine, 4 adjoint combine
+hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dtype, int64_t max_elems,
+                            hipStream_t s);
 hipError_t launch_conv_check(const orth_check_args* a, const void* kernel, const float* x,
                              double* partial, float* out, int adjoint, hipStream_t s);
 

@@ -24,6 +24,7 @@ EXPORTED = [
     "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched",
     "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
+    "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
     "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
 ]
@@ -62,6 +63,11 @@ class orth_conv_desc(ctypes.Structure):
                 ("kernel", ctypes.c_void_p)]
 
 
+class orth_conv_vjp_desc(ctypes.Structure):
+    _fields_ = [("geom", orth_conv_geom), ("rko", ctypes.c_void_p), ("proj", ctypes.c_void_p),
+                ("grad_kernel", ctypes.c_void_p), ("grad_rko", ctypes.c_void_p), ("grad_proj", ctypes.c_void_p)]
+
+
 class orth_check_args(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("mats", ctypes.POINTER(orth_mat)), ("n_mats", ctypes.c_int32),
                 ("mat_dtype", ctypes.c_int32), ("kernel", ctypes.c_void_p), ("kernel_dtype", ctypes.c_int32),
@@ -86,6 +92,8 @@ def lib():
         L.orth_build_conv_kernels_workspace_size.argtypes = [P(orth_conv_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_batched.argtypes = [P(orth_conv_desc), i32, i32, vp, sz, vp]
         L.orth_build_conv_kernel.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp, sz, vp]
+        L.orth_build_conv_kernels_vjp_workspace_size.argtypes = [P(orth_conv_vjp_desc), i32, i32, P(sz)]
+        L.orth_build_conv_kernels_vjp_batched.argtypes = [P(orth_conv_vjp_desc), i32, i32, vp, sz, vp]
         L.orth_check_workspace_size.argtypes = [P(orth_check_args), P(sz)]
         L.orth_check_norm.argtypes = [P(orth_check_args), vp, vp, sz, vp]
         L.orth_status_string.argtypes = [ctypes.c_int]
@@ -277,6 +285,32 @@ def orth_build_conv_kernel(rko, proj, cin, cout, k, stride, dilation, groups, ke
     return orth_build_conv_kernels_batched(
         [dict(geom=(cin, cout, k, stride, dilation, groups), rko=rko, proj=proj, kernel=kernel_out)],
         workspace, stream)
+
+
+def orth_build_conv_kernels_vjp_batched(layers, workspace=None, stream=None):
+    """layers: list of dicts with geom, rko, proj (or None), grad_kernel,
+    grad_rko and grad_proj (or None) tensors (contiguous, one dtype).
+    Writes dL/d rko and dL/d proj given dL/d kernel."""
+    if not layers:
+        return None
+    dt = _dtype_code(layers[0]["grad_kernel"])
+    arr = (orth_conv_vjp_desc * len(layers))()
+    for i, L in enumerate(layers):
+        for key in ("rko", "proj", "grad_kernel", "grad_rko", "grad_proj"):
+            t = L.get(key)
+            if t is not None and (not t.is_contiguous() or _dtype_code(t) != dt):
+                raise ValueError(f"{key} must be contiguous and of one dtype")
+        ptr = lambda key: L[key].data_ptr() if L.get(key) is not None else None
+        arr[i] = orth_conv_vjp_desc(orth_conv_geom(*L["geom"]), ptr("rko"), ptr("proj"), ptr("grad_kernel"),
+                                    ptr("grad_rko"), ptr("grad_proj"))
+    n = ctypes.c_size_t()
+    _check(lib().orth_build_conv_kernels_vjp_workspace_size(arr, len(layers), dt, ctypes.byref(n)),
+           "orth_build_conv_kernels_vjp_workspace_size")
+    ws, nbytes = _workspace(n.value, layers[0]["grad_kernel"].device, workspace)
+    rc = lib().orth_build_conv_kernels_vjp_batched(arr, len(layers), dt, ws.data_ptr() if ws is not None else None,
+                                                   nbytes, _stream(stream))
+    _check(rc, "orth_build_conv_kernels_vjp_batched")
+    return ws
 
 
 def _check_call(args, out, workspace, stream):

@@ -226,3 +226,18 @@ def test_vjp_rejects_bad_matrices(L):
     arr = _vjp_mats([(8, 4)], alias="grad_out")
     assert L.orth_orthogonalize_vjp_workspace_size(arr, 1, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_EINVAL
     assert b"alias" in L.orth_last_error()
+
+
+def test_conv_vjp_validation(L):
+    n = ctypes.c_size_t()
+    arr = (orth.orth_conv_vjp_desc * 1)()
+    arr[0] = orth.orth_conv_vjp_desc(orth.orth_conv_geom(16, 16, 3, 1, 1, 1), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000)
+    assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_OK
+    assert n.value > 0
+    arr[0].grad_proj = None
+    assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_EINVAL
+    # k == s needs no projector gradient
+    arr[0] = orth.orth_conv_vjp_desc(orth.orth_conv_geom(16, 32, 2, 2, 1, 1), 0x1000, None, 0x3000, 0x4000, None)
+    assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_OK
+    arr[0] = orth.orth_conv_vjp_desc(orth.orth_conv_geom(16, 16, 1, 2, 1, 1), 0x1000, None, 0x3000, 0x4000, None)
+    assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_EUNSUPPORTED

@@ -156,3 +156,111 @@ def test_vjp_aliasing_and_strides(alias):
     torch.cuda.synchronize()
     for o, ref, shape in zip(gis, refs, shapes):
         assert checks.relative_difference(to_f64(o), ref) <= REL_F32, shape
+
+
+# ------------------------------------------------- composition VJP ---
+from oracle import aoc, aoc_grad, bjorck  # noqa: E402
+
+CONV_GEOMS = [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (128, 512, 2, 2, 1, 1), (32, 32, 3, 1, 1, 4),
+              (32, 32, 3, 1, 2, 1), (8, 8, 1, 1, 1, 1), (6, 6, 5, 2, 3, 3), (24, 16, 4, 2, 1, 2),
+              (4, 6, 3, 1, 1, 1), (100, 70, 3, 1, 1, 1)]
+
+
+def conv_factors(geom, seed, iters=40):
+    rr, rc, npj, pr, pc = aoc.param_shapes(*geom)
+    g = geom[5]
+    rng = np.random.default_rng(seed)
+    rko = np.stack([bjorck.bjorck(rng.standard_normal((rr, rc)), iters) for _ in range(g)]).astype(np.float32)
+    proj = None
+    if npj:
+        proj = np.stack([np.stack([bjorck.bjorck(rng.standard_normal((pr, pc)), iters) for _ in range(npj)])
+                         for _ in range(g)]).astype(np.float32)
+    cin, cout, k = geom[0], geom[1], geom[2]
+    dk = rng.standard_normal((cout, cin // g, k, k)).astype(np.float32)
+    return rko, proj, dk
+
+
+def conv_vjp_gpu(items, dtype=torch.float32):
+    layers = []
+    for geom, rko, proj, dk in items:
+        t = lambda a: torch.from_numpy(a).to(DEV).to(dtype).contiguous()
+        layers.append(dict(geom=geom, rko=t(rko), proj=t(proj) if proj is not None else None, grad_kernel=t(dk),
+                           grad_rko=torch.full(rko.shape, float("nan"), dtype=dtype, device=DEV),
+                           grad_proj=torch.full(proj.shape, float("nan"), dtype=dtype, device=DEV)
+                           if proj is not None else None))
+    orth.orth_build_conv_kernels_vjp_batched(layers)
+    torch.cuda.synchronize()
+    return layers
+
+
+def test_conv_vjp_parity_batched():
+    """Every geometry in one batched call (mixed k, stride, groups)."""
+    items = [(geom, *conv_factors(geom, 300 + i)) for i, geom in enumerate(CONV_GEOMS)]
+    layers = conv_vjp_gpu(items)
+    for (geom, rko, proj, dk), L in zip(items, layers):
+        ref_r, ref_p = aoc_grad.aoc_kernel_vjp(rko.astype(np.float64),
+                                               None if proj is None else proj.astype(np.float64), *geom,
+                                               dk.astype(np.float64))
+        assert checks.relative_difference(to_f64(L["grad_rko"]), ref_r) <= REL_F32, geom
+        if proj is not None:
+            assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= REL_F32, geom
+
+
+@pytest.mark.parametrize("geom", [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (6, 6, 5, 2, 3, 3)])
+def test_conv_vjp_parity_single(geom):
+    rko, proj, dk = conv_factors(geom, 400)
+    L = conv_vjp_gpu([(geom, rko, proj, dk)])[0]
+    ref_r, ref_p = aoc_grad.aoc_kernel_vjp(rko.astype(np.float64), None if proj is None else proj.astype(np.float64),
+                                           *geom, dk.astype(np.float64))
+    assert checks.relative_difference(to_f64(L["grad_rko"]), ref_r) <= REL_F32
+    if proj is not None:
+        assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= REL_F32
+
+
+def test_conv_vjp_bf16_storage():
+    """bf16 storage of factors, kernel gradient and outputs (fp32 arithmetic):
+    the oracle sees the bf16-rounded inputs; the outputs are rounded once
+    (u = 2^-9), bound 1e-2."""
+    geoms = [(64, 64, 3, 1, 1, 1), (32, 64, 4, 2, 1, 2)]
+    items = []
+    for i, geom in enumerate(geoms):
+        rko, proj, dk = conv_factors(geom, 500 + i)
+        r16 = lambda a: torch.from_numpy(a).to(torch.bfloat16).float().numpy()
+        items.append((geom, r16(rko), r16(proj), r16(dk)))
+    layers = conv_vjp_gpu(items, torch.bfloat16)
+    for (geom, rko, proj, dk), L in zip(items, layers):
+        ref_r, ref_p = aoc_grad.aoc_kernel_vjp(rko.astype(np.float64), proj.astype(np.float64), *geom,
+                                               dk.astype(np.float64))
+        assert checks.relative_difference(to_f64(L["grad_rko"]), ref_r) <= 1e-2
+        assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= 1e-2
+
+
+def test_layer_vjp_chain():
+    """Raw parameters -> kernel gradient -> raw-parameter gradients, all on
+    the GPU (Björck forward, composition VJP, Björck VJP), against the
+    oracle's whole-layer VJP."""
+    geom, iters = (32, 32, 3, 1, 1, 2), 15
+    cin, cout, k, s, d, g = geom
+    rr, rc, npj, pr, pc = aoc.param_shapes(*geom)
+    rng = np.random.default_rng(600)
+    raw_rko = rng.standard_normal((g, rr, rc)).astype(np.float32)
+    raw_proj = rng.standard_normal((g, npj, pr, pc)).astype(np.float32)
+    dk = rng.standard_normal((cout, cin // g, k, k)).astype(np.float32)
+    raws = [torch.from_numpy(m).to(DEV) for m in list(raw_rko) + list(raw_proj.reshape(-1, pr, pc))]
+    outs = [torch.empty_like(t) for t in raws]
+    orth.orth_orthogonalize_batched(raws, outs, iters)
+    rko = torch.stack(outs[:g]).contiguous()
+    proj = torch.stack(outs[g:]).reshape(g, npj, pr, pc).contiguous()
+    L = dict(geom=geom, rko=rko, proj=proj, grad_kernel=torch.from_numpy(dk).to(DEV),
+             grad_rko=torch.empty_like(rko), grad_proj=torch.empty_like(proj))
+    orth.orth_build_conv_kernels_vjp_batched([L])
+    gouts = list(L["grad_rko"]) + list(L["grad_proj"].reshape(-1, pr, pc))
+    gins = [torch.empty_like(t) for t in raws]
+    orth.orth_orthogonalize_vjp_batched(raws, [t.contiguous() for t in gouts], gins, iters)
+    torch.cuda.synchronize()
+    ref_r, ref_p = aoc_grad.aoc_layer_vjp(raw_rko.astype(np.float64), raw_proj.astype(np.float64), *geom, iters,
+                                          dk.astype(np.float64))
+    got_r = np.stack([to_f64(t) for t in gins[:g]])
+    got_p = np.stack([to_f64(t) for t in gins[g:]]).reshape(ref_p.shape)
+    assert checks.relative_difference(got_r, ref_r) <= REL_F32
+    assert checks.relative_difference(got_p, ref_p) <= REL_F32
