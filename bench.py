@@ -6,7 +6,10 @@ A step orthogonalizes every free matrix of a workload in one batched call
 already resident in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline] [--copy-calibration]
+                    [--no-cpu-baseline] [--vjp [--vjp-steps K]] [--copy-calibration]
+
+With --vjp the backward pass (dL/dK and dL/d(output) back to the raw
+parameters) is timed too and reported under "vjp".
 """
 
 import argparse
@@ -78,9 +81,9 @@ def allocate_outputs(w, ins, torch, dev, out_dtype):
     return outs, layers
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bjorck_bf16_256_stress_4096x64_32x4096.md")
+# traffic records: profiles/traffic_<kernel>_<workload>.md
 # the traffic depends on the kernel and on the tile order the host planner builds
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2601_13776_amd", "csrc", f) for f in ("bjorck_bf16.hip", "host.hip")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2601_13776_amd", "csrc", f) for f in ("bjorck_bf16.hip", "tile_order.h")]
 
 
 def measured_traffic(kernel_name, workload):
@@ -90,9 +93,10 @@ def measured_traffic(kernel_name, workload):
     since."""
     import hashlib
     import re
-    if not os.path.exists(TRAFFIC_FILE):
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_name}_{workload}.md")
+    if not os.path.exists(path):
         return None
-    text = open(TRAFFIC_FILE).read()
+    text = open(path).read()
     fields = dict(re.findall(r"^- (\w+): (\S+)$", text, flags=re.M))
     try:
         h = hashlib.sha256()
@@ -122,6 +126,151 @@ def class_flops(w, kernel_name):
                 continue
         out += 4 * m * n * n * w.iters
     return out
+
+
+def vjp_flops(w):
+    """Algorithmic flops of one vector-Jacobian product of the whole
+    workload: the forward recomputation (a Gram and an update product per
+    step, the last update skipped: (4T - 2) m n^2) and the gradient
+    recurrence (X^T Y, Y E and X S per step: 6 T m n^2)."""
+    out = 0
+    for r, c in w.matrix_shapes():
+        m, n = max(r, c), min(r, c)
+        out += (10 * w.iters - 2) * m * n * n
+    return out
+
+
+def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, dev):
+    """Time steps of the backward pass: dL/dK -> factor gradients for every
+    conv layer (composition VJP), then dL/d(factor) -> dL/d(raw parameter)
+    for every matrix (Björck VJP).  Upstream gradients are seeded N(0, 1)."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 200)
+    gouts = [torch.randn(o.shape, generator=gen, device=dev, dtype=torch.float32) for o in outs]
+    gins = [torch.empty_like(t) for t in ins]
+    vlayers = []
+    for L in layers:
+        gk = torch.randn(L["kernel"].shape, generator=gen, device=dev, dtype=L["kernel"].dtype)
+        vlayers.append(dict(geom=L["geom"], rko=L["rko"], proj=L["proj"], grad_kernel=gk,
+                            grad_rko=torch.empty_like(L["rko"]),
+                            grad_proj=torch.empty_like(L["proj"]) if L["proj"] is not None else None))
+    # the conv factors' upstream gradients are the composition VJP's outputs
+    k = 0
+    for layer, (a, b) in zip(w.layers, wl.layer_matrix_ranges(w)):
+        if not isinstance(layer, wl.ConvLayer):
+            continue
+        V = vlayers[k]
+        k += 1
+        per = 1 + layer.n_proj
+        for j in range(layer.groups):
+            gouts[a + j * per] = V["grad_rko"][j]
+            for t in range(layer.n_proj):
+                gouts[a + j * per + 1 + t] = V["grad_proj"][j, t]
+    bws = orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, compute=compute, status=status)
+    cws = orth.orth_build_conv_kernels_vjp_batched(vlayers) if vlayers else None
+    torch.cuda.synchronize()
+    log(f"[bench] vjp workspace {bws.numel() / 2**30:.2f} GiB")
+
+    def vstep():
+        if vlayers:
+            orth.orth_build_conv_kernels_vjp_batched(vlayers, workspace=cws)
+        orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, compute=compute, status=status,
+                                            workspace=bws)
+
+    for i in range(warmup):
+        vstep()
+        torch.cuda.synchronize()
+        log(f"[bench] vjp warmup {i + 1}/{warmup}")
+    orth.orth_timing_enable(True)
+    orth.orth_timing_reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        vstep()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"[bench] vjp timed {steps} steps")
+    names = orth.orth_timing_names()
+    kt = {n: orth.orth_timing_read(n) for n in names}
+    orth.orth_timing_enable(False)
+    ms = (t1 - t0) * 1e3 / steps
+    flops = vjp_flops(w)
+    gemm_ms = sum(kt[n][0] for n in names if n.startswith(("bjorck_", "vjp_fwd_", "vjp_s_", "vjp_update_")))
+    gemm_ms /= steps
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    # roofline of the dominant gradient-recurrence kernel: its class's
+    # algorithmic 6 m n^2 T flops per step over its measured time
+    cands = [n for n in names if n.startswith("bjorck_vjp_bf16") or n in ("vjp_s_f32", "vjp_update_f32")]
+    roof = None
+    if cands:
+        dom = max(cands, key=lambda n: kt[n][0])
+        tot_ms, launches = kt[dom]
+        cf_ = class_flops(w, dom[len("bjorck_vjp"):] if dom.startswith("bjorck_vjp") else "") * 6 // 4 * steps
+        if not dom.startswith("bjorck_vjp"):   # fp32: S and update launches timed apart, each half
+            cf_ = (vjp_class_flops_f32(w) * steps) // 2
+        ach = cf_ / (tot_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom, w.name),
+                "avg_launch_ms": round(tot_ms / launches, 4),
+                "algorithmic_flops_per_launch": int(cf_ / launches)}
+    return {"ms_per_step": round(ms, 3), "layers_per_s": round(w.n_layers / (ms / 1e3), 3),
+            "algorithmic_flops_per_step": flops,
+            "tflops_algorithmic": round(flops / (ms / 1e3) / 1e12, 1),
+            "gemm_tflops_algorithmic": round(flops / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms > 0 else None,
+            "gemm_pct_peak": round(100 * flops / (gemm_ms / 1e3) / 1e12 / peak, 2) if gemm_ms > 0 else None,
+            "kernel_ms_per_step": {n: round(kt[n][0] / steps, 4) for n in names},
+            "roofline": roof}
+
+
+def vjp_class_flops_f32(w):
+    """Gradient-recurrence flops (6 m n^2 T) of the matrices that run on the
+    fp32 tile GEMM (every matrix with fp32 products, the small bucket with
+    bf16 products)."""
+    out = 0
+    for r, c in w.matrix_shapes():
+        m, n = max(r, c), min(r, c)
+        if w.dtype == "bf16" and not (n <= 64 and m <= 128):
+            continue
+        out += 6 * m * n * n * w.iters
+    return out
+
+
+def vjp_cpu_baseline(w, budget_s=25.0):
+    """Time the float64 oracle VJP on a bounded sample: per shape, one matrix
+    (up to 64 for small shapes) at T = 2, scaled to the workload's T by the
+    (10 T - 2) algorithmic step count and to all matrices by count."""
+    from oracle import bjorck_grad
+    shapes = w.matrix_shapes()
+    by_shape = {}
+    for i, s in enumerate(shapes):
+        by_shape.setdefault(s, []).append(i)
+    rng = np.random.default_rng(7)
+    per_shape, desc = {}, []
+    t_start = time.perf_counter()
+    t_s = 2
+    for s, idx in sorted(by_shape.items(), key=lambda kv: kv[0][0] * kv[0][1]):
+        n_take = 1 if s[0] * s[1] >= 512 * 512 else min(len(idx), 64)
+        y = rng.standard_normal(s)
+        t0 = time.perf_counter()
+        for i in idx[:n_take]:
+            bjorck_grad.bjorck_vjp(wl.as_f64(wl.stored_matrix(w, i, *s)), y, t_s)
+        per_shape[s] = (time.perf_counter() - t0) / n_take * (10 * w.iters - 2) / (10 * t_s - 2)
+        desc.append(f"{n_take}x{s[0]}x{s[1]}")
+        if time.perf_counter() - t_start > budget_s:
+            break
+    ref_s = max(per_shape, key=lambda s: s[0] * s[1] * min(s))
+    ref_f = ref_s[0] * ref_s[1] * min(ref_s)
+    total = sum(per_shape.get(s, per_shape[ref_s] * s[0] * s[1] * min(s) / ref_f) * len(idx)
+                for s, idx in by_shape.items())
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    return {"value": w.n_layers / total, "unit": "layers/s", "cores": threads, "kind": "oracle",
+            "sample": f"float64 numpy oracle VJP (Björck only), timed {'+'.join(desc)} at T={t_s} and scaled to "
+                      f"T={w.iters} by (10T-2) and by matrix count (estimated full backward {total:.1f} s)",
+            "est_step_s": total}
 
 
 def cpu_baseline(w, budget_s=25.0):
@@ -174,6 +323,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=wl.WORKLOAD_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--vjp", action="store_true",
+                    help="also time the backward pass (composition and Björck vector-Jacobian products)")
+    ap.add_argument("--vjp-steps", type=int, default=3)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
     args = ap.parse_args()
@@ -254,10 +406,17 @@ def main():
                 "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(flops / launches)}
 
+    vjp = None
+    if args.vjp:
+        vjp = run_vjp(w, ins, outs, layers, status, compute, args.vjp_steps, 1, torch, orth, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         cpu = cpu_baseline(w)
+        if vjp is not None:
+            log("[bench] timing the CPU oracle VJP sample")
+            vjp["cpu_baseline"] = vjp_cpu_baseline(w)
 
     if args.copy_calibration:
         # a plain streaming kernel of known traffic: reads 1 GiB, writes 1 GiB
@@ -280,6 +439,8 @@ def main():
         "kernel_ms_per_step": {n: round(ktimes[n][0] / args.steps, 4) for n in names},
         "roofline": roof, "cpu_baseline": cpu,
     }
+    if vjp is not None:
+        rec["vjp"] = vjp
     print(json.dumps(rec), flush=True)
 
 

@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "internal.h"
+#include "tile_order.h"
 
 namespace orth {
 
@@ -142,31 +143,6 @@ struct Arena {
   }
 };
 
-// Reorders a logical work list so that physical block p (dispatched to XCD
-// p % 8) gets consecutive logical items: XCD x owns one contiguous chunk.
-template <typename T>
-std::vector<T> xcd_order(const std::vector<T>& logical) {
-  const size_t n = logical.size();
-  std::vector<T> phys(n);
-  size_t start = 0;
-  for (size_t x = 0; x < 8; ++x) {
-    const size_t cnt = n > x ? (n - x + 7) / 8 : 0;
-    for (size_t slot = 0; slot < cnt; ++slot) phys[x + 8 * slot] = logical[start + slot];
-    start += cnt;
-  }
-  return phys;
-}
-
-// Tiles of a tr x tc grid in groups of `gm` tile rows (column-major inside a
-// group), so concurrently running tiles share operand panels.
-void grouped_tiles(int mat, int tr, int tc, int gm, bool upper_only, std::vector<TileItem>& out) {
-  for (int r0 = 0; r0 < tr; r0 += gm) {
-    const int r1 = std::min(tr, r0 + gm);
-    for (int j = 0; j < tc; ++j)
-      for (int i = r0; i < r1; ++i)
-        if (!upper_only || i <= j) out.push_back(TileItem{mat, i, j, 0});
-  }
-}
 }  // namespace
 
 // ---------------------------------------------------- orthogonalize plan --
@@ -279,8 +255,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
       const MatPlan& q = P.mp[i];
       const int tn = q.Np / tsz, tm = q.Mp / tsz;
       std::vector<TileItem> gt, ut;
-      grouped_tiles(tiled_of[i], tn, tn, 4, true, gt);
-      grouped_tiles(tiled_of[i], tm, tn, 4, false, ut);
+      bf16_matrix_tiles(tiled_of[i], tm, tn, gt, ut);
       for (int par = 0; par < 2; ++par) {
         for (TileItem t : gt) {
           t.flags = par ? TILE_PARITY : 0;
@@ -292,10 +267,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
         }
       }
     }
-    // Dispatched in the grouped order itself (block b runs on XCD b % 8), so
-    // all XCDs work on the same matrix and its operand panels are shared
-    // through the memory-side cache; measured 7% faster for update launches
-    // than giving each XCD its own contiguous chunk of matrices.
+    // dispatched in the order bf16_matrix_tiles builds (tile_order.h)
     for (int par = 0; par < 2; ++par) {
       P.tabs[cls][TAB_GRAM + par] = g[par];
       P.tabs[cls][TAB_UPDATE + par] = u[par];
@@ -1007,8 +979,7 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       n_fu += tm * tn;
     } else {
       const int cls = b == V_BF16_256 ? 1 : 0, tsz = cls ? 256 : 128;
-      grouped_tiles(i, t.Np / tsz, t.Np / tsz, 4, true, tg[cls]);
-      grouped_tiles(i, t.Mp / tsz, t.Np / tsz, 4, false, tu[cls]);
+      bf16_matrix_tiles(i, t.Mp / tsz, t.Np / tsz, tg[cls], tu[cls]);
     }
   }
   for (int cls = 0; cls < 2; ++cls) {
