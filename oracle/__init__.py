@@ -17,6 +17,8 @@ conv     Circular convolution with stride, dilation and groups, its adjoint,
          the impulse-response Toeplitz matrix and the per-frequency FFT
          singular values (Section 4 and Appendix C, unit-testing scheme).
 checks   Orthogonality deviation and norm ratios used as gates.
+spectral Spectral pre-scaling by power iteration from a cached vector
+         (Appendix A.5, Section 3), then Björck.
 bjorck_grad  Vector-Jacobian product of pre-scaling + Björck (the
          derivative of the Appendix A.5 step, chained backwards).
 aoc_grad Vector-Jacobian product of the composition (adjoint of each ⊛
@@ -27,6 +29,6 @@ forms, library routines (torch CPU conv2d, numpy SVD) or brute force; see the
 docstrings for which pin covers which function.
 """
 
-from . import bjorck, aoc, conv, checks, bjorck_grad, aoc_grad  # noqa: F401
+from . import bjorck, aoc, conv, checks, bjorck_grad, aoc_grad, spectral  # noqa: F401
 
-__all__ = ["bjorck", "aoc", "conv", "checks", "bjorck_grad", "aoc_grad"]
+__all__ = ["bjorck", "aoc", "conv", "checks", "bjorck_grad", "aoc_grad", "spectral"]

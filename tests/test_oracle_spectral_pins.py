@@ -1,0 +1,147 @@
+"""Pins of the spectral pre-scaling oracle (oracle/spectral.py):
+
+S1  hand-derived cases on small diagonal matrices (tests/golden/spectral_hand.json);
+S2  with enough power steps the estimate reaches the SVD's largest singular
+    value and the vector its right singular vector (numpy SVD);
+S3  bounds that hold for any cached vector: ||X v|| <= sigma_hat and
+    sigma <= sigma_max (so the largest singular value of W_0 is >= 1);
+S4  the wide case is the transpose of the tall case;
+S5  the point of the step: from a good cached vector, spectral scaling
+    needs fewer Björck iterations than Frobenius scaling;
+S6  statuses, and planted mistakes that the pins catch.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import bjorck, spectral
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+RNG = np.random.default_rng(20260114)
+
+
+def ev(expr):
+    return float(eval(expr, {"sqrt": math.sqrt}))
+
+
+CASES = json.load(open(os.path.join(HERE, "golden", "spectral_hand.json")))["cases"]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
+def test_hand_cases(case):
+    w = np.array(case["w"], dtype=np.float64)
+    w0, v, sigma, status = spectral.spectral_prescale(w, case["u"], case["q"])
+    assert status == bjorck.STATUS_OK
+    assert abs(sigma - ev(case["sigma"])) <= 1e-14 * ev(case["sigma"])
+    np.testing.assert_allclose(v, [ev(e) for e in case["v"]], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(w0, w / ev(case["sigma"]), rtol=1e-14, atol=0)
+
+
+@pytest.mark.parametrize("shape", [(40, 12), (12, 40), (30, 30)])
+def test_converges_to_svd(shape):
+    w = RNG.standard_normal(shape)
+    u, s, vt = np.linalg.svd(w if shape[0] >= shape[1] else w.T)
+    _, v, sigma, _ = spectral.spectral_prescale(w, RNG.standard_normal(min(shape)), 400)
+    assert abs(sigma - s[0]) <= 1e-9 * s[0]
+    assert abs(abs(float(v @ vt[0])) - 1.0) <= 1e-9
+
+
+@pytest.mark.parametrize("q", [1, 2, 5])
+def test_bounds_any_vector(q):
+    for _ in range(20):
+        m, n = RNG.integers(2, 30, size=2)
+        w = RNG.standard_normal((m, n)) * RNG.uniform(0.01, 100)
+        x_mat = w if m >= n else w.T
+        u = RNG.standard_normal(min(m, n))
+        w0, v, sigma, _ = spectral.spectral_prescale(w, u, q)
+        smax = np.linalg.svd(w, compute_uv=False)[0]
+        # both sigma_hat and ||W||_F / sqrt(N) are lower bounds of sigma_max
+        assert sigma <= smax * (1 + 1e-12)
+        assert sigma >= np.linalg.norm(w) / math.sqrt(min(m, n)) * (1 - 1e-12)
+        assert np.linalg.svd(w0, compute_uv=False)[0] >= 1 - 1e-12
+        # one step from a unit vector: sigma_hat >= ||X v_in||
+        uin = u / np.linalg.norm(u)
+        _, _, s1, _ = spectral.spectral_prescale(w, u, 1)
+        assert s1 >= np.linalg.norm(x_mat @ uin) * (1 - 1e-12)
+        assert abs(np.linalg.norm(v) - 1.0) <= 1e-12
+
+
+def test_transpose_relation():
+    w = RNG.standard_normal((9, 21))
+    u = RNG.standard_normal(9)
+    a0, av, asig, _ = spectral.spectral_prescale(w, u, 3)
+    b0, bv, bsig, _ = spectral.spectral_prescale(w.T, u, 3)
+    assert asig == pytest.approx(bsig, rel=1e-14)
+    np.testing.assert_allclose(a0, b0.T, rtol=1e-14)
+    np.testing.assert_allclose(av, bv, rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("n", [64, 128])
+def test_fewer_iterations_than_frobenius(n):
+    """Square Gaussian matrices: with the cached top vector (a previous
+    step's result), one power step gives sigma close to sigma_max and the
+    iteration converges in fewer steps than after Frobenius scaling."""
+    w = RNG.standard_normal((n, n)) / math.sqrt(n)
+    _, cached, _, _ = spectral.spectral_prescale(w, RNG.standard_normal(n), 30)
+    w_next = w + 1e-3 * RNG.standard_normal((n, n)) / math.sqrt(n)   # a small parameter update
+    _, _, sigma, _ = spectral.spectral_prescale(w_next, cached, 1)
+    t_spec = spectral.iterations_to_converge_scaled(w_next, sigma, tol=1e-3)
+    t_frob = spectral.iterations_to_converge_scaled(w_next, np.linalg.norm(w_next), tol=1e-3)
+    assert t_spec is not None and t_frob is not None
+    assert t_spec + 3 <= t_frob
+
+
+def test_bjorck_spectral_and_statuses():
+    w = RNG.standard_normal((20, 8))
+    out, v, st = spectral.bjorck_spectral(w, np.ones(8), 30, 2)
+    assert st == 0
+    assert np.max(np.abs(out.T @ out - np.eye(8))) <= 1e-10
+    z, vz, st = spectral.bjorck_spectral(np.zeros((5, 3)), np.arange(3.0), 4)
+    assert st == bjorck.STATUS_ZERO and np.all(z == 0) and np.array_equal(vz, np.arange(3.0))
+    bad = w.copy()
+    bad[0, 0] = np.nan
+    o, vb, st = spectral.bjorck_spectral(bad, np.ones(8), 4)
+    assert st == bjorck.STATUS_NONFINITE and np.all(np.isnan(o)) and np.array_equal(vb, np.ones(8))
+    with pytest.raises(ValueError):
+        spectral.spectral_prescale(w, np.ones(8), 0)
+
+
+def test_planted_missing_lower_bound(monkeypatch):
+    """Without max(., ||W||_F / sqrt(N)) a cached vector in the null space of
+    the top direction leaves W_0 outside the basin (0, sqrt(3)); with it the
+    hand case "null-space start" stays inside."""
+    w = np.diag([10.0, 1.0, 1.0])
+    u = np.array([0.0, 1.0, 1.0])
+    w0, _, _, _ = spectral.spectral_prescale(w, u, 1)
+    assert np.linalg.svd(w0, compute_uv=False)[0] < math.sqrt(3)
+    orig = spectral.spectral_prescale
+
+    def no_bound(w, u, q):
+        w0, v, sigma, st = orig(w, u, q)
+        x_mat = w if w.shape[0] >= w.shape[1] else w.T
+        x = x_mat @ (u / np.linalg.norm(u))
+        y = x_mat.T @ x
+        s_hat = np.linalg.norm(y) / np.linalg.norm(x)
+        return w / s_hat, v, s_hat, st
+    monkeypatch.setattr(spectral, "spectral_prescale", no_bound)
+    w0, _, _, _ = spectral.spectral_prescale(w, u, 1)
+    assert np.linalg.svd(w0, compute_uv=False)[0] > math.sqrt(3)
+    with pytest.raises(AssertionError):
+        test_hand_cases(CASES[4])
+
+
+def test_planted_norm_instead_of_ratio(monkeypatch):
+    """Using ||X v|| instead of ||X^T X v|| / ||X v|| fails the hand case."""
+    def wrong(w, u, q):
+        x_mat = w if w.shape[0] >= w.shape[1] else w.T
+        v = np.asarray(u, float) / np.linalg.norm(u)
+        s = np.linalg.norm(x_mat @ v)
+        sigma = max(s, np.linalg.norm(w) / math.sqrt(min(w.shape)))
+        return w / sigma, v, sigma, 0
+    monkeypatch.setattr(spectral, "spectral_prescale", wrong)
+    with pytest.raises(AssertionError):
+        test_hand_cases(CASES[2])
