@@ -51,7 +51,10 @@ typedef enum { ORTH_F32 = 0, ORTH_BF16 = 1 } orth_dtype;
  * kept in fp32). */
 typedef enum { ORTH_COMPUTE_F32 = 0, ORTH_COMPUTE_BF16 = 1 } orth_compute;
 
-typedef enum { ORTH_PRESCALE_NONE = 0, ORTH_PRESCALE_FROBENIUS = 1 } orth_prescale;
+/* Pre-scaling of W before the iteration: none, W / ||W||_F, or W / sigma
+ * with sigma from power iteration on a caller-owned cached vector (see
+ * orth_bjorck_opts.power_iters and .u). */
+typedef enum { ORTH_PRESCALE_NONE = 0, ORTH_PRESCALE_FROBENIUS = 1, ORTH_PRESCALE_SPECTRAL = 2 } orth_prescale;
 
 /* Per-matrix status written to status_dev. */
 typedef enum {
@@ -77,6 +80,12 @@ typedef struct {
   int32_t in_dtype;   /* orth_dtype of every mats[i].in */
   int32_t out_dtype;  /* orth_dtype of every mats[i].out */
   int32_t compute;    /* orth_compute */
+  /* ORTH_PRESCALE_SPECTRAL only (ignored otherwise): */
+  int32_t power_iters;  /* power steps q in [1, 1024] */
+  float* u;             /* device, fp32: the cached vectors of all matrices
+                           packed in batch order, min(rows, cols) values for
+                           each; read, and overwritten with the new estimate
+                           (left unchanged for a zero or non-finite matrix) */
 } orth_bjorck_opts;
 
 /*
@@ -87,11 +96,22 @@ typedef struct {
  * in the limit, wide ones orthonormal rows.  All matrices of the batch are
  * processed by the same few launches per step, whatever their shapes.
  *
+ * Spectral pre-scaling (App. A.5 and Section 3: spectral normalization by
+ * batched power iteration, with the estimate of the top singular vector
+ * cached across parameter updates): with X the tall orientation of W and
+ * v the matrix's cached vector (N = min(rows, cols) values; a zero vector
+ * starts as ones), q steps of x = X v, y = X^T x, sigma_hat = |y| / |x|,
+ * v = y / |y| (fp64 arithmetic), then W_0 = W / max(sigma_hat,
+ * ||W||_F / sqrt(N)) and v is written back.  Both terms are lower bounds of
+ * the largest singular value, so W_0's is >= 1; convergence needs it below
+ * sqrt(3), which a cached vector from the previous step gives.
+ *
  * status_dev: optional device array of n int32 (orth_mat_status).  A zero
  * or non-finite matrix does not fail the call.
  * Returns ORTH_EINVAL for n < 0, a NULL pointer, rows or cols < 1,
  * ld < cols, iters < 0, beta outside (0, 0.5], an unknown dtype, compute or
- * prescale mode, or in == out with differing dtype/leading dim.
+ * prescale mode, in == out with differing dtype/leading dim, or (spectral)
+ * power_iters outside [1, 1024] or u == NULL.
  */
 int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n,
                                       const orth_bjorck_opts* opts, size_t* bytes);
@@ -132,7 +152,8 @@ typedef struct {
  * status_dev: optional, as for the forward (1: zero matrix -> zero gradient;
  * 2: non-finite input -> NaN gradient).
  * Returns ORTH_EINVAL for the argument errors of the forward call, iters >
- * 4096, or aliasing other than the two allowed above.
+ * 4096, or aliasing other than the two allowed above; ORTH_EUNSUPPORTED for
+ * spectral pre-scaling (its derivative is not provided).
  */
 int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n,
                                           const orth_bjorck_opts* opts, size_t* bytes);

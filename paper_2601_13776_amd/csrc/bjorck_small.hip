@@ -1,6 +1,6 @@
 // Fused Björck for small matrices: one workgroup owns one matrix and keeps
 // it in LDS for the whole run — load (transposing wide inputs to the tall
-// orientation), Frobenius pre-scaling, T steps of
+// orientation), Frobenius or spectral pre-scaling, T steps of
 //     E = I - X^T X,   X <- X + beta X E      (Appendix A.5, E-form of
 //                                              (1+beta) X - beta X X^T X)
 // and the final store.  Products run on fp32 MFMA (v_mfma_f32_32x32x2f32);
@@ -29,10 +29,72 @@ __device__ inline int wave_or(int v) {
 // row 8 (r / 4) + 4 (l / 32) + (r % 4), column l % 32.
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// sum over the block, fixed order; valid in every thread
+template <int NWAVES>
+__device__ inline double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double t = 0.0;
+#pragma unroll
+  for (int w = 0; w < NWAVES; ++w) t += red[w];
+  return t;
+}
+
+// Spectral pre-scaling on the unscaled tall X in LDS (power iteration on
+// X^T X from the caller's cached vector, fp64): returns
+// max(|X^T X v| / |X v|, ||X||_F / sqrt(N)) and writes the new vector back.
+template <int NP, int NWAVES>
+__device__ double spectral_sigma(const float* X, const SmallMat& d, int power_iters, double tot, double* red) {
+  constexpr int XP = NP + 1, NTHR = 64 * NWAVES;
+  __shared__ double v[NP], y[NP], x[128];
+  const int tid = threadIdx.x, M = d.M, N = d.N;
+  double ss = 0.0;
+  for (int j = tid; j < N; j += NTHR) {
+    const double u = d.u[j];
+    ss += u * u;
+  }
+  const double nu = sqrt(block_sum<NWAVES>(ss, red));
+  const bool ok = nu > 0.0 && isfinite(nu);
+  for (int j = tid; j < N; j += NTHR) v[j] = ok ? d.u[j] / nu : 1.0 / sqrt((double)N);
+  __syncthreads();
+  double sig = 0.0;
+  for (int q = 0; q < power_iters; ++q) {
+    for (int i = tid; i < M; i += NTHR) {
+      double a = 0.0;
+      for (int j = 0; j < N; ++j) a += (double)X[i * XP + j] * v[j];
+      x[i] = a;
+    }
+    __syncthreads();
+    for (int j = tid; j < N; j += NTHR) {
+      double a = 0.0;
+      for (int i = 0; i < M; ++i) a += (double)X[i * XP + j] * x[i];
+      y[j] = a;
+    }
+    __syncthreads();
+    double sx = 0.0, sy = 0.0;
+    for (int i = tid; i < M; i += NTHR) sx += x[i] * x[i];
+    for (int j = tid; j < N; j += NTHR) sy += y[j] * y[j];
+    const double nx = sqrt(block_sum<NWAVES>(sx, red));
+    const double ny = sqrt(block_sum<NWAVES>(sy, red));
+    if (ny == 0.0) {   // uniform: v stays, and so would every later step
+      sig = 0.0;
+      break;
+    }
+    sig = ny / nx;
+    for (int j = tid; j < N; j += NTHR) v[j] = y[j] / ny;
+    __syncthreads();
+  }
+  for (int j = tid; j < N; j += NTHR) d.u[j] = (float)v[j];
+  return fmax(sig, sqrt(tot) / sqrt((double)N));
+}
+
 template <int NP, int NWAVES>
 __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMat* __restrict__ mats, int iters,
-                                                                  float beta, int prescale, int in_dtype,
-                                                                  int out_dtype, int32_t* __restrict__ status) {
+                                                                  float beta, int prescale, int power_iters,
+                                                                  int in_dtype, int out_dtype,
+                                                                  int32_t* __restrict__ status) {
   constexpr int NT = NP / 32;
   constexpr int XP = NP + 1;                      // row pitch of X and E in LDS (floats)
   constexpr int MAXT = (4 * NT + NWAVES - 1) / NWAVES;  // update tiles per wave (Mp <= 128)
@@ -74,13 +136,13 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMa
   if (bad_any) {
     st = ORTH_MAT_NONFINITE;
     scale = __builtin_nanf("");
+  } else if (prescale != ORTH_PRESCALE_NONE && tot == 0.0) {
+    st = ORTH_MAT_ZERO;
+    scale = 0.f;
   } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
-    if (tot == 0.0) {
-      st = ORTH_MAT_ZERO;
-      scale = 0.f;
-    } else {
-      scale = (float)(1.0 / sqrt(tot));
-    }
+    scale = (float)(1.0 / sqrt(tot));
+  } else if (prescale == ORTH_PRESCALE_SPECTRAL) {
+    scale = (float)(1.0 / spectral_sigma<NP, NWAVES>(X, d, power_iters, tot, red));
   }
   if (tid == 0 && status) status[d.status_index] = st;
   for (int idx = tid; idx < Mp * NP; idx += NTHR) {
@@ -149,7 +211,8 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMa
 }  // namespace
 
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
-                               int prescale, int in_dtype, int out_dtype, int32_t* status, hipStream_t s) {
+                               int prescale, int power_iters, int in_dtype, int out_dtype, int32_t* status,
+                               hipStream_t s) {
   if (n <= 0) return hipSuccess;
   // dynamic LDS sized for the tallest matrix of this launch (max_mp <= 128)
   const size_t lds = (size_t)(max_mp + np) * (np + 1) * sizeof(float);
@@ -157,11 +220,11 @@ hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, 
   // 32-wide matrices: one wavefront each (a single Gram tile); 64-wide: four
   // wavefronts share the 4 Gram tiles and up to 8 update tiles
   if (np == 32)
-    hipLaunchKernelGGL((bjorck_small_kernel<32, 1>), dim3(n), dim3(64), lds, s, mats, iters, beta, prescale, in_dtype,
-                       out_dtype, status);
+    hipLaunchKernelGGL((bjorck_small_kernel<32, 1>), dim3(n), dim3(64), lds, s, mats, iters, beta, prescale,
+                       power_iters, in_dtype, out_dtype, status);
   else
     hipLaunchKernelGGL((bjorck_small_kernel<64, 4>), dim3(n), dim3(256), lds, s, mats, iters, beta, prescale,
-                       in_dtype, out_dtype, status);
+                       power_iters, in_dtype, out_dtype, status);
   hipError_t e = hipGetLastError();
   timing_end("bjorck_small", s);
   return e;

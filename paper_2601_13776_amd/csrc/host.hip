@@ -165,12 +165,14 @@ struct OrthoPlan {
   std::vector<TileItem> partial_items, scale_items, writeout_items;
   std::vector<TileItem> tabs[2][N_TABS];        // bf16: [0] = 128 tiles, [1] = 256 tiles
   std::vector<GemmItem> f32_gram, f32_update[2];
+  std::vector<PowerItem> power[2];              // spectral: v -> x and x -> y products
   int max_mp[2] = {32, 32};
   int total_partials = 0;
   // offsets in the workspace
   size_t off_small[2] = {0, 0}, off_tiled = 0, off_partial_items = 0, off_scale_items = 0, off_writeout_items = 0;
   size_t off_tabs[2][N_TABS] = {};
   size_t off_f32_gram = 0, off_f32_update[2] = {0, 0};
+  size_t off_power[2] = {0, 0};
   size_t off_partials = 0, off_inv = 0, off_status = 0;
   size_t table_bytes = 0, total_bytes = 0;
 };
@@ -181,8 +183,13 @@ int validate_ortho(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o) {
   if (!o) return fail(ORTH_EINVAL, "opts is NULL");
   if (o->iters < 0) return fail(ORTH_EINVAL, "iters must be >= 0");
   if (!(o->beta > 0.f && o->beta <= 0.5f)) return fail(ORTH_EINVAL, "beta must lie in (0, 0.5]");
-  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS)
+  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS &&
+      o->prescale != ORTH_PRESCALE_SPECTRAL)
     return fail(ORTH_EINVAL, "unknown prescale mode");
+  if (o->prescale == ORTH_PRESCALE_SPECTRAL) {
+    if (o->power_iters < 1 || o->power_iters > 1024) return fail(ORTH_EINVAL, "power_iters must lie in [1, 1024]");
+    if (n > 0 && !o->u) return fail(ORTH_EINVAL, "spectral pre-scaling needs the cached vectors u");
+  }
   if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
     return fail(ORTH_EINVAL, "unknown dtype");
   if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
@@ -302,6 +309,16 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   P.off_f32_gram = A.take(sizeof(GemmItem) * n_fg);
   P.off_f32_update[0] = A.take(sizeof(GemmItem) * n_fu);
   P.off_f32_update[1] = A.take(sizeof(GemmItem) * n_fu);
+  const bool spectral = o->prescale == ORTH_PRESCALE_SPECTRAL;
+  int64_t n_pw[2] = {0, 0};
+  if (spectral)
+    for (int i = 0; i < n; ++i) {
+      if (P.mp[i].bucket <= SMALL64) continue;
+      n_pw[0] += (P.mp[i].M + 63) / 64;   // outputs of X v
+      n_pw[1] += (P.mp[i].N + 63) / 64;   // outputs of X^T x
+    }
+  P.off_power[0] = A.take(sizeof(PowerItem) * n_pw[0]);
+  P.off_power[1] = A.take(sizeof(PowerItem) * n_pw[1]);
   P.table_bytes = align_up(A.off);
   P.off_partials = A.take(sizeof(double) * n_part);
   P.off_inv = A.take(sizeof(float) * n_tiled);
@@ -311,11 +328,15 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
 
   // per-matrix buffers and descriptors
   int part_base = 0;
+  int64_t u_off = 0;   // this matrix's cached vector in the packed array
   for (int i = 0; i < n; ++i) {
     const orth_mat& m = mats[i];
     const MatPlan& q = P.mp[i];
+    float* u_i = spectral ? o->u + u_off : nullptr;
+    u_off += q.N;
     if (q.bucket <= SMALL64) {
       SmallMat s{};
+      s.u = u_i;
       s.in = m.in;
       s.out = m.out;
       s.ld_in = m.ld_in;
@@ -358,6 +379,17 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     t.xt = bf16 ? nullptr : dev(A.take(elems * csz));   // the bf16 Gram reads X itself
     t.e = dev(A.take((size_t)q.Np * q.Np * csz));
     t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + tiled_idx;
+    if (spectral) {
+      t.u = u_i;
+      t.pv = reinterpret_cast<double*>(dev(A.take(sizeof(double) * q.N)));
+      t.px = reinterpret_cast<double*>(dev(A.take(sizeof(double) * q.M)));
+      t.py = reinterpret_cast<double*>(dev(A.take(sizeof(double) * q.N)));
+      t.sig = reinterpret_cast<double*>(dev(A.take(sizeof(double))));
+      // X v is a row product of W for a tall input and a column product for
+      // a wide one; X^T x the other way round
+      for (int b = 0; b < (q.M + 63) / 64; ++b) P.power[0].push_back(PowerItem{tiled_idx, b, q.transposed, 0});
+      for (int b = 0; b < (q.N + 63) / 64; ++b) P.power[1].push_back(PowerItem{tiled_idx, b, !q.transposed, 1});
+    }
     P.tiled.push_back(t);
 
     for (int a = 0; a < pr; ++a)
@@ -903,6 +935,8 @@ int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o)
   if (o->iters < 0) return fail(ORTH_EINVAL, "iters must be >= 0");
   if (o->iters > 4096) return fail(ORTH_EINVAL, "iters must be <= 4096");
   if (!(o->beta > 0.f && o->beta <= 0.5f)) return fail(ORTH_EINVAL, "beta must lie in (0, 0.5]");
+  if (o->prescale == ORTH_PRESCALE_SPECTRAL)
+    return fail(ORTH_EUNSUPPORTED, "the vector-Jacobian product supports no spectral pre-scaling");
   if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS)
     return fail(ORTH_EINVAL, "unknown prescale mode");
   if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
@@ -1228,6 +1262,8 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   put(img, P.off_f32_gram, P.f32_gram);
   put(img, P.off_f32_update[0], P.f32_update[0]);
   put(img, P.off_f32_update[1], P.f32_update[1]);
+  put(img, P.off_power[0], P.power[0]);
+  put(img, P.off_power[1], P.power[1]);
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
 
@@ -1240,6 +1276,15 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
     double* partials = reinterpret_cast<double*>(ws + P.off_partials);
     ORTH_HIP(launch_prescale_partial(tm, T(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                      partials, s));
+    if (opts->prescale == ORTH_PRESCALE_SPECTRAL) {
+      ORTH_HIP(launch_power_init(tm, nt, s));
+      for (int q = 0; q < opts->power_iters; ++q) {
+        for (int h = 0; h < 2; ++h)
+          ORTH_HIP(launch_power_dot(tm, reinterpret_cast<const PowerItem*>(ws + P.off_power[h]),
+                                    (int)P.power[h].size(), opts->in_dtype, s));
+        ORTH_HIP(launch_power_normalize(tm, nt, s));
+      }
+    }
     ORTH_HIP(launch_prescale_finish(tm, nt, partials, opts->prescale, status, s));
     ORTH_HIP(launch_prescale_scale(tm, T(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
                                    opts->compute, s));
@@ -1263,7 +1308,8 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   }
   for (int b = 0; b < 2; ++b)
     ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
-                                 b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale, opts->in_dtype,
+                                 b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale,
+                                 opts->prescale == ORTH_PRESCALE_SPECTRAL ? opts->power_iters : 0, opts->in_dtype,
                                  opts->out_dtype, status, s));
   return ORTH_OK;
 }

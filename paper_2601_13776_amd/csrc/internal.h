@@ -65,6 +65,12 @@ struct TiledMat {
   double* dot;               // <Y_0, W_0>, one per matrix
   int32_t gy_final;          // gy[] index holding dL/dW_0 after the last step
   int32_t pad;
+  // Spectral pre-scaling only.
+  float* u;                  // the caller's cached vector (N values)
+  double* pv;                // power-iteration vector v (N)
+  double* px;                // X v (M)
+  double* py;                // X^T X v (N)
+  double* sig;               // sigma_hat
 };
 
 struct TileItem {
@@ -88,6 +94,16 @@ struct SmallMat {
   int32_t transposed;
   int32_t status_index;
   int32_t pad;
+  float* u;                  // spectral pre-scaling: the caller's cached vector
+};
+
+// One batched power-iteration work item: 64 outputs of a matrix-vector
+// product with a matrix in the caller's layout.
+struct PowerItem {
+  int32_t mat;
+  int32_t block;             // outputs [64 block, 64 block + 64)
+  int32_t coldot;            // 0: out[r] = sum_c W[r][c] in[c]; 1: out[c] = sum_r W[r][c] in[r]
+  int32_t second;            // 0: v -> x, 1: x -> y
 };
 
 // Generic bounds-checked fp32 GEMM work item: C = A * B^T (+ A2 * B2^T)
@@ -174,8 +190,12 @@ void timing_end(const char* name, hipStream_t s);
 
 // Kernel launchers (defined next to their kernels).
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
-                               int prescale, int in_dtype, int out_dtype, int32_t* status,
+                               int prescale, int power_iters, int in_dtype, int out_dtype, int32_t* status,
                                hipStream_t s);
+hipError_t launch_power_init(const TiledMat* mats, int n_mats, hipStream_t s);
+hipError_t launch_power_dot(const TiledMat* mats, const PowerItem* items, int n_items, int in_dtype,
+                            hipStream_t s);
+hipError_t launch_power_normalize(const TiledMat* mats, int n_mats, hipStream_t s);
 hipError_t launch_prescale_partial(const TiledMat* mats, const TileItem* items, int n_items,
                                    int in_dtype, double* partials, hipStream_t s);
 hipError_t launch_prescale_finish(const TiledMat* mats, int n_mats, const double* partials,

@@ -1,0 +1,122 @@
+// Batched power iteration for spectral pre-scaling (App. A.5, Section 3):
+// with X the tall orientation of W and v the cached vector,
+//     x = X v,  y = X^T x,  sigma_hat = |y| / |x|,  v = y / |y|,
+// for every tiled matrix of a batch at once.  The two matrix-vector
+// products run on the caller's W directly (row dot products for W v or W x,
+// column dot products for W^T v or W^T x, depending on the orientation);
+// vectors and sums are fp64, every reduction has a fixed order.  One pass
+// over W per product: HBM-bound.
+#include "internal.h"
+
+namespace orth {
+namespace {
+
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// sum over the 256 threads of a block, fixed order; valid in every thread
+__device__ inline double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// v = u / |u| (ones / sqrt(N) for a zero or non-finite u)
+__global__ __launch_bounds__(256) void power_init_kernel(const TiledMat* __restrict__ mats) {
+  __shared__ double red[4];
+  const TiledMat& d = mats[blockIdx.x];
+  double ss = 0.0;
+  for (int j = threadIdx.x; j < d.N; j += 256) {
+    const double u = d.u[j];
+    ss += u * u;
+  }
+  const double nu = sqrt(block_sum(ss, red));
+  const bool ok = nu > 0.0 && isfinite(nu);
+  for (int j = threadIdx.x; j < d.N; j += 256) d.pv[j] = ok ? d.u[j] / nu : 1.0 / sqrt((double)d.N);
+}
+
+__global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restrict__ mats,
+                                                        const PowerItem* __restrict__ items, int in_dtype) {
+  __shared__ double part[4][64];
+  const PowerItem it = items[blockIdx.x];
+  const TiledMat& d = mats[it.mat];
+  const double* in = it.second ? d.px : d.pv;
+  double* out = it.second ? d.py : d.px;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (!it.coldot) {
+    // out[r] = sum_c W[r][c] in[c]: a wave per row, lanes along the row
+    for (int i = wave; i < 64; i += 4) {
+      const int r = it.block * 64 + i;
+      if (r >= d.rows) break;
+      double acc = 0.0;
+      for (int c = lane; c < d.cols; c += 64)
+        acc += (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype) * in[c];
+      acc = wave_sum(acc);
+      if (lane == 0) out[r] = acc;
+    }
+  } else {
+    // out[c] = sum_r W[r][c] in[r]: lanes along 64 columns, waves interleave rows
+    const int c = it.block * 64 + lane;
+    double acc = 0.0;
+    if (c < d.cols)
+      for (int r = wave; r < d.rows; r += 4)
+        acc += (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype) * in[r];
+    part[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && c < d.cols) out[c] = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+  }
+}
+
+// sigma_hat = |y| / |x| and v = y / |y| (v and sigma_hat = 0 kept if y = 0)
+__global__ __launch_bounds__(256) void power_normalize_kernel(const TiledMat* __restrict__ mats) {
+  __shared__ double red[4];
+  const TiledMat& d = mats[blockIdx.x];
+  double sx = 0.0, sy = 0.0;
+  for (int i = threadIdx.x; i < d.M; i += 256) sx += d.px[i] * d.px[i];
+  for (int j = threadIdx.x; j < d.N; j += 256) sy += d.py[j] * d.py[j];
+  const double nx = sqrt(block_sum(sx, red));
+  const double ny = sqrt(block_sum(sy, red));
+  if (ny == 0.0) {
+    if (threadIdx.x == 0) *d.sig = 0.0;
+    return;
+  }
+  if (threadIdx.x == 0) *d.sig = ny / nx;
+  for (int j = threadIdx.x; j < d.N; j += 256) d.pv[j] = d.py[j] / ny;
+}
+
+}  // namespace
+
+hipError_t launch_power_init(const TiledMat* mats, int n_mats, hipStream_t s) {
+  if (n_mats <= 0) return hipSuccess;
+  timing_begin("power_init", s);
+  hipLaunchKernelGGL(power_init_kernel, dim3(n_mats), dim3(256), 0, s, mats);
+  hipError_t e = hipGetLastError();
+  timing_end("power_init", s);
+  return e;
+}
+
+hipError_t launch_power_dot(const TiledMat* mats, const PowerItem* items, int n_items, int in_dtype,
+                            hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  timing_begin("power_dot", s);
+  hipLaunchKernelGGL(power_dot_kernel, dim3(n_items), dim3(256), 0, s, mats, items, in_dtype);
+  hipError_t e = hipGetLastError();
+  timing_end("power_dot", s);
+  return e;
+}
+
+hipError_t launch_power_normalize(const TiledMat* mats, int n_mats, hipStream_t s) {
+  if (n_mats <= 0) return hipSuccess;
+  timing_begin("power_normalize", s);
+  hipLaunchKernelGGL(power_normalize_kernel, dim3(n_mats), dim3(256), 0, s, mats);
+  hipError_t e = hipGetLastError();
+  timing_end("power_normalize", s);
+  return e;
+}
+
+}  // namespace orth

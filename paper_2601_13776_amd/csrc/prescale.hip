@@ -2,8 +2,9 @@
 //
 //   partial  : squared norm of every 64x64 tile of every input (fp64 sums,
 //              NaN when the tile holds a non-finite value)
-//   finish   : per matrix, fixed-order sum of its partials -> 1/||W||_F and
-//              the per-matrix status (deterministic: no atomics)
+//   finish   : per matrix, fixed-order sum of its partials -> the scale
+//              (1/||W||_F, or 1/sigma from the power iteration of power.hip)
+//              and the per-matrix status (deterministic: no atomics)
 //   scale    : W_0 = W / ||W||_F in the tall orientation, zero padded to the
 //              tile grid, written as the fp32 iterate plus its bf16 copy
 //              (bf16 products) or its transpose (fp32 products)
@@ -64,23 +65,31 @@ __global__ __launch_bounds__(256) void prescale_finish_kernel(const TiledMat* __
   double ss = 0.0;
   for (int i = threadIdx.x; i < d.n_partials; i += 256) ss += partials[d.partial_base + i];
   const double tot = block_sum_256(ss, red);
+  __shared__ int st_sh;
   if (threadIdx.x == 0) {
     int st = ORTH_MAT_OK;
     float inv = 1.f;
     if (isnan(tot)) {
       st = ORTH_MAT_NONFINITE;
       inv = __builtin_nanf("");
+    } else if (prescale != ORTH_PRESCALE_NONE && tot == 0.0) {
+      st = ORTH_MAT_ZERO;
+      inv = 0.f;
     } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
-      if (tot == 0.0) {
-        st = ORTH_MAT_ZERO;
-        inv = 0.f;
-      } else {
-        inv = (float)(1.0 / sqrt(tot));
-      }
+      inv = (float)(1.0 / sqrt(tot));
+    } else if (prescale == ORTH_PRESCALE_SPECTRAL) {
+      // both terms are lower bounds of the largest singular value
+      const double sigma = fmax(*d.sig, sqrt(tot) / sqrt((double)d.N));
+      inv = (float)(1.0 / sigma);
     }
     *d.inv_norm = inv;
     if (status) status[d.status_index] = st;
+    st_sh = st;
   }
+  __syncthreads();
+  // spectral: hand the new estimate back (a degenerate matrix keeps the old one)
+  if (prescale == ORTH_PRESCALE_SPECTRAL && st_sh == ORTH_MAT_OK)
+    for (int j = threadIdx.x; j < d.N; j += 256) d.u[j] = (float)d.pv[j];
 }
 
 __global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __restrict__ mats,

@@ -17,7 +17,7 @@ _lib = None
 ORTH_OK, ORTH_EINVAL, ORTH_EUNSUPPORTED, ORTH_EWORKSPACE, ORTH_EHIP = range(5)
 ORTH_F32, ORTH_BF16 = 0, 1
 ORTH_COMPUTE_F32, ORTH_COMPUTE_BF16 = 0, 1
-ORTH_PRESCALE_NONE, ORTH_PRESCALE_FROBENIUS = 0, 1
+ORTH_PRESCALE_NONE, ORTH_PRESCALE_FROBENIUS, ORTH_PRESCALE_SPECTRAL = 0, 1, 2
 ORTH_CHECK_GRAM, ORTH_CHECK_CONV, ORTH_CHECK_CONV_ADJOINT = 0, 1, 2
 
 EXPORTED = [
@@ -44,7 +44,8 @@ class orth_mat(ctypes.Structure):
 
 class orth_bjorck_opts(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("beta", ctypes.c_float), ("prescale", ctypes.c_int32),
-                ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("compute", ctypes.c_int32)]
+                ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
+                ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p)]
 
 
 class orth_vjp_mat(ctypes.Structure):
@@ -152,21 +153,30 @@ def _mats(ins, outs):
     return arr
 
 
-def _opts(ins, outs, iters, beta, prescale, compute):
+def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None):
     in_dt = _dtype_code(ins[0]) if ins else ORTH_F32
     out_dt = _dtype_code(outs[0]) if outs else ORTH_F32
     for a, b in zip(ins, outs):
         if _dtype_code(a) != in_dt or _dtype_code(b) != out_dt:
             raise TypeError("all inputs (and all outputs) must share one dtype")
-    pres = {"frobenius": ORTH_PRESCALE_FROBENIUS, "none": ORTH_PRESCALE_NONE}[prescale]
+    pres = {"frobenius": ORTH_PRESCALE_FROBENIUS, "none": ORTH_PRESCALE_NONE,
+            "spectral": ORTH_PRESCALE_SPECTRAL}[prescale]
     comp = {"f32": ORTH_COMPUTE_F32, "bf16": ORTH_COMPUTE_BF16}[compute]
-    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp)
+    uptr = None
+    if pres == ORTH_PRESCALE_SPECTRAL and ins:
+        need = sum(min(t.shape[0], t.shape[1]) for t in ins)
+        if u is None or u.dtype != torch.float32 or not u.is_contiguous() or u.numel() < need:
+            raise ValueError(f"spectral pre-scaling needs u: a contiguous float32 tensor of {need} values "
+                             "(min(rows, cols) per matrix, packed in batch order)")
+        uptr = u.data_ptr()
+    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp, power_iters, uptr)
 
 
-def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius", compute="f32", outs=None):
+def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius", compute="f32", outs=None,
+                                      power_iters=1, u=None):
     outs = ins if outs is None else outs
     mats = _mats(ins, outs)
-    opts = _opts(ins, outs, iters, beta, prescale, compute)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_workspace_size")
@@ -174,11 +184,13 @@ def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius"
 
 
 def orth_orthogonalize_batched(ins, outs, iters, beta=0.5, prescale="frobenius", compute="f32", status=None,
-                               workspace=None, stream=None):
+                               workspace=None, stream=None, power_iters=1, u=None):
     """Björck-orthogonalize every ins[i] into outs[i] (see include/orth.h).
+    prescale="spectral" takes power_iters and u, the packed float32 cached
+    vectors (min(rows, cols) per matrix), updated in place.
     Returns the workspace tensor so that callers can reuse it."""
     mats = _mats(ins, outs)
-    opts = _opts(ins, outs, iters, beta, prescale, compute)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_workspace_size")

@@ -241,3 +241,19 @@ def test_conv_vjp_validation(L):
     assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_OK
     arr[0] = orth.orth_conv_vjp_desc(orth.orth_conv_geom(16, 16, 1, 2, 1, 1), 0x1000, None, 0x3000, 0x4000, None)
     assert L.orth_build_conv_kernels_vjp_workspace_size(arr, 1, 0, ctypes.byref(n)) == orth.ORTH_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("q,u,code", [(1, 0x1000, orth.ORTH_OK), (0, 0x1000, orth.ORTH_EINVAL),
+                                      (1025, 0x1000, orth.ORTH_EINVAL), (2, None, orth.ORTH_EINVAL)])
+def test_spectral_validation(L, q, u, code):
+    opts = orth.orth_bjorck_opts(5, 0.5, orth.ORTH_PRESCALE_SPECTRAL, 0, 0, 0, q, u)
+    n = ctypes.c_size_t()
+    rc = L.orth_orthogonalize_workspace_size(_mats([(64, 32), (300, 200)]), 2, ctypes.byref(opts), ctypes.byref(n))
+    assert rc == code
+
+
+def test_vjp_rejects_spectral(L):
+    opts = orth.orth_bjorck_opts(5, 0.5, orth.ORTH_PRESCALE_SPECTRAL, 0, 0, 0, 1, 0x1000)
+    n = ctypes.c_size_t()
+    rc = L.orth_orthogonalize_vjp_workspace_size(_vjp_mats([(64, 32)]), 1, ctypes.byref(opts), ctypes.byref(n))
+    assert rc == orth.ORTH_EUNSUPPORTED
