@@ -7,6 +7,7 @@ already resident in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--vjp [--vjp-steps K]] [--copy-calibration]
+                    [--prescale spectral [--power-iters Q]] [--iters T]
 
 With --vjp the backward pass (dL/dK and dL/d(output) back to the raw
 parameters) is timed too and reported under "vjp".
@@ -323,6 +324,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=wl.WORKLOAD_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--prescale", default="frobenius", choices=["frobenius", "spectral"],
+                    help="spectral: power iteration from cached vectors (warmed once before timing)")
+    ap.add_argument("--power-iters", type=int, default=1)
+    ap.add_argument("--iters", type=int, default=None, help="override the workload's Björck step count")
     ap.add_argument("--vjp", action="store_true",
                     help="also time the backward pass (composition and Björck vector-Jacobian products)")
     ap.add_argument("--vjp-steps", type=int, default=3)
@@ -342,20 +347,32 @@ def main():
         build.build()
     dev = torch.device("cuda:0")
     w = wl.WORKLOADS[args.workload]
+    if args.iters is not None:
+        import dataclasses
+        w = dataclasses.replace(w, iters=args.iters)
     log(f"[bench] generating {w.name}: {len(w.matrix_shapes())} matrices")
     ins = make_inputs(w, torch, dev)
     out_dtype = torch.float32
     outs, layers = allocate_outputs(w, ins, torch, dev, out_dtype)
     status = torch.zeros(len(ins), dtype=torch.int32, device=dev)
     compute = "bf16" if w.dtype == "bf16" else "f32"
-    ws = orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status)
+    pkw = {}
+    if args.prescale == "spectral":
+        # cached vectors warmed by a few power steps, as after earlier parameter updates
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(w.seed + 300)
+        u = torch.randn(sum(min(t.shape) for t in ins), generator=gen, device=dev)
+        orth.orth_orthogonalize_batched(ins, outs, 0, compute=compute, status=status, prescale="spectral",
+                                        power_iters=5, u=u)
+        pkw = dict(prescale="spectral", power_iters=args.power_iters, u=u)
+    ws = orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status, **pkw)
     conv_ws = None
     torch.cuda.synchronize()
     log(f"[bench] workspace {ws.numel() / 2**30:.2f} GiB")
 
     def step():
         nonlocal conv_ws
-        orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status, workspace=ws)
+        orth.orth_orthogonalize_batched(ins, outs, w.iters, compute=compute, status=status, workspace=ws, **pkw)
         if layers:
             conv_ws = orth.orth_build_conv_kernels_batched(layers, workspace=conv_ws)
 
@@ -406,6 +423,22 @@ def main():
                 "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(flops / launches)}
 
+    power = None
+    if args.prescale == "spectral" and "power_dot" in ktimes:
+        # HBM roofline of the power-iteration products: each reads every
+        # tiled matrix once (the fused small kernel does its own in LDS)
+        esz = 2 if w.dtype == "bf16" else 4
+        mbytes = sum(r * c * esz for r, c in shapes if not (min(r, c) <= 64 and max(r, c) <= 128))
+        tot_ms, launches = ktimes["power_dot"]
+        per_launch = mbytes
+        ach = per_launch * launches / (tot_ms / 1e3) / 1e9
+        power = {"power_iters": args.power_iters,
+                 "ms_per_step": round(sum(ktimes[n][0] for n in names if n.startswith("power_")) / args.steps, 4),
+                 "roofline": {"bound": "hbm", "kernel": "power_dot", "achieved": round(ach, 1),
+                              "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                              "traffic": None, "avg_launch_ms": round(tot_ms / launches, 4),
+                              "algorithmic_bytes_per_launch": per_launch}}
+
     vjp = None
     if args.vjp:
         vjp = run_vjp(w, ins, outs, layers, status, compute, args.vjp_steps, 1, torch, orth, dev)
@@ -432,13 +465,16 @@ def main():
         "vs_baseline": None, "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded N(0,1/fan_in) parameters)",
         "config": {"workload": w.name, "matrices": len(shapes), "layers": w.n_layers, "iters": w.iters,
-                   "compute": "bf16 operands, fp32 accumulate" if w.dtype == "bf16" else "fp32"},
+                   "compute": "bf16 operands, fp32 accumulate" if w.dtype == "bf16" else "fp32",
+                   "prescale": args.prescale},
         "bjorck_tflops_algorithmic": round(bjorck_tflops, 1) if bjorck_tflops else None,
         "bjorck_pct_peak": round(100 * bjorck_tflops / peak, 2) if bjorck_tflops else None,
         "step_tflops_algorithmic": round(step_tflops, 1),
         "kernel_ms_per_step": {n: round(ktimes[n][0] / args.steps, 4) for n in names},
         "roofline": roof, "cpu_baseline": cpu,
     }
+    if power is not None:
+        rec["power_iteration"] = power
     if vjp is not None:
         rec["vjp"] = vjp
     print(json.dumps(rec), flush=True)

@@ -7,7 +7,8 @@ S3  bounds that hold for any cached vector: ||X v|| <= sigma_hat and
     sigma <= sigma_max (so the largest singular value of W_0 is >= 1);
 S4  the wide case is the transpose of the tall case;
 S5  the point of the step: from a good cached vector, spectral scaling
-    needs fewer Björck iterations than Frobenius scaling;
+    needs fewer Björck iterations than Frobenius scaling, about
+    log_1.5(||W||_F / sigma) fewer on the workload's matrices;
 S6  statuses, and planted mistakes that the pins catch.
 """
 
@@ -145,3 +146,28 @@ def test_planted_norm_instead_of_ratio(monkeypatch):
     monkeypatch.setattr(spectral, "spectral_prescale", wrong)
     with pytest.raises(AssertionError):
         test_hand_cases(CASES[2])
+
+
+def test_workload_shapes_step_saving():
+    """On matrices of the ImageNet-like stack (seeded as the workload draws
+    them): in the linear phase of the scalar map (small singular values grow
+    by 1.5 per step) spectral scaling starts every singular value
+    ||W||_F / sigma times larger than Frobenius scaling does, which saves
+    about log_1.5(||W||_F / sigma) steps.  Spectral scaling from a warmed
+    vector at T - (that count, rounded down, minus one) is at least as
+    orthogonal as Frobenius scaling at T = 20."""
+    from paper_2601_13776_amd import workloads as wl
+    w = wl.WORKLOADS["imagenet_backbone25"]
+    shapes = w.matrix_shapes()
+    saved = []
+    for i in (0, 1, 20, 61, 80):   # 128^2, 128x64, 256^2, 1024x512, dense 1024^2
+        x = wl.as_f64(wl.stored_matrix(w, i, *shapes[i]))
+        _, warm, _, _ = spectral.spectral_prescale(x, np.ones(min(x.shape)), 20)
+        _, _, sigma, _ = spectral.spectral_prescale(x, warm, 1)
+        k = int(math.floor(math.log(np.linalg.norm(x) / sigma, 1.5))) - 1
+        spec, _, _ = spectral.bjorck_spectral(x, warm, 20 - k, 1)
+        frob = bjorck.bjorck(x, 20)
+        dev = lambda m: np.max(np.abs((m.T @ m if m.shape[0] >= m.shape[1] else m @ m.T) - np.eye(min(m.shape))))
+        assert dev(spec) <= max(dev(frob), 1e-12), (i, shapes[i], k, dev(spec), dev(frob))
+        saved.append(k)
+    assert min(saved) >= 2 and max(saved) >= 5
