@@ -163,6 +163,41 @@ def test_adjoint_inner_product(cin, cout, k, s, d, g):
     assert abs(lhs - rhs) <= 1e-10 * abs(lhs)
 
 
+@pytest.mark.parametrize("cin,cout,k,s,d,g,hw", [
+    (4, 6, 3, 1, 1, 1, 8), (4, 4, 3, 2, 1, 1, 8), (4, 8, 3, 1, 2, 2, 8),
+    (6, 6, 5, 2, 3, 3, 12), (2, 8, 2, 2, 1, 1, 6), (8, 4, 4, 2, 1, 2, 8),
+])
+def test_transposed_conv_matches_torch_fold(cin, cout, k, s, d, g, hw):
+    """The transposed conv (adjoint) equals torch's conv_transpose2d without
+    padding followed by folding its output back onto the H x W torus with
+    the left padding removed: an independent route to the same operator."""
+    rng = np.random.default_rng(17)
+    kern = rng.standard_normal((cout, cin // g, k, k))
+    y = rng.standard_normal((2, cout, hw // s, hw // s))
+    full = F.conv_transpose2d(torch.from_numpy(y), torch.from_numpy(kern), stride=s, dilation=d,
+                              groups=g).numpy()
+    pl = (d * (k - 1) + 1 - s) // 2
+    want = np.zeros((2, cin, hw, hw))
+    for t in range(full.shape[2]):
+        for u in range(full.shape[3]):
+            want[:, :, (t - pl) % hw, (u - pl) % hw] += full[:, :, t, u]
+    got = conv.conv_circular_adjoint(kern, y, (hw, hw), s, d, g)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_transposed_toeplitz_is_transpose():
+    """Impulse responses of the transposed conv give the transpose of the
+    forward conv's Toeplitz matrix."""
+    rng = np.random.default_rng(18)
+    cin, cout, k, s, d, g, hw = 4, 6, 3, 2, 1, 2, 6
+    kern = rng.standard_normal((cout, cin // g, k, k))
+    fwd = conv.toeplitz_matrix(kern, hw, hw, s, d, g)
+    dim = cout * (hw // s) ** 2
+    basis = np.eye(dim).reshape(dim, cout, hw // s, hw // s)
+    cols = conv.conv_circular_adjoint(kern, basis, (hw, hw), s, d, g).reshape(dim, -1).T
+    np.testing.assert_allclose(cols, fwd.T, rtol=0, atol=1e-13)
+
+
 @pytest.mark.parametrize("shape_a,shape_b,stride", [
     ((5, 4, 2, 2), (4, 3, 1, 2), 2), ((3, 4, 1, 1), (4, 4, 2, 1), 1),
     ((4, 4, 2, 3), (4, 2, 3, 2), 1),
