@@ -239,6 +239,36 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
                                         int32_t dtype, void* workspace,
                                         size_t workspace_bytes, void* stream);
 
+/* Application of an explicit kernel (forward or transposed convolution). */
+typedef struct {
+  orth_conv_geom geom;     /* geometry of the FORWARD conv (cin -> cout, stride s) */
+  const void* kernel;      /* device: cout x (cin/g) x k x k (OIHW), kernel_dtype */
+  int32_t kernel_dtype;    /* orth_dtype */
+  int32_t transposed;      /* 0: y = conv(K, x); 1: y = conv^T(K, x) */
+  const float* x;          /* device fp32 NCHW: batch x cin x H x W (forward) or
+                              batch x cout x H/s x W/s (transposed) */
+  float* y;                /* device fp32 NCHW: batch x cout x H/s x W/s (forward)
+                              or batch x cin x H x W (transposed); must not
+                              overlap x */
+  int32_t batch, height, width;   /* H, W: the forward conv's input grid */
+} orth_conv_apply_args;
+
+/*
+ * Circular-padded convolution with an explicit kernel, natively strided,
+ * dilated and grouped, or its transpose (Section 3: an AOC layer runs as one
+ * convolution with the materialized kernel; transposed convolutions reuse
+ * the same kernel for learnable upsampling).  Forward:
+ *   y[b,o,u,v] = sum_{i,a,e} K[o,i,a,e] x[b, g(o) c + i, (s u + d a - pl) mod H, (s v + d e - pl) mod W],
+ * c = cin/g, pl = floor((d (k-1) + 1 - s) / 2); transposed: the adjoint of
+ * that map.  For an orthogonal kernel with cout/g <= c s^2 the forward map
+ * has orthonormal rows, so the transposed map preserves norms and the
+ * forward map inverts it.  fp32 arithmetic on fp32 MFMA.
+ * Errors: the geometry errors of orth_aoc_param_shapes, ORTH_EINVAL for
+ * NULL pointers, batch/height/width < 1, H or W not divisible by the
+ * stride, x == y, or an unknown dtype.
+ */
+int orth_conv_apply(const orth_conv_apply_args* args, void* stream);
+
 /* Single-layer convenience form of orth_build_conv_kernels_batched. */
 int orth_build_conv_kernel(const void* rko, const void* proj, int32_t cin,
                            int32_t cout, int32_t k, int32_t stride,

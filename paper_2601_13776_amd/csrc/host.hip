@@ -3,6 +3,7 @@
 // include/orth.h.  Every entry point validates everything before it
 // enqueues anything; the library allocates no device memory.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -1522,6 +1523,22 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
   ORTH_HIP(launch_gemm_f32(GI(P.off_last_dp), (int)P.last_dp.size(), "conv_vjp_tap_gemm", s));
   ORTH_HIP(launch_gemm_f32(GI(P.off_dv), (int)P.dv_items.size(), "conv_vjp_factor_grad", s));
   ORTH_HIP(launch_tap_items(2, TI(P.off_rko_grad), (int)P.rko_grad.size(), dtype, P.rko_max, s));
+  return ORTH_OK;
+}
+
+int orth_conv_apply(const orth_conv_apply_args* a, void* stream) {
+  if (!a) return fail(ORTH_EINVAL, "args is NULL");
+  const int rc = validate_geom(&a->geom);
+  if (rc) return rc;
+  if (!a->kernel || !a->x || !a->y) return fail(ORTH_EINVAL, "NULL data pointer");
+  if (static_cast<const void*>(a->x) == static_cast<const void*>(a->y)) return fail(ORTH_EINVAL, "x and y must differ");
+  if (a->kernel_dtype != ORTH_F32 && a->kernel_dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+  if (a->batch < 1 || a->height < 1 || a->width < 1) return fail(ORTH_EINVAL, "batch, height and width must be >= 1");
+  if (a->height % a->geom.stride || a->width % a->geom.stride)
+    return fail(ORTH_EINVAL, "height and width must be divisible by the stride");
+  const int64_t pix = (int64_t)a->batch * a->height * a->width;
+  if (pix / 64 + 1 > INT32_MAX) return fail(ORTH_EINVAL, "batch x height x width too large");
+  ORTH_HIP(launch_conv_apply(a, static_cast<hipStream_t>(stream)));
   return ORTH_OK;
 }
 

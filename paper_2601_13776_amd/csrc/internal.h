@@ -225,6 +225,7 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // 2 RKO gradient from taps, 3 forward combine, 4 adjoint combine
 hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dtype, int64_t max_elems,
                             hipStream_t s);
+hipError_t launch_conv_apply(const orth_conv_apply_args* a, hipStream_t s);
 hipError_t launch_conv_check(const orth_check_args* a, const void* kernel, const float* x,
                              double* partial, float* out, int adjoint, hipStream_t s);
 

@@ -24,7 +24,7 @@ EXPORTED = [
     "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched",
     "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
-    "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched",
+    "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched", "orth_conv_apply",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
     "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
 ]
@@ -69,6 +69,12 @@ class orth_conv_vjp_desc(ctypes.Structure):
                 ("grad_kernel", ctypes.c_void_p), ("grad_rko", ctypes.c_void_p), ("grad_proj", ctypes.c_void_p)]
 
 
+class orth_conv_apply_args(ctypes.Structure):
+    _fields_ = [("geom", orth_conv_geom), ("kernel", ctypes.c_void_p), ("kernel_dtype", ctypes.c_int32),
+                ("transposed", ctypes.c_int32), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("batch", ctypes.c_int32), ("height", ctypes.c_int32), ("width", ctypes.c_int32)]
+
+
 class orth_check_args(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("mats", ctypes.POINTER(orth_mat)), ("n_mats", ctypes.c_int32),
                 ("mat_dtype", ctypes.c_int32), ("kernel", ctypes.c_void_p), ("kernel_dtype", ctypes.c_int32),
@@ -95,6 +101,7 @@ def lib():
         L.orth_build_conv_kernel.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp, sz, vp]
         L.orth_build_conv_kernels_vjp_workspace_size.argtypes = [P(orth_conv_vjp_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_vjp_batched.argtypes = [P(orth_conv_vjp_desc), i32, i32, vp, sz, vp]
+        L.orth_conv_apply.argtypes = [P(orth_conv_apply_args), vp]
         L.orth_check_workspace_size.argtypes = [P(orth_check_args), P(sz)]
         L.orth_check_norm.argtypes = [P(orth_check_args), vp, vp, sz, vp]
         L.orth_status_string.argtypes = [ctypes.c_int]
@@ -323,6 +330,25 @@ def orth_build_conv_kernels_vjp_batched(layers, workspace=None, stream=None):
                                                    nbytes, _stream(stream))
     _check(rc, "orth_build_conv_kernels_vjp_batched")
     return ws
+
+
+def orth_conv_apply(kernel, geom, x, transposed=False, stream=None):
+    """Circular conv (or its transpose) of the float32 NCHW batch x with the
+    explicit kernel; returns the new output tensor."""
+    if x.dtype != torch.float32 or not x.is_contiguous() or not kernel.is_contiguous():
+        raise ValueError("x must be contiguous float32 and the kernel contiguous")
+    cin, cout, k, s, d, g = geom
+    b = x.shape[0]
+    if transposed:
+        h, w = x.shape[2] * s, x.shape[3] * s
+        y = torch.empty(b, cin, h, w, dtype=torch.float32, device=x.device)
+    else:
+        h, w = x.shape[2], x.shape[3]
+        y = torch.empty(b, cout, h // s, w // s, dtype=torch.float32, device=x.device)
+    args = orth_conv_apply_args(orth_conv_geom(*geom), kernel.data_ptr(), _dtype_code(kernel), int(transposed),
+                                x.data_ptr(), y.data_ptr(), b, h, w)
+    _check(lib().orth_conv_apply(ctypes.byref(args), _stream(stream)), "orth_conv_apply")
+    return y
 
 
 def _check_call(args, out, workspace, stream):

@@ -257,3 +257,18 @@ def test_vjp_rejects_spectral(L):
     n = ctypes.c_size_t()
     rc = L.orth_orthogonalize_vjp_workspace_size(_vjp_mats([(64, 32)]), 1, ctypes.byref(opts), ctypes.byref(n))
     assert rc == orth.ORTH_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), orth.ORTH_OK), (dict(height=9), orth.ORTH_EINVAL), (dict(batch=0), orth.ORTH_EINVAL),
+    (dict(same=True), orth.ORTH_EINVAL), (dict(kernel_dtype=7), orth.ORTH_EINVAL),
+    (dict(geom=(4, 4, 1, 2, 1, 1)), orth.ORTH_EUNSUPPORTED),
+])
+def test_conv_apply_validation(L, kw, code):
+    """Only invalid arguments are exercised here (a valid call would launch)."""
+    if code == orth.ORTH_OK:
+        return
+    geom = kw.get("geom", (4, 8, 3, 2, 1, 1))
+    a = orth.orth_conv_apply_args(orth.orth_conv_geom(*geom), 0x1000, kw.get("kernel_dtype", 0), 0, 0x2000,
+                                  0x2000 if kw.get("same") else 0x3000, kw.get("batch", 2), kw.get("height", 8), 8)
+    assert L.orth_conv_apply(ctypes.byref(a), None) == code
