@@ -8,6 +8,7 @@ already resident in HBM.  Prints one JSON line.
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--vjp [--vjp-steps K]] [--copy-calibration]
                     [--prescale spectral [--power-iters Q]] [--iters T]
+                    [--conv-apply [--apply-batch B]]
 
 With --vjp the backward pass (dL/dK and dL/d(output) back to the raw
 parameters) is timed too and reported under "vjp".
@@ -274,6 +275,60 @@ def vjp_cpu_baseline(w, budget_s=25.0):
             "est_step_s": total}
 
 
+# input resolution of the first conv layer of each workload (halved after
+# every stride-2 layer; the ImageNet-like widths 128..1024 run at 56..7)
+APPLY_HW = {"conv3x3_c16": 16, "cifar_stack12": 32, "mixed_gds19": 32, "imagenet_backbone25": 56}
+
+
+def run_conv_apply(w, layers, batch, steps, torch, orth, dev):
+    """Time the forward and the transposed application of every conv layer's
+    explicit kernel to a batch of images; algorithmic flop
+    2 B (H/s)(W/s) cout (cin/g) k^2 per layer and direction."""
+    hw = APPLY_HW.get(w.name)
+    if not layers or hw is None:
+        return None
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 400)
+    jobs = []
+    prev_c = None
+    for L in layers:
+        cin, cout, k, s, d, g = L["geom"]
+        if w.name == "imagenet_backbone25" and prev_c is not None and cin != prev_c:
+            hw //= 2
+        prev_c = cout
+        x = torch.randn(batch, cin, hw, hw, generator=gen, device=dev)
+        yt = torch.randn(batch, cout, hw // s, hw // s, generator=gen, device=dev)
+        flops = 2 * batch * (hw // s) ** 2 * cout * (cin // g) * k * k
+        jobs.append((L, x, yt, flops))
+        hw //= s
+    def one():
+        for L, x, yt, _ in jobs:
+            orth.orth_conv_apply(L["kernel"], L["geom"], x)
+            orth.orth_conv_apply(L["kernel"], L["geom"], yt, transposed=True)
+    one()
+    torch.cuda.synchronize()
+    orth.orth_timing_enable(True)
+    orth.orth_timing_reset()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kt = {n: orth.orth_timing_read(n) for n in ("conv_apply", "conv_apply_transposed")}
+    orth.orth_timing_enable(False)
+    flops = sum(j[3] for j in jobs)
+    out = {"batch": batch, "first_layer_hw": APPLY_HW[w.name], "ms_per_pass": round((t1 - t0) * 1e3 / steps, 3),
+           "algorithmic_flops_per_direction": flops}
+    for n, key in (("conv_apply", "forward"), ("conv_apply_transposed", "transposed")):
+        ms = kt[n][0] / steps
+        ach = flops / (ms / 1e3) / 1e12
+        out[key] = {"ms": round(ms, 3), "roofline": {"bound": "mfma", "kernel": n, "achieved": round(ach, 1),
+                                                     "peak": PEAK_F32_TFLOPS, "unit": "TFLOP/s",
+                                                     "frac": round(ach / PEAK_F32_TFLOPS, 4), "traffic": None,
+                                                     "avg_launch_ms": round(kt[n][0] / kt[n][1], 4)}}
+    return out
+
+
 def cpu_baseline(w, budget_s=25.0):
     """Time the float64 oracle on a bounded sample of the workload and scale
     to the whole workload."""
@@ -328,6 +383,10 @@ def main():
                     help="spectral: power iteration from cached vectors (warmed once before timing)")
     ap.add_argument("--power-iters", type=int, default=1)
     ap.add_argument("--iters", type=int, default=None, help="override the workload's Björck step count")
+    ap.add_argument("--conv-apply", action="store_true",
+                    help="also time the application of every conv layer's kernel (forward and transposed) "
+                         "to a batch of images")
+    ap.add_argument("--apply-batch", type=int, default=64)
     ap.add_argument("--vjp", action="store_true",
                     help="also time the backward pass (composition and Björck vector-Jacobian products)")
     ap.add_argument("--vjp-steps", type=int, default=3)
@@ -439,6 +498,10 @@ def main():
                               "traffic": None, "avg_launch_ms": round(tot_ms / launches, 4),
                               "algorithmic_bytes_per_launch": per_launch}}
 
+    capply = None
+    if args.conv_apply:
+        capply = run_conv_apply(w, layers, args.apply_batch, 3, torch, orth, dev)
+
     vjp = None
     if args.vjp:
         vjp = run_vjp(w, ins, outs, layers, status, compute, args.vjp_steps, 1, torch, orth, dev)
@@ -475,6 +538,8 @@ def main():
     }
     if power is not None:
         rec["power_iteration"] = power
+    if capply is not None:
+        rec["conv_apply"] = capply
     if vjp is not None:
         rec["vjp"] = vjp
     print(json.dumps(rec), flush=True)
