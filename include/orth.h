@@ -96,7 +96,7 @@ typedef struct {
  * in the limit, wide ones orthonormal rows.  All matrices of the batch are
  * processed by the same few launches per step, whatever their shapes.
  *
- * Spectral pre-scaling (App. A.5 and Section 3: spectral normalization by
+ * Spectral pre-scaling (App. A.5 and Section 2: spectral normalization by
  * batched power iteration, with the estimate of the top singular vector
  * cached across parameter updates): with X the tall orientation of W and
  * v the matrix's cached vector (N = min(rows, cols) values; a zero vector

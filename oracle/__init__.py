@@ -18,17 +18,21 @@ conv     Circular convolution with stride, dilation and groups, its adjoint,
          singular values (Section 4 and Appendix C, unit-testing scheme).
 checks   Orthogonality deviation and norm ratios used as gates.
 spectral Spectral pre-scaling by power iteration from a cached vector
-         (Appendix A.5, Section 3), then Björck.
+         (Appendix A.5, Section 2), then Björck.
+expo     Exponential map with spectral normalization (Appendix A.3) and the
+         explicit conv exponential of Adaptive-SOC (Appendix B.2 theorem).
 bjorck_grad  Vector-Jacobian product of pre-scaling + Björck (the
          derivative of the Appendix A.5 step, chained backwards).
 aoc_grad Vector-Jacobian product of the composition (adjoint of each ⊛
          step, of the projector blocks and of P = V V^T).
 
-Every function is pinned by ``tests/test_oracle_pins.py`` against closed
-forms, library routines (torch CPU conv2d, numpy SVD) or brute force; see the
-docstrings for which pin covers which function.
+Every function is pinned against closed forms, library routines (torch CPU
+conv2d and conv_transpose2d, numpy SVD, scipy expm, torch.autograd), finite
+differences or brute force: ``tests/test_oracle_pins.py``,
+``tests/test_oracle_grad_pins.py``, ``tests/test_oracle_spectral_pins.py``,
+``tests/test_oracle_expo_pins.py``; each module's docstring names its pins.
 """
 
-from . import bjorck, aoc, conv, checks, bjorck_grad, aoc_grad, spectral  # noqa: F401
+from . import bjorck, aoc, conv, checks, bjorck_grad, aoc_grad, spectral, expo  # noqa: F401
 
-__all__ = ["bjorck", "aoc", "conv", "checks", "bjorck_grad", "aoc_grad", "spectral"]
+__all__ = ["bjorck", "aoc", "conv", "checks", "bjorck_grad", "aoc_grad", "spectral", "expo"]

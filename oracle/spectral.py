@@ -1,7 +1,7 @@
 """Spectral pre-scaling by power iteration with a caller-owned cached
 vector, float64 (Appendix A.5: spectral normalization of W_0 before the
 Björck iteration, reusing a cached power-iteration estimate of the top
-singular vector across updates; Section 3: spectral normalization by batched
+singular vector across updates; Section 2: spectral normalization by batched
 power iteration).
 
 Reading (the paper gives no formulas for this step): with X the tall

@@ -1,4 +1,4 @@
-// Batched power iteration for spectral pre-scaling (App. A.5, Section 3):
+// Batched power iteration for spectral pre-scaling (App. A.5, Section 2):
 // with X the tall orientation of W and v the cached vector,
 //     x = X v,  y = X^T x,  sigma_hat = |y| / |x|,  v = y / |y|,
 // for every tiled matrix of a batch at once.  The two matrix-vector
