@@ -162,6 +162,65 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n,
                                    size_t workspace_bytes, int32_t* status_dev,
                                    void* stream);
 
+/* Options of the exponential map. */
+typedef struct {
+  int32_t terms;        /* p in [1, 64]: the series is truncated after Ahat^p / p! */
+  int32_t power_iters;  /* power steps q in [1, 1024] of the spectral normalization */
+  float* u;             /* device, fp32: cached vectors, C values per matrix packed in
+                           batch order; read and overwritten with the new estimate */
+  int32_t in_dtype;     /* orth_dtype of every mats[i].in */
+  int32_t out_dtype;    /* orth_dtype of every mats[i].out */
+} orth_exp_opts;
+
+/*
+ * Exponential map with spectral normalization (Appendix A.3, algorithm
+ * "Exponential Map with Spectral Normalization"): for every square C x C
+ * matrix W, A = W - W^T, Ahat = A / sigma, and
+ *     What = I + sum_{k=1}^{p} P_k,   P_k = P_{k-1} Ahat / k,  P_0 = I,
+ * an element of SO(C) up to the truncation error |Ahat|^(p+1) e^|Ahat| / (p+1)!.
+ * sigma is the spectral-normalization estimate of orth_orthogonalize_batched's
+ * ORTH_PRESCALE_SPECTRAL applied to A (power iteration from the cached
+ * vector, at least ||A||_F / sqrt(C)).  fp32 products; a symmetric W (A = 0)
+ * gives I and status 1 with its vector unchanged; a non-finite W gives NaN
+ * and status 2.  Returns ORTH_EINVAL for non-square or NULL matrices, in ==
+ * out, terms outside [1, 64], power_iters outside [1, 1024], u == NULL or
+ * an unknown dtype.
+ */
+int orth_exp_map_workspace_size(const orth_mat* mats, int32_t n, const orth_exp_opts* opts,
+                                size_t* bytes);
+int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* opts,
+                         void* workspace, size_t workspace_bytes, int32_t* status_dev,
+                         void* stream);
+
+/* One explicit conv exponential. */
+typedef struct {
+  int32_t channels;     /* c: the kernel maps c channels to c channels */
+  int32_t k;            /* odd kernel size, <= 15 */
+  int32_t terms;        /* p in [1, 32] */
+  float scale;          /* t: the exponential of t (K - K*) */
+  const void* kernel;   /* device: K, c x c x k x k (OIHW), contiguous */
+  void* out;            /* device: c x c x S x S, S = p (k - 1) + 1, contiguous */
+} orth_conv_exp_desc;
+
+/*
+ * Explicit exponential of a skew-symmetric convolution (Appendix B.2,
+ * theorem "Explicit conv exponential", the Adaptive-SOC layer): with
+ * K*[o, i, a, b] = K[i, o, k-1-a, k-1-b] (the kernel of the adjoint of a
+ * stride-1 circular conv with centred padding) and L = t (K - K*),
+ *     E = sum_{j=0}^{p} L^(⊛j) / j!,
+ * ⊛ the block-convolution operator, L^(⊛0) the identity, every term centred
+ * in the S x S output.  conv(E, .) equals the per-input series
+ * sum_j conv(L, .)^j / j!, so one convolution replaces p.  dtype is the
+ * storage of kernel and out; arithmetic is fp32.  Returns ORTH_EINVAL for
+ * NULL pointers, kernel == out, channels outside [1, 8192], terms outside
+ * [1, 32], a non-finite scale or an unknown dtype; ORTH_EUNSUPPORTED for
+ * an even kernel size (no centre) or k > 15.
+ */
+int orth_conv_exp_workspace_size(const orth_conv_exp_desc* descs, int32_t n, int32_t dtype,
+                                 size_t* bytes);
+int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dtype,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
 /* Geometry of one orthogonal convolution (groups g, stride s, dilation d). */
 typedef struct {
   int32_t cin, cout, k, stride, dilation, groups;

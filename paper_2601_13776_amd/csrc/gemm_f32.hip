@@ -1,6 +1,7 @@
 // Table-driven fp32 "NT" GEMM on gfx950 fp32 MFMA (v_mfma_f32_32x32x2f32):
-// every work item is one 64 x 64 tile of C = A B^T (+ A2 B2^T, a second
-// operand pair accumulated into the same tile) with its own operands,
+// every work item is one 64 x 64 tile of C = A B^T (+ A2 B2^T and any
+// further pairs from a table, accumulated into the same tile) with its own
+// operands,
 // shapes and epilogue, so a single launch covers a whole ragged batch
 // (all matrices of a Björck step, all tap products of a composition step,
 // all Gram checks).  Operands may be fp32 or bf16 and stored either
@@ -25,7 +26,8 @@ namespace {
 
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items, int step) {
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items, int step,
+                                                       const GemmPair* __restrict__ extra) {
   constexpr int BM = 64, BN = 64, BK = 32, PITCH = BK + 4;
   __shared__ __attribute__((aligned(16))) float As[2][BM * PITCH];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * PITCH];
@@ -39,15 +41,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
   f32x16 acc = {};
   const int aoff = (wm * 32 + (lane & 31)) * PITCH + (lane >> 5) * 4;
   const int boff = (wn * 32 + (lane & 31)) * PITCH + (lane >> 5) * 4;
-  for (int pair = 0; pair < 2; ++pair) {
-    const int K = pair ? g->K2 : g->K;
+  const int npairs = 2 + g->pair_count;
+  for (int pair = 0; pair < npairs; ++pair) {
+    // pairs 0 and 1 live in the item (with per-step offsets), the others in
+    // the launch's pair table; all are stored like the first
+    const GemmPair* xp = pair >= 2 ? extra + g->pair_base + (pair - 2) : nullptr;
+    const int K = xp ? xp->K : (pair ? g->K2 : g->K);
     if (K <= 0) continue;
-    const int adt = g->a_dtype, bdt = g->b_dtype;   // the second pair is stored like the first
-    const int atr = pair ? g->a2_trans : g->a_trans, btr = pair ? g->b2_trans : g->b_trans;
-    const int64_t lda = pair ? g->lda2 : g->lda, ldb = pair ? g->ldb2 : g->ldb;
+    const int adt = g->a_dtype, bdt = g->b_dtype;
+    const int atr = xp ? xp->a_trans : (pair ? g->a2_trans : g->a_trans);
+    const int btr = xp ? xp->b_trans : (pair ? g->b2_trans : g->b_trans);
+    const int64_t lda = xp ? xp->lda : (pair ? g->lda2 : g->lda), ldb = xp ? xp->ldb : (pair ? g->ldb2 : g->ldb);
     const int esz_a = adt == ORTH_BF16 ? 2 : 4, esz_b = bdt == ORTH_BF16 ? 2 : 4;
-    const void* A = static_cast<const char*>(pair ? g->A2 : g->A) + (pair ? g->a2_step : g->a_step) * st * esz_a;
-    const void* B = static_cast<const char*>(pair ? g->B2 : g->B) + (pair ? g->b2_step : g->b_step) * st * esz_b;
+    const void* A = xp ? xp->A
+                       : static_cast<const char*>(pair ? g->A2 : g->A) + (pair ? g->a2_step : g->a_step) * st * esz_a;
+    const void* B = xp ? xp->B
+                       : static_cast<const char*>(pair ? g->B2 : g->B) + (pair ? g->b2_step : g->b_step) * st * esz_b;
 
     // thread -> (row, first k of 8) for each operand
     const int ar = atr ? (tid & 63) : (tid >> 2);
@@ -160,6 +169,19 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         if (mirror) C[(int64_t)j * ldc + i] = v;
       }
     }
+  } else if (epi == EPI_SERIES) {
+    float* dst2 = g->dst2;
+    const int64_t ld2 = g->ld2;
+    const float beta = g->beta;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = ibase + acc_row(r, lane);
+      if (i < M) {
+        const float v = beta * acc[r];
+        C[(int64_t)i * ldc + j] = v;
+        dst2[(int64_t)i * ld2 + j] += v;   // each element belongs to one item of the launch
+      }
+    }
   } else if (epi == EPI_NEG) {
     const bool mirror = g->mirror != 0;
 #pragma unroll
@@ -189,10 +211,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
 
 }  // namespace
 
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step) {
+hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step,
+                           const GemmPair* pairs) {
   if (n_items <= 0) return hipSuccess;
   timing_begin(name, s);
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_items), dim3(256), 0, s, items, step);
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_items), dim3(256), 0, s, items, step, pairs);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
   return e;

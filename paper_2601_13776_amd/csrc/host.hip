@@ -906,6 +906,248 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
 }
 }  // namespace
 
+// ------------------------------------------------------ exponentials ----
+// Exponential map: per matrix A = W - W^T, the spectral-normalization
+// kernels on A (power iteration from the caller's cached vector, lower bound
+// ||A||_F / sqrt(C)), Ahat = A / sigma, then P_k = P_{k-1} Ahat / k and
+// What += P_k on the tile GEMM (Ahat^T = -Ahat, so the products read Ahat
+// row-major and negate), and What written out.
+// Conv exponential: L = scale (K - K*) as k x k taps, E = centred I + L,
+// then Q_j = (Q_{j-1} ⊛ L) / j tap by tap (each output tap sums the products
+// of the Q_{j-1} taps and L taps that meet there; L_{r,t}^T = -L_{k-1-r,k-1-t}
+// lets every product read row-major operands) with E += Q_j, and E
+// scattered to OIHW.
+namespace {
+struct ExpPlan {
+  std::vector<ExpItem> items;
+  std::vector<TiledMat> mats;                 // exp map: views of A for the spectral kernels
+  std::vector<TileItem> partial_items, writeout_items;
+  std::vector<PowerItem> power[2];
+  std::vector<std::vector<GemmItem>> steps;   // per power k = 2..p (index k - 2)
+  std::vector<GemmPair> pairs;                // conv: operand pairs of all steps
+  std::vector<TapItem> scatter;               // conv: E taps -> OIHW
+  int64_t max_elems = 0, max_init = 0, max_scatter = 0;
+  size_t off_items = 0, off_mats = 0, off_partial = 0, off_writeout = 0, off_power[2] = {}, off_pairs = 0,
+         off_scatter = 0, off_partials = 0, off_inv = 0, off_status = 0;
+  std::vector<size_t> off_steps;
+  size_t table_bytes = 0, total_bytes = 0;
+};
+
+int validate_exp(const orth_mat* mats, int32_t n, const orth_exp_opts* o) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !mats) return fail(ORTH_EINVAL, "mats is NULL");
+  if (!o) return fail(ORTH_EINVAL, "opts is NULL");
+  if (o->terms < 1 || o->terms > 64) return fail(ORTH_EINVAL, "terms must lie in [1, 64]");
+  if (o->power_iters < 1 || o->power_iters > 1024) return fail(ORTH_EINVAL, "power_iters must lie in [1, 1024]");
+  if (n > 0 && !o->u) return fail(ORTH_EINVAL, "u is NULL");
+  if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
+    return fail(ORTH_EINVAL, "unknown dtype");
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    char buf[160];
+    if (!m.in || !m.out || m.rows != m.cols || m.rows < 1 || m.rows > (1 << 16) || m.ld_in < m.cols ||
+        m.ld_out < m.cols) {
+      snprintf(buf, sizeof buf, "matrix %d: needs non-NULL square C x C data, 1 <= C <= 65536, ld >= C", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    if (m.in == m.out) {
+      snprintf(buf, sizeof buf, "matrix %d: in and out must differ", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+  }
+  return ORTH_OK;
+}
+
+void build_exp_plan(const orth_mat* mats, int32_t n, const orth_exp_opts* o, ExpPlan& P, unsigned char* ws) {
+  const int p = o->terms;
+  P.steps.assign(std::max(p - 1, 0), {});
+  int64_t n_part = 0, n_pw = 0, n_gemm = 0;
+  for (int i = 0; i < n; ++i) {
+    const int64_t t = (mats[i].rows + 63) / 64;
+    n_part += t * t;
+    n_pw += t;
+    n_gemm += t * t;
+  }
+  Arena A;
+  P.off_items = A.take(sizeof(ExpItem) * n);
+  P.off_mats = A.take(sizeof(TiledMat) * n);
+  P.off_partial = A.take(sizeof(TileItem) * n_part);
+  P.off_writeout = A.take(sizeof(TileItem) * n_part);
+  P.off_power[0] = A.take(sizeof(PowerItem) * n_pw);
+  P.off_power[1] = A.take(sizeof(PowerItem) * n_pw);
+  P.off_steps.resize(P.steps.size());
+  for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(sizeof(GemmItem) * n_gemm);
+  P.table_bytes = align_up(A.off);
+  P.off_partials = A.take(sizeof(double) * n_part);
+  P.off_inv = A.take(sizeof(float) * n);
+  P.off_status = A.take(sizeof(int32_t) * n);
+  auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
+  auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
+  int64_t u_off = 0;
+  int part_base = 0;
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    const int C = m.rows;
+    const int64_t cc = (int64_t)C * C;
+    float* a = fbuf(cc);
+    float* ahat = fbuf(cc);
+    float* pp[2] = {fbuf(cc), p > 2 ? fbuf(cc) : nullptr};
+    float* acc = fbuf(cc);
+    float* inv = reinterpret_cast<float*>(dev(P.off_inv)) + i;
+    TiledMat t{};
+    t.in = a;
+    t.out = m.out;
+    t.ld_in = C;
+    t.ld_out = m.ld_out;
+    t.rows = t.cols = t.M = t.N = t.Mp = t.Np = C;
+    t.status_index = i;
+    const int tiles = (C + 63) / 64;
+    t.partial_base = part_base;
+    t.n_partials = tiles * tiles;
+    part_base += tiles * tiles;
+    t.master[0] = acc;
+    t.inv_norm = inv;
+    t.u = o->u + u_off;
+    u_off += C;
+    t.pv = reinterpret_cast<double*>(dev(A.take(sizeof(double) * C)));
+    t.px = reinterpret_cast<double*>(dev(A.take(sizeof(double) * C)));
+    t.py = reinterpret_cast<double*>(dev(A.take(sizeof(double) * C)));
+    t.sig = reinterpret_cast<double*>(dev(A.take(sizeof(double))));
+    P.mats.push_back(t);
+    for (int r = 0; r < tiles; ++r) {
+      P.power[0].push_back(PowerItem{i, r, 0, 0});
+      P.power[1].push_back(PowerItem{i, r, 1, 1});
+      for (int c2 = 0; c2 < tiles; ++c2) {
+        P.partial_items.push_back(TileItem{i, r, c2, 0});
+        P.writeout_items.push_back(TileItem{i, r, c2, 0});
+      }
+    }
+    ExpItem e{};
+    e.in = m.in;
+    e.ld_in = m.ld_in;
+    e.a = a;
+    e.out = acc;
+    e.p0 = ahat;
+    e.inv = inv;
+    e.c = C;
+    e.k = 1;
+    e.size = 1;
+    e.scale = 1.f;
+    P.items.push_back(e);
+    P.max_elems = std::max(P.max_elems, cc);
+    for (int k = 2; k <= p; ++k) {
+      GemmItem g{};
+      g.A = k == 2 ? ahat : pp[(k - 1) & 1];
+      g.B = ahat;              // A^T = -A: C = P_{k-1} Ahat = -(P_{k-1} Ahat^T)
+      g.lda = g.ldb = C;
+      g.K = C;
+      g.M = g.N = C;
+      g.C = pp[k & 1];
+      g.ldc = C;
+      g.dst2 = acc;
+      g.ld2 = C;
+      g.beta = -1.f / k;
+      g.epi = EPI_SERIES;
+      gemm_tiles(g, P.steps[k - 2]);
+    }
+  }
+  P.total_bytes = align_up(A.off);
+}
+
+int validate_conv_exp(const orth_conv_exp_desc* d, int32_t n, int32_t dtype) {
+  if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
+  if (n > 0 && !d) return fail(ORTH_EINVAL, "descs is NULL");
+  if (dtype != ORTH_F32 && dtype != ORTH_BF16) return fail(ORTH_EINVAL, "unknown dtype");
+  for (int i = 0; i < n; ++i) {
+    if (!d[i].kernel || !d[i].out) return fail(ORTH_EINVAL, "NULL data pointer");
+    if (d[i].channels < 1 || d[i].channels > 8192) return fail(ORTH_EINVAL, "channels must lie in [1, 8192]");
+    if (d[i].k < 1 || d[i].k > 15 || d[i].k % 2 == 0) return fail(ORTH_EUNSUPPORTED, "kernel size must be odd, <= 15");
+    if (d[i].terms < 1 || d[i].terms > 32) return fail(ORTH_EINVAL, "terms must lie in [1, 32]");
+    if (!std::isfinite(d[i].scale)) return fail(ORTH_EINVAL, "scale must be finite");
+    if (d[i].kernel == d[i].out) return fail(ORTH_EINVAL, "kernel and out must differ");
+  }
+  return ORTH_OK;
+}
+
+void build_conv_exp_plan(const orth_conv_exp_desc* d, int32_t n, int32_t dtype, ExpPlan& P, unsigned char* ws) {
+  int max_p = 1;
+  for (int i = 0; i < n; ++i) max_p = std::max(max_p, d[i].terms);
+  P.steps.assign(max_p - 1, {});
+  // two passes: count tables, then lay out tables followed by buffers
+  for (int pass = 0; pass < 2; ++pass) {
+    Arena A;
+    if (pass == 1) {
+      P.off_items = A.take(sizeof(ExpItem) * P.items.size());
+      P.off_pairs = A.take(sizeof(GemmPair) * P.pairs.size());
+      P.off_scatter = A.take(sizeof(TapItem) * P.scatter.size());
+      P.off_steps.resize(P.steps.size());
+      for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(sizeof(GemmItem) * P.steps[k].size());
+      P.table_bytes = align_up(A.off);
+      P.items.clear();
+      P.pairs.clear();
+      P.scatter.clear();
+      for (auto& s : P.steps) s.clear();
+    }
+    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 && ws) ? ws + off : nullptr; };
+    auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
+    for (int li = 0; li < n; ++li) {
+      const orth_conv_exp_desc& L = d[li];
+      const int c = L.channels, k = L.k, p = L.terms, S = p * (k - 1) + 1;
+      const int64_t cc = (int64_t)c * c;
+      float* lt = fbuf((int64_t)k * k * cc);
+      float* acc = fbuf((int64_t)S * S * cc);
+      float* q[2] = {p > 1 ? fbuf((int64_t)S * S * cc) : nullptr, p > 2 ? fbuf((int64_t)S * S * cc) : nullptr};
+      ExpItem e{};
+      e.in = L.kernel;
+      e.a = lt;
+      e.out = acc;
+      e.c = c;
+      e.k = k;
+      e.size = S;
+      e.scale = L.scale;
+      P.items.push_back(e);
+      P.max_elems = std::max(P.max_elems, (int64_t)k * k * cc);
+      P.max_init = std::max(P.max_init, (int64_t)S * S * cc);
+      for (int j = 2; j <= p; ++j) {
+        const int sp = (j - 1) * (k - 1) + 1, sj = j * (k - 1) + 1, off = (S - sj) / 2;
+        const float* prev = j == 2 ? lt : q[(j - 1) & 1];
+        float* cur = q[j & 1];
+        for (int y = 0; y < sj; ++y)
+          for (int x = 0; x < sj; ++x) {
+            const int base = (int)P.pairs.size();
+            for (int r = 0; r < k; ++r)
+              for (int t = 0; t < k; ++t) {
+                const int py = y - r, px = x - t;
+                if (py < 0 || py >= sp || px < 0 || px >= sp) continue;
+                GemmPair gp{};
+                gp.A = prev + (int64_t)(py * sp + px) * cc;
+                gp.B = lt + (int64_t)((k - 1 - r) * k + (k - 1 - t)) * cc;   // L_{r,t}^T = -L_{k-1-r,k-1-t}
+                gp.lda = gp.ldb = c;
+                gp.K = c;
+                P.pairs.push_back(gp);
+              }
+            GemmItem g{};
+            g.pair_base = base;
+            g.pair_count = (int)P.pairs.size() - base;
+            g.M = g.N = c;
+            g.C = cur + (int64_t)(y * sj + x) * cc;
+            g.ldc = c;
+            g.dst2 = acc + (int64_t)((y + off) * S + x + off) * cc;
+            g.ld2 = c;
+            g.beta = -1.f / j;
+            g.epi = EPI_SERIES;
+            gemm_tiles(g, P.steps[j - 2]);
+          }
+      }
+      P.scatter.push_back(TapItem{acc, nullptr, L.out, nullptr, c, c, S, S, 0, 0});
+      P.max_scatter = std::max(P.max_scatter, (int64_t)S * S * cc);
+    }
+    P.total_bytes = align_up(A.off);
+  }
+  (void)dtype;
+}
+}  // namespace
+
 // ------------------------------------------------ Björck VJP planning ---
 // The vector-Jacobian product recomputes the forward iterates, saving every
 // X_t and E_t = I - X_t^T X_t (step after step in the workspace), then runs
@@ -1539,6 +1781,105 @@ int orth_conv_apply(const orth_conv_apply_args* a, void* stream) {
   const int64_t pix = (int64_t)a->batch * a->height * a->width;
   if (pix / 64 + 1 > INT32_MAX) return fail(ORTH_EINVAL, "batch x height x width too large");
   ORTH_HIP(launch_conv_apply(a, static_cast<hipStream_t>(stream)));
+  return ORTH_OK;
+}
+
+int orth_exp_map_workspace_size(const orth_mat* mats, int32_t n, const orth_exp_opts* opts, size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  const int rc = validate_exp(mats, n, opts);
+  if (rc) return rc;
+  ExpPlan P;
+  build_exp_plan(mats, n, opts, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* opts, void* workspace,
+                         size_t workspace_bytes, int32_t* status_dev, void* stream) {
+  int rc = validate_exp(mats, n, opts);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  ExpPlan P;
+  build_exp_plan(mats, n, opts, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = ExpPlan();
+  build_exp_plan(mats, n, opts, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_items, P.items);
+  put(img, P.off_mats, P.mats);
+  put(img, P.off_partial, P.partial_items);
+  put(img, P.off_writeout, P.writeout_items);
+  put(img, P.off_power[0], P.power[0]);
+  put(img, P.off_power[1], P.power[1]);
+  for (size_t k = 0; k < P.steps.size(); ++k) put(img, P.off_steps[k], P.steps[k]);
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+  const ExpItem* items = reinterpret_cast<const ExpItem*>(ws + P.off_items);
+  const TiledMat* tm = reinterpret_cast<const TiledMat*>(ws + P.off_mats);
+  auto TI = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
+  double* partials = reinterpret_cast<double*>(ws + P.off_partials);
+  ORTH_HIP(launch_exp_skew(items, n, 0, opts->in_dtype, P.max_elems, s));
+  // spectral normalization of A (the fp32 A in the workspace is the input)
+  ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial), (int)P.partial_items.size(), ORTH_F32, partials, s));
+  ORTH_HIP(launch_power_init(tm, n, s));
+  for (int q = 0; q < opts->power_iters; ++q) {
+    for (int h = 0; h < 2; ++h)
+      ORTH_HIP(launch_power_dot(tm, reinterpret_cast<const PowerItem*>(ws + P.off_power[h]), (int)P.power[h].size(),
+                                ORTH_F32, s));
+    ORTH_HIP(launch_power_normalize(tm, n, s));
+  }
+  ORTH_HIP(launch_prescale_finish(tm, n, partials, ORTH_PRESCALE_SPECTRAL, status, s));
+  ORTH_HIP(launch_exp_init(items, n, 0, P.max_elems, s));
+  for (size_t k = 0; k < P.steps.size(); ++k)
+    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_steps[k]), (int)P.steps[k].size(),
+                             "exp_map_series", s));
+  ORTH_HIP(launch_writeout(tm, TI(P.off_writeout), (int)P.writeout_items.size(), 0, opts->out_dtype, s));
+  return ORTH_OK;
+}
+
+int orth_conv_exp_workspace_size(const orth_conv_exp_desc* descs, int32_t n, int32_t dtype, size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  const int rc = validate_conv_exp(descs, n, dtype);
+  if (rc) return rc;
+  ExpPlan P;
+  build_conv_exp_plan(descs, n, dtype, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  int rc = validate_conv_exp(descs, n, dtype);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  ExpPlan P;
+  build_conv_exp_plan(descs, n, dtype, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = ExpPlan();
+  build_conv_exp_plan(descs, n, dtype, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  std::vector<unsigned char> img(P.table_bytes, 0);
+  put(img, P.off_items, P.items);
+  put(img, P.off_pairs, P.pairs);
+  put(img, P.off_scatter, P.scatter);
+  for (size_t k = 0; k < P.steps.size(); ++k) put(img, P.off_steps[k], P.steps[k]);
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+  const ExpItem* items = reinterpret_cast<const ExpItem*>(ws + P.off_items);
+  ORTH_HIP(launch_exp_skew(items, n, 1, dtype, P.max_elems, s));
+  ORTH_HIP(launch_exp_init(items, n, 1, P.max_init, s));
+  const GemmPair* pairs = reinterpret_cast<const GemmPair*>(ws + P.off_pairs);
+  for (size_t k = 0; k < P.steps.size(); ++k)
+    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_steps[k]), (int)P.steps[k].size(),
+                             "conv_exp_series", s, 0, pairs));
+  ORTH_HIP(launch_tap_items(2, reinterpret_cast<const TapItem*>(ws + P.off_scatter), (int)P.scatter.size(), dtype,
+                            P.max_scatter, s));
   return ORTH_OK;
 }
 

@@ -114,7 +114,19 @@ enum GemmEpi : int32_t {
   EPI_GRAM_E = 1,    // C[i][j] = delta_ij - acc  (and C[j][i] if mirror)
   EPI_UPDATE = 2,    // v = src[i][j] + beta acc; C[i][j] = v; dst2[j][i] = v if dst2
   EPI_MAXDEV = 3,    // red[0] = max(red[0], |delta_ij - acc|)
-  EPI_NEG = 4        // C[i][j] = -acc  (and C[j][i] if mirror)
+  EPI_NEG = 4,       // C[i][j] = -acc  (and C[j][i] if mirror)
+  EPI_SERIES = 5     // v = beta acc; C[i][j] = v (fp32); dst2[i][j] += v (ld2)
+};
+
+// A further operand pair of a GEMM item (same storage dtypes as the item's
+// first pair): C += A B^T with A logically M x K, B logically N x K.
+struct GemmPair {
+  const void* A;
+  const void* B;
+  int64_t lda, ldb;
+  int32_t K;
+  int32_t a_trans, b_trans;
+  int32_t pad;
 };
 
 struct GemmItem {
@@ -138,6 +150,8 @@ struct GemmItem {
   int32_t mirror;
   float beta;
   int32_t c_dtype;           // EPI_STORE: storage of C
+  int32_t pair_base;         // further operand pairs: the launch's pair table
+  int32_t pair_count;        //   [pair_base, pair_base + pair_count)
 };
 
 // Compose (AOC) descriptors: one entry per (layer, group).
@@ -206,7 +220,8 @@ hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_it
                            int master_index, int out_dtype, hipStream_t s);
 hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
                              hipStream_t s, int vjp = 0, int step = 0);
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step = 0);
+hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step = 0,
+                           const GemmPair* pairs = nullptr);
 hipError_t launch_vjp_load_grad(const TiledMat* mats, const TileItem* items, int n_items, int gout_dtype,
                                 hipStream_t s);
 hipError_t launch_vjp_dot_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
@@ -222,9 +237,27 @@ hipError_t launch_compose_scatter(const ComposeGroup* groups, int n_groups, int 
                                   int64_t max_elems, hipStream_t s);
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // kind: 0 taps from the RKO matrix, 1 taps from an OIHW kernel gradient,
-// 2 RKO gradient from taps, 3 forward combine, 4 adjoint combine
+// 2 RKO gradient (or any OIHW tensor) from taps, 3 forward combine,
+// 4 adjoint combine
 hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dtype, int64_t max_elems,
                             hipStream_t s);
+
+// Exponentials (expo.hip).  One item per matrix or conv layer.
+struct ExpItem {
+  const void* in;            // W (C x C, caller layout) or the kernel K (c x c x k x k, OIHW)
+  float* a;                  // exp map: A = W - W^T (C x C); conv: L taps (k x k grid)
+  float* out;                // the fp32 series accumulator (C x C, or S x S taps)
+  float* p0;                 // exp map: first power Ahat; unused for conv
+  const float* inv;          // exp map: 1 / sigma of A (from the spectral pre-scaling kernels)
+  int64_t ld_in;
+  int32_t c;                 // C, or channels c
+  int32_t k;                 // conv: kernel size (1 for the exp map)
+  int32_t size;              // conv: S = terms (k - 1) + 1 (1 for the exp map)
+  float scale;               // conv: L = scale (K - K*)
+};
+hipError_t launch_exp_skew(const ExpItem* items, int n_items, int conv, int in_dtype, int64_t max_elems,
+                           hipStream_t s);
+hipError_t launch_exp_init(const ExpItem* items, int n_items, int conv, int64_t max_elems, hipStream_t s);
 hipError_t launch_conv_apply(const orth_conv_apply_args* a, hipStream_t s);
 hipError_t launch_conv_check(const orth_check_args* a, const void* kernel, const float* x,
                              double* partial, float* out, int adjoint, hipStream_t s);

@@ -25,6 +25,7 @@ EXPORTED = [
     "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
     "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched", "orth_conv_apply",
+    "orth_exp_map_workspace_size", "orth_exp_map_batched", "orth_conv_exp_workspace_size", "orth_conv_exp_batched",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
     "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
 ]
@@ -52,6 +53,16 @@ class orth_vjp_mat(ctypes.Structure):
     _fields_ = [("w", ctypes.c_void_p), ("grad_out", ctypes.c_void_p), ("grad_in", ctypes.c_void_p),
                 ("rows", ctypes.c_int32), ("cols", ctypes.c_int32), ("ld_w", ctypes.c_int64),
                 ("ld_grad_out", ctypes.c_int64), ("ld_grad_in", ctypes.c_int64)]
+
+
+class orth_exp_opts(ctypes.Structure):
+    _fields_ = [("terms", ctypes.c_int32), ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p),
+                ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32)]
+
+
+class orth_conv_exp_desc(ctypes.Structure):
+    _fields_ = [("channels", ctypes.c_int32), ("k", ctypes.c_int32), ("terms", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("kernel", ctypes.c_void_p), ("out", ctypes.c_void_p)]
 
 
 class orth_conv_geom(ctypes.Structure):
@@ -102,6 +113,10 @@ def lib():
         L.orth_build_conv_kernels_vjp_workspace_size.argtypes = [P(orth_conv_vjp_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_vjp_batched.argtypes = [P(orth_conv_vjp_desc), i32, i32, vp, sz, vp]
         L.orth_conv_apply.argtypes = [P(orth_conv_apply_args), vp]
+        L.orth_exp_map_workspace_size.argtypes = [P(orth_mat), i32, P(orth_exp_opts), P(sz)]
+        L.orth_exp_map_batched.argtypes = [P(orth_mat), i32, P(orth_exp_opts), vp, sz, vp, vp]
+        L.orth_conv_exp_workspace_size.argtypes = [P(orth_conv_exp_desc), i32, i32, P(sz)]
+        L.orth_conv_exp_batched.argtypes = [P(orth_conv_exp_desc), i32, i32, vp, sz, vp]
         L.orth_check_workspace_size.argtypes = [P(orth_check_args), P(sz)]
         L.orth_check_norm.argtypes = [P(orth_check_args), vp, vp, sz, vp]
         L.orth_status_string.argtypes = [ctypes.c_int]
@@ -349,6 +364,55 @@ def orth_conv_apply(kernel, geom, x, transposed=False, stream=None):
                                 x.data_ptr(), y.data_ptr(), b, h, w)
     _check(lib().orth_conv_apply(ctypes.byref(args), _stream(stream)), "orth_conv_apply")
     return y
+
+
+def orth_exp_map_batched(ins, outs, terms, u, power_iters=1, status=None, workspace=None, stream=None):
+    """What = exp(A / sigma), A = W - W^T, for every square ins[i] into
+    outs[i] (see include/orth.h); u: packed float32 cached vectors (C per
+    matrix), updated in place.  Returns the workspace tensor."""
+    if not ins:
+        return None
+    mats = _mats(ins, outs)
+    in_dt, out_dt = _dtype_code(ins[0]), _dtype_code(outs[0])
+    for a, b in zip(ins, outs):
+        if _dtype_code(a) != in_dt or _dtype_code(b) != out_dt:
+            raise TypeError("all inputs (and all outputs) must share one dtype")
+    need = sum(t.shape[0] for t in ins)
+    if u.dtype != torch.float32 or not u.is_contiguous() or u.numel() < need:
+        raise ValueError(f"u must be a contiguous float32 tensor of {need} values")
+    opts = orth_exp_opts(terms, power_iters, u.data_ptr(), in_dt, out_dt)
+    n = ctypes.c_size_t()
+    _check(lib().orth_exp_map_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
+           "orth_exp_map_workspace_size")
+    ws, nbytes = _workspace(n.value, ins[0].device, workspace)
+    if status is not None and (status.dtype != torch.int32 or status.numel() < len(ins)):
+        raise ValueError("status must be an int32 tensor with one slot per matrix")
+    rc = lib().orth_exp_map_batched(mats, len(ins), ctypes.byref(opts), ws.data_ptr() if ws is not None else None,
+                                    nbytes, status.data_ptr() if status is not None else None, _stream(stream))
+    _check(rc, "orth_exp_map_batched")
+    return ws
+
+
+def orth_conv_exp_batched(layers, workspace=None, stream=None):
+    """layers: dicts with kernel (c x c x k x k), out (c x c x S x S,
+    S = terms (k - 1) + 1), terms and scale; contiguous, one dtype."""
+    if not layers:
+        return None
+    dt = _dtype_code(layers[0]["kernel"])
+    arr = (orth_conv_exp_desc * len(layers))()
+    for i, L in enumerate(layers):
+        kern, out = L["kernel"], L["out"]
+        if not kern.is_contiguous() or not out.is_contiguous() or _dtype_code(kern) != dt or _dtype_code(out) != dt:
+            raise ValueError("kernel and out must be contiguous and of one dtype")
+        c, k = kern.shape[0], kern.shape[2]
+        arr[i] = orth_conv_exp_desc(c, k, L["terms"], float(L.get("scale", 1.0)), kern.data_ptr(), out.data_ptr())
+    n = ctypes.c_size_t()
+    _check(lib().orth_conv_exp_workspace_size(arr, len(layers), dt, ctypes.byref(n)), "orth_conv_exp_workspace_size")
+    ws, nbytes = _workspace(n.value, layers[0]["kernel"].device, workspace)
+    rc = lib().orth_conv_exp_batched(arr, len(layers), dt, ws.data_ptr() if ws is not None else None, nbytes,
+                                     _stream(stream))
+    _check(rc, "orth_conv_exp_batched")
+    return ws
 
 
 def _check_call(args, out, workspace, stream):

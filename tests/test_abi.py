@@ -272,3 +272,30 @@ def test_conv_apply_validation(L, kw, code):
     a = orth.orth_conv_apply_args(orth.orth_conv_geom(*geom), 0x1000, kw.get("kernel_dtype", 0), 0, 0x2000,
                                   0x2000 if kw.get("same") else 0x3000, kw.get("batch", 2), kw.get("height", 8), 8)
     assert L.orth_conv_apply(ctypes.byref(a), None) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), orth.ORTH_OK), (dict(terms=0), orth.ORTH_EINVAL), (dict(terms=65), orth.ORTH_EINVAL),
+    (dict(q=0), orth.ORTH_EINVAL), (dict(u=None), orth.ORTH_EINVAL), (dict(shape=(8, 6)), orth.ORTH_EINVAL),
+])
+def test_exp_map_validation(L, kw, code):
+    shape = kw.get("shape", (64, 64))
+    opts = orth.orth_exp_opts(kw.get("terms", 12), kw.get("q", 1), kw.get("u", 0x1000), 0, 0)
+    n = ctypes.c_size_t()
+    rc = L.orth_exp_map_workspace_size(_mats([shape, (130, 130)]), 2, ctypes.byref(opts), ctypes.byref(n))
+    assert rc == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(), orth.ORTH_OK), (dict(k=4), orth.ORTH_EUNSUPPORTED), (dict(terms=0), orth.ORTH_EINVAL),
+    (dict(c=0), orth.ORTH_EINVAL), (dict(scale=float("nan")), orth.ORTH_EINVAL), (dict(same=True), orth.ORTH_EINVAL),
+])
+def test_conv_exp_validation(L, kw, code):
+    d = (orth.orth_conv_exp_desc * 1)()
+    d[0] = orth.orth_conv_exp_desc(kw.get("c", 16), kw.get("k", 3), kw.get("terms", 6), kw.get("scale", 1.0), 0x1000,
+                                   0x1000 if kw.get("same") else 0x2000)
+    n = ctypes.c_size_t()
+    assert L.orth_conv_exp_workspace_size(d, 1, 0, ctypes.byref(n)) == code
+    if code == orth.ORTH_OK:
+        # tables plus L (9 taps), E and two power grids of 13 x 13 taps of 16 x 16 fp32
+        assert n.value >= (9 + 3 * 169) * 256 * 4
