@@ -8,7 +8,7 @@ already resident in HBM.  Prints one JSON line.
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--vjp [--vjp-steps K]] [--copy-calibration]
                     [--prescale spectral [--power-iters Q]] [--iters T]
-                    [--conv-apply [--apply-batch B]]
+                    [--conv-apply [--apply-batch B]] [--expo]
 
 With --vjp the backward pass (dL/dK and dL/d(output) back to the raw
 parameters) is timed too and reported under "vjp".
@@ -329,6 +329,64 @@ def run_conv_apply(w, layers, batch, steps, torch, orth, dev):
     return out
 
 
+def run_expo(w, ins, steps, torch, orth, dev, terms=12, conv_terms=6):
+    """Exponential map of every square matrix of the workload and explicit
+    conv exponential of every stride-1 c -> c conv layer; algorithmic flop:
+    (p - 1) 2 C^3 per matrix, and 2 c^3 per tap product of the conv series."""
+    sq = [t for t in ins if t.shape[0] == t.shape[1] and t.shape[0] > 1]
+    convs = [L for L in w.layers if hasattr(L, "k") and L.stride == 1 and L.cin == L.cout and L.groups == 1
+             and L.k % 2 == 1]
+    out = {}
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed + 500)
+    jobs = []
+    if sq:
+        outs = [torch.empty(t.shape, dtype=torch.float32, device=dev) for t in sq]
+        u = torch.randn(sum(t.shape[0] for t in sq), generator=gen, device=dev)
+        ws = orth.orth_exp_map_batched(sq, outs, terms, u, 1)
+        flops = sum((terms - 1) * 2 * t.shape[0] ** 3 for t in sq)
+        jobs.append(("exp_map", lambda: orth.orth_exp_map_batched(sq, outs, terms, u, 1, workspace=ws), flops,
+                     "exp_map_series", len(sq)))
+    if convs:
+        layers = []
+        flops = 0
+        for L in convs:
+            c, k = L.cin, L.k
+            S = conv_terms * (k - 1) + 1
+            kern = torch.randn(c, c, k, k, generator=gen, device=dev)
+            layers.append(dict(kernel=kern, out=torch.empty(c, c, S, S, device=dev), terms=conv_terms, scale=0.1))
+            for j in range(2, conv_terms + 1):
+                sp, sj = (j - 1) * (k - 1) + 1, j * (k - 1) + 1
+                pairs = sum(1 for y in range(sj) for x in range(sj) for r in range(k) for t in range(k)
+                            if 0 <= y - r < sp and 0 <= x - t < sp)
+                flops += pairs * 2 * c ** 3
+        cws = orth.orth_conv_exp_batched(layers)
+        jobs.append(("conv_exp", lambda: orth.orth_conv_exp_batched(layers, workspace=cws), flops,
+                     "conv_exp_series", len(layers)))
+    torch.cuda.synchronize()
+    for name, fn, flops, kname, count in jobs:
+        fn()
+        torch.cuda.synchronize()
+        orth.orth_timing_enable(True)
+        orth.orth_timing_reset()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        kt = orth.orth_timing_read(kname)
+        orth.orth_timing_enable(False)
+        ms = (t1 - t0) * 1e3 / steps
+        kms = kt[0] / steps
+        ach = flops / (kms / 1e3) / 1e12
+        out[name] = {"count": count, "terms": terms if name == "exp_map" else conv_terms,
+                     "ms_per_call": round(ms, 3), "algorithmic_flops": flops,
+                     "roofline": {"bound": "mfma", "kernel": kname, "achieved": round(ach, 1),
+                                  "peak": PEAK_F32_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_F32_TFLOPS, 4),
+                                  "traffic": None, "avg_launch_ms": round(kt[0] / kt[1], 4)}}
+    return out or None
+
+
 def cpu_baseline(w, budget_s=25.0):
     """Time the float64 oracle on a bounded sample of the workload and scale
     to the whole workload."""
@@ -387,6 +445,9 @@ def main():
                     help="also time the application of every conv layer's kernel (forward and transposed) "
                          "to a batch of images")
     ap.add_argument("--apply-batch", type=int, default=64)
+    ap.add_argument("--expo", action="store_true",
+                    help="also time the exponential map of every square matrix (12 terms) and the explicit conv "
+                         "exponential of every stride-1 c -> c conv layer (6 terms)")
     ap.add_argument("--vjp", action="store_true",
                     help="also time the backward pass (composition and Björck vector-Jacobian products)")
     ap.add_argument("--vjp-steps", type=int, default=3)
@@ -502,6 +563,10 @@ def main():
     if args.conv_apply:
         capply = run_conv_apply(w, layers, args.apply_batch, 3, torch, orth, dev)
 
+    expo_rec = None
+    if args.expo:
+        expo_rec = run_expo(w, ins, 3, torch, orth, dev)
+
     vjp = None
     if args.vjp:
         vjp = run_vjp(w, ins, outs, layers, status, compute, args.vjp_steps, 1, torch, orth, dev)
@@ -540,6 +605,8 @@ def main():
         rec["power_iteration"] = power
     if capply is not None:
         rec["conv_apply"] = capply
+    if expo_rec is not None:
+        rec["exponentials"] = expo_rec
     if vjp is not None:
         rec["vjp"] = vjp
     print(json.dumps(rec), flush=True)
