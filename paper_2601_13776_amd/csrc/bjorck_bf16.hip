@@ -73,10 +73,13 @@ __device__ __forceinline__ void dma16(const void* g, void* lds) { __builtin_amdg
 // group of 16 lanes, if lane j addresses row k0 + j / 4, columns
 // c0 + 4 (j % 4) .. + 3 of a [k][column] bf16 tile, lane l receives
 // columns c0 + l, rows k0 .. k0 + 3: half of an MFMA A/B fragment.
+// The address is cast pointer to pointer (not through an integer) so that
+// alias analysis still sees which LDS array it reads: a read of one stage
+// then needs no wait for the asynchronous loads into the other.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint2 lds_read_tr(const uint16_t* p) {
   const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) s16x4*)(reinterpret_cast<uintptr_t>(p)));
+      (__attribute__((address_space(3))) s16x4*)(const_cast<uint16_t*>(p)));
   return __builtin_bit_cast(uint2, v);
 }
 
@@ -194,18 +197,24 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
   };
   constexpr int NR = (AT ? 2 : 1) * MI + (BT ? 2 : 1) * NI, NM = MI * NI;
   constexpr int NRF = NR < NM ? NR : NM;
+  // The loads of a sub-step go out before its fragment reads, fenced off by a
+  // scheduling barrier: every load sets M0, and an M0 write waits for all
+  // LDS reads in flight, so reads issued ahead of the loads would stall the
+  // wave (with the MFMA pipe draining) until they return.
   auto kstep = [&](uint16_t* ca, uint16_t* cb, uint16_t* na, uint16_t* nb, int kt) {
     const int kn = kb + (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
     lds_settle();
-    rd(1, ca, cb, 1);
     oa.issue(na, kn, wave);
+    __builtin_amdgcn_sched_barrier(0);
+    rd(1, ca, cb, 1);
     mma(0);
-    fence_substep<NM, NRF, decltype(oa)::NBLK>();
+    fence_substep<NM, NRF, 0>();
     lds_settle();
-    rd(0, ca, cb, 2);
     ob.issue(nb, kn, wave);
+    __builtin_amdgcn_sched_barrier(0);
+    rd(0, ca, cb, 2);
     mma(1);
-    fence_substep<NM, NRF, decltype(ob)::NBLK>();
+    fence_substep<NM, NRF, 0>();
     lds_settle();
     rd(1, ca, cb, 3);
     mma(0);
