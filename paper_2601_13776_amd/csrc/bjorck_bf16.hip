@@ -98,6 +98,36 @@ __device__ __forceinline__ void fence_substep() {
 }
 __device__ __forceinline__ void lds_settle() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Scheduling plan of one sub-step of NMFMA MFMAs: its NDMA loads go out
+// DPS per MFMA over the first slots (each load sets M0, and an M0 write
+// waits for every LDS read in flight, so no read is issued before them),
+// then its NREADS fragment reads are spread over the following slots, and
+// the last TAIL MFMAs issue no read, so that the reads have returned when
+// the next sub-step waits for them.
+template <int Q, int NMFMA, int NREADS, int NDMA, int DPS, int TAIL>
+__device__ __forceinline__ void plan_slots() {
+  if constexpr (Q < NMFMA) {
+    constexpr int DSLOTS = (NDMA + DPS - 1) / DPS;
+    constexpr int RSLOTS = NMFMA - TAIL - DSLOTS;
+    static_assert(RSLOTS > 0 || NREADS == 0, "no MFMA slot left for the fragment reads");
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (Q < DSLOTS) {
+      constexpr int n = (Q + 1) * DPS <= NDMA ? DPS : NDMA - Q * DPS;
+      __builtin_amdgcn_sched_group_barrier(0x010, n, 0);
+    } else if constexpr (Q < DSLOTS + RSLOTS) {
+      constexpr int slot = Q - DSLOTS;
+      constexpr int lo = slot * NREADS / RSLOTS, hi = (slot + 1) * NREADS / RSLOTS;
+      if constexpr (hi > lo) __builtin_amdgcn_sched_group_barrier(0x100, hi - lo, 0);
+    }
+    plan_slots<Q + 1, NMFMA, NREADS, NDMA, DPS, TAIL>();
+  }
+}
+template <int NMFMA, int NREADS, int NDMA, int DPS, int TAIL>
+__device__ __forceinline__ void fence_plan() {
+  plan_slots<0, NMFMA, NREADS, NDMA, DPS, TAIL>();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // One operand of the tile product, staged in LDS either as [row][k]
 // (TRANS = false: the operand's rows are contiguous along k in memory) or
 // as [k][row] (TRANS = true: memory holds it k-major, each k a contiguous
@@ -156,6 +186,11 @@ struct Operand {
   }
 };
 
+// Measured on the 256-tiles: one load per MFMA slot and four read-free MFMAs
+// at the end of each sub-step (two loads per slot or no tail were slower).
+constexpr int DMA_PER_SLOT = 1;
+constexpr int READ_TAIL = 4;
+
 template <int BM, int BN, int WM, int WN>
 struct Tile {
   static constexpr int BK = 64, NW = WM * WN, TM = BM / WM, TN = BN / WN, MI = TM / 32, NI = TN / 32;
@@ -197,34 +232,49 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
   };
   constexpr int NR = (AT ? 2 : 1) * MI + (BT ? 2 : 1) * NI, NM = MI * NI;
   constexpr int NRF = NR < NM ? NR : NM;
-  // The loads of a sub-step go out before its fragment reads, fenced off by a
-  // scheduling barrier: every load sets M0, and an M0 write waits for all
-  // LDS reads in flight, so reads issued ahead of the loads would stall the
-  // wave (with the MFMA pipe draining) until they return.
+  // The loads of a sub-step go out before its fragment reads: every load sets
+  // M0, and an M0 write waits for all LDS reads in flight, so reads issued
+  // ahead of the loads would stall the wave (with the MFMA pipe draining)
+  // until they return.  On 256-tiles the loads ride along the first MFMAs of
+  // the sub-step (fence_plan); on 128-tiles, with four MFMAs per sub-step,
+  // they go out first behind a scheduling barrier.
   auto kstep = [&](uint16_t* ca, uint16_t* cb, uint16_t* na, uint16_t* nb, int kt) {
     const int kn = kb + (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+    constexpr bool BIG = NM >= 16;   // 256-tiles: loads and reads spread over the sub-step
     lds_settle();
     oa.issue(na, kn, wave);
-    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(1, ca, cb, 1);
     mma(0);
-    fence_substep<NM, NRF, 0>();
+    if constexpr (BIG)
+      fence_plan<NM, NR, decltype(oa)::NBLK, DMA_PER_SLOT, READ_TAIL>();
+    else
+      fence_substep<NM, NRF, 0>();
     lds_settle();
     ob.issue(nb, kn, wave);
-    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(0, ca, cb, 2);
     mma(1);
-    fence_substep<NM, NRF, 0>();
+    if constexpr (BIG)
+      fence_plan<NM, NR, decltype(ob)::NBLK, DMA_PER_SLOT, READ_TAIL>();
+    else
+      fence_substep<NM, NRF, 0>();
     lds_settle();
     rd(1, ca, cb, 3);
     mma(0);
-    fence_substep<NM, NRF, 0>();
+    if constexpr (BIG)
+      fence_plan<NM, NR, 0, 1, READ_TAIL>();
+    else
+      fence_substep<NM, NRF, 0>();
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
     __syncthreads();
     __builtin_amdgcn_sched_barrier(0);
     rd(0, na, nb, 0);
     mma(1);
-    fence_substep<NM, NRF, 0>();
+    if constexpr (BIG)
+      fence_plan<NM, NR, 0, 1, READ_TAIL>();
+    else
+      fence_substep<NM, NRF, 0>();
   };
   oa.issue(sA0, kb, wave);
   ob.issue(sB0, kb, wave);
