@@ -88,3 +88,75 @@ def test_imagenet_stack_full_size():
         L, r, p, k = layers[li]
         ref = aoc.aoc_kernel(to_f64(r), to_f64(p), L.cin, L.cout, L.k, L.stride, L.dilation, L.groups)
         assert checks.relative_difference(to_f64(k), ref) <= REL_F32, li
+
+
+def test_stress_vjp_full_size():
+    """The backward pass of the whole stress batch in one call (bench.py
+    --vjp's configuration): every gradient finite; the 32^2 samples (fp32
+    products) against the oracle; the 4096^2 gradients, too costly for the
+    oracle at T = 25, through properties that hold at any size: orthogonal
+    to W (Frobenius scale invariance) and linear in the upstream gradient."""
+    from oracle import bjorck_grad
+    w = wl.WORKLOADS["stress_4096x64_32x4096"]
+    shapes = w.matrix_shapes()
+    ins = [to_dev(wl.stored_matrix(w, i, *s)) for i, s in enumerate(shapes)]
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(9)
+    gouts = [torch.randn(s, generator=gen, device=DEV) for s in shapes]
+    gins = [torch.empty_like(t) for t in ins]
+    status = torch.full((len(ins),), -1, dtype=torch.int32, device=DEV)
+    ws = orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, compute="bf16", status=status)
+    torch.cuda.synchronize()
+    print("[stress vjp] done", flush=True)
+    assert np.all(status.cpu().numpy() == 0)
+    for g in gins[:64]:
+        assert bool(torch.isfinite(g.float()).all())
+    for i in list(range(64, 4160, 257)):
+        # fp32 products, but the gradient is returned in the parameters'
+        # dtype (bf16): one rounding of every element bounds the difference
+        ref = bjorck_grad.bjorck_vjp(wl.as_f64(wl.stored_matrix(w, i, 32, 32)), to_f64(gouts[i]), w.iters)
+        assert checks.relative_difference(to_f64(gins[i]), ref) <= BF16_REL, i
+    for i in (0, 37, 63):
+        wf, gf = to_f64(ins[i]), to_f64(gins[i])
+        assert abs(float(np.sum(wf * gf))) <= 2e-2 * np.linalg.norm(wf) * np.linalg.norm(gf), i
+    # linearity in the upstream gradient on three of the large matrices
+    sel = [0, 37, 63]
+    g2 = [torch.randn(shapes[i], generator=gen, device=DEV) for i in sel]
+    comb = [(2.0 * gouts[i] - g).contiguous() for i, g in zip(sel, g2)]
+    outs = {}
+    for key, gl in (("a", [gouts[i] for i in sel]), ("b", g2), ("c", comb)):
+        gi = [torch.empty_like(ins[i]) for i in sel]
+        orth.orth_orthogonalize_vjp_batched([ins[i] for i in sel], gl, gi, w.iters, compute="bf16")
+        outs[key] = gi
+    torch.cuda.synchronize()
+    del ws
+    for a, b, c in zip(outs["a"], outs["b"], outs["c"]):
+        lin = 2.0 * to_f64(a) - to_f64(b)
+        assert checks.relative_difference(to_f64(c), lin) <= 5e-2
+
+
+def test_imagenet_spectral_full_size():
+    """Spectral pre-scaling (one power step from vectors warmed by five) on
+    all 89 factors of the ImageNet-like stack in one call; sampled factors
+    and their new vectors against the oracle."""
+    from oracle import spectral
+    w = wl.WORKLOADS["imagenet_backbone25"]
+    shapes = w.matrix_shapes()
+    ins = [to_dev(wl.stored_matrix(w, i, *s)) for i, s in enumerate(shapes)]
+    outs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in ins]
+    rng = np.random.default_rng(11)
+    u0 = [rng.standard_normal(min(s)).astype(np.float32) for s in shapes]
+    u = torch.from_numpy(np.concatenate(u0)).to(DEV)
+    orth.orth_orthogonalize_batched(ins, outs, 0, compute="bf16", prescale="spectral", power_iters=5, u=u)
+    warm = u.cpu().numpy().copy()
+    orth.orth_orthogonalize_batched(ins, outs, w.iters, compute="bf16", prescale="spectral", power_iters=1, u=u)
+    torch.cuda.synchronize()
+    un = u.cpu().numpy()
+    offs = np.cumsum([0] + [min(s) for s in shapes])
+    for i in (0, 1, 20, 61, 80, 88):
+        print(f"[imagenet spectral] factor {i} {shapes[i]}", flush=True)
+        x = wl.as_f64(wl.stored_matrix(w, i, *shapes[i]))
+        v0 = warm[offs[i]:offs[i + 1]].astype(np.float64)
+        ref, v, _ = spectral.bjorck_spectral(x, v0, w.iters, 1)
+        assert checks.relative_difference(to_f64(outs[i]), ref) <= BF16_REL, i
+        assert np.max(np.abs(un[offs[i]:offs[i + 1]] - v)) <= 1e-5, i
