@@ -370,6 +370,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
     buf = reinterpret_cast<float*>((wave < 2 ? sA0 : sB0) + (wave & 1) * (32 * TN * 2));
   else
     buf = reinterpret_cast<float*>(wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1);
+  // update tiles: each wave's fp32 iterate chunk (32 x TN) is prefetched by
+  // direct-to-LDS loads into a second private buffer, so that the loads of
+  // chunk mi + 1 fly while chunk mi is written (no registers held)
+  uint16_t* mbuf;
+  if (BM == 256)
+    mbuf = (wave < 2 ? sA1 : sB1) + (wave & 1) * (32 * TN * 2);
+  else
+    mbuf = (wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1) + 32 * TN * 2;
   auto bidx = [&](int r, int c) {  // float index of element (r, c) of the staging buffer
     return r * TN + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 2) + (c & 3);
   };
@@ -384,17 +392,30 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   uint16_t* Xo = static_cast<uint16_t*>(VJP ? d->yc[parity ^ 1] : d->xc[parity ^ 1]) + (VJP ? 0 : xoff);
   constexpr float DELTA = VJP ? 0.f : 1.f;
   constexpr int NQ = 32 * TN / 256;        // 4-column groups per lane and chunk
+  // chunk mi of the iterate into mbuf, row-major (TN floats per row): load q
+  // of a lane covers the same (row, 4 columns) that its row-major pass reads
+  auto load_chunk = [&](int mi) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int e4 = q * 64 + lane;
+      const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
+      dma16(Xm + (int64_t)(gi0 + mi * 32 + r) * Np + gj0 + c, mbuf + q * 512);
+    }
+  };
+  if (MODE == 1) load_chunk(0);
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
     const int gi = gi0 + mi * 32;
-    // update tiles: this chunk's fp32 iterate loads go out first
     float4 mpre[NQ];
     if (MODE == 1) {
+      // this chunk's iterate from LDS, then the next chunk's loads
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int e4 = q * 64 + lane;
-        const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
-        mpre[q] = *reinterpret_cast<const float4*>(Xm + (int64_t)(gi + r) * Np + gj0 + c);
+      for (int q = 0; q < NQ; ++q)
+        mpre[q] = *reinterpret_cast<const float4*>(mbuf + q * 512 + lane * 8);
+      if (mi + 1 < MI) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        load_chunk(mi + 1);
       }
     }
     // accumulators -> LDS, row-major
