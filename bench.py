@@ -118,12 +118,15 @@ def class_flops(w, kernel_name):
     named tiled kernel: every matrix of its size class contributes
     4 m n min(m, n) T (a Gram and an update product per iteration)."""
     out = 0
-    for r, c in w.matrix_shapes():
-        m, n = max(r, c), min(r, c)
+    shapes = [(max(r, c), min(r, c)) for r, c in w.matrix_shapes()]
+    # 256-tiles only when the wide matrices' update tiles fill four waves of
+    # the 256 compute units (the library's planning rule)
+    big = sum(-(-m // 256) * -(-n // 256) for m, n in shapes if n >= 1024) >= 4 * 256
+    for m, n in shapes:
         if n <= 64 and m <= 128:          # fused small-matrix kernel
             continue
         if w.dtype == "bf16":
-            cls = "256" if n >= 1024 else "128"
+            cls = "256" if n >= 1024 and big else "128"
             if not kernel_name.endswith(cls):
                 continue
         out += 4 * m * n * n * w.iters

@@ -86,6 +86,12 @@ typedef struct {
                            packed in batch order, min(rows, cols) values for
                            each; read, and overwritten with the new estimate
                            (left unchanged for a zero or non-finite matrix) */
+  /* bf16 products only (ignored otherwise): tile edge of the matrices with
+   * min(rows, cols) >= 1024.  0 chooses by occupancy (256 x 256 tiles when
+   * those matrices hold at least 1024 of them, else 128 x 128); 128 or 256
+   * forces that size.  The result does not depend on it beyond fp32
+   * rounding order. */
+  int32_t tile;
 } orth_bjorck_opts;
 
 /*
@@ -110,8 +116,8 @@ typedef struct {
  * or non-finite matrix does not fail the call.
  * Returns ORTH_EINVAL for n < 0, a NULL pointer, rows or cols < 1,
  * ld < cols, iters < 0, beta outside (0, 0.5], an unknown dtype, compute or
- * prescale mode, in == out with differing dtype/leading dim, or (spectral)
- * power_iters outside [1, 1024] or u == NULL.
+ * prescale mode, in == out with differing dtype/leading dim, tile not in
+ * {0, 128, 256}, or (spectral) power_iters outside [1, 1024] or u == NULL.
  */
 int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n,
                                       const orth_bjorck_opts* opts, size_t* bytes);

@@ -194,6 +194,7 @@ int validate_ortho(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o) {
   if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
     return fail(ORTH_EINVAL, "unknown dtype");
   if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
+  if (o->tile != 0 && o->tile != 128 && o->tile != 256) return fail(ORTH_EINVAL, "tile must be 0, 128 or 256");
   for (int i = 0; i < n; ++i) {
     const orth_mat& m = mats[i];
     char buf[160];
@@ -225,6 +226,10 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   P.mp.resize(n);
   std::vector<int> tiled_of(n, -1);
   int n_tiled = 0;
+  std::vector<std::pair<int, int>> dims(n);
+  for (int i = 0; i < n; ++i)
+    dims[i] = {std::max(mats[i].rows, mats[i].cols), std::min(mats[i].rows, mats[i].cols)};
+  const bool big_tiles = use_big_tiles(dims, o->tile);
   for (int i = 0; i < n; ++i) {
     const orth_mat& m = mats[i];
     MatPlan& q = P.mp[i];
@@ -239,7 +244,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
       q.bucket = TILED_F32;
       q.Mp = (int32_t)round_up(q.M, 64);
       q.Np = (int32_t)round_up(q.N, 64);
-    } else if (q.N >= 1024) {
+    } else if (q.N >= 1024 && big_tiles) {
       q.bucket = TILED_BF16_256;
       q.Mp = (int32_t)round_up(q.M, 256);
       q.Np = (int32_t)round_up(q.N, 256);
@@ -1185,6 +1190,7 @@ int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o)
   if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
     return fail(ORTH_EINVAL, "unknown dtype");
   if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
+  if (o->tile != 0 && o->tile != 128 && o->tile != 256) return fail(ORTH_EINVAL, "tile must be 0, 128 or 256");
   for (int i = 0; i < n; ++i) {
     const orth_vjp_mat& m = mats[i];
     char buf[160];
@@ -1221,6 +1227,10 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
   P.mats.resize(n);
   int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
   std::vector<TileItem> tg[2], tu[2];
+  std::vector<std::pair<int, int>> dims(n);
+  for (int i = 0; i < n; ++i)
+    dims[i] = {std::max(mats[i].rows, mats[i].cols), std::min(mats[i].rows, mats[i].cols)};
+  const bool big_tiles = use_big_tiles(dims, o->tile);
   for (int i = 0; i < n; ++i) {
     const orth_vjp_mat& m = mats[i];
     TiledMat& t = P.mats[i];
@@ -1239,8 +1249,9 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
     t.status_index = i;
     int b = V_F32, pad = 64;
     if (bf16 && !(t.N <= 64 && t.M <= 128)) {
-      b = t.N >= 1024 ? V_BF16_256 : V_BF16_128;
-      pad = t.N >= 1024 ? 256 : 128;
+      const bool big = t.N >= 1024 && big_tiles;
+      b = big ? V_BF16_256 : V_BF16_128;
+      pad = big ? 256 : 128;
     }
     P.bucket[i] = b;
     t.Mp = (int32_t)round_up(t.M, pad);

@@ -4,6 +4,8 @@
 #pragma once
 
 #include <algorithm>
+#include <cstdint>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -45,6 +47,20 @@ inline void grouped_tiles(int mat, int tr, int tc, int gm, bool upper_only, std:
 inline void bf16_matrix_tiles(int mat, int tm, int tn, std::vector<TileItem>& gram, std::vector<TileItem>& upd) {
   grouped_tiles(mat, tn, tn, 4, true, gram);
   grouped_tiles(mat, tm, tn, 4, false, upd);
+}
+
+// Size class of the bf16 tiles: matrices with N >= 1024 use 256 x 256 tiles
+// only when those tiles fill at least four waves of the 256 compute units
+// (update tiles of the whole batch); otherwise the 128 x 128 tiles keep more
+// units busy (measured on the ImageNet-like stack: 8 x 1024^2 + 4 x 2048^2
+// gives 384 update tiles of 256, 1536 of 128).
+constexpr int64_t kBigTileMinTiles = 4 * 256;
+inline bool use_big_tiles(const std::vector<std::pair<int, int>>& tall_dims, int forced = 0) {
+  if (forced) return forced == 256;
+  int64_t tiles = 0;
+  for (const auto& d : tall_dims)
+    if (d.second >= 1024) tiles += (int64_t)((d.first + 255) / 256) * ((d.second + 255) / 256);
+  return tiles >= kBigTileMinTiles;
 }
 
 }  // namespace orth

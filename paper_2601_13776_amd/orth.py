@@ -46,7 +46,7 @@ class orth_mat(ctypes.Structure):
 class orth_bjorck_opts(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("beta", ctypes.c_float), ("prescale", ctypes.c_int32),
                 ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
-                ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p)]
+                ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p), ("tile", ctypes.c_int32)]
 
 
 class orth_vjp_mat(ctypes.Structure):
@@ -175,7 +175,7 @@ def _mats(ins, outs):
     return arr
 
 
-def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None):
+def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile=0):
     in_dt = _dtype_code(ins[0]) if ins else ORTH_F32
     out_dt = _dtype_code(outs[0]) if outs else ORTH_F32
     for a, b in zip(ins, outs):
@@ -191,14 +191,14 @@ def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None):
             raise ValueError(f"spectral pre-scaling needs u: a contiguous float32 tensor of {need} values "
                              "(min(rows, cols) per matrix, packed in batch order)")
         uptr = u.data_ptr()
-    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp, power_iters, uptr)
+    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp, power_iters, uptr, tile)
 
 
 def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius", compute="f32", outs=None,
-                                      power_iters=1, u=None):
+                                      power_iters=1, u=None, tile=0):
     outs = ins if outs is None else outs
     mats = _mats(ins, outs)
-    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u, tile)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_workspace_size")
@@ -206,13 +206,15 @@ def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius"
 
 
 def orth_orthogonalize_batched(ins, outs, iters, beta=0.5, prescale="frobenius", compute="f32", status=None,
-                               workspace=None, stream=None, power_iters=1, u=None):
+                               workspace=None, stream=None, power_iters=1, u=None, tile=0):
     """Björck-orthogonalize every ins[i] into outs[i] (see include/orth.h).
     prescale="spectral" takes power_iters and u, the packed float32 cached
-    vectors (min(rows, cols) per matrix), updated in place.
+    vectors (min(rows, cols) per matrix), updated in place.  tile (0, 128
+    or 256) is the bf16 tile edge of matrices with min(rows, cols) >= 1024
+    (0: chosen by occupancy).
     Returns the workspace tensor so that callers can reuse it."""
     mats = _mats(ins, outs)
-    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u, tile)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_workspace_size")
@@ -238,7 +240,7 @@ def _vjp_mats(ws, gouts, gins):
 
 
 def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, prescale="frobenius", compute="f32",
-                                   status=None, workspace=None, stream=None):
+                                   status=None, workspace=None, stream=None, tile=0):
     """dL/dW into grads_in[i] for L depending on ws[i] through
     orth_orthogonalize_batched with the same options, given grads_out[i] =
     dL/d(output) (see include/orth.h).  grads_in share the dtype of ws,
@@ -249,7 +251,7 @@ def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, pre
         if w.dtype != gi.dtype:
             raise TypeError("grads_in must have the dtype of ws")
     mats = _vjp_mats(ws, grads_out, grads_in)
-    opts = _opts(ws, grads_out, iters, beta, prescale, compute)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_vjp_workspace_size")
@@ -265,10 +267,10 @@ def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, pre
 
 
 def orth_orthogonalize_vjp_workspace_size(ws, iters, beta=0.5, prescale="frobenius", compute="f32",
-                                          grads_out=None):
+                                          grads_out=None, tile=0):
     grads_out = ws if grads_out is None else grads_out
     mats = _vjp_mats(ws, grads_out, ws)
-    opts = _opts(ws, grads_out, iters, beta, prescale, compute)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_vjp_workspace_size")

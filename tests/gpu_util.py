@@ -21,12 +21,13 @@ def to_f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def gpu_orthogonalize(stored_list, iters, compute="f32", out_dtype=torch.float32, beta=0.5, prescale="frobenius"):
+def gpu_orthogonalize(stored_list, iters, compute="f32", out_dtype=torch.float32, beta=0.5, prescale="frobenius",
+                      tile=0):
     ins = [to_dev(s) for s in stored_list]
     outs = [torch.empty(t.shape, dtype=out_dtype, device=DEV) for t in ins]
     status = torch.full((len(ins),), -1, dtype=torch.int32, device=DEV)
     orth.orth_orthogonalize_batched(ins, outs, iters, beta=beta, prescale=prescale, compute=compute,
-                                    status=status)
+                                    status=status, tile=tile)
     torch.cuda.synchronize()
     return outs, status.cpu().numpy()
 

@@ -75,7 +75,7 @@ def _mats(shapes, base=0x10000):
 
 def _ws_size(L, shapes, **kw):
     opts = orth.orth_bjorck_opts(kw.get("iters", 5), kw.get("beta", 0.5), 1, kw.get("dt", 0), kw.get("dt", 0),
-                                 kw.get("compute", 0))
+                                 kw.get("compute", 0), 1, None, kw.get("tile", 0))
     n = ctypes.c_size_t()
     rc = L.orth_orthogonalize_workspace_size(_mats(shapes), len(shapes), ctypes.byref(opts), ctypes.byref(n))
     return rc, n.value
@@ -99,14 +99,36 @@ def test_workspace_sizes(L):
     (dict(dt=3), [(4, 4)], orth.ORTH_EINVAL),
     (dict(), [(0, 4)], orth.ORTH_EINVAL),
     (dict(), [(4, 0)], orth.ORTH_EINVAL),
+    (dict(tile=64), [(4, 4)], orth.ORTH_EINVAL),
+    (dict(tile=512, compute=1), [(4, 4)], orth.ORTH_EINVAL),
 ])
 def test_invalid_orthogonalize_args(L, kw, shapes, code):
     rc, _ = _ws_size(L, shapes, **kw)
     assert rc == code
     opts = orth.orth_bjorck_opts(kw.get("iters", 5), kw.get("beta", 0.5), 1, kw.get("dt", 0), kw.get("dt", 0),
-                                 kw.get("compute", 0))
+                                 kw.get("compute", 0), 1, None, kw.get("tile", 0))
     rc = L.orth_orthogonalize_batched(_mats(shapes), len(shapes), ctypes.byref(opts), None, 0, None, None)
     assert rc == code
+
+
+def test_tile_class_choice(L):
+    """bf16 matrices with min(rows, cols) >= 1024 are padded to the chosen
+    tile edge: a lone 1100 x 1030 matrix gets 128-tiles by occupancy (its
+    20 tiles of 256 would leave most compute units idle), 256-tiles when
+    forced; a batch with >= 1024 tiles of 256 gets 256-tiles."""
+    one = [(1100, 1030)]
+    _, auto = _ws_size(L, one, compute=1, dt=1)
+    _, t128 = _ws_size(L, one, compute=1, dt=1, tile=128)
+    _, t256 = _ws_size(L, one, compute=1, dt=1, tile=256)
+    assert auto == t128 < t256
+    many = [(4096, 4096)] * 4                        # 4 x 256 tiles of 256
+    _, auto = _ws_size(L, many, compute=1, dt=1)
+    _, t256 = _ws_size(L, many, compute=1, dt=1, tile=256)
+    assert auto == t256
+    # fp32 products ignore the option
+    _, a = _ws_size(L, one)
+    _, b = _ws_size(L, one, tile=256)
+    assert a == b
 
 
 def test_bad_leading_dim_and_inplace(L):
@@ -175,8 +197,8 @@ def _vjp_mats(shapes, alias=None):
     return arr
 
 
-def _vjp_ws(L, shapes, iters=5, compute=0, dt=0, prescale=1, beta=0.5, alias=None):
-    opts = orth.orth_bjorck_opts(iters, beta, prescale, dt, dt, compute)
+def _vjp_ws(L, shapes, iters=5, compute=0, dt=0, prescale=1, beta=0.5, alias=None, tile=0):
+    opts = orth.orth_bjorck_opts(iters, beta, prescale, dt, dt, compute, 1, None, tile)
     n = ctypes.c_size_t()
     rc = L.orth_orthogonalize_vjp_workspace_size(_vjp_mats(shapes, alias), len(shapes), ctypes.byref(opts),
                                                  ctypes.byref(n))
@@ -206,6 +228,8 @@ def test_vjp_workspace_grows_with_saved_steps(L):
     (dict(alias="grad_out"), orth.ORTH_OK),
     (dict(alias="w"), orth.ORTH_OK),
     (dict(iters=0), orth.ORTH_OK),
+    (dict(tile=100), orth.ORTH_EINVAL),
+    (dict(tile=256, compute=1, dt=1), orth.ORTH_OK),
 ])
 def test_vjp_validation(L, kw, code):
     rc, _ = _vjp_ws(L, [(64, 32), (16, 48)], **kw)

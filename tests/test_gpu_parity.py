@@ -96,11 +96,15 @@ BF16_SHAPES = [(256, 128), (128, 256), (384, 200), (1024, 512), (2048, 1000), (1
                (1100, 1030), (64, 32), (32, 32)]
 
 
-def test_bf16_mixed_batch():
+@pytest.mark.parametrize("tile", [0, 128, 256])
+def test_bf16_mixed_batch(tile):
+    """Every size class; the matrices with min(rows, cols) >= 1024 run on
+    the tile size chosen by occupancy (0) or forced to 128 / 256."""
+    print(f"[bf16 mixed] tile={tile}", flush=True)
     st = stored(104, BF16_SHAPES, dtype="bf16")
     x64 = oracle_inputs(st)
     iters = 20
-    outs, status = gpu_orthogonalize(st, iters, compute="bf16")
+    outs, status = gpu_orthogonalize(st, iters, compute="bf16", tile=tile)
     assert np.all(status == 0)
     for s, o, shape in zip(x64, outs, BF16_SHAPES):
         ref = bjorck.bjorck(s, iters)
@@ -114,12 +118,13 @@ def test_bf16_mixed_batch():
             assert abs(checks.gram_deviation(got) - checks.gram_deviation(ref)) <= ORTH_BF16, shape
 
 
-def test_bf16_converged_all():
+@pytest.mark.parametrize("tile", [0, 256])
+def test_bf16_converged_all(tile):
     shapes = [(256, 256), (1024, 1024), (512, 256)]
     st = stored(105, shapes, dtype="bf16")
     x64 = oracle_inputs(st)
     iters = t_conv(x64)
-    outs, _ = gpu_orthogonalize(st, iters, compute="bf16")
+    outs, _ = gpu_orthogonalize(st, iters, compute="bf16", tile=tile)
     for o, shape in zip(outs, shapes):
         assert checks.gram_deviation(to_f64(o)) <= ORTH_BF16, shape
 

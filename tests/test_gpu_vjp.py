@@ -42,13 +42,13 @@ def upstream(seed, shapes):
     return [rng.standard_normal(s).astype(np.float32) for s in shapes]
 
 
-def run_vjp(st, gouts, iters, compute="f32", beta=0.5, prescale="frobenius", gin_dtype=None):
+def run_vjp(st, gouts, iters, compute="f32", beta=0.5, prescale="frobenius", gin_dtype=None, tile=0):
     ws = [to_dev(s) for s in st]
     gos = [torch.from_numpy(g).to(DEV) for g in gouts]
     gis = [torch.empty(w.shape, dtype=w.dtype, device=DEV) for w in ws]
     status = torch.full((len(ws),), -1, dtype=torch.int32, device=DEV)
     orth.orth_orthogonalize_vjp_batched(ws, gos, gis, iters, beta=beta, prescale=prescale, compute=compute,
-                                        status=status)
+                                        status=status, tile=tile)
     torch.cuda.synchronize()
     return gis, status.cpu().numpy()
 
@@ -89,13 +89,15 @@ def test_vjp_f32_beta_and_no_prescale(beta, prescale):
 SHAPES_BF16 = [(128, 64), (64, 100), (256, 128), (300, 700), (1024, 512), (256, 256), (512, 512), (1100, 1030)]
 
 
-def test_vjp_bf16_mixed_batch():
+@pytest.mark.parametrize("tile", [0, 256])
+def test_vjp_bf16_mixed_batch(tile):
     """bf16 parameters, fp32 upstream gradient, bf16 products (the small
-    bucket runs in fp32 as in the forward)."""
-    print("[vjp bf16] mixed batch", flush=True)
+    bucket runs in fp32 as in the forward); matrices with min(rows, cols)
+    >= 1024 on the tile size chosen by occupancy or forced to 256."""
+    print(f"[vjp bf16] mixed batch tile={tile}", flush=True)
     st = stored(205, SHAPES_BF16, "bf16")
     gouts = upstream(206, SHAPES_BF16)
-    gis, status = run_vjp(st, gouts, 20, compute="bf16")
+    gis, status = run_vjp(st, gouts, 20, compute="bf16", tile=tile)
     assert np.all(status == 0)
     for s, g, o, shape in zip(st, gouts, gis, SHAPES_BF16):
         assert o.dtype == torch.bfloat16
@@ -110,7 +112,7 @@ def test_vjp_scale_invariance_property():
     shapes = [(384, 200), (200, 384), (2048, 1024)]
     st = stored(207, shapes, "bf16")
     gouts = upstream(208, shapes)
-    gis, _ = run_vjp(st, gouts, 15, compute="bf16")
+    gis, _ = run_vjp(st, gouts, 15, compute="bf16", tile=256)
     for s, o in zip(st, gis):
         w, g = wl.as_f64(s), to_f64(o)
         assert abs(float(np.sum(w * g))) <= 1e-2 * np.linalg.norm(w) * np.linalg.norm(g)
