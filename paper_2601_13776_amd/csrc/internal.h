@@ -32,6 +32,44 @@ __device__ inline void store_from_f32(void* p, int64_t idx, int dtype, float v) 
     static_cast<float*>(p)[idx] = v;
 }
 
+// Runs of 8 consecutive elements moved as 16-byte vectors (one for bf16,
+// two for fp32).  vec8_ok tells whether every run starting at a multiple
+// of 8 of every row of a (pointer, leading dim) pair is 16-byte aligned.
+__device__ inline bool vec8_ok(const void* p, int64_t ld, int dtype) {
+  const int64_t es = dtype == ORTH_BF16 ? 2 : 4;
+  return ((reinterpret_cast<uintptr_t>(p) | (uintptr_t)(ld * es)) & 15) == 0;
+}
+__device__ inline void load8_f32(const void* p, int64_t idx, int dtype, float (&v)[8]) {
+  if (dtype == ORTH_BF16) {
+    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + idx);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + idx);
+    const float4 b = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + idx + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+__device__ inline uint4 pack8_bf16(const float (&v)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(v[2 * i]) | ((uint32_t)f32_to_bf16(v[2 * i + 1]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ inline void store8_f32(void* p, int64_t idx, int dtype, const float (&v)[8]) {
+  if (dtype == ORTH_BF16) {
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + idx) = pack8_bf16(v);
+  } else {
+    *reinterpret_cast<float4*>(static_cast<float*>(p) + idx) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(static_cast<float*>(p) + idx + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Björck batch descriptors (device-resident tables built by the host).
 // Every matrix is processed in its tall orientation M x N (M >= N); a wide

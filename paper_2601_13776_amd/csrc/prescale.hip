@@ -41,12 +41,28 @@ __global__ __launch_bounds__(256) void prescale_partial_kernel(const TiledMat* _
   __syncthreads();
   double ss = 0.0;
   int bad = 0;
-  for (int e = threadIdx.x; e < TB * TB; e += 256) {
-    const int r = it.ti * TB + e / TB, c = it.tj * TB + (e % TB);
-    if (r < d.rows && c < d.cols) {
-      const float v = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
-      bad |= !isfinite(v);
-      ss += (double)v * (double)v;
+  const int R = it.ti * TB, C = it.tj * TB;
+  if (R + TB <= d.rows && C + TB <= d.cols && vec8_ok(d.in, d.ld_in, in_dtype)) {
+    // interior tile: 16-byte vector loads, rows t / 8 and t / 8 + 32,
+    // columns 8 (t % 8) .. + 7
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float v[8];
+      load8_f32(d.in, (int64_t)(R + (threadIdx.x >> 3) + 32 * h) * d.ld_in + C + 8 * (threadIdx.x & 7), in_dtype, v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        bad |= !isfinite(v[i]);
+        ss += (double)v[i] * (double)v[i];
+      }
+    }
+  } else {
+    for (int e = threadIdx.x; e < TB * TB; e += 256) {
+      const int r = R + e / TB, c = C + (e % TB);
+      if (r < d.rows && c < d.cols) {
+        const float v = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+        bad |= !isfinite(v);
+        ss += (double)v * (double)v;
+      }
     }
   }
   if (bad) atomicOr(&bad_any, 1);
@@ -100,6 +116,24 @@ __global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __r
   const TiledMat& d = mats[it.mat];
   const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the tall padded layout
   const float inv = *d.inv_norm;
+  if (!d.transposed && compute == ORTH_COMPUTE_BF16 && R + TB <= d.M && C + TB <= d.N &&
+      vec8_ok(d.in, d.ld_in, in_dtype) && vec8_ok(d.master[0], d.Np, ORTH_F32) &&
+      (!d.xc[0] || vec8_ok(d.xc[0], d.Np, ORTH_BF16))) {
+    // interior tile of an untransposed matrix: no staging, 16-byte vectors
+    // (rows t / 8 and t / 8 + 32, columns 8 (t % 8) .. + 7)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = R + (threadIdx.x >> 3) + 32 * h, c = C + 8 * (threadIdx.x & 7);
+      float v[8];
+      load8_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype, v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] *= inv;
+      const int64_t off = (int64_t)r * d.Np + c;
+      store8_f32(d.master[0], off, ORTH_F32, v);
+      if (d.xc[0]) store8_f32(d.xc[0], off, ORTH_BF16, v);
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int a = e / TB, b = e % TB;
     if (!d.transposed) {
@@ -139,6 +173,17 @@ __global__ __launch_bounds__(256) void writeout_kernel(const TiledMat* __restric
   const float* master = d.master[master_index];
   const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the ORIGINAL layout
   if (!d.transposed) {
+    if (R + TB <= d.rows && C + TB <= d.cols && vec8_ok(d.out, d.ld_out, out_dtype) &&
+        vec8_ok(master, d.Np, ORTH_F32)) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = R + (threadIdx.x >> 3) + 32 * h, c = C + 8 * (threadIdx.x & 7);
+        float v[8];
+        load8_f32(master, (int64_t)r * d.Np + c, ORTH_F32, v);
+        store8_f32(d.out, (int64_t)r * d.ld_out + c, out_dtype, v);
+      }
+      return;
+    }
     for (int e = threadIdx.x; e < TB * TB; e += 256) {
       const int r = R + e / TB, c = C + e % TB;
       if (r < d.rows && c < d.cols)

@@ -44,6 +44,22 @@ __global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __re
   const TileItem it = items[blockIdx.x];
   const TiledMat& d = mats[it.mat];
   const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the tall padded layout
+  float* y = d.gy[0];
+  uint16_t* yc = static_cast<uint16_t*>(d.yc[0]);
+  if (!d.transposed && R + TB <= d.M && C + TB <= d.N && vec8_ok(d.gout, d.ld_gout, gout_dtype) &&
+      vec8_ok(y, d.Np, ORTH_F32) && (!yc || vec8_ok(yc, d.Np, ORTH_BF16))) {
+    // interior tile of an untransposed matrix: 16-byte vectors, no staging
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = R + (threadIdx.x >> 3) + 32 * h, c = C + 8 * (threadIdx.x & 7);
+      float v[8];
+      load8_f32(d.gout, (int64_t)r * d.ld_gout + c, gout_dtype, v);
+      const int64_t off = (int64_t)r * d.Np + c;
+      store8_f32(y, off, ORTH_F32, v);
+      if (yc) store8_f32(yc, off, ORTH_BF16, v);
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int a = e / TB, b = e % TB;
     if (!d.transposed) {
@@ -57,8 +73,6 @@ __global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __re
     }
   }
   __syncthreads();
-  float* y = d.gy[0];
-  uint16_t* yc = static_cast<uint16_t*>(d.yc[0]);
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int a = e / TB, b = e % TB;
     const int64_t off = (int64_t)(R + a) * d.Np + C + b;
@@ -86,13 +100,27 @@ __global__ __launch_bounds__(256) void vjp_dot_partial_kernel(const TiledMat* __
   const TileItem it = items[blockIdx.x];
   const TiledMat& d = mats[it.mat];
   const int R = it.ti * TB, C = it.tj * TB;  // caller layout
-  caller_tile(d, d.gy[d.gy_final], R, C, tile);
+  const float* gy = d.gy[d.gy_final];
   double acc = 0.0;
-  for (int e = threadIdx.x; e < TB * TB; e += 256) {
-    const int x = e / TB, y = e % TB;
-    const int r = R + x, c = C + y;
-    if (r < d.rows && c < d.cols)
-      acc += (double)tile[x][y] * (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+  if (!d.transposed && R + TB <= d.rows && C + TB <= d.cols && vec8_ok(d.in, d.ld_in, in_dtype) &&
+      vec8_ok(gy, d.Np, ORTH_F32)) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = R + (threadIdx.x >> 3) + 32 * h, c = C + 8 * (threadIdx.x & 7);
+      float g[8], w[8];
+      load8_f32(gy, (int64_t)r * d.Np + c, ORTH_F32, g);
+      load8_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype, w);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc += (double)g[i] * (double)w[i];
+    }
+  } else {
+    caller_tile(d, gy, R, C, tile);
+    for (int e = threadIdx.x; e < TB * TB; e += 256) {
+      const int x = e / TB, y = e % TB;
+      const int r = R + x, c = C + y;
+      if (r < d.rows && c < d.cols)
+        acc += (double)tile[x][y] * (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
+    }
   }
   const double tot = block_sum_256(acc, red);
   if (threadIdx.x == 0) {
@@ -118,11 +146,35 @@ __global__ __launch_bounds__(256) void vjp_writeout_kernel(const TiledMat* __res
   const TileItem it = items[blockIdx.x];
   const TiledMat& d = mats[it.mat];
   const int R = it.ti * TB, C = it.tj * TB;  // caller layout
-  caller_tile(d, d.gy[d.gy_final], R, C, tile);
+  const float* gy = d.gy[d.gy_final];
   const int st = status[d.status_index];
   const float inv = *d.inv_norm;
   const bool frob = prescale == ORTH_PRESCALE_FROBENIUS;
   const float dscale = frob && st == ORTH_MAT_OK ? (float)(*d.dot) * inv : 0.f;
+  if (!d.transposed && R + TB <= d.rows && C + TB <= d.cols && vec8_ok(d.in, d.ld_in, in_dtype) &&
+      vec8_ok(d.out, d.ld_out, in_dtype) && vec8_ok(gy, d.Np, ORTH_F32)) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int r = R + (threadIdx.x >> 3) + 32 * h, c = C + 8 * (threadIdx.x & 7);
+      float v[8];
+      if (st == ORTH_MAT_NONFINITE || st == ORTH_MAT_ZERO) {
+        const float f = st == ORTH_MAT_ZERO ? 0.f : __builtin_nanf("");
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = f;
+      } else {
+        load8_f32(gy, (int64_t)r * d.Np + c, ORTH_F32, v);
+        if (frob) {
+          float w[8];
+          load8_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype, w);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) v[i] = inv * (v[i] - dscale * w[i]);
+        }
+      }
+      store8_f32(d.out, (int64_t)r * d.ld_out + c, in_dtype, v);
+    }
+    return;
+  }
+  caller_tile(d, gy, R, C, tile);
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int x = e / TB, y = e % TB;
     const int r = R + x, c = C + y;
