@@ -42,6 +42,40 @@ __device__ inline double block_sum(double v, double* red) {
   return t;
 }
 
+// The caller's M x N matrix (or its transpose, for a wide one) into the tall
+// zero-padded Mp x NP LDS layout (pitch NP + 1), with U independent loads
+// of every thread in flight before their LDS stores.  With `stats`, also
+// the finiteness flag and the squared norm (fp64) of the loaded values.
+template <int NP, int NTHR>
+__device__ inline void load_tall(float* dst, const void* src, int64_t ld, int transposed, int M, int N, int Mp,
+                                 int dtype, bool stats, double& ss, int& bad) {
+  constexpr int U = 8, XP = NP + 1;
+  const int total = Mp * NP;
+  for (int base = 0; base < total; base += NTHR * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = base + u * NTHR + (int)threadIdx.x;
+      const int r = idx / NP, c = idx % NP;
+      v[u] = 0.f;
+      if (idx < total && r < M && c < N)
+        v[u] = load_as_f32(src, transposed ? (int64_t)c * ld + r : (int64_t)r * ld + c, dtype);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = base + u * NTHR + (int)threadIdx.x;
+      if (idx < total) {
+        const int r = idx / NP, c = idx % NP;
+        dst[r * XP + c] = v[u];
+        if (stats && r < M && c < N) {
+          bad |= !isfinite(v[u]);
+          ss += (double)v[u] * (double)v[u];
+        }
+      }
+    }
+  }
+}
+
 // Spectral pre-scaling on the unscaled tall X in LDS (power iteration on
 // X^T X from the caller's cached vector, fp64): returns
 // max(|X^T X v| / |X v|, ||X||_F / sqrt(N)) and writes the new vector back.
@@ -113,17 +147,7 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMa
   __syncthreads();
   double ss = 0.0;
   int bad = 0;
-  for (int idx = tid; idx < Mp * NP; idx += NTHR) {
-    const int r = idx / NP, c = idx - (idx / NP) * NP;
-    float v = 0.f;
-    if (r < M && c < N) {
-      const int64_t src = d.transposed ? (int64_t)c * d.ld_in + r : (int64_t)r * d.ld_in + c;
-      v = load_as_f32(d.in, src, in_dtype);
-      bad |= !isfinite(v);
-      ss += (double)v * (double)v;
-    }
-    X[r * XP + c] = v;
-  }
+  load_tall<NP, NTHR>(X, d.in, d.ld_in, d.transposed, M, N, Mp, in_dtype, true, ss, bad);
   ss = wave_sum(ss);
   if (wave_or(bad) && lane == 0) bad_any = 1;
   if (lane == 0) red[wave] = ss;
@@ -208,6 +232,213 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMa
   }
 }
 
+
+// Vector-Jacobian product of the fused small-matrix Björck (Appendix A.5
+// iteration, differentiated): with Y the gradient with respect to X_{t+1},
+//     S' = -(X_t^T Y + Y^T X_t),   Y <- Y + beta (Y E_t + X_t S'),
+// for t = T-1 .. 0, after a forward recomputation that saves X_t and E_t;
+// then the pre-scaling derivative dL/dW = inv (Y_0 - <Y_0, X_0> X_0)
+// (Frobenius, X_0 = inv W) or Y_0 (none), written in the caller's layout.
+// LDS holds X, E, Y and S' (row pitch NP + 1 floats).
+template <int NP, int NWAVES>
+__global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const SmallVjpMat* __restrict__ mats,
+                                                                      int iters, float beta, int prescale,
+                                                                      int in_dtype, int gout_dtype,
+                                                                      int32_t* __restrict__ status) {
+  constexpr int NT = NP / 32;
+  constexpr int XP = NP + 1;
+  constexpr int MAXT = (4 * NT + NWAVES - 1) / NWAVES;  // update tiles per wave (Mp <= 128)
+  constexpr int NTHR = 64 * NWAVES;
+  extern __shared__ float smem[];
+  __shared__ double red[NWAVES];
+  __shared__ int bad_any;
+  const SmallVjpMat d = mats[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int M = d.M, N = d.N, Mp = d.Mp, MT = Mp / 32;
+  float* X = smem;
+  float* Y = X + Mp * XP;
+  float* E = Y + Mp * XP;
+  float* S = E + NP * XP;
+  const int half = lane >> 5, col = lane & 31;
+  const int64_t step_floats = (int64_t)Mp * NP + NP * NP;
+
+  // -- W into X (tall), finiteness and squared norm (fp64, fixed order)
+  if (tid == 0) bad_any = 0;
+  __syncthreads();
+  double ss = 0.0;
+  int bad = 0;
+  load_tall<NP, NTHR>(X, d.w, d.ld_w, d.transposed, M, N, Mp, in_dtype, true, ss, bad);
+  ss = wave_sum(ss);
+  if (wave_or(bad) && lane == 0) bad_any = 1;
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  double tot = 0.0;
+#pragma unroll
+  for (int w = 0; w < NWAVES; ++w) tot += red[w];
+  int st = ORTH_MAT_OK;
+  float scale = 1.f;
+  if (bad_any) {
+    st = ORTH_MAT_NONFINITE;
+    scale = __builtin_nanf("");
+  } else if (prescale != ORTH_PRESCALE_NONE && tot == 0.0) {
+    st = ORTH_MAT_ZERO;
+    scale = 0.f;
+  } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
+    scale = (float)(1.0 / sqrt(tot));
+  }
+  if (tid == 0 && status) status[d.status_index] = st;
+  for (int idx = tid; idx < Mp * NP; idx += NTHR) {
+    const int r = idx / NP, c = idx - (idx / NP) * NP;
+    X[r * XP + c] *= scale;
+  }
+  __syncthreads();
+
+  // E = I - X^T X into E
+  auto gram = [&]() {
+    for (int tile = wave; tile < NT * NT; tile += NWAVES) {
+      const int gi = tile / NT, gj = tile % NT;
+      f32x16 acc = {};
+      for (int kk = 0; kk < Mp; kk += 2) {
+        const float* row = X + (kk + half) * XP;
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(row[gi * 32 + col], row[gj * 32 + col], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = gi * 32 + acc_row(r, lane), j = gj * 32 + col;
+        E[i * XP + j] = (i == j ? 1.f : 0.f) - acc[r];
+      }
+    }
+  };
+  // P <- P + beta (P Q + P2 Q2) over the Mp x NP update tiles (P2 may be
+  // null); every wave computes from the old P, then all write after a barrier
+  auto update = [&](float* P, const float* Q, const float* P2, const float* Q2) {
+    f32x16 acc[MAXT];
+#pragma unroll
+    for (int q = 0; q < MAXT; ++q) {
+      acc[q] = f32x16{};
+      const int tile = wave + q * NWAVES;
+      if (tile < MT * NT) {
+        const int ri = tile / NT, cj = tile % NT;
+        const float* prow = P + (ri * 32 + col) * XP;
+        for (int kk = 0; kk < NP; kk += 2)
+          acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(prow[kk + half], Q[(kk + half) * XP + cj * 32 + col], acc[q],
+                                                        0, 0, 0);
+        if (P2) {
+          const float* p2row = P2 + (ri * 32 + col) * XP;
+          for (int kk = 0; kk < NP; kk += 2)
+            acc[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(p2row[kk + half], Q2[(kk + half) * XP + cj * 32 + col],
+                                                          acc[q], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < MAXT; ++q) {
+      const int tile = wave + q * NWAVES;
+      if (tile < MT * NT) {
+        const int ri = tile / NT, cj = tile % NT;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int i = ri * 32 + acc_row(r, lane), j = cj * 32 + col;
+          P[i * XP + j] += beta * acc[q][r];
+        }
+      }
+    }
+    __syncthreads();
+  };
+  // LDS <-> the saved slot of step t (pitch NP in memory)
+  auto save_step = [&](int t) {
+    float* xs = d.save + t * step_floats;
+    float* es = xs + (int64_t)Mp * NP;
+    for (int idx = tid; idx < Mp * NP; idx += NTHR) xs[idx] = X[(idx / NP) * XP + idx % NP];
+    for (int idx = tid; idx < NP * NP; idx += NTHR) es[idx] = E[(idx / NP) * XP + idx % NP];
+  };
+  // (X and E are contiguous in the slot: 16-byte loads, U of them in
+  // flight per thread before their LDS stores)
+  auto load_step = [&](int t) {
+    constexpr int U = 4;
+    const float4* src = reinterpret_cast<const float4*>(d.save + t * step_floats);
+    const int xq = Mp * NP / 4, total = xq + NP * NP / 4;
+    for (int base = 0; base < total; base += NTHR * U) {
+      float4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = base + u * NTHR + tid;
+        if (q < total) v[u] = src[q];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int q = base + u * NTHR + tid;
+        if (q < total) {
+          const int e = 4 * (q < xq ? q : q - xq);
+          float* dst = (q < xq ? X : E) + (e / NP) * XP + e % NP;
+          dst[0] = v[u].x;
+          dst[1] = v[u].y;
+          dst[2] = v[u].z;
+          dst[3] = v[u].w;
+        }
+      }
+    }
+    __syncthreads();
+  };
+
+  // -- forward recomputation: X_t, E_t saved for t < T (X_T is never needed)
+  for (int t = 0; t < iters; ++t) {
+    gram();
+    __syncthreads();
+    save_step(t);
+    if (t + 1 < iters) update(X, E, nullptr, nullptr);
+  }
+
+  // -- dL/dX_T from the caller's layout (tall, zero padded)
+  load_tall<NP, NTHR>(Y, d.gout, d.ld_gout, d.transposed, M, N, Mp, gout_dtype, false, ss, bad);
+  __syncthreads();
+
+  // -- gradient recurrence, last step first (X_{T-1}, E_{T-1} are in LDS)
+  for (int t = iters - 1; t >= 0; --t) {
+    if (t + 1 < iters) load_step(t);
+    for (int tile = wave; tile < NT * NT; tile += NWAVES) {
+      const int gi = tile / NT, gj = tile % NT;
+      f32x16 acc = {};
+      for (int kk = 0; kk < Mp; kk += 2) {
+        const float* xr = X + (kk + half) * XP;
+        const float* yr = Y + (kk + half) * XP;
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(xr[gi * 32 + col], yr[gj * 32 + col], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(yr[gi * 32 + col], xr[gj * 32 + col], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) S[(gi * 32 + acc_row(r, lane)) * XP + gj * 32 + col] = -acc[r];
+    }
+    __syncthreads();
+    update(Y, E, X, S);
+  }
+
+  // -- pre-scaling derivative (X holds X_0 here) in the caller's layout
+  float dot = 0.f;
+  if (prescale == ORTH_PRESCALE_FROBENIUS && st == ORTH_MAT_OK) {
+    double a = 0.0;
+    for (int idx = tid; idx < M * N; idx += NTHR) {
+      const int r = idx / N, c = idx - (idx / N) * N;
+      a += (double)Y[r * XP + c] * (double)X[r * XP + c];
+    }
+    dot = (float)block_sum<NWAVES>(a, red);
+  }
+  for (int idx = tid; idx < M * N; idx += NTHR) {
+    const int r = idx / N, c = idx - (idx / N) * N;
+    float v;
+    if (st == ORTH_MAT_NONFINITE)
+      v = __builtin_nanf("");
+    else if (st == ORTH_MAT_ZERO)
+      v = 0.f;
+    else if (prescale == ORTH_PRESCALE_FROBENIUS)
+      v = scale * (Y[r * XP + c] - dot * X[r * XP + c]);
+    else
+      v = Y[r * XP + c];
+    const int64_t dst = d.transposed ? (int64_t)c * d.ld_gin + r : (int64_t)r * d.ld_gin + c;
+    store_from_f32(d.gin, dst, in_dtype, v);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
@@ -227,6 +458,31 @@ hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, 
                        power_iters, in_dtype, out_dtype, status);
   hipError_t e = hipGetLastError();
   timing_end("bjorck_small", s);
+  return e;
+}
+
+hipError_t launch_bjorck_small_vjp(const SmallVjpMat* mats, int n, int np, int max_mp, int iters, float beta,
+                                   int prescale, int in_dtype, int gout_dtype, int32_t* status, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  // X and Y (max_mp rows), E and S' (np rows), pitch np + 1: at most 99.8 KB
+  const size_t lds = (size_t)(2 * max_mp + 2 * np) * (np + 1) * sizeof(float);
+  timing_begin("bjorck_small_vjp", s);
+  hipError_t e;
+  if (np == 32) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bjorck_small_vjp_kernel<32, 1>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess)
+      hipLaunchKernelGGL((bjorck_small_vjp_kernel<32, 1>), dim3(n), dim3(64), lds, s, mats, iters, beta, prescale,
+                         in_dtype, gout_dtype, status);
+  } else {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bjorck_small_vjp_kernel<64, 4>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess)
+      hipLaunchKernelGGL((bjorck_small_vjp_kernel<64, 4>), dim3(n), dim3(256), lds, s, mats, iters, beta, prescale,
+                         in_dtype, gout_dtype, status);
+  }
+  if (e == hipSuccess) e = hipGetLastError();
+  timing_end("bjorck_small_vjp", s);
   return e;
 }
 

@@ -1157,11 +1157,12 @@ void build_conv_exp_plan(const orth_conv_exp_desc* d, int32_t n, int32_t dtype, 
 // The vector-Jacobian product recomputes the forward iterates, saving every
 // X_t and E_t = I - X_t^T X_t (step after step in the workspace), then runs
 // the gradient recurrence from t = T-1 down to 0 and finally the derivative
-// of the pre-scaling.  Matrices the forward would run in fp32 (fp32 products,
-// or the small fused bucket) use the fp32 tile GEMM; the others use the
-// bf16 tile kernel in its saved-iterate and gradient modes.
+// of the pre-scaling.  Small matrices (N <= 64, M <= 128) run all of it in
+// one workgroup each (fp32 MFMA, as in the forward); the others with fp32
+// products use the fp32 tile GEMM, those with bf16 products the bf16 tile
+// kernel in its saved-iterate and gradient modes.
 namespace {
-enum VBucket { V_F32 = 0, V_BF16_128 = 1, V_BF16_256 = 2 };
+enum VBucket { V_F32 = 0, V_BF16_128 = 1, V_BF16_256 = 2, V_SMALL = 3 };
 
 struct VjpPlan {
   std::vector<int> bucket;
@@ -1169,6 +1170,9 @@ struct VjpPlan {
   std::vector<TileItem> partial_items, scale_items;
   std::vector<GemmItem> f_gram, f_upd, b_s[2], b_upd[2];
   std::vector<TileItem> t_gram[2], t_upd[2], t_s[2][2], t_yu[2][2];  // [class][parity]
+  std::vector<SmallVjpMat> small[2];  // N <= 32, N <= 64 (fused kernel)
+  int small_max_mp[2] = {0, 0};
+  size_t off_small[2] = {0, 0};
   size_t off_mats = 0, off_partial_items = 0, off_scale_items = 0;
   size_t off_f_gram = 0, off_f_upd = 0, off_b_s[2] = {}, off_b_upd[2] = {};
   size_t off_t_gram[2] = {}, off_t_upd[2] = {}, off_t_s[2][2] = {}, off_t_yu[2][2] = {};
@@ -1248,7 +1252,32 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
     t.N = std::min(m.rows, m.cols);
     t.status_index = i;
     int b = V_F32, pad = 64;
-    if (bf16 && !(t.N <= 64 && t.M <= 128)) {
+    if (t.N <= 64 && t.M <= 128) {
+      // the whole product in one workgroup (both compute modes, as in the
+      // forward): no tables, only the saved iterates
+      P.bucket[i] = V_SMALL;
+      t.fused = 1;
+      const int k = t.N <= 32 ? 0 : 1, np = k ? 64 : 32;
+      SmallVjpMat q{};
+      q.w = m.w;
+      q.gout = m.grad_out;
+      q.gin = m.grad_in;
+      q.ld_w = m.ld_w;
+      q.ld_gout = m.ld_grad_out;
+      q.ld_gin = m.ld_grad_in;
+      q.rows = m.rows;
+      q.cols = m.cols;
+      q.M = t.M;
+      q.N = t.N;
+      q.Mp = (int32_t)round_up(t.M, 32);
+      q.transposed = t.transposed;
+      q.status_index = i;
+      q.np = np;
+      P.small[k].push_back(q);
+      P.small_max_mp[k] = std::max(P.small_max_mp[k], q.Mp);
+      continue;
+    }
+    if (bf16) {
       const bool big = t.N >= 1024 && big_tiles;
       b = big ? V_BF16_256 : V_BF16_128;
       pad = big ? 256 : 128;
@@ -1284,6 +1313,7 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
 
   Arena A;
   P.off_mats = A.take(sizeof(TiledMat) * n);
+  for (int k = 0; k < 2; ++k) P.off_small[k] = A.take(sizeof(SmallVjpMat) * P.small[k].size());
   P.off_partial_items = A.take(sizeof(TileItem) * n_part);
   P.off_scale_items = A.take(sizeof(TileItem) * n_scale);
   P.off_f_gram = A.take(sizeof(GemmItem) * n_fg);
@@ -1307,8 +1337,15 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
   P.off_status = A.take(sizeof(int32_t) * n);
 
   auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
+  // saved X_t and E_t of the fused small matrices, pitch np
+  for (int k = 0; k < 2; ++k)
+    for (SmallVjpMat& q : P.small[k]) {
+      const int np = q.np;
+      q.save = reinterpret_cast<float*>(dev(A.take((size_t)T * ((size_t)q.Mp * np + (size_t)np * np) * 4)));
+    }
   for (int i = 0; i < n; ++i) {
     TiledMat& t = P.mats[i];
+    if (t.fused) continue;
     const int64_t xe = (int64_t)t.Mp * t.Np, ee = (int64_t)t.Np * t.Np;
     t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + i;
     t.dot = reinterpret_cast<double*>(dev(P.off_dot)) + i;
@@ -1596,6 +1633,7 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
 
   std::vector<unsigned char> img(P.table_bytes, 0);
   put(img, P.off_mats, P.mats);
+  for (int k = 0; k < 2; ++k) put(img, P.off_small[k], P.small[k]);
   put(img, P.off_partial_items, P.partial_items);
   put(img, P.off_scale_items, P.scale_items);
   put(img, P.off_f_gram, P.f_gram);
@@ -1621,6 +1659,11 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   const int T = opts->iters;
   const float beta = opts->beta;
   double* partials = reinterpret_cast<double*>(ws + P.off_partials);
+  // small matrices: the whole product per workgroup
+  for (int k = 0; k < 2; ++k)
+    ORTH_HIP(launch_bjorck_small_vjp(reinterpret_cast<const SmallVjpMat*>(ws + P.off_small[k]),
+                                     (int)P.small[k].size(), k ? 64 : 32, P.small_max_mp[k], T, beta,
+                                     opts->prescale, opts->in_dtype, opts->out_dtype, status, s));
   ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                    partials, s));
   ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s));

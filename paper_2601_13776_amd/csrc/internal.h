@@ -102,7 +102,8 @@ struct TiledMat {
   void* s;                   // -(X^T Y + Y^T X), Np x Np (bf16: upper tiles only)
   double* dot;               // <Y_0, W_0>, one per matrix
   int32_t gy_final;          // gy[] index holding dL/dW_0 after the last step
-  int32_t pad;
+  int32_t fused;             // 1: handled whole by the small-matrix kernel (per-matrix
+                             // finish kernels skip it)
   // Spectral pre-scaling only.
   float* u;                  // the caller's cached vector (N values)
   double* pv;                // power-iteration vector v (N)
@@ -133,6 +134,24 @@ struct SmallMat {
   int32_t status_index;
   int32_t pad;
   float* u;                  // spectral pre-scaling: the caller's cached vector
+};
+
+// A small matrix (N <= 64, M <= 128) of the vector-Jacobian product: the
+// whole computation (forward recomputation, gradient recurrence, pre-scaling
+// derivative) runs in one workgroup; X_t and E_t of the recomputation go to
+// `save` (T (Mp NP + NP NP) floats, pitch NP) for the way back.
+struct SmallVjpMat {
+  const void* w;             // the forward's input, caller layout
+  const void* gout;          // dL/d(output), caller layout
+  void* gin;                 // dL/dW, caller layout (dtype of w)
+  int64_t ld_w, ld_gout, ld_gin;
+  int32_t rows, cols;
+  int32_t M, N;              // tall orientation
+  int32_t Mp;                // M rounded up to 32
+  int32_t transposed;
+  int32_t status_index;
+  int32_t np;                // LDS columns: 32 or 64
+  float* save;
 };
 
 // One batched power-iteration work item: 64 outputs of a matrix-vector
@@ -244,6 +263,8 @@ void timing_end(const char* name, hipStream_t s);
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
                                int prescale, int power_iters, int in_dtype, int out_dtype, int32_t* status,
                                hipStream_t s);
+hipError_t launch_bjorck_small_vjp(const SmallVjpMat* mats, int n, int np, int max_mp, int iters, float beta,
+                                   int prescale, int in_dtype, int gout_dtype, int32_t* status, hipStream_t s);
 hipError_t launch_power_init(const TiledMat* mats, int n_mats, hipStream_t s);
 hipError_t launch_power_dot(const TiledMat* mats, const PowerItem* items, int n_items, int in_dtype,
                             hipStream_t s);

@@ -133,6 +133,7 @@ __global__ __launch_bounds__(256) void vjp_dot_finish_kernel(const TiledMat* __r
                                                              const double* __restrict__ partials) {
   __shared__ double red[4];
   const TiledMat& d = mats[blockIdx.x];
+  if (d.fused) return;   // handled by the fused small-matrix kernel
   double ss = 0.0;
   for (int i = threadIdx.x; i < d.n_partials; i += 256) ss += partials[d.partial_base + i];
   const double tot = block_sum_256(ss, red);
