@@ -27,11 +27,12 @@
 //
 // One workgroup of 4 waves (2 x 2) computes a BM x BN tile; each wave holds
 // a (BM/2) x (BN/2) block of 32x32 accumulators.  K advances in steps of 64
-// through a 2-stage LDS ring filled by direct global->LDS loads; 16-byte
-// chunks are XOR-swizzled so fragment reads are bank-conflict free.  The
-// scheduling fences keep LDS reads and loads interleaved with MFMAs.
-// Work items come from a table that the host orders so that consecutive
-// tiles of one matrix land on one XCD.
+// through five LDS buffers (160 KB for 256-tiles) filled by direct
+// global->LDS loads up to two k-steps ahead; 16-byte chunks are
+// XOR-swizzled so fragment reads are bank-conflict free.  The scheduling
+// fences keep LDS reads and loads interleaved with MFMAs.  Work items come
+// from a table whose order the host chooses so that concurrently running
+// tiles share operand panels through the caches.
 #include "internal.h"
 
 namespace orth {
@@ -196,21 +197,23 @@ struct Tile {
   static constexpr int BK = 64, NW = WM * WN, TM = BM / WM, TN = BN / WN, MI = TM / 32, NI = TN / 32;
 };
 
-// K loop over [kb, ke) (multiples of 64, an even number of k-steps) of one
-// tile: two LDS stages; sub-steps 0-2 run their MFMAs with the next
-// sub-step's fragment reads interleaved (sub-step 0 also issues the B loads
-// of the next stage), then every wave waits for its loads and meets the
-// others at the barrier, after which sub-step 3 (fragments already in
-// registers) keeps the MFMA pipe busy while the first fragments of the next
-// stage are read and the A loads of the stage after it go out into the
-// stage just read.  Each operand's loads thus get three or four sub-steps
-// to land (A measured 2% faster there than beside the B loads; both after
-// the barrier, 11% slower).  Past the end, loads re-read a valid k-step
-// instead of branching, which keeps the loop body one block.
+// K loop over [kb, ke) (multiples of 64) of one tile, through five LDS
+// buffers: the A operand cycles through three, B through two.  In k-step t,
+// sub-step 0 sends the A loads of k-step t + 2 into the free A buffer;
+// sub-steps 0-2 run their MFMAs with the next sub-step's fragment reads
+// interleaved; then every wave waits for the loads of k-step t + 1 (the
+// newest A loads may stay in flight) and meets the others at the barrier,
+// after which sub-step 3 (fragments already in registers) keeps the MFMA
+// pipe busy while the first fragments of k-step t + 1 are read and the B
+// loads of k-step t + 2 go into the B buffer just read.  A loads get seven
+// sub-steps to land, B loads four (two stages: three and two; measured 4%
+// faster).  Past the end, loads re-read a valid k-step instead of
+// branching.
 template <int BM, int BN, int WM, int WN, bool AT, bool BT>
 __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32], const uint16_t* A, int64_t lda,
                                       const uint16_t* B, int64_t ldb, int kb, int ke, uint16_t* sA0, uint16_t* sB0,
-                                      uint16_t* sA1, uint16_t* sB1, int wave, int lane, int wm, int wn) {
+                                      uint16_t* sA1, uint16_t* sB1, uint16_t* sX, int wave, int lane, int wm,
+                                      int wn) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int MI = T::MI, NI = T::NI, BK = T::BK;
   const int nk = (ke - kb) / BK;
@@ -241,17 +244,21 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
   // until they return.  On 256-tiles the loads ride along the first MFMAs of
   // the sub-step (fence_plan); on 128-tiles, with four MFMAs per sub-step,
   // they go out first behind a scheduling barrier.
-  auto kstep = [&](uint16_t* ca, uint16_t* cb, uint16_t* na, uint16_t* nb, int kt) {
-    const int kn = kb + (kt + 1 < nk ? kt + 1 : nk - 1) * BK;
+  constexpr int NA = decltype(oa)::NBLK, NBL = decltype(ob)::NBLK;
+  static_assert(NA == 8 || NA == 4, "wait counts are spelled out for 4 or 8 loads");
+  // ca/cb: this k-step's stage; na/nb: the next one's; sa: free buffer that
+  // receives A of k-step kt + 2 in sub-step 0; B of kt + 2 goes into cb
+  // after the barrier
+  auto kstep = [&](uint16_t* ca, uint16_t* cb, uint16_t* na, uint16_t* nb, uint16_t* sa, int kt) {
     const int kn2 = kb + (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
     constexpr bool BIG = NM >= 16;   // 256-tiles: loads and reads spread over the sub-step
     lds_settle();
-    ob.issue(nb, kn, wave);
+    oa.issue(sa, kn2, wave);
     if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(1, ca, cb, 1);
     mma(0);
     if constexpr (BIG)
-      fence_plan<NM, NR, decltype(ob)::NBLK, DMA_PER_SLOT, READ_TAIL>();
+      fence_plan<NM, NR, NA, DMA_PER_SLOT, READ_TAIL>();
     else
       fence_substep<NM, NRF, 0>();
     lds_settle();
@@ -268,28 +275,57 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
       fence_plan<NM, NR, 0, 1, READ_TAIL>();
     else
       fence_substep<NM, NRF, 0>();
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-    __syncthreads();
+    // every load but this k-step's A loads for k-step kt + 2 has landed and
+    // every LDS read is done; a plain s_barrier (a workgroup fence would
+    // wait for all loads)
+    // (s_waitcnt vmcnt(NA) expcnt(7) lgkmcnt(0) as a builtin, so that the
+    // compiler's own wait analysis sees it)
+    __builtin_amdgcn_s_waitcnt((NA & 15) | (7 << 4) | ((NA >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    oa.issue(ca, kn2, wave);
+    ob.issue(cb, kn2, wave);
     if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(0, na, nb, 0);
     mma(1);
     if constexpr (BIG)
-      fence_plan<NM, NR, decltype(oa)::NBLK, DMA_PER_SLOT, READ_TAIL>();
+      fence_plan<NM, NR, NBL, DMA_PER_SLOT, READ_TAIL>();
     else
       fence_substep<NM, NRF, 0>();
   };
+  // A cycles through three buffers (sA0, sA1, sX), B through two (sB0,
+  // sB1): the pattern repeats every six k-steps
   oa.issue(sA0, kb, wave);
   ob.issue(sB0, kb, wave);
   oa.issue(sA1, kb + (nk > 1 ? BK : 0), wave);
+  ob.issue(sB1, kb + (nk > 1 ? BK : 0), wave);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   rd(0, sA0, sB0, 0);
   __builtin_amdgcn_sched_barrier(0);
-  for (int kt = 0; kt < nk; kt += 2) {
-    kstep(sA0, sB0, sA1, sB1, kt);
-    kstep(sA1, sB1, sA0, sB0, kt + 1);
+  // whole periods in the loop; the remainder in straight-line code, so that
+  // the loop head only ever follows the last k-step of a period (the
+  // compiler's wait analysis then sees which buffers have loads in flight)
+  int kt = 0;
+  for (; kt + 6 <= nk; kt += 6) {
+    kstep(sA0, sB0, sA1, sB1, sX, kt);
+    kstep(sA1, sB1, sX, sB0, sA0, kt + 1);
+    kstep(sX, sB0, sA0, sB1, sA1, kt + 2);
+    kstep(sA0, sB1, sA1, sB0, sX, kt + 3);
+    kstep(sA1, sB0, sX, sB1, sA0, kt + 4);
+    kstep(sX, sB1, sA0, sB0, sA1, kt + 5);
+  }
+  if (kt < nk) {
+    kstep(sA0, sB0, sA1, sB1, sX, kt);
+    if (kt + 1 < nk) {
+      kstep(sA1, sB1, sX, sB0, sA0, kt + 1);
+      if (kt + 2 < nk) {
+        kstep(sX, sB0, sA0, sB1, sA1, kt + 2);
+        if (kt + 3 < nk) {
+          kstep(sA0, sB1, sA1, sB0, sX, kt + 3);
+          if (kt + 4 < nk) kstep(sA1, sB0, sX, sB1, sA0, kt + 4);
+        }
+      }
+    }
   }
   // every wave is done with both stages before anyone refills them
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
@@ -303,13 +339,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   using T = Tile<BM, BN, WM, WN>;
   constexpr int BK = T::BK, TM = T::TM, TN = T::TN, MI = T::MI, NI = T::NI;
   static_assert(MI * NI >= MI + NI, "a sub-step needs at least as many MFMAs as fragment reads");
-  // Two LDS stages held in distinct arrays and selected at compile time, so
-  // that the compiler can tell the reads of one stage from the asynchronous
-  // direct-to-LDS writes into the other.
+  // Five LDS buffers held in distinct arrays and selected at compile time,
+  // so that the compiler can tell the reads of one buffer from the
+  // asynchronous direct-to-LDS writes into the others.
   __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
   __shared__ __attribute__((aligned(1024))) uint16_t sB0[BN * BK];
   __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
   __shared__ __attribute__((aligned(1024))) uint16_t sB1[BN * BK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sX[BM * BK];
 
   const TileItem it = items[blockIdx.x];
   const TiledMat* d = mats + it.mat;
@@ -337,14 +374,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   auto panel_times_sym = [&](const uint16_t* P, const uint16_t* Q) {
     const int ksplit = it.tj * BN;
     kloop<BM, BN, WM, WN, false, true>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN, Np, 0,
-                                       ksplit, sA0, sB0, sA1, sB1, wave, lane, wm, wn);
+                                       ksplit, sA0, sB0, sA1, sB1, sX, wave, lane, wm, wn);
     kloop<BM, BN, WM, WN, false, false>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN * Np, Np,
-                                        ksplit, Np, sA0, sB0, sA1, sB1, wave, lane, wm, wn);
+                                        ksplit, Np, sA0, sB0, sA1, sB1, sX, wave, lane, wm, wn);
   };
   // column panels I of P and J of Q, k over all Mp rows: P[:, I]^T Q[:, J]
   auto cols_t_cols = [&](const uint16_t* P, const uint16_t* Q) {
     kloop<BM, BN, WM, WN, true, true>(acc, P + (int64_t)it.ti * BM, Np, Q + (int64_t)it.tj * BN, Np, 0, Mp, sA0,
-                                      sB0, sA1, sB1, wave, lane, wm, wn);
+                                      sB0, sA1, sB1, sX, wave, lane, wm, wn);
   };
 
   const uint16_t* Y = nullptr;
