@@ -1,8 +1,8 @@
 // Table-driven fp32 "NT" GEMM on gfx950 fp32 MFMA (v_mfma_f32_32x32x2f32):
-// every work item is one 64 x 64 tile of C = A B^T (+ A2 B2^T and any
-// further pairs from a table, accumulated into the same tile) with its own
-// operands,
-// shapes and epilogue, so a single launch covers a whole ragged batch
+// every work item is one product C = A B^T (+ A2 B2^T and any further pairs
+// from a table, accumulated into the same tile) with its own operands,
+// shapes and epilogue, and every block one 64 x 64 tile of such an item
+// (from a tile list), so a single launch covers a whole ragged batch
 // (all matrices of a Björck step, all tap products of a composition step,
 // all Gram checks).  Operands may be fp32 or bf16 and stored either
 // K-contiguous ([M][K]) or transposed ([K][M]); loads are bounds-checked
@@ -26,14 +26,17 @@ namespace {
 
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items, int step,
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items,
+                                                       const GemmTile* __restrict__ tiles, int step,
                                                        const GemmPair* __restrict__ extra) {
   constexpr int BM = 64, BN = 64, BK = 32, PITCH = BK + 4;
   __shared__ __attribute__((aligned(16))) float As[2][BM * PITCH];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * PITCH];
-  const GemmItem* g = items + blockIdx.x;
+  const GemmTile tl = tiles[blockIdx.x];
+  const GemmItem* g = items + tl.item;
   const int M = g->M, N = g->N;
-  const int row0 = g->ti * BM, col0 = g->tj * BN;
+  const int row0 = tl.ti * BM, col0 = tl.tj * BN;
+  const bool mirror = g->mirror != 0 && tl.ti != tl.tj;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int64_t st = step;
@@ -159,7 +162,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       if (i < M) store_from_f32(Cv, (int64_t)i * ldc + j, cdt, acc[r]);
     }
   } else if (epi == EPI_GRAM_E) {
-    const bool mirror = g->mirror != 0;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = ibase + acc_row(r, lane);
@@ -183,7 +185,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       }
     }
   } else if (epi == EPI_NEG) {
-    const bool mirror = g->mirror != 0;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = ibase + acc_row(r, lane);
@@ -211,11 +212,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
 
 }  // namespace
 
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step,
-                           const GemmPair* pairs) {
-  if (n_items <= 0) return hipSuccess;
+hipError_t launch_gemm_f32(const GemmItem* items, const GemmTile* tiles, int n_tiles, const char* name,
+                           hipStream_t s, int step, const GemmPair* pairs) {
+  if (n_tiles <= 0) return hipSuccess;
   timing_begin(name, s);
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_items), dim3(256), 0, s, items, step, pairs);
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_tiles), dim3(256), 0, s, items, tiles, step, pairs);
   hipError_t e = hipGetLastError();
   timing_end(name, s);
   return e;

@@ -93,8 +93,8 @@ void timing_end(const char* name, hipStream_t s) {
 }
 
 // ------------------------------------------------- descriptor staging ----
-// Descriptor tables are built on the host and copied into the head of the
-// caller's workspace.  The copy source is a pinned staging buffer from a
+// Descriptor tables are built on the host and copied into the caller's
+// workspace (the regions that each call's layout reserves for them).  The copy source is a pinned staging buffer from a
 // small ring; an event recorded after each copy guards reuse of the buffer.
 namespace {
 struct StageSlot {
@@ -107,23 +107,59 @@ StageSlot g_stage[4];
 int g_stage_next = 0;
 }  // namespace
 
-static int upload_tables(const std::vector<unsigned char>& img, void* dst, hipStream_t s) {
-  if (img.empty()) return ORTH_OK;
+// Host image of a call's tables: the spans that put() fills (workspace
+// offset, bytes), their bytes back to back.  Only the spans are copied; a
+// span that starts less than kSpanGap bytes after the previous one (in
+// increasing offset order) extends it over the gap instead, which saves a
+// copy call for a few zero bytes.
+struct TableImage {
+  static constexpr size_t kSpanGap = 64 << 10;
+  std::vector<unsigned char> data;
+  std::vector<std::pair<size_t, size_t>> spans;
+  void add(size_t off, const void* p, size_t bytes) {
+    if (!bytes) return;
+    if (!spans.empty()) {
+      const size_t end = spans.back().first + spans.back().second;
+      if (off >= end && off - end < kSpanGap) {
+        data.resize(data.size() + (off - end), 0);
+        spans.back().second += off - end;
+        const size_t at = data.size();
+        data.resize(at + bytes);
+        std::memcpy(data.data() + at, p, bytes);
+        spans.back().second += bytes;
+        return;
+      }
+    }
+    const size_t at = data.size();
+    data.resize(at + bytes);
+    std::memcpy(data.data() + at, p, bytes);
+    spans.push_back({off, bytes});
+  }
+};
+
+static int upload_tables(const TableImage& img, void* dst, hipStream_t s) {
+  if (img.data.empty()) return ORTH_OK;
   std::lock_guard<std::mutex> lk(g_smu);
   StageSlot& sl = g_stage[g_stage_next];
   g_stage_next = (g_stage_next + 1) % 4;
   if (sl.done) ORTH_HIP(hipEventSynchronize(sl.done));
-  if (sl.cap < img.size()) {
+  const size_t total = img.data.size();
+  if (sl.cap < total) {
     if (sl.buf) ORTH_HIP(hipHostFree(sl.buf));
     sl.buf = nullptr;
-    size_t cap = std::max<size_t>(img.size(), 1 << 16);
+    size_t cap = std::max<size_t>(total, 1 << 16);
     cap = (cap + 4095) & ~size_t(4095);
     ORTH_HIP(hipHostMalloc(&sl.buf, cap, hipHostMallocDefault));
     sl.cap = cap;
   }
   if (!sl.done) ORTH_HIP(hipEventCreateWithFlags(&sl.done, hipEventDisableTiming));
-  std::memcpy(sl.buf, img.data(), img.size());
-  ORTH_HIP(hipMemcpyAsync(dst, sl.buf, img.size(), hipMemcpyHostToDevice, s));
+  std::memcpy(sl.buf, img.data.data(), total);
+  size_t at = 0;
+  for (const auto& sp : img.spans) {
+    ORTH_HIP(hipMemcpyAsync(static_cast<unsigned char*>(dst) + sp.first, static_cast<unsigned char*>(sl.buf) + at,
+                            sp.second, hipMemcpyHostToDevice, s));
+    at += sp.second;
+  }
   ORTH_HIP(hipEventRecord(sl.done, s));
   return ORTH_OK;
 }
@@ -143,6 +179,75 @@ struct Arena {
     return o;
   }
 };
+
+// fp32 GEMM work of one launch: one item per product, one GemmTile per
+// 64 x 64 output tile (consecutive tiles of a product share its item).  In
+// the workspace: the items, then the tiles.
+static_assert(sizeof(GemmItem) % 8 == 0 && sizeof(GemmItem) == 8 * 8 + 13 * 8 + 18 * 4,
+              "GemmItem must have no padding: items are compared bytewise");
+struct GemmList {
+  std::vector<GemmItem> items;
+  std::vector<GemmTile> tiles;
+  GemmItem last{};   // items.back() with its tile and mirror fields cleared
+  size_t size() const { return tiles.size(); }
+  void clear() {
+    items.clear();
+    tiles.clear();
+  }
+  // one tile, given as a whole item with its ti, tj (and mirror for an
+  // off-diagonal tile); it shares the previous tile's item when the rest
+  // matches
+  void push_back(const GemmItem& g) {
+    GemmItem k = g;
+    k.ti = k.tj = 0;
+    k.mirror = 0;
+    if (items.empty() || std::memcmp(&k, &last, sizeof k) != 0) {
+      items.push_back(k);
+      last = k;
+    }
+    if (g.mirror) items.back().mirror = 1;
+    tiles.push_back(GemmTile{(int32_t)items.size() - 1, g.ti, g.tj, 0});
+  }
+  // every tile of proto's M x N output
+  void add_all(const GemmItem& proto) {
+    GemmItem k = proto;
+    k.ti = k.tj = 0;
+    items.push_back(k);
+    last = k;
+    last.mirror = 0;
+    const int32_t idx = (int32_t)items.size() - 1;
+    for (int a = 0; a < (proto.M + 63) / 64; ++a)
+      for (int b = 0; b < (proto.N + 63) / 64; ++b) tiles.push_back(GemmTile{idx, a, b, 0});
+  }
+  size_t items_bytes() const { return align_up(items.size() * sizeof(GemmItem)); }
+  // workspace bytes for at most n tiles, each of its own product
+  static size_t bound(size_t n) { return align_up(n * sizeof(GemmItem)) + align_up(n * sizeof(GemmTile)); }
+  size_t bytes() const { return items_bytes() + align_up(tiles.size() * sizeof(GemmTile)); }
+};
+
+void put(TableImage& img, size_t off, const GemmList& g) {
+  img.add(off, g.items.data(), g.items.size() * sizeof(GemmItem));
+  img.add(off + g.items_bytes(), g.tiles.data(), g.tiles.size() * sizeof(GemmTile));
+}
+
+// Longest reductions first (stable: a product's tiles keep their order), so
+// that short tiles fill a launch's tail; extra pairs are counted at the
+// first pair's depth.
+void longest_first(GemmList& g) {
+  auto work = [&](const GemmTile& t) {
+    const GemmItem& it = g.items[t.item];
+    return (int64_t)it.K * (1 + it.pair_count) + it.K2;
+  };
+  std::stable_sort(g.tiles.begin(), g.tiles.end(),
+                   [&](const GemmTile& a, const GemmTile& b) { return work(a) > work(b); });
+}
+
+hipError_t launch_list(const unsigned char* ws, size_t off, const GemmList& g, const char* name, hipStream_t s,
+                       int step = 0, const GemmPair* pairs = nullptr) {
+  return launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + off),
+                         reinterpret_cast<const GemmTile*>(ws + off + g.items_bytes()), (int)g.size(), name, s,
+                         step, pairs);
+}
 
 }  // namespace
 
@@ -165,7 +270,7 @@ struct OrthoPlan {
   std::vector<TiledMat> tiled;                  // host copy with device pointers
   std::vector<TileItem> partial_items, scale_items, writeout_items;
   std::vector<TileItem> tabs[2][N_TABS];        // bf16: [0] = 128 tiles, [1] = 256 tiles
-  std::vector<GemmItem> f32_gram, f32_update[2];
+  GemmList f32_gram, f32_update[2];
   std::vector<PowerItem> power[2];              // spectral: v -> x and x -> y products
   int max_mp[2] = {32, 32};
   int total_partials = 0;
@@ -264,11 +369,18 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     for (int i = 0; i < n; ++i)
       if (P.mp[i].bucket == bucket) members.push_back(i);
     std::vector<TileItem> g[2], u[2];
-    for (int i : members) {
-      const MatPlan& q = P.mp[i];
-      const int tn = q.Np / tsz, tm = q.Mp / tsz;
-      std::vector<TileItem> gt, ut;
-      bf16_matrix_tiles(tiled_of[i], tm, tn, gt, ut);
+    // longest tiles first (a Gram tile runs over Mp, an update tile over Np),
+    // so that the short ones fill the launch's tail
+    std::vector<int> gm = members, um = members;
+    std::stable_sort(gm.begin(), gm.end(), [&](int a, int b) { return P.mp[a].Mp > P.mp[b].Mp; });
+    std::stable_sort(um.begin(), um.end(), [&](int a, int b) { return P.mp[a].Np > P.mp[b].Np; });
+    for (int k = 0; k < (int)members.size(); ++k) {
+      std::vector<TileItem> gt, ut, unused;
+      const MatPlan& qg = P.mp[gm[k]];
+      bf16_matrix_tiles(tiled_of[gm[k]], qg.Mp / tsz, qg.Np / tsz, gt, unused);
+      const MatPlan& qu = P.mp[um[k]];
+      unused.clear();
+      bf16_matrix_tiles(tiled_of[um[k]], qu.Mp / tsz, qu.Np / tsz, unused, ut);
       for (int par = 0; par < 2; ++par) {
         for (TileItem t : gt) {
           t.flags = par ? TILE_PARITY : 0;
@@ -312,9 +424,9 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   P.off_writeout_items = A.take(sizeof(TileItem) * n_part);
   for (int cls = 0; cls < 2; ++cls)
     for (int t = 0; t < N_TABS; ++t) P.off_tabs[cls][t] = A.take(sizeof(TileItem) * P.tabs[cls][t].size());
-  P.off_f32_gram = A.take(sizeof(GemmItem) * n_fg);
-  P.off_f32_update[0] = A.take(sizeof(GemmItem) * n_fu);
-  P.off_f32_update[1] = A.take(sizeof(GemmItem) * n_fu);
+  P.off_f32_gram = A.take(GemmList::bound(n_fg));
+  P.off_f32_update[0] = A.take(GemmList::bound(n_fu));
+  P.off_f32_update[1] = A.take(GemmList::bound(n_fu));
   const bool spectral = o->prescale == ORTH_PRESCALE_SPECTRAL;
   int64_t n_pw[2] = {0, 0};
   if (spectral)
@@ -456,16 +568,16 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
   P.total_bytes = align_up(A.off);
 
   // XCD-aware physical order of the fp32 GEMM work lists
-  P.f32_gram = xcd_order(P.f32_gram);
-  P.f32_update[0] = xcd_order(P.f32_update[0]);
-  P.f32_update[1] = xcd_order(P.f32_update[1]);
+  longest_first(P.f32_gram);
+  longest_first(P.f32_update[0]);
+  longest_first(P.f32_update[1]);
 }
 
 template <typename T>
-void put(std::vector<unsigned char>& img, size_t off, const std::vector<T>& v) {
-  if (v.empty()) return;
-  std::memcpy(img.data() + off, v.data(), sizeof(T) * v.size());
+void put(TableImage& img, size_t off, const std::vector<T>& v) {
+  img.add(off, v.data(), sizeof(T) * v.size());
 }
+
 
 int check_workspace(void* ws, size_t have, size_t need) {
   if (need == 0) return ORTH_OK;
@@ -504,8 +616,8 @@ int validate_geom(const orth_conv_geom* g) {
 
 struct ConvPlan {
   std::vector<ComposeGroup> groups;
-  std::vector<GemmItem> proj_items;
-  std::vector<std::vector<GemmItem>> phase_gemm;
+  GemmList proj_items;
+  std::vector<GemmList> phase_gemm;
   std::vector<std::vector<CombineItem>> phase_comb;
   std::vector<int64_t> phase_max_elems;
   int64_t init_max = 0, scatter_max = 0;
@@ -570,11 +682,11 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
       n_pc[ph] += 1;
     }
   }
-  P.off_proj_items = A.take(sizeof(GemmItem) * n_proj_items);
+  P.off_proj_items = A.take(GemmList::bound(n_proj_items));
   P.off_phase_gemm.resize(n_phase);
   P.off_phase_comb.resize(n_phase);
   for (int ph = 0; ph < n_phase; ++ph) {
-    P.off_phase_gemm[ph] = A.take(sizeof(GemmItem) * n_pg[ph]);
+    P.off_phase_gemm[ph] = A.take(GemmList::bound(n_pg[ph]));
     P.off_phase_comb[ph] = A.take(sizeof(CombineItem) * n_pc[ph]);
   }
   P.table_bytes = align_up(A.off);
@@ -659,7 +771,7 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
     P.groups.push_back(G);
   }
   P.total_bytes = align_up(A.off);
-  for (int ph = 0; ph < n_phase; ++ph) P.phase_gemm[ph] = xcd_order(P.phase_gemm[ph]);
+  for (int ph = 0; ph < n_phase; ++ph) longest_first(P.phase_gemm[ph]);
 }
 }  // namespace
 
@@ -672,8 +784,8 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
 // at global steps 0.., vertical ones after the longest horizontal run).
 namespace {
 struct ConvVjpPlan {
-  std::vector<GemmItem> proj_items, last_dp, dv_items;
-  std::vector<std::vector<GemmItem>> fwd_gemm, bwd_gemm;
+  GemmList proj_items, last_dp, dv_items;
+  std::vector<GemmList> fwd_gemm, bwd_gemm;
   std::vector<std::vector<TapItem>> fwd_comb, bwd_comb;
   std::vector<TapItem> rko_taps, grad_taps, rko_grad;
   std::vector<int64_t> fwd_max, bwd_max;
@@ -697,16 +809,8 @@ int validate_conv_vjp_descs(const orth_conv_vjp_desc* d, int32_t n, int32_t dtyp
   return ORTH_OK;
 }
 
-// tiles of an M x N output for the fp32 tile GEMM
-void gemm_tiles(const GemmItem& proto, std::vector<GemmItem>& out) {
-  for (int a = 0; a < (proto.M + 63) / 64; ++a)
-    for (int b = 0; b < (proto.N + 63) / 64; ++b) {
-      GemmItem g = proto;
-      g.ti = a;
-      g.tj = b;
-      out.push_back(g);
-    }
-}
+// every tile of an M x N output for the fp32 tile GEMM
+void gemm_tiles(const GemmItem& proto, GemmList& out) { out.add_all(proto); }
 
 void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, ConvVjpPlan& P,
                          unsigned char* ws) {
@@ -726,9 +830,9 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
   for (int pass = 0; pass < 2; ++pass) {
     Arena A;
     if (pass == 1) {
-      P.off_proj = A.take(sizeof(GemmItem) * P.proj_items.size());
-      P.off_last_dp = A.take(sizeof(GemmItem) * P.last_dp.size());
-      P.off_dv = A.take(sizeof(GemmItem) * P.dv_items.size());
+      P.off_proj = A.take(GemmList::bound(P.proj_items.size()));
+      P.off_last_dp = A.take(GemmList::bound(P.last_dp.size()));
+      P.off_dv = A.take(GemmList::bound(P.dv_items.size()));
       P.off_rko_taps = A.take(sizeof(TapItem) * P.rko_taps.size());
       P.off_grad_taps = A.take(sizeof(TapItem) * P.grad_taps.size());
       P.off_rko_grad = A.take(sizeof(TapItem) * P.rko_grad.size());
@@ -737,8 +841,8 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
       P.off_fwd_comb.resize(n_phase);
       P.off_bwd_comb.resize(n_phase);
       for (int ph = 0; ph < n_phase; ++ph) {
-        P.off_fwd_gemm[ph] = A.take(sizeof(GemmItem) * P.fwd_gemm[ph].size());
-        P.off_bwd_gemm[ph] = A.take(sizeof(GemmItem) * P.bwd_gemm[ph].size());
+        P.off_fwd_gemm[ph] = A.take(GemmList::bound(P.fwd_gemm[ph].size()));
+        P.off_bwd_gemm[ph] = A.take(GemmList::bound(P.bwd_gemm[ph].size()));
         P.off_fwd_comb[ph] = A.take(sizeof(TapItem) * P.fwd_comb[ph].size());
         P.off_bwd_comb[ph] = A.take(sizeof(TapItem) * P.bwd_comb[ph].size());
       }
@@ -928,7 +1032,7 @@ struct ExpPlan {
   std::vector<TiledMat> mats;                 // exp map: views of A for the spectral kernels
   std::vector<TileItem> partial_items, writeout_items;
   std::vector<PowerItem> power[2];
-  std::vector<std::vector<GemmItem>> steps;   // per power k = 2..p (index k - 2)
+  std::vector<GemmList> steps;   // per power k = 2..p (index k - 2)
   std::vector<GemmPair> pairs;                // conv: operand pairs of all steps
   std::vector<TapItem> scatter;               // conv: E taps -> OIHW
   int64_t max_elems = 0, max_init = 0, max_scatter = 0;
@@ -981,7 +1085,7 @@ void build_exp_plan(const orth_mat* mats, int32_t n, const orth_exp_opts* o, Exp
   P.off_power[0] = A.take(sizeof(PowerItem) * n_pw);
   P.off_power[1] = A.take(sizeof(PowerItem) * n_pw);
   P.off_steps.resize(P.steps.size());
-  for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(sizeof(GemmItem) * n_gemm);
+  for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(GemmList::bound(n_gemm));
   P.table_bytes = align_up(A.off);
   P.off_partials = A.take(sizeof(double) * n_part);
   P.off_inv = A.take(sizeof(float) * n);
@@ -1086,7 +1190,7 @@ void build_conv_exp_plan(const orth_conv_exp_desc* d, int32_t n, int32_t dtype, 
       P.off_pairs = A.take(sizeof(GemmPair) * P.pairs.size());
       P.off_scatter = A.take(sizeof(TapItem) * P.scatter.size());
       P.off_steps.resize(P.steps.size());
-      for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(sizeof(GemmItem) * P.steps[k].size());
+      for (size_t k = 0; k < P.steps.size(); ++k) P.off_steps[k] = A.take(GemmList::bound(P.steps[k].size()));
       P.table_bytes = align_up(A.off);
       P.items.clear();
       P.pairs.clear();
@@ -1168,7 +1272,7 @@ struct VjpPlan {
   std::vector<int> bucket;
   std::vector<TiledMat> mats;
   std::vector<TileItem> partial_items, scale_items;
-  std::vector<GemmItem> f_gram, f_upd, b_s[2], b_upd[2];
+  GemmList f_gram, f_upd, b_s[2], b_upd[2];
   std::vector<TileItem> t_gram[2], t_upd[2], t_s[2][2], t_yu[2][2];  // [class][parity]
   std::vector<SmallVjpMat> small[2];  // N <= 32, N <= 64 (fused kernel)
   int small_max_mp[2] = {0, 0};
@@ -1231,6 +1335,7 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
   P.mats.resize(n);
   int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
   std::vector<TileItem> tg[2], tu[2];
+  std::vector<int> bf16_members[2];
   std::vector<std::pair<int, int>> dims(n);
   for (int i = 0; i < n; ++i)
     dims[i] = {std::max(mats[i].rows, mats[i].cols), std::min(mats[i].rows, mats[i].cols)};
@@ -1295,8 +1400,24 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       n_fg += tn * (tn + 1) / 2;
       n_fu += tm * tn;
     } else {
-      const int cls = b == V_BF16_256 ? 1 : 0, tsz = cls ? 256 : 128;
-      bf16_matrix_tiles(i, t.Mp / tsz, t.Np / tsz, tg[cls], tu[cls]);
+      bf16_members[b == V_BF16_256 ? 1 : 0].push_back(i);
+    }
+  }
+  // bf16 tile lists, longest tiles first (Gram and S' tiles run over Mp,
+  // update tiles over Np)
+  for (int cls = 0; cls < 2; ++cls) {
+    const int tsz = cls ? 256 : 128;
+    std::vector<int> gm = bf16_members[cls], um = bf16_members[cls];
+    std::stable_sort(gm.begin(), gm.end(), [&](int a, int c) { return P.mats[a].Mp > P.mats[c].Mp; });
+    std::stable_sort(um.begin(), um.end(), [&](int a, int c) { return P.mats[a].Np > P.mats[c].Np; });
+    std::vector<TileItem> unused;
+    for (int i : gm) {
+      unused.clear();
+      bf16_matrix_tiles(i, P.mats[i].Mp / tsz, P.mats[i].Np / tsz, tg[cls], unused);
+    }
+    for (int i : um) {
+      unused.clear();
+      bf16_matrix_tiles(i, P.mats[i].Mp / tsz, P.mats[i].Np / tsz, unused, tu[cls]);
     }
   }
   for (int cls = 0; cls < 2; ++cls) {
@@ -1316,11 +1437,11 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
   for (int k = 0; k < 2; ++k) P.off_small[k] = A.take(sizeof(SmallVjpMat) * P.small[k].size());
   P.off_partial_items = A.take(sizeof(TileItem) * n_part);
   P.off_scale_items = A.take(sizeof(TileItem) * n_scale);
-  P.off_f_gram = A.take(sizeof(GemmItem) * n_fg);
-  P.off_f_upd = A.take(sizeof(GemmItem) * n_fu);
+  P.off_f_gram = A.take(GemmList::bound(n_fg));
+  P.off_f_upd = A.take(GemmList::bound(n_fu));
   for (int par = 0; par < 2; ++par) {
-    P.off_b_s[par] = A.take(sizeof(GemmItem) * n_fg);
-    P.off_b_upd[par] = A.take(sizeof(GemmItem) * n_fu);
+    P.off_b_s[par] = A.take(GemmList::bound(n_fg));
+    P.off_b_upd[par] = A.take(GemmList::bound(n_fu));
   }
   for (int cls = 0; cls < 2; ++cls) {
     P.off_t_gram[cls] = A.take(sizeof(TileItem) * P.t_gram[cls].size());
@@ -1484,11 +1605,11 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       }
   }
   P.total_bytes = align_up(A.off);
-  P.f_gram = xcd_order(P.f_gram);
-  P.f_upd = xcd_order(P.f_upd);
+  longest_first(P.f_gram);
+  longest_first(P.f_upd);
   for (int par = 0; par < 2; ++par) {
-    P.b_s[par] = xcd_order(P.b_s[par]);
-    P.b_upd[par] = xcd_order(P.b_upd[par]);
+    longest_first(P.b_s[par]);
+    longest_first(P.b_upd[par]);
   }
 }
 }  // namespace
@@ -1541,7 +1662,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_small[0], P.small[0]);
   put(img, P.off_small[1], P.small[1]);
   put(img, P.off_tiled, P.tiled);
@@ -1588,10 +1709,9 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
                                        s));
     } else {
       for (int t = 0; t < iters; ++t) {
-        ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_gram), (int)P.f32_gram.size(),
+        ORTH_HIP(launch_list(ws, P.off_f32_gram, P.f32_gram,
                                  "bjorck_gram_f32", s));
-        ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_f32_update[t & 1]),
-                                 (int)P.f32_update[t & 1].size(), "bjorck_update_f32", s));
+        ORTH_HIP(launch_list(ws, P.off_f32_update[t & 1], P.f32_update[t & 1], "bjorck_update_f32", s));
       }
     }
     ORTH_HIP(launch_writeout(tm, T(P.off_writeout_items), (int)P.writeout_items.size(), bf16 ? 0 : (iters & 1),
@@ -1631,7 +1751,7 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_mats, P.mats);
   for (int k = 0; k < 2; ++k) put(img, P.off_small[k], P.small[k]);
   put(img, P.off_partial_items, P.partial_items);
@@ -1654,7 +1774,6 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   if (rc) return rc;
 
   auto TI = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
-  auto GI = [&](size_t off) { return reinterpret_cast<const GemmItem*>(ws + off); };
   const TiledMat* tm = reinterpret_cast<const TiledMat*>(ws + P.off_mats);
   const int T = opts->iters;
   const float beta = opts->beta;
@@ -1671,11 +1790,11 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
                                  opts->compute, s));
   // forward recomputation, saving X_t and E_t (X_T itself is never needed)
   for (int t = 0; t < T; ++t) {
-    ORTH_HIP(launch_gemm_f32(GI(P.off_f_gram), (int)P.f_gram.size(), "vjp_fwd_gram_f32", s, t));
+    ORTH_HIP(launch_list(ws, P.off_f_gram, P.f_gram, "vjp_fwd_gram_f32", s, t));
     for (int cls = 1; cls >= 0; --cls)
       ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_gram[cls]), (int)P.t_gram[cls].size(), beta, s, 0, t));
     if (t + 1 == T) break;
-    ORTH_HIP(launch_gemm_f32(GI(P.off_f_upd), (int)P.f_upd.size(), "vjp_fwd_update_f32", s, t));
+    ORTH_HIP(launch_list(ws, P.off_f_upd, P.f_upd, "vjp_fwd_update_f32", s, t));
     for (int cls = 1; cls >= 0; --cls)
       ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_upd[cls]), (int)P.t_upd[cls].size(), beta, s, 0, t));
   }
@@ -1683,10 +1802,10 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   ORTH_HIP(launch_vjp_load_grad(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->out_dtype, s));
   for (int b = 0; b < T; ++b) {
     const int t = T - 1 - b, par = b & 1;
-    ORTH_HIP(launch_gemm_f32(GI(P.off_b_s[par]), (int)P.b_s[par].size(), "vjp_s_f32", s, t));
+    ORTH_HIP(launch_list(ws, P.off_b_s[par], P.b_s[par], "vjp_s_f32", s, t));
     for (int cls = 1; cls >= 0; --cls)
       ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_s[cls][par]), (int)P.t_s[cls][par].size(), beta, s, 1, t));
-    ORTH_HIP(launch_gemm_f32(GI(P.off_b_upd[par]), (int)P.b_upd[par].size(), "vjp_update_f32", s, t));
+    ORTH_HIP(launch_list(ws, P.off_b_upd[par], P.b_upd[par], "vjp_update_f32", s, t));
     for (int cls = 1; cls >= 0; --cls)
       ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_yu[cls][par]), (int)P.t_yu[cls][par].size(), beta, s, 1, t));
   }
@@ -1738,7 +1857,7 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
   build_conv_plan(descs, n, dtype, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_groups, P.groups);
   put(img, P.off_proj_items, P.proj_items);
   for (size_t ph = 0; ph < P.phase_gemm.size(); ++ph) {
@@ -1750,11 +1869,9 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
   const ComposeGroup* G = reinterpret_cast<const ComposeGroup*>(ws + P.off_groups);
   const int ng = (int)P.groups.size();
   ORTH_HIP(launch_compose_init(G, ng, dtype, P.init_max, s));
-  ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_proj_items), (int)P.proj_items.size(),
-                           "compose_projector", s));
+  ORTH_HIP(launch_list(ws, P.off_proj_items, P.proj_items, "compose_projector", s));
   for (size_t ph = 0; ph < P.phase_gemm.size(); ++ph) {
-    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_phase_gemm[ph]),
-                             (int)P.phase_gemm[ph].size(), "compose_tap_gemm", s));
+    ORTH_HIP(launch_list(ws, P.off_phase_gemm[ph], P.phase_gemm[ph], "compose_tap_gemm", s));
     ORTH_HIP(launch_compose_combine(G, reinterpret_cast<const CombineItem*>(ws + P.off_phase_comb[ph]),
                                     (int)P.phase_comb[ph].size(), P.phase_max_elems[ph], s));
   }
@@ -1788,7 +1905,7 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int n_phase = (int)P.fwd_gemm.size();
 
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_proj, P.proj_items);
   put(img, P.off_last_dp, P.last_dp);
   put(img, P.off_dv, P.dv_items);
@@ -1803,21 +1920,20 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
   }
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
-  auto GI = [&](size_t off) { return reinterpret_cast<const GemmItem*>(ws + off); };
   auto TI = [&](size_t off) { return reinterpret_cast<const TapItem*>(ws + off); };
   ORTH_HIP(launch_tap_items(0, TI(P.off_rko_taps), (int)P.rko_taps.size(), dtype, P.rko_max, s));
-  ORTH_HIP(launch_gemm_f32(GI(P.off_proj), (int)P.proj_items.size(), "conv_vjp_projector", s));
+  ORTH_HIP(launch_list(ws, P.off_proj, P.proj_items, "conv_vjp_projector", s));
   for (int ph = 0; ph < n_phase; ++ph) {
-    ORTH_HIP(launch_gemm_f32(GI(P.off_fwd_gemm[ph]), (int)P.fwd_gemm[ph].size(), "conv_vjp_tap_gemm", s));
+    ORTH_HIP(launch_list(ws, P.off_fwd_gemm[ph], P.fwd_gemm[ph], "conv_vjp_tap_gemm", s));
     ORTH_HIP(launch_tap_items(3, TI(P.off_fwd_comb[ph]), (int)P.fwd_comb[ph].size(), dtype, P.fwd_max[ph], s));
   }
   ORTH_HIP(launch_tap_items(1, TI(P.off_grad_taps), (int)P.grad_taps.size(), dtype, P.grad_max, s));
   for (int ph = n_phase - 1; ph >= 0; --ph) {
-    ORTH_HIP(launch_gemm_f32(GI(P.off_bwd_gemm[ph]), (int)P.bwd_gemm[ph].size(), "conv_vjp_tap_gemm", s));
+    ORTH_HIP(launch_list(ws, P.off_bwd_gemm[ph], P.bwd_gemm[ph], "conv_vjp_tap_gemm", s));
     ORTH_HIP(launch_tap_items(4, TI(P.off_bwd_comb[ph]), (int)P.bwd_comb[ph].size(), dtype, P.bwd_max[ph], s));
   }
-  ORTH_HIP(launch_gemm_f32(GI(P.off_last_dp), (int)P.last_dp.size(), "conv_vjp_tap_gemm", s));
-  ORTH_HIP(launch_gemm_f32(GI(P.off_dv), (int)P.dv_items.size(), "conv_vjp_factor_grad", s));
+  ORTH_HIP(launch_list(ws, P.off_last_dp, P.last_dp, "conv_vjp_tap_gemm", s));
+  ORTH_HIP(launch_list(ws, P.off_dv, P.dv_items, "conv_vjp_factor_grad", s));
   ORTH_HIP(launch_tap_items(2, TI(P.off_rko_grad), (int)P.rko_grad.size(), dtype, P.rko_max, s));
   return ORTH_OK;
 }
@@ -1862,7 +1978,7 @@ int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* o
   build_exp_plan(mats, n, opts, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_items, P.items);
   put(img, P.off_mats, P.mats);
   put(img, P.off_partial, P.partial_items);
@@ -1889,8 +2005,7 @@ int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* o
   ORTH_HIP(launch_prescale_finish(tm, n, partials, ORTH_PRESCALE_SPECTRAL, status, s));
   ORTH_HIP(launch_exp_init(items, n, 0, P.max_elems, s));
   for (size_t k = 0; k < P.steps.size(); ++k)
-    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_steps[k]), (int)P.steps[k].size(),
-                             "exp_map_series", s));
+    ORTH_HIP(launch_list(ws, P.off_steps[k], P.steps[k], "exp_map_series", s));
   ORTH_HIP(launch_writeout(tm, TI(P.off_writeout), (int)P.writeout_items.size(), 0, opts->out_dtype, s));
   return ORTH_OK;
 }
@@ -1918,7 +2033,7 @@ int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dt
   P = ExpPlan();
   build_conv_exp_plan(descs, n, dtype, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  std::vector<unsigned char> img(P.table_bytes, 0);
+  TableImage img;
   put(img, P.off_items, P.items);
   put(img, P.off_pairs, P.pairs);
   put(img, P.off_scatter, P.scatter);
@@ -1930,8 +2045,7 @@ int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dt
   ORTH_HIP(launch_exp_init(items, n, 1, P.max_init, s));
   const GemmPair* pairs = reinterpret_cast<const GemmPair*>(ws + P.off_pairs);
   for (size_t k = 0; k < P.steps.size(); ++k)
-    ORTH_HIP(launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + P.off_steps[k]), (int)P.steps[k].size(),
-                             "conv_exp_series", s, 0, pairs));
+    ORTH_HIP(launch_list(ws, P.off_steps[k], P.steps[k], "conv_exp_series", s, 0, pairs));
   ORTH_HIP(launch_tap_items(2, reinterpret_cast<const TapItem*>(ws + P.off_scatter), (int)P.scatter.size(), dtype,
                             P.max_scatter, s));
   return ORTH_OK;
@@ -1976,7 +2090,7 @@ int validate_check(const orth_check_args* a) {
   return ORTH_OK;
 }
 
-void gram_check_items(const orth_check_args* a, float* out, std::vector<GemmItem>& items) {
+void gram_check_items(const orth_check_args* a, float* out, GemmList& items) {
   for (int i = 0; i < a->n_mats; ++i) {
     const orth_mat& m = a->mats[i];
     const bool tall = m.rows >= m.cols;
@@ -2019,9 +2133,9 @@ int orth_check_workspace_size(const orth_check_args* args, size_t* bytes) {
   int rc = validate_check(args);
   if (rc) return rc;
   if (args->mode == ORTH_CHECK_GRAM) {
-    std::vector<GemmItem> items;
+    GemmList items;
     gram_check_items(args, nullptr, items);
-    *bytes = align_up(sizeof(GemmItem) * items.size());
+    *bytes = GemmList::bound(items.size());
   } else {
     *bytes = align_up(sizeof(double) * conv_partial_doubles(args));
   }
@@ -2040,14 +2154,14 @@ int orth_check_norm(const orth_check_args* args, float* out_dev, void* workspace
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (args->mode == ORTH_CHECK_GRAM) {
     if (args->n_mats == 0) return ORTH_OK;
-    std::vector<GemmItem> items;
+    GemmList items;
     gram_check_items(args, out_dev, items);
-    std::vector<unsigned char> img(sizeof(GemmItem) * items.size());
-    std::memcpy(img.data(), items.data(), img.size());
+    TableImage img;
+    put(img, 0, items);
     ORTH_HIP(launch_fill_f32(out_dev, args->n_mats, 0.f, s));
     rc = upload_tables(img, workspace, s);
     if (rc) return rc;
-    ORTH_HIP(launch_gemm_f32(static_cast<const GemmItem*>(workspace), (int)items.size(), "check_gram", s));
+    ORTH_HIP(launch_list(static_cast<const unsigned char*>(workspace), 0, items, "check_gram", s));
     return ORTH_OK;
   }
   ORTH_HIP(launch_conv_check(args, args->kernel, args->x, static_cast<double*>(workspace), out_dev,

@@ -211,6 +211,15 @@ struct GemmItem {
   int32_t pair_count;        //   [pair_base, pair_base + pair_count)
 };
 
+// One 64 x 64 output tile of a GemmItem's product (the item's own ti, tj are
+// not read on the device).  With a product's `mirror` set, its off-diagonal
+// tiles also write the transposed tile.
+struct GemmTile {
+  int32_t item;
+  int32_t ti, tj;
+  int32_t pad;
+};
+
 // Compose (AOC) descriptors: one entry per (layer, group).
 struct ComposeGroup {
   const void* rko;           // this group's RKO matrix, cout_g x (c s^2)
@@ -279,8 +288,8 @@ hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_it
                            int master_index, int out_dtype, hipStream_t s);
 hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
                              hipStream_t s, int vjp = 0, int step = 0);
-hipError_t launch_gemm_f32(const GemmItem* items, int n_items, const char* name, hipStream_t s, int step = 0,
-                           const GemmPair* pairs = nullptr);
+hipError_t launch_gemm_f32(const GemmItem* items, const GemmTile* tiles, int n_tiles, const char* name,
+                           hipStream_t s, int step = 0, const GemmPair* pairs = nullptr);
 hipError_t launch_vjp_load_grad(const TiledMat* mats, const TileItem* items, int n_items, int gout_dtype,
                                 hipStream_t s);
 hipError_t launch_vjp_dot_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
