@@ -22,6 +22,10 @@ GEOMS = [  # (cin, cout, k, s, d, g), H
     ((16, 16, 3, 1, 1, 1), 16), ((64, 128, 3, 2, 1, 1), 16), ((32, 32, 3, 1, 1, 4), 12),
     ((32, 32, 3, 1, 2, 1), 10), ((6, 6, 5, 2, 3, 3), 12), ((24, 16, 4, 2, 1, 2), 8),
     ((4, 6, 3, 1, 1, 1), 7), ((128, 512, 2, 2, 1, 1), 8), ((100, 70, 3, 1, 1, 1), 9),
+    # dilated span beyond one period of a 4 x 4 grid: the general modulo path
+    ((4, 4, 5, 1, 3, 1), 4), ((8, 8, 3, 2, 5, 2), 4),
+    # 128 x 128 tiles with ragged rows both ways (200 and 130 output rows)
+    ((130, 200, 3, 1, 1, 1), 6),
 ]
 
 
