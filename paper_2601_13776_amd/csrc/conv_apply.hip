@@ -215,6 +215,222 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Halo-staged variant for k <= 3: per chunk of CB = 8 reduction channels,
+// every input row that a 64-pixel tile needs (per output row it touches and
+// per tap row) is staged once in LDS, circularly extended by the taps'
+// reach, and all k^2 taps read from there.  The per-element global gather
+// (index arithmetic, wraps and one load per tap) becomes one load per
+// staged element (each read by up to k^2 taps x pixels) plus one LDS read
+// per MFMA operand value; the offsets of every staged element are computed
+// once per block.
+//
+// Staged layout per chunk: [ch][j][a][col], j the tile's output row slot
+// (J of them), a the tap row, col in [0, WX):
+//   forward    input row (s u + d a - pl) mod H of output row u, input
+//              column (col - pl) mod W; pixel v at tap e reads col s v + d e
+//   transposed row (u + pl - d a) mod H and column (col - span + pl) mod W of
+//              the stride-upsampled input (zero off the stride lattice);
+//              pixel v at tap e reads col v + span - d e
+struct HaloGeom {
+  int J;            // output rows a 64-pixel tile touches, at most
+  int RC;           // staged rows per channel: J k
+  int WX;           // staged columns
+  int tpr_log2;     // threads per staged row: 1 << tpr_log2 >= WX
+  int b_floats;     // CB RC WX rounded up to 4
+  int nch;          // reduction channels per group (c forward, og transposed)
+  int Hout, Wout;   // the output grid
+  int nchunks;      // ceil(nch / CB)
+};
+
+// 64 x 64 pixels per workgroup (128 pixels, for twice the reuse of the
+// staged kernel tile, measured 25-50% slower: more staged rows per chunk)
+constexpr int HALO_CB = 8, HALO_BNP = 64, HALO_MAXE = 24;
+
+// 64 output rows x BN pixels per workgroup; each wave 32 rows x BN / 2
+// pixels (NI accumulators)
+template <bool TR, int KS, int BN>
+__global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloGeom Hg,
+                                                              const void* __restrict__ kern,
+                                                              const float* __restrict__ x, float* __restrict__ y) {
+  constexpr int CB = HALO_CB, KK = KS * KS, KCH = CB * KK, AP = KCH + 4, NI = BN / 64;
+  constexpr int MAXA = (64 * KCH + 255) / 256;
+  static_assert(KCH % 8 == 0, "a chunk is a whole number of 8-deep groups");
+  extern __shared__ float smem[];
+  float* const As = smem;
+  float* const Bs = smem + 64 * AP;
+  int* koff = reinterpret_cast<int*>(Bs + Hg.b_floats);
+
+  const int grp = blockIdx.z;
+  const int row0 = blockIdx.y * 64;
+  const int64_t p0 = (int64_t)blockIdx.x * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int span = G.d * (KS - 1);
+  const int WX = Hg.WX, RC = Hg.RC;
+
+  // LDS offset of tap (ch, a, e) relative to a pixel's base
+  for (int kk = tid; kk < KCH; kk += 256) {
+    const int ch = kk / KK, tap = kk % KK, a = tap / KS, e = tap % KS;
+    koff[kk] = ch * RC * WX + a * WX + (TR ? -G.d * e : G.d * e);
+  }
+  // this lane's B-operand pixel: its base offset in a channel's block
+  const int64_t first_row = p0 / Hg.Wout;
+  int poff[NI];
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) {
+    const int64_t pn = p0 + wn * (BN / 2) + ni * 32 + (lane & 31);
+    poff[ni] = 0;
+    if (pn < G.pix) {
+      const int64_t orow = pn / Hg.Wout;
+      const int v = (int)(pn - orow * Hg.Wout);
+      poff[ni] = (int)(orow - first_row) * KS * WX + (TR ? v + span : G.s * v);
+    }
+  }
+
+  // staged elements of this thread: rows r = (tid >> tpr_log2) + i RPP,
+  // column tid & (TPR - 1); offsets relative to the chunk's first channel
+  const int rpp = 256 >> Hg.tpr_log2;
+  const int scol = tid & ((1 << Hg.tpr_log2) - 1);
+  const int srow0 = tid >> Hg.tpr_log2;
+  const int64_t cplane = TR ? (int64_t)G.Ho * G.Wo : (int64_t)G.H * G.W;   // one channel of the source
+  const int src_ch = TR ? G.cout : G.cin;
+  const int ch_base = grp * Hg.nch;
+  int boff[HALO_MAXE];
+#pragma unroll
+  for (int i = 0; i < HALO_MAXE; ++i) {
+    boff[i] = -1;
+    const int r = srow0 + i * rpp;
+    if (r >= CB * RC || scol >= WX) continue;
+    const int ch = r / RC, rr = r - ch * RC, j = rr / KS, a = rr - j * KS;
+    const int64_t orow = first_row + j;
+    const int64_t b = orow / Hg.Hout;
+    const int u = (int)(orow - b * Hg.Hout);
+    if (b >= G.batch) continue;
+    int off;
+    if (!TR) {
+      const int sr = pmod(G.s * u + G.d * a - G.pl, G.H), sc = pmod(scol - G.pl, G.W);
+      off = (int)(((b * src_ch + ch_base + ch) * cplane) + (int64_t)sr * G.W + sc);
+    } else {
+      const int R = pmod(u + G.pl - G.d * a, G.H), C = pmod(scol - span + G.pl, G.W);
+      if (R % G.s || C % G.s) continue;
+      off = (int)(((b * src_ch + ch_base + ch) * cplane) + (int64_t)(R / G.s) * G.Wo + C / G.s);
+    }
+    boff[i] = off;
+  }
+  // kernel elements of this thread: e = tid + i 256 over 64 rows x KCH
+  int aoff[MAXA];
+#pragma unroll
+  for (int i = 0; i < MAXA; ++i) {
+    aoff[i] = -1;
+    const int e = tid + i * 256;
+    if (e >= 64 * KCH) continue;
+    const int row = e / KCH, col = e - (e / KCH) * KCH;
+    if (row0 + row >= G.rows) continue;
+    if (!TR)
+      aoff[i] = (grp * G.og + row0 + row) * G.red + col;            // + ch0 KK per chunk
+    else
+      aoff[i] = ((grp * G.og + col / KK) * G.c + row0 + row) * KK + col % KK;   // + ch0 c KK
+  }
+
+  // one LDS stage: every chunk is staged (all loads in flight, then the
+  // stores), computed between two barriers; the two or three other
+  // workgroups on the compute unit overlap their staging with this one's
+  // MFMAs
+  // loads address a uniform base (this chunk's first channel) plus a
+  // 32-bit byte offset (the host keeps both tensors below 2^30 elements),
+  // one VGPR per address
+  auto stage = [&](int ch0) {
+    const int nvalid = Hg.nch - ch0;   // channels of this chunk that exist
+    const int kes = G.kdtype == ORTH_BF16 ? 2 : 4;
+    const char* kq = static_cast<const char*>(kern) + (TR ? (int64_t)ch0 * G.c * KK : (int64_t)ch0 * KK) * kes;
+    const char* xq = reinterpret_cast<const char*>(x + (int64_t)ch0 * cplane);
+    float ra[MAXA], rb[HALO_MAXE];
+#pragma unroll
+    for (int i = 0; i < MAXA; ++i) {
+      const int e = tid + i * 256, col = e - (e / KCH) * KCH;
+      float v = 0.f;
+      if (aoff[i] >= 0 && col / KK < nvalid) {
+        const uint32_t bo = (uint32_t)aoff[i] * (uint32_t)kes;
+        v = kes == 2 ? bf16_to_f32(*reinterpret_cast<const uint16_t*>(kq + bo))
+                     : *reinterpret_cast<const float*>(kq + bo);
+      }
+      ra[i] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < HALO_MAXE; ++i) {
+      const int r = srow0 + i * rpp;
+      float v = 0.f;
+      if (boff[i] >= 0 && r < nvalid * RC) v = *reinterpret_cast<const float*>(xq + (uint32_t)boff[i] * 4u);
+      rb[i] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < MAXA; ++i) {
+      const int e = tid + i * 256;
+      if (e < 64 * KCH) As[(e / KCH) * AP + e % KCH] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < HALO_MAXE; ++i) {
+      const int r = srow0 + i * rpp;
+      if (r < CB * RC && scol < WX) Bs[r * WX + scol] = rb[i];
+    }
+  };
+
+  f32x16 acc[NI];
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) acc[ni] = f32x16{};
+  const int aread = (wm * 32 + (lane & 31)) * AP + (lane >> 5) * 4;
+  for (int q = 0; q < Hg.nchunks; ++q) {
+    stage(q * CB);
+    __syncthreads();
+#pragma unroll
+    for (int g8 = 0; g8 < KCH / 8; ++g8) {
+      // k = 8 g8 + 4 (lane / 32) + t for instruction t, on both operands
+      const float4 a4 = *reinterpret_cast<const float4*>(&As[aread + g8 * 8]);
+      const int4 k4 = *reinterpret_cast<const int4*>(&koff[g8 * 8 + (lane >> 5) * 4]);
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni) {
+        const float* bs = Bs + poff[ni];
+        acc[ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, bs[k4.x], acc[ni], 0, 0, 0);
+        acc[ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, bs[k4.y], acc[ni], 0, 0, 0);
+        acc[ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, bs[k4.z], acc[ni], 0, 0, 0);
+        acc[ni] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, bs[k4.w], acc[ni], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  const int ow = Hg.Wout, oh = Hg.Hout;
+  const int ych = TR ? G.cin : G.cout;
+  const int chb = grp * (TR ? G.c : G.og);
+  const int64_t plane = (int64_t)oh * ow;
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) {
+    const int64_t pn = p0 + wn * (BN / 2) + ni * 32 + (lane & 31);
+    if (pn >= G.pix) continue;
+    const int ov = (int)(pn % ow);
+    const int ou = (int)((pn / ow) % oh);
+    const int ob = (int)(pn / ((int64_t)ow * oh));
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ch = row0 + wm * 32 + acc_row(r, lane);
+      if (ch < G.rows) y[((int64_t)ob * ych + chb + ch) * plane + (int64_t)ou * ow + ov] = acc[ni][r];
+    }
+  }
+}
+
+template <bool TR, int KS>
+hipError_t launch_halo(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
+                       hipStream_t s) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_apply_halo_kernel<TR, KS, HALO_BNP>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((conv_apply_halo_kernel<TR, KS, HALO_BNP>), grid, dim3(256), lds, s, G, Hg, a->kernel, a->x,
+                     a->y);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_conv_apply(const orth_conv_apply_args* a, hipStream_t s) {
@@ -238,6 +454,46 @@ hipError_t launch_conv_apply(const orth_conv_apply_args* a, hipStream_t s) {
   G.red = (a->transposed ? G.og : G.c) * g.k * g.k;
   G.pix = (int64_t)a->batch * (a->transposed ? (int64_t)G.H * G.W : (int64_t)G.Ho * G.Wo);
   G.kdtype = a->kernel_dtype;
+  // halo-staged kernel where it applies (k <= 3, staged rows within the
+  // per-thread budget, three workgroups' LDS per compute unit)
+  if (g.k <= 3) {
+    const bool TRn = a->transposed != 0;
+    HaloGeom Hg{};
+    Hg.Hout = TRn ? G.H : G.Ho;
+    Hg.Wout = TRn ? G.W : G.Wo;
+    Hg.nch = TRn ? G.og : G.c;
+    const int span = G.d * (G.k - 1);
+    Hg.J = (Hg.Wout - 1 + HALO_BNP - 1) / Hg.Wout + 1;
+    Hg.RC = Hg.J * G.k;
+    Hg.WX = TRn ? G.W + span : G.s * (G.Wo - 1) + span + 1;
+    int t = 0;
+    while ((1 << t) < Hg.WX) ++t;
+    Hg.tpr_log2 = t;
+    Hg.b_floats = (HALO_CB * Hg.RC * Hg.WX + 3) / 4 * 4;
+    Hg.nchunks = (Hg.nch + HALO_CB - 1) / HALO_CB;
+    const int kch = HALO_CB * G.k * G.k;
+    const size_t lds = (size_t)(64 * (kch + 4) + Hg.b_floats + kch) * sizeof(float);
+    const int64_t src_elems = (int64_t)G.batch * (TRn ? (int64_t)G.cout * G.Ho * G.Wo : (int64_t)G.cin * G.H * G.W);
+    const bool fits = t <= 8 && (HALO_CB * Hg.RC + (256 >> t) - 1) / (256 >> t) <= HALO_MAXE && lds <= 52 * 1024 &&
+                      src_elems < ((int64_t)1 << 30) && (int64_t)G.cout * G.c * G.k * G.k < ((int64_t)1 << 30) &&
+                      Hg.nch > 0;
+    if (fits) {
+      const dim3 grid((unsigned)((G.pix + HALO_BNP - 1) / HALO_BNP), (unsigned)((G.rows + 63) / 64),
+                      (unsigned)g.groups);
+      const char* name = TRn ? "conv_apply_transposed" : "conv_apply";
+      timing_begin(name, s);
+      hipError_t e;
+      if (TRn)
+        e = G.k == 1 ? launch_halo<true, 1>(G, Hg, grid, lds, a, s)
+                     : G.k == 2 ? launch_halo<true, 2>(G, Hg, grid, lds, a, s) : launch_halo<true, 3>(G, Hg, grid, lds, a, s);
+      else
+        e = G.k == 1 ? launch_halo<false, 1>(G, Hg, grid, lds, a, s)
+                     : G.k == 2 ? launch_halo<false, 2>(G, Hg, grid, lds, a, s)
+                                : launch_halo<false, 3>(G, Hg, grid, lds, a, s);
+      timing_end(name, s);
+      return e;
+    }
+  }
   // 64 x 64 tiles: measured on the CIFAR- and ImageNet-like stacks, 128 x
   // 128 tiles (four times the MFMA work per gathered element) were no
   // faster on wide layers and up to 2x slower where the small late grids
