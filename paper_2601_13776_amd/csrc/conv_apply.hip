@@ -81,20 +81,24 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
   const int xch = TR ? G.cout : G.cin;
   const float* xb = x + (int64_t)pb * xch * xplane;
 
-  float ra[EA], rb[EB];
+  uint32_t ra[EA];
+  float rb[EB];
   auto gload = [&](int k0) {
     // kernel values
     {
       const int row = row0 + ar;
       int kk = k0 + ak;
       int ch = kk / kk2, tap = kk - ch * kk2;   // (input channel, tap) or (output channel, tap)
+      // raw bits, widened at the LDS store (a conversion inside the guarded
+      // load would make every load wait for its data)
 #pragma unroll
       for (int j = 0; j < EA; ++j) {
-        float v = 0.f;
+        uint32_t v = 0;
         if (row < G.rows && kk < G.red) {
           const int64_t idx = TR ? ((int64_t)(grp * G.og + ch) * G.c + row) * kk2 + tap
                                  : (int64_t)(grp * G.og + row) * G.red + kk;
-          v = load_as_f32(kern, idx, G.kdtype);
+          v = G.kdtype == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(kern)[idx]
+                                    : static_cast<const uint32_t*>(kern)[idx];
         }
         ra[j] = v;
         ++kk;
@@ -104,6 +108,10 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
         }
       }
     }
+    // materialize the raw values after the guarded loads (otherwise the
+    // widening shift is moved into each guarded block, where it waits)
+#pragma unroll
+    for (int j = 0; j < EA; ++j) asm volatile("" : "+v"(ra[j]));
     // gathered input values
     {
       int kk = k0 + bk;
@@ -147,8 +155,11 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
   };
   auto sstore = [&](int buf) {
     float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
+    const int sh = G.kdtype == ORTH_BF16 ? 16 : 0;
 #pragma unroll
-    for (int q = 0; q < EA / 4; ++q) pa[q] = make_float4(ra[4 * q], ra[4 * q + 1], ra[4 * q + 2], ra[4 * q + 3]);
+    for (int q = 0; q < EA / 4; ++q)
+      pa[q] = make_float4(__uint_as_float(ra[4 * q] << sh), __uint_as_float(ra[4 * q + 1] << sh),
+                          __uint_as_float(ra[4 * q + 2] << sh), __uint_as_float(ra[4 * q + 3] << sh));
     float4* pbv = reinterpret_cast<float4*>(&Bs[buf][bp * PITCH + bk]);
 #pragma unroll
     for (int q = 0; q < EB / 4; ++q) pbv[q] = make_float4(rb[4 * q], rb[4 * q + 1], rb[4 * q + 2], rb[4 * q + 3]);
@@ -250,7 +261,7 @@ constexpr int HALO_CB = 8, HALO_BNP = 64, HALO_MAXE = 24;
 
 // 64 output rows x BN pixels per workgroup; each wave 32 rows x BN / 2
 // pixels (NI accumulators)
-template <bool TR, int KS, int BN>
+template <bool TR, int KS, int BN, bool KBF16>
 __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloGeom Hg,
                                                               const void* __restrict__ kern,
                                                               const float* __restrict__ x, float* __restrict__ y) {
@@ -343,21 +354,30 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
   // one VGPR per address
   auto stage = [&](int ch0) {
     const int nvalid = Hg.nch - ch0;   // channels of this chunk that exist
-    const int kes = G.kdtype == ORTH_BF16 ? 2 : 4;
+    constexpr int kes = KBF16 ? 2 : 4;   // kernel element bytes
     const char* kq = static_cast<const char*>(kern) + (TR ? (int64_t)ch0 * G.c * KK : (int64_t)ch0 * KK) * kes;
     const char* xq = reinterpret_cast<const char*>(x + (int64_t)ch0 * cplane);
-    float ra[MAXA], rb[HALO_MAXE];
+    // raw bits first, widened at the LDS store: a conversion inside the
+    // guarded load would make every load wait for its data
+    uint32_t ra[MAXA];
+    float rb[HALO_MAXE];
 #pragma unroll
     for (int i = 0; i < MAXA; ++i) {
       const int e = tid + i * 256, col = e - (e / KCH) * KCH;
-      float v = 0.f;
+      uint32_t v = 0;
       if (aoff[i] >= 0 && col / KK < nvalid) {
         const uint32_t bo = (uint32_t)aoff[i] * (uint32_t)kes;
-        v = kes == 2 ? bf16_to_f32(*reinterpret_cast<const uint16_t*>(kq + bo))
-                     : *reinterpret_cast<const float*>(kq + bo);
+        if constexpr (KBF16)
+          v = *reinterpret_cast<const uint16_t*>(kq + bo);
+        else
+          v = *reinterpret_cast<const uint32_t*>(kq + bo);
       }
       ra[i] = v;
     }
+    // materialize the raw values after the guarded loads (otherwise the
+    // widening shift is moved into each guarded block, where it waits)
+#pragma unroll
+    for (int i = 0; i < MAXA; ++i) asm volatile("" : "+v"(ra[i]));
 #pragma unroll
     for (int i = 0; i < HALO_MAXE; ++i) {
       const int r = srow0 + i * rpp;
@@ -368,7 +388,7 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
 #pragma unroll
     for (int i = 0; i < MAXA; ++i) {
       const int e = tid + i * 256;
-      if (e < 64 * KCH) As[(e / KCH) * AP + e % KCH] = ra[i];
+      if (e < 64 * KCH) As[(e / KCH) * AP + e % KCH] = __uint_as_float(KBF16 ? ra[i] << 16 : ra[i]);
     }
 #pragma unroll
     for (int i = 0; i < HALO_MAXE; ++i) {
@@ -420,15 +440,21 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
   }
 }
 
+template <bool TR, int KS, bool KBF16>
+hipError_t launch_halo_k(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
+                         hipStream_t s) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16>), grid, dim3(256), lds, s, G, Hg, a->kernel,
+                     a->x, a->y);
+  return hipGetLastError();
+}
 template <bool TR, int KS>
 hipError_t launch_halo(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
                        hipStream_t s) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_apply_halo_kernel<TR, KS, HALO_BNP>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((conv_apply_halo_kernel<TR, KS, HALO_BNP>), grid, dim3(256), lds, s, G, Hg, a->kernel, a->x,
-                     a->y);
-  return hipGetLastError();
+  return G.kdtype == ORTH_BF16 ? launch_halo_k<TR, KS, true>(G, Hg, grid, lds, a, s)
+                               : launch_halo_k<TR, KS, false>(G, Hg, grid, lds, a, s);
 }
 
 }  // namespace
