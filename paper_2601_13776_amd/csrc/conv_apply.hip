@@ -108,10 +108,7 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
         }
       }
     }
-    // materialize the raw values after the guarded loads (otherwise the
-    // widening shift is moved into each guarded block, where it waits)
-#pragma unroll
-    for (int j = 0; j < EA; ++j) asm volatile("" : "+v"(ra[j]));
+
     // gathered input values
     {
       int kk = k0 + bk;
@@ -154,6 +151,11 @@ __global__ __launch_bounds__(256) void conv_apply_kernel(ApplyGeom G, const void
     }
   };
   auto sstore = [&](int buf) {
+    // the raw values materialize here, after the MFMAs that the loads
+    // overlap (otherwise the widening shift is moved into each guarded
+    // load's block, where it waits for the data)
+#pragma unroll
+    for (int j = 0; j < EA; ++j) asm volatile("" : "+v"(ra[j]));
     float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
     const int sh = G.kdtype == ORTH_BF16 ? 16 : 0;
 #pragma unroll

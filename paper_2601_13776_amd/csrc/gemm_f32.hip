@@ -67,42 +67,79 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     const int br = btr ? (tid & 63) : (tid >> 2);
     const int bk = btr ? (tid >> 6) * 8 : (tid & 3) * 8;
 
-    float ra[8], rb[8];
+    // Raw operand words: fp32 bits, bf16 bits in the low half (widened at
+    // the LDS store), or (packed) eight bf16 values in words 0-3 from one
+    // 16-byte load.  Widening only at the store keeps each guarded load
+    // from waiting for its data.
+    uint32_t ra[8], rb[8];
+    bool apk = false, bpk = false;
     auto load_op = [&](const void* P, int64_t ld, int dt, int tr, int r, int kq, int rows_lim, int rbase, int k0,
-                       float* dst) {
+                       uint32_t* dst, bool& packed) {
       const int gr = rbase + r;
       const int gk = k0 + kq;
-      if (!tr && dt == ORTH_F32 && gr < rows_lim && gk + 8 <= K) {
-        const float* p = static_cast<const float*>(P) + (int64_t)gr * ld + gk;
-        if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-          const float4 x = reinterpret_cast<const float4*>(p)[0];
-          const float4 y = reinterpret_cast<const float4*>(p)[1];
-          dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
-          dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
-          return;
+      packed = false;
+      if (!tr && gr < rows_lim && gk + 8 <= K) {
+        if (dt == ORTH_F32) {
+          const float* p = static_cast<const float*>(P) + (int64_t)gr * ld + gk;
+          if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+            const uint4 x = reinterpret_cast<const uint4*>(p)[0];
+            const uint4 y = reinterpret_cast<const uint4*>(p)[1];
+            dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
+            dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
+            return;
+          }
+        } else {
+          const uint16_t* p = static_cast<const uint16_t*>(P) + (int64_t)gr * ld + gk;
+          if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+            const uint4 x = *reinterpret_cast<const uint4*>(p);
+            dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
+            packed = true;
+            return;
+          }
         }
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        float v = 0.f;
+        uint32_t v = 0;
         if (gr < rows_lim && gk + q < K) {
           const int64_t idx = tr ? (int64_t)(gk + q) * ld + gr : (int64_t)gr * ld + gk + q;
-          v = load_as_f32(P, idx, dt);
+          v = dt == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(P)[idx] : static_cast<const uint32_t*>(P)[idx];
         }
         dst[q] = v;
       }
     };
     auto gload = [&](int k0) {
-      load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra);
-      load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb);
+      load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra, apk);
+      load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb, bpk);
+    };
+    auto widen = [&](const uint32_t* w, bool packed, int dt, float* f) {
+      if (packed) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          f[2 * q] = __uint_as_float(w[q] << 16);
+          f[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+        }
+      } else {
+        const int sh = dt == ORTH_BF16 ? 16 : 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) f[q] = __uint_as_float(w[q] << sh);
+      }
     };
     auto sstore = [&](int buf) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        asm volatile("" : "+v"(ra[q]));
+        asm volatile("" : "+v"(rb[q]));
+      }
+      float fa[8], fb[8];
+      widen(ra, apk, adt, fa);
+      widen(rb, bpk, bdt, fb);
       float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
-      pa[0] = make_float4(ra[0], ra[1], ra[2], ra[3]);
-      pa[1] = make_float4(ra[4], ra[5], ra[6], ra[7]);
+      pa[0] = make_float4(fa[0], fa[1], fa[2], fa[3]);
+      pa[1] = make_float4(fa[4], fa[5], fa[6], fa[7]);
       float4* pb = reinterpret_cast<float4*>(&Bs[buf][br * PITCH + bk]);
-      pb[0] = make_float4(rb[0], rb[1], rb[2], rb[3]);
-      pb[1] = make_float4(rb[4], rb[5], rb[6], rb[7]);
+      pb[0] = make_float4(fb[0], fb[1], fb[2], fb[3]);
+      pb[1] = make_float4(fb[4], fb[5], fb[6], fb[7]);
     };
 
     // stage 0 is free here: every wave passed the last barrier of the
