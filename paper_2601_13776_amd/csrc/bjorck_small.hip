@@ -51,15 +51,26 @@ __device__ inline void load_tall(float* dst, const void* src, int64_t ld, int tr
                                  int dtype, bool stats, double& ss, int& bad) {
   constexpr int U = 8, XP = NP + 1;
   const int total = Mp * NP;
+  const int sh = dtype == ORTH_BF16 ? 16 : 0;
   for (int base = 0; base < total; base += NTHR * U) {
-    float v[U];
+    // raw bits, widened after the batch (a conversion inside the guarded
+    // load would make each load wait for its data)
+    uint32_t w[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int idx = base + u * NTHR + (int)threadIdx.x;
       const int r = idx / NP, c = idx % NP;
-      v[u] = 0.f;
-      if (idx < total && r < M && c < N)
-        v[u] = load_as_f32(src, transposed ? (int64_t)c * ld + r : (int64_t)r * ld + c, dtype);
+      w[u] = 0;
+      if (idx < total && r < M && c < N) {
+        const int64_t e = transposed ? (int64_t)c * ld + r : (int64_t)r * ld + c;
+        w[u] = dtype == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(src)[e] : static_cast<const uint32_t*>(src)[e];
+      }
+    }
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      asm volatile("" : "+v"(w[u]));
+      v[u] = __uint_as_float(w[u] << sh);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {

@@ -48,17 +48,55 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
   const double* in = it.second ? d.px : d.pv;
   double* out = it.second ? d.py : d.px;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // rows and columns start 16-byte aligned: runs of 8 elements are loaded
+  // with one 16-byte (bf16) or two (fp32) vector loads
+  const bool vec = vec8_ok(d.in, d.ld_in, in_dtype);
   if (!it.coldot) {
     // out[r] = sum_c W[r][c] in[c]: a wave per row, lanes along the row
+    const int cols8 = vec ? d.cols / 8 * 8 : 0;
     for (int i = wave; i < 64; i += 4) {
       const int r = it.block * 64 + i;
       if (r >= d.rows) break;
       double acc = 0.0;
-      for (int c = lane; c < d.cols; c += 64)
-        acc += (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype) * in[c];
+      const int64_t row = (int64_t)r * d.ld_in;
+      for (int c0 = lane * 8; c0 < cols8; c0 += 512) {
+        float w[8];
+        load8_f32(d.in, row + c0, in_dtype, w);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc += (double)w[q] * in[c0 + q];
+      }
+      for (int c = cols8 + lane; c < d.cols; c += 64) acc += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
       acc = wave_sum(acc);
       if (lane == 0) out[r] = acc;
     }
+  } else if (vec && (d.cols - it.block * 64 >= 64 || d.cols % 8 == 0)) {
+    // out[c] = sum_r W[r][c] in[r] over this item's 64 columns: eight lanes
+    // cover them with 8-element runs, a wave reads eight rows at a time
+    const int cg = lane & 7, rsub = lane >> 3;
+    const int c0 = it.block * 64 + cg * 8;
+    double acc[8] = {};
+    if (c0 < d.cols)
+      for (int r = wave * 8 + rsub; r < d.rows; r += 32) {
+        float w[8];
+        load8_f32(d.in, (int64_t)r * d.ld_in + c0, in_dtype, w);
+        const double x = in[r];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += (double)w[q] * x;
+      }
+    // fixed-order reduction: over the eight row groups of a wave (lanes
+    // with the same column group), then over the four waves
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+#pragma unroll
+      for (int off = 8; off < 64; off <<= 1) acc[q] += __shfl_xor(acc[q], off, 64);
+    }
+    __shared__ double colsum[4][64];
+    if (rsub == 0)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) colsum[wave][cg * 8 + q] = acc[q];
+    __syncthreads();
+    const int c = it.block * 64 + lane;
+    if (wave == 0 && c < d.cols) out[c] = ((colsum[0][lane] + colsum[1][lane]) + colsum[2][lane]) + colsum[3][lane];
   } else {
     // out[c] = sum_r W[r][c] in[r]: lanes along 64 columns, waves interleave rows
     const int c = it.block * 64 + lane;
