@@ -185,14 +185,28 @@ struct Arena {
 // the workspace: the items, then the tiles.
 static_assert(sizeof(GemmItem) % 8 == 0 && sizeof(GemmItem) == 8 * 8 + 13 * 8 + 18 * 4,
               "GemmItem must have no padding: items are compared bytewise");
+// Products added whole (add_all) get their tiles at finalize().  (128 x 128
+// tiles for lists of large products were measured 5-30% slower with this
+// kernel's register-staged loads, so every list uses 64 x 64.)
 struct GemmList {
   std::vector<GemmItem> items;
   std::vector<GemmTile> tiles;
+  std::vector<int32_t> pending;   // add_all products without tiles yet
+  int64_t pending64 = 0;          // their tile count
   GemmItem last{};   // items.back() with its tile and mirror fields cleared
-  size_t size() const { return tiles.size(); }
+  size_t size() const { return tiles.size() + (size_t)pending64; }
   void clear() {
     items.clear();
     tiles.clear();
+    pending.clear();
+    pending64 = 0;
+  }
+  void finalize() {
+    for (int32_t idx : pending)
+      for (int a = 0; a < (items[idx].M + 63) / 64; ++a)
+        for (int b = 0; b < (items[idx].N + 63) / 64; ++b) tiles.push_back(GemmTile{idx, a, b, 0});
+    pending.clear();
+    pending64 = 0;
   }
   // one tile, given as a whole item with its ti, tj (and mirror for an
   // off-diagonal tile); it shares the previous tile's item when the rest
@@ -208,16 +222,15 @@ struct GemmList {
     if (g.mirror) items.back().mirror = 1;
     tiles.push_back(GemmTile{(int32_t)items.size() - 1, g.ti, g.tj, 0});
   }
-  // every tile of proto's M x N output
+  // every tile of proto's M x N output (made by finalize)
   void add_all(const GemmItem& proto) {
     GemmItem k = proto;
     k.ti = k.tj = 0;
     items.push_back(k);
     last = k;
     last.mirror = 0;
-    const int32_t idx = (int32_t)items.size() - 1;
-    for (int a = 0; a < (proto.M + 63) / 64; ++a)
-      for (int b = 0; b < (proto.N + 63) / 64; ++b) tiles.push_back(GemmTile{idx, a, b, 0});
+    pending.push_back((int32_t)items.size() - 1);
+    pending64 += (int64_t)((proto.M + 63) / 64) * ((proto.N + 63) / 64);
   }
   size_t items_bytes() const { return align_up(items.size() * sizeof(GemmItem)); }
   // workspace bytes for at most n tiles, each of its own product
@@ -225,7 +238,8 @@ struct GemmList {
   size_t bytes() const { return items_bytes() + align_up(tiles.size() * sizeof(GemmTile)); }
 };
 
-void put(TableImage& img, size_t off, const GemmList& g) {
+void put(TableImage& img, size_t off, GemmList& g) {
+  g.finalize();
   img.add(off, g.items.data(), g.items.size() * sizeof(GemmItem));
   img.add(off + g.items_bytes(), g.tiles.data(), g.tiles.size() * sizeof(GemmTile));
 }
@@ -234,6 +248,7 @@ void put(TableImage& img, size_t off, const GemmList& g) {
 // that short tiles fill a launch's tail; extra pairs are counted at the
 // first pair's depth.
 void longest_first(GemmList& g) {
+  g.finalize();
   auto work = [&](const GemmTile& t) {
     const GemmItem& it = g.items[t.item];
     return (int64_t)it.K * (1 + it.pair_count) + it.K2;
@@ -716,24 +731,19 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
     P.init_max = std::max<int64_t>(P.init_max, (int64_t)s * s * og * c);
     P.scatter_max = std::max<int64_t>(P.scatter_max, (int64_t)k * k * og * c);
 
-    const int ct = (c + 63) / 64, ot = (og + 63) / 64;
-    for (int j = 0; j < nproj; ++j)
-      for (int a = 0; a < ct; ++a)
-        for (int b = 0; b < ct; ++b) {
-          GemmItem gi{};
-          gi.A = static_cast<const unsigned char*>(G.proj) + (size_t)j * c * h * esz;
-          gi.B = gi.A;
-          gi.C = G.p + (size_t)j * c * c;
-          gi.lda = gi.ldb = h;
-          gi.ldc = c;
-          gi.M = gi.N = c;
-          gi.K = h;
-          gi.ti = a;
-          gi.tj = b;
-          gi.a_dtype = gi.b_dtype = dtype;
-          gi.epi = EPI_STORE;
-          P.proj_items.push_back(gi);
-        }
+    for (int j = 0; j < nproj; ++j) {
+      GemmItem gi{};
+      gi.A = static_cast<const unsigned char*>(G.proj) + (size_t)j * c * h * esz;
+      gi.B = gi.A;
+      gi.C = G.p + (size_t)j * c * c;
+      gi.lda = gi.ldb = h;
+      gi.ldc = c;
+      gi.M = gi.N = c;
+      gi.K = h;
+      gi.a_dtype = gi.b_dtype = dtype;
+      gi.epi = EPI_STORE;
+      P.proj_items.add_all(gi);
+    }
     int cur = 0;
     for (int ph = 0; ph < n_phase; ++ph) {
       const bool vert = ph >= max_kp - 1;
@@ -743,25 +753,21 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
       const int pj = vert ? (kp - 1) + j : j;  // projector index: h blocks first
       const size_t tap = (size_t)og * c;
       for (int a = 0; a < in_h; ++a)
-        for (int b = 0; b < in_w; ++b)
-          for (int ti = 0; ti < ot; ++ti)
-            for (int tj = 0; tj < ct; ++tj) {
-              GemmItem gi{};
-              gi.A = G.taps[cur] + (size_t)(a * k + b) * tap;
-              gi.B = G.p + (size_t)pj * c * c;
-              gi.C = G.y + (size_t)(a * k + b) * tap;
-              gi.lda = c;
-              gi.ldb = c;
-              gi.ldc = c;
-              gi.M = og;
-              gi.N = c;
-              gi.K = c;
-              gi.ti = ti;
-              gi.tj = tj;
-              gi.a_dtype = gi.b_dtype = ORTH_F32;
-              gi.epi = EPI_STORE;
-              P.phase_gemm[ph].push_back(gi);
-            }
+        for (int b = 0; b < in_w; ++b) {
+          GemmItem gi{};
+          gi.A = G.taps[cur] + (size_t)(a * k + b) * tap;
+          gi.B = G.p + (size_t)pj * c * c;
+          gi.C = G.y + (size_t)(a * k + b) * tap;
+          gi.lda = c;
+          gi.ldb = c;
+          gi.ldc = c;
+          gi.M = og;
+          gi.N = c;
+          gi.K = c;
+          gi.a_dtype = gi.b_dtype = ORTH_F32;
+          gi.epi = EPI_STORE;
+          P.phase_gemm[ph].add_all(gi);
+        }
       P.phase_comb[ph].push_back(CombineItem{gidx, vert ? 1 : 0, in_h, in_w, cur, 0});
       const int out_taps = (in_h + (vert ? 1 : 0)) * (in_w + (vert ? 0 : 1));
       P.phase_max_elems[ph] = std::max<int64_t>(P.phase_max_elems[ph], (int64_t)out_taps * og * c);
