@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     }
   } else {  // EPI_UPDATE
     const float* src = g->src + g->src_step * st;
-    float* dst2 = g->dst2;
+    float* dst2 = g->dst2 ? g->dst2 + g->d2_step * st : nullptr;
     const int64_t lds_ = g->ld_src, ld2 = g->ld2;
     const float beta = g->beta;
 #pragma unroll

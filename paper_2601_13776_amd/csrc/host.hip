@@ -183,7 +183,7 @@ struct Arena {
 // fp32 GEMM work of one launch: one item per product, one GemmTile per
 // 64 x 64 output tile (consecutive tiles of a product share its item).  In
 // the workspace: the items, then the tiles.
-static_assert(sizeof(GemmItem) % 8 == 0 && sizeof(GemmItem) == 8 * 8 + 13 * 8 + 18 * 4,
+static_assert(sizeof(GemmItem) % 8 == 0 && sizeof(GemmItem) == 8 * 8 + 14 * 8 + 18 * 4,
               "GemmItem must have no padding: items are compared bytewise");
 // Products added whole (add_all) get their tiles at finalize().  (128 x 128
 // tiles for lists of large products were measured 5-30% slower with this
@@ -1495,25 +1495,32 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       t.gy_final = 0;
       continue;
     }
+    // X_t and its transpose per step, E_t per step, the gradient iterate
+    // and its transpose (ping-pong): every product reads row-major operands
     float* xs = reinterpret_cast<float*>(dev(A.take((size_t)slots * xe * 4)));
+    float* xts = reinterpret_cast<float*>(dev(A.take((size_t)slots * xe * 4)));
     float* es = reinterpret_cast<float*>(dev(A.take((size_t)T * ee * 4)));
     float* gy0 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
     float* gy1 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+    float* gyt0 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
+    float* gyt1 = reinterpret_cast<float*>(dev(A.take(xe * 4)));
     float* sb = reinterpret_cast<float*>(dev(A.take(ee * 4)));
     t.master[0] = xs;
+    t.xt = xts;
     t.e = es;
     t.gy[0] = gy0;
     t.gy[1] = gy1;
+    t.gyt[0] = gyt0;
+    t.gyt[1] = gyt1;
     t.s = sb;
     t.gy_final = T & 1;
     const int tn = t.Np / 64, tm = t.Mp / 64;
     for (int a = 0; a < tn; ++a)
       for (int b = a; b < tn; ++b) {
         GemmItem g{};
-        g.A = xs;
-        g.B = xs;
-        g.a_trans = g.b_trans = 1;
-        g.lda = g.ldb = t.Np;
+        g.A = xts;
+        g.B = xts;
+        g.lda = g.ldb = t.Mp;
         g.a_step = g.b_step = xe;
         g.K = t.Mp;
         g.M = g.N = t.Np;
@@ -1528,20 +1535,16 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
         P.f_gram.push_back(g);
         for (int par = 0; par < 2; ++par) {
           GemmItem h{};
-          h.A = xs;
-          h.a_trans = 1;
-          h.lda = t.Np;
+          h.A = xts;
+          h.lda = t.Mp;
           h.a_step = xe;
-          h.B = par ? gy1 : gy0;
-          h.b_trans = 1;
-          h.ldb = t.Np;
+          h.B = par ? gyt1 : gyt0;
+          h.ldb = t.Mp;
           h.K = t.Mp;
-          h.A2 = par ? gy1 : gy0;
-          h.a2_trans = 1;
-          h.lda2 = t.Np;
-          h.B2 = xs;
-          h.b2_trans = 1;
-          h.ldb2 = t.Np;
+          h.A2 = par ? gyt1 : gyt0;
+          h.lda2 = t.Mp;
+          h.B2 = xts;
+          h.ldb2 = t.Mp;
           h.b2_step = xe;
           h.K2 = t.Mp;
           h.M = h.N = t.Np;
@@ -1573,6 +1576,9 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
         g.C = xs + xe;
         g.ldc = t.Np;
         g.c_step = xe;
+        g.dst2 = xts + xe;   // X_{t+1}^T
+        g.ld2 = t.Mp;
+        g.d2_step = xe;
         g.ti = a;
         g.tj = b;
         g.a_dtype = g.b_dtype = ORTH_F32;
@@ -1601,6 +1607,8 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
           h.ld_src = t.Np;
           h.C = yn;
           h.ldc = t.Np;
+          h.dst2 = par ? gyt0 : gyt1;   // the new gradient's transpose
+          h.ld2 = t.Mp;
           h.ti = a;
           h.tj = b;
           h.a_dtype = h.b_dtype = ORTH_F32;

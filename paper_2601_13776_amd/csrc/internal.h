@@ -98,6 +98,7 @@ struct TiledMat {
   const void* gout;          // dL/d(output) in the caller's layout
   int64_t ld_gout;
   float* gy[2];              // fp32 gradient iterate, Mp x Np (bf16 mode: [0], in place)
+  float* gyt[2];             // fp32 products: its transposes, Np x Mp (the X^T Y operands)
   void* yc[2];               // bf16 copies of the gradient iterate (bf16 mode)
   void* s;                   // -(X^T Y + Y^T X), Np x Np (bf16: upper tiles only)
   double* dot;               // <Y_0, W_0>, one per matrix
@@ -197,7 +198,7 @@ struct GemmItem {
   float* red;
   int64_t lda, ldb, lda2, ldb2, ldc, ld_src, ld2;
   // element offsets added per unit of the launch's step argument
-  int64_t a_step, b_step, a2_step, b2_step, c_step, src_step;
+  int64_t a_step, b_step, a2_step, b2_step, c_step, src_step, d2_step;
   int32_t M, N, K, K2;
   int32_t ti, tj;
   int32_t a_dtype, b_dtype;  // storage of A and A2, of B and B2

@@ -46,7 +46,8 @@ __global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __re
   const int R = it.ti * TB, C = it.tj * TB;  // tile origin in the tall padded layout
   float* y = d.gy[0];
   uint16_t* yc = static_cast<uint16_t*>(d.yc[0]);
-  if (!d.transposed && R + TB <= d.M && C + TB <= d.N && vec8_ok(d.gout, d.ld_gout, gout_dtype) &&
+  float* yt = d.gyt[0];
+  if (!d.transposed && !yt && R + TB <= d.M && C + TB <= d.N && vec8_ok(d.gout, d.ld_gout, gout_dtype) &&
       vec8_ok(y, d.Np, ORTH_F32) && (!yc || vec8_ok(yc, d.Np, ORTH_BF16))) {
     // interior tile of an untransposed matrix: 16-byte vectors, no staging
 #pragma unroll
@@ -78,6 +79,9 @@ __global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __re
     const int64_t off = (int64_t)(R + a) * d.Np + C + b;
     y[off] = tile[a][b];
     if (yc) yc[off] = f32_to_bf16(tile[a][b]);
+    // fp32 products: the transpose too, Np x Mp (consecutive threads along
+    // a, so its rows are written coalesced)
+    if (yt) yt[(int64_t)(C + a) * d.Mp + R + b] = tile[b][a];
   }
 }
 
