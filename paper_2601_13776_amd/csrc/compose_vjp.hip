@@ -17,26 +17,59 @@
 namespace orth {
 namespace {
 
+// Layout changes between a tap grid and the per-(o, i) layout, both seen as
+// matrices with M = og c and T = n^2 (n x n grid of taps):
 // kind 0: out = taps (s x s grid) of the RKO matrix a (og x c s^2, dtype):
 //         out[(x s + y)][o][i] = a[o][i s^2 + x s + y]
 // kind 1: out = taps (k x k grid) of an OIHW kernel slice a (og x c x k x k):
 //         out[(x k + y)][o][i] = a[o][i][x][y]
 // kind 2: out (RKO matrix, dtype) from taps a (s x s grid), inverse of 0
+// Kinds 0 and 1 transpose a [M][T] matrix into [T][M], kind 2 the reverse.
+// Each tile of 64 (o, i) rows and up to 64 taps goes through LDS so that
+// both the reads and the writes are contiguous runs (a tile of all T taps
+// covers one contiguous span of the [M][T] side).
 template <int KIND>
 __global__ __launch_bounds__(256) void tap_layout_kernel(const TapItem* __restrict__ items, int dtype) {
+  constexpr int TM = 64, TTMAX = 64;
+  __shared__ float tile[TTMAX][TM + 1];
   const TapItem it = items[blockIdx.y];
-  const int og = it.og, c = it.c, n = it.h;   // square grid of n x n taps
-  const int64_t total = (int64_t)n * n * og * c;
-  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    // e enumerates (o, i, x, y) with y fastest: the OIHW / RKO side is contiguous
-    const int y = (int)(e % n);
-    const int x = (int)((e / n) % n);
-    const int64_t oi = e / ((int64_t)n * n);
-    const int64_t t = ((int64_t)(x * n + y) * og) * c + oi;
-    if (KIND == 0 || KIND == 1)
-      static_cast<float*>(it.out)[t] = load_as_f32(it.a, e, dtype);
-    else
-      store_from_f32(it.out, e, dtype, static_cast<const float*>(it.a)[t]);
+  const int n = it.h;
+  const int T = n * n;
+  const int64_t M = (int64_t)it.og * it.c;
+  if (T == 0 || M == 0) return;
+  const int TT = T < TTMAX ? T : TTMAX;
+  const int64_t mt = (M + TM - 1) / TM;
+  const int64_t ntiles = mt * ((T + TT - 1) / TT);
+  for (int64_t q = blockIdx.x; q < ntiles; q += gridDim.x) {
+    const int64_t m0 = (q % mt) * TM;
+    const int t0 = (int)(q / mt) * TT;
+    const int tn = T - t0 < TT ? T - t0 : TT;
+    const int mn = M - m0 < TM ? (int)(M - m0) : TM;
+    __syncthreads();  // the previous tile's reads of `tile` are done
+    if (KIND == 0 || KIND == 1) {
+      // read [M][T] side: row m holds tn contiguous taps
+      for (int j = threadIdx.x; j < mn * tn; j += 256) {
+        const int m = j / tn, t = j - m * tn;
+        tile[t][m] = load_as_f32(it.a, (m0 + m) * T + t0 + t, dtype);
+      }
+      __syncthreads();
+      float* out = static_cast<float*>(it.out);
+      for (int j = threadIdx.x; j < tn * TM; j += 256) {
+        const int t = j >> 6, m = j & 63;
+        if (m < mn) out[(int64_t)(t0 + t) * M + m0 + m] = tile[t][m];
+      }
+    } else {
+      const float* a = static_cast<const float*>(it.a);
+      for (int j = threadIdx.x; j < tn * TM; j += 256) {
+        const int t = j >> 6, m = j & 63;
+        if (m < mn) tile[t][m] = a[(int64_t)(t0 + t) * M + m0 + m];
+      }
+      __syncthreads();
+      for (int j = threadIdx.x; j < mn * tn; j += 256) {
+        const int m = j / tn, t = j - m * tn;
+        store_from_f32(it.out, (m0 + m) * T + t0 + t, dtype, tile[t][m]);
+      }
+    }
   }
 }
 
@@ -105,7 +138,8 @@ hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dty
                                  "conv_vjp_combine_fwd", "conv_vjp_combine_bwd"};
   if (kind < 0 || kind > 4) return hipErrorInvalidValue;
   timing_begin(names[kind], s);
-  const dim3 grid(grid_x(max_elems), n_items);
+  // the layout kernels take a 64 x 64 tile per grid-stride step
+  const dim3 grid(kind <= 2 ? grid_x((max_elems + 15) / 16) : grid_x(max_elems), n_items);
   switch (kind) {
     case 0: hipLaunchKernelGGL(tap_layout_kernel<0>, grid, dim3(256), 0, s, items, dtype); break;
     case 1: hipLaunchKernelGGL(tap_layout_kernel<1>, grid, dim3(256), 0, s, items, dtype); break;
