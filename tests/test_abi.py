@@ -207,12 +207,13 @@ def _vjp_ws(L, shapes, iters=5, compute=0, dt=0, prescale=1, beta=0.5, alias=Non
 
 def test_vjp_workspace_grows_with_saved_steps(L):
     """The VJP keeps X_t and E_t of every step: fp32 products hold
-    T (M N + N^2) fp32 values beside a few fixed buffers, bf16 products
-    T (M N + N^2) bf16 values."""
+    T (2 M N + N^2) fp32 values beside a few fixed buffers (X_t also
+    transposed, so that every product reads K-contiguous operands), bf16
+    products T (M N + N^2) bf16 values."""
     rc, w5 = _vjp_ws(L, [(256, 128)], iters=5)
     rc2, w10 = _vjp_ws(L, [(256, 128)], iters=10)
     assert rc == rc2 == orth.ORTH_OK
-    assert w10 - w5 == pytest.approx(5 * (256 * 128 + 128 * 128) * 4, rel=0.01)
+    assert w10 - w5 == pytest.approx(5 * (2 * 256 * 128 + 128 * 128) * 4, rel=0.01)
     rc, b5 = _vjp_ws(L, [(2048, 1024)], iters=5, compute=1, dt=1)
     rc2, b10 = _vjp_ws(L, [(2048, 1024)], iters=10, compute=1, dt=1)
     assert rc == rc2 == orth.ORTH_OK
