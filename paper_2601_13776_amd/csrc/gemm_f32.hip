@@ -26,6 +26,12 @@ namespace {
 
 __device__ inline int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// KM: every tile of the launch is of a single-pair product whose operands
+// are both stored k-major ([K][M] and [K][N]); each thread then loads eight
+// consecutive rows of one k (16-byte vectors along the stored rows) and
+// writes them to the [row][k] LDS tile one element at a time.  A separate
+// instantiation, so that the general loads keep their registers.
+template <bool KM>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restrict__ items,
                                                        const GemmTile* __restrict__ tiles, int step,
                                                        const GemmPair* __restrict__ extra) {
@@ -61,11 +67,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     const void* B = xp ? xp->B
                        : static_cast<const char*>(pair ? g->B2 : g->B) + (pair ? g->b2_step : g->b_step) * st * esz_b;
 
-    // thread -> (row, first k of 8) for each operand
-    const int ar = atr ? (tid & 63) : (tid >> 2);
-    const int ak = atr ? (tid >> 6) * 8 : (tid & 3) * 8;
-    const int br = btr ? (tid & 63) : (tid >> 2);
-    const int bk = btr ? (tid >> 6) * 8 : (tid & 3) * 8;
+    // thread -> (row, first k of 8) for each operand; KM: (first row of 8, k)
+    const int ar = KM ? (tid & 7) * 8 : atr ? (tid & 63) : (tid >> 2);
+    const int ak = KM ? (tid >> 3) : atr ? (tid >> 6) * 8 : (tid & 3) * 8;
+    const int br = KM ? (tid & 7) * 8 : btr ? (tid & 63) : (tid >> 2);
+    const int bk = KM ? (tid >> 3) : btr ? (tid >> 6) * 8 : (tid & 3) * 8;
 
     // Raw operand words: fp32 bits, bf16 bits in the low half (widened at
     // the LDS store), or (packed) eight bf16 values in words 0-3 from one
@@ -108,9 +114,50 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         dst[q] = v;
       }
     };
+    // KM: rows r .. r + 7 of stored row k (eight consecutive elements)
+    auto load_km = [&](const void* P, int64_t ld, int dt, int r, int kq, int rows_lim, int rbase, int k0,
+                       uint32_t* dst, bool& packed) {
+      const int gr = rbase + r;
+      const int gk = k0 + kq;
+      packed = false;
+      if (gk < K && gr + 8 <= rows_lim) {
+        if (dt == ORTH_F32) {
+          const float* p = static_cast<const float*>(P) + (int64_t)gk * ld + gr;
+          if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+            const uint4 x = reinterpret_cast<const uint4*>(p)[0];
+            const uint4 y = reinterpret_cast<const uint4*>(p)[1];
+            dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
+            dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
+            return;
+          }
+        } else {
+          const uint16_t* p = static_cast<const uint16_t*>(P) + (int64_t)gk * ld + gr;
+          if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+            const uint4 x = *reinterpret_cast<const uint4*>(p);
+            dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
+            packed = true;
+            return;
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        uint32_t v = 0;
+        if (gk < K && gr + q < rows_lim) {
+          const int64_t idx = (int64_t)gk * ld + gr + q;
+          v = dt == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(P)[idx] : static_cast<const uint32_t*>(P)[idx];
+        }
+        dst[q] = v;
+      }
+    };
     auto gload = [&](int k0) {
-      load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra, apk);
-      load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb, bpk);
+      if constexpr (KM) {
+        load_km(A, lda, adt, ar, ak, M, row0, k0, ra, apk);
+        load_km(B, ldb, bdt, br, bk, N, col0, k0, rb, bpk);
+      } else {
+        load_op(A, lda, adt, atr, ar, ak, M, row0, k0, ra, apk);
+        load_op(B, ldb, bdt, btr, br, bk, N, col0, k0, rb, bpk);
+      }
     };
     auto widen = [&](const uint32_t* w, bool packed, int dt, float* f) {
       if (packed) {
@@ -134,6 +181,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       float fa[8], fb[8];
       widen(ra, apk, adt, fa);
       widen(rb, bpk, bdt, fb);
+      if constexpr (KM) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          As[buf][(ar + q) * PITCH + ak] = fa[q];
+          Bs[buf][(br + q) * PITCH + bk] = fb[q];
+        }
+        return;
+      }
       float4* pa = reinterpret_cast<float4*>(&As[buf][ar * PITCH + ak]);
       pa[0] = make_float4(fa[0], fa[1], fa[2], fa[3]);
       pa[1] = make_float4(fa[4], fa[5], fa[6], fa[7]);
@@ -250,11 +305,20 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
 }  // namespace
 
 hipError_t launch_gemm_f32(const GemmItem* items, const GemmTile* tiles, int n_tiles, const char* name,
-                           hipStream_t s, int step, const GemmPair* pairs) {
+                           hipStream_t s, int step, const GemmPair* pairs, int n_km) {
   if (n_tiles <= 0) return hipSuccess;
+  if (n_km < 0 || n_km > n_tiles) return hipErrorInvalidValue;
   timing_begin(name, s);
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(n_tiles), dim3(256), 0, s, items, tiles, step, pairs);
-  hipError_t e = hipGetLastError();
+  hipError_t e = hipSuccess;
+  if (n_tiles > n_km) {
+    hipLaunchKernelGGL(gemm_f32_kernel<false>, dim3(n_tiles - n_km), dim3(256), 0, s, items, tiles, step, pairs);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess && n_km > 0) {
+    hipLaunchKernelGGL(gemm_f32_kernel<true>, dim3(n_km), dim3(256), 0, s, items, tiles + (n_tiles - n_km), step,
+                       pairs);
+    e = hipGetLastError();
+  }
   timing_end(name, s);
   return e;
 }

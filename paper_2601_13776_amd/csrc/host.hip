@@ -194,12 +194,22 @@ struct GemmList {
   std::vector<int32_t> pending;   // add_all products without tiles yet
   int64_t pending64 = 0;          // their tile count
   GemmItem last{};   // items.back() with its tile and mirror fields cleared
+  int64_t n_km = 0;  // trailing tiles for the k-major instantiation (set by put)
   size_t size() const { return tiles.size() + (size_t)pending64; }
   void clear() {
     items.clear();
     tiles.clear();
     pending.clear();
     pending64 = 0;
+    n_km = 0;
+  }
+  // single-pair products with both operands stored k-major
+  static bool kmajor(const GemmItem& it) { return it.a_trans && it.b_trans && it.K2 <= 0 && it.pair_count == 0; }
+  // moves the k-major tiles to the end (stable: each part keeps its order)
+  void partition_km() {
+    auto it = std::stable_partition(tiles.begin(), tiles.end(),
+                                    [&](const GemmTile& t) { return !kmajor(items[t.item]); });
+    n_km = tiles.end() - it;
   }
   void finalize() {
     for (int32_t idx : pending)
@@ -240,6 +250,7 @@ struct GemmList {
 
 void put(TableImage& img, size_t off, GemmList& g) {
   g.finalize();
+  g.partition_km();
   img.add(off, g.items.data(), g.items.size() * sizeof(GemmItem));
   img.add(off + g.items_bytes(), g.tiles.data(), g.tiles.size() * sizeof(GemmTile));
 }
@@ -261,7 +272,7 @@ hipError_t launch_list(const unsigned char* ws, size_t off, const GemmList& g, c
                        int step = 0, const GemmPair* pairs = nullptr) {
   return launch_gemm_f32(reinterpret_cast<const GemmItem*>(ws + off),
                          reinterpret_cast<const GemmTile*>(ws + off + g.items_bytes()), (int)g.size(), name, s,
-                         step, pairs);
+                         step, pairs, (int)g.n_km);
 }
 
 }  // namespace

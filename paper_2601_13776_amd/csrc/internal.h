@@ -289,8 +289,10 @@ hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_it
                            int master_index, int out_dtype, hipStream_t s);
 hipError_t launch_bf16_tiles(int big, const TiledMat* mats, const TileItem* items, int n_items, float beta,
                              hipStream_t s, int vjp = 0, int step = 0);
+// The last n_km tiles must be of single-pair products with both operands
+// stored k-major; they run on the k-major instantiation.
 hipError_t launch_gemm_f32(const GemmItem* items, const GemmTile* tiles, int n_tiles, const char* name,
-                           hipStream_t s, int step = 0, const GemmPair* pairs = nullptr);
+                           hipStream_t s, int step = 0, const GemmPair* pairs = nullptr, int n_km = 0);
 hipError_t launch_vjp_load_grad(const TiledMat* mats, const TileItem* items, int n_items, int gout_dtype,
                                 hipStream_t s);
 hipError_t launch_vjp_dot_partial(const TiledMat* mats, const TileItem* items, int n_items, int in_dtype,
