@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import aoc, bjorck, checks
+from oracle import aoc, aoc_grad, bjorck, checks
 from paper_2601_13776_amd import orth
 from paper_2601_13776_amd import workloads as wl
 
@@ -88,6 +88,74 @@ def test_imagenet_stack_full_size():
         L, r, p, k = layers[li]
         ref = aoc.aoc_kernel(to_f64(r), to_f64(p), L.cin, L.cout, L.k, L.stride, L.dilation, L.groups)
         assert checks.relative_difference(to_f64(k), ref) <= REL_F32, li
+
+
+def test_imagenet_conv_vjp_full_size():
+    """The composition VJP of all 16 conv layers of the ImageNet-like stack
+    in one call (bench.py --vjp's configuration, fp32).  Widths 128 and 256
+    against the oracle; at 512 and 1024 channels, where the float64 oracle
+    takes minutes, exact adjoint identities with the library's forward
+    composition (checked against the oracle elsewhere): K is linear in the
+    RKO factor R and affine in each projector P_j = V_j V_j^T, whose central
+    difference P(V + D) - P(V - D) = 2 (D V^T + V D^T) is exact, so
+    <dL/dR, D> = <dK, K(D, V)> and <dL/dV_j, D> = <dK, K(V_j + D) - K(V_j - D)> / 2
+    hold for any D."""
+    w = wl.WORKLOADS["imagenet_backbone25"]
+    rng = np.random.default_rng(1100)
+    convs = [L for L in w.layers if isinstance(L, wl.ConvLayer)]
+    items = []
+    for L in convs:
+        geom = (L.cin, L.cout, L.k, L.stride, L.dilation, L.groups)
+        rr, rc, npj, pr, pc = aoc.param_shapes(*geom)
+        rko = (rng.standard_normal((L.groups, rr, rc)) / np.sqrt(rc)).astype(np.float32)
+        proj = (rng.standard_normal((L.groups, npj, pr, pc)) / np.sqrt(pr)).astype(np.float32)
+        dk = rng.standard_normal((L.cout, L.cin // L.groups, L.k, L.k)).astype(np.float32)
+        items.append((geom, rko, proj, dk))
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    layers = [dict(geom=g, rko=dev(r), proj=dev(p), grad_kernel=dev(d),
+                   grad_rko=torch.full(r.shape, float("nan"), device=DEV),
+                   grad_proj=torch.full(p.shape, float("nan"), device=DEV)) for g, r, p, d in items]
+    print("[imagenet conv vjp] all 16 layers", flush=True)
+    orth.orth_build_conv_kernels_vjp_batched(layers)
+    torch.cuda.synchronize()
+    for li in (0, 4):                  # widths 128 and 256
+        print(f"[imagenet conv vjp] oracle layer {li}", flush=True)
+        geom, rko, proj, dk = items[li]
+        ref_r, ref_p = aoc_grad.aoc_kernel_vjp(rko.astype(np.float64), proj.astype(np.float64), *geom,
+                                               dk.astype(np.float64))
+        assert checks.relative_difference(to_f64(layers[li]["grad_rko"]), ref_r) <= REL_F32, li
+        assert checks.relative_difference(to_f64(layers[li]["grad_proj"]), ref_p) <= REL_F32, li
+    # adjoint identities at widths 512 and 1024: every perturbed forward in one call
+    fwd, cases = [], []
+    for li in (8, 12):
+        geom, rko, proj, dk = items[li]
+        d_r = (rng.standard_normal(rko.shape) / np.sqrt(rko.shape[-1])).astype(np.float32)
+        fwd.append((geom, d_r, proj))
+        cases.append((li, "rko", None, d_r, len(fwd) - 1, None))
+        for j in range(proj.shape[1]):
+            d_v = (rng.standard_normal(proj.shape[2:]) / np.sqrt(proj.shape[2])).astype(np.float32)
+            plus, minus = proj.copy(), proj.copy()
+            plus[0, j] += d_v
+            minus[0, j] -= d_v
+            fwd.append((geom, rko, plus))
+            fwd.append((geom, rko, minus))
+            cases.append((li, "proj", j, d_v, len(fwd) - 2, len(fwd) - 1))
+    kl = [dict(geom=g, rko=dev(r), proj=dev(p),
+               kernel=torch.empty(g[1], g[0] // g[5], g[2], g[2], device=DEV)) for g, r, p in fwd]
+    print(f"[imagenet conv vjp] {len(kl)} perturbed compositions", flush=True)
+    orth.orth_build_conv_kernels_batched(kl)
+    torch.cuda.synchronize()
+    for li, kind, j, d, a, b in cases:
+        dk = items[li][3].astype(np.float64)
+        if kind == "rko":
+            got = float(np.sum(to_f64(layers[li]["grad_rko"]) * d))
+            dK = to_f64(kl[a]["kernel"])
+        else:
+            got = float(np.sum(to_f64(layers[li]["grad_proj"])[0, j] * d))
+            dK = (to_f64(kl[a]["kernel"]) - to_f64(kl[b]["kernel"])) / 2
+        ref = float(np.sum(dk * dK))
+        scale = np.linalg.norm(dk) * np.linalg.norm(dK)
+        assert abs(got - ref) <= 1e-5 * scale, (li, kind, j, got, ref, scale)
 
 
 def test_stress_vjp_full_size():
