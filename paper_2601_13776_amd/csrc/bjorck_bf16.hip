@@ -208,7 +208,9 @@ struct Tile {
 // loads of k-step t + 2 go into the B buffer just read.  A loads get seven
 // sub-steps to land, B loads four (two stages: three and two; measured 4%
 // faster).  Past the end, loads re-read a valid k-step instead of
-// branching.
+// branching: the barrier's partial wait relies on this k-step's A loads
+// being the newest in flight (skipped, they would let the next k-step's B
+// loads pass the barrier unfinished).
 template <int BM, int BN, int WM, int WN, bool AT, bool BT>
 __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32], const uint16_t* A, int64_t lda,
                                       const uint16_t* B, int64_t ldb, int kb, int ke, uint16_t* sA0, uint16_t* sB0,
