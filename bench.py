@@ -218,13 +218,42 @@ def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, d
                 "frac": round(ach / peak, 4), "traffic": measured_traffic(dom, w.name),
                 "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(cf_ / launches)}
+    # The training pattern: a forward that keeps its iterates in the VJP
+    # workspace (orth_orthogonalize_save_batched) and a VJP that reuses them
+    # instead of recomputing the forward steps.
+    def save_step():
+        orth.orth_orthogonalize_save_batched(ins, outs, w.iters, compute=compute, status=status, workspace=bws)
+
+    def saved_step():
+        if vlayers:
+            orth.orth_build_conv_kernels_vjp_batched(vlayers, workspace=cws)
+        orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, compute=compute, status=status,
+                                            workspace=bws, saved=True)
+
+    save_step()
+    saved_step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        save_step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        saved_step()
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    log(f"[bench] saving forward and saved vjp timed {steps} steps each")
+    save_ms = (t1 - t0) * 1e3 / steps
+    saved_ms = (t2 - t1) * 1e3 / steps
     return {"ms_per_step": round(ms, 3), "layers_per_s": round(w.n_layers / (ms / 1e3), 3),
             "algorithmic_flops_per_step": flops,
             "tflops_algorithmic": round(flops / (ms / 1e3) / 1e12, 1),
             "gemm_tflops_algorithmic": round(flops / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms > 0 else None,
             "gemm_pct_peak": round(100 * flops / (gemm_ms / 1e3) / 1e12 / peak, 2) if gemm_ms > 0 else None,
             "kernel_ms_per_step": {n: round(kt[n][0] / steps, 4) for n in names},
-            "roofline": roof}
+            "roofline": roof,
+            "saved": {"save_forward_ms": round(save_ms, 3), "vjp_ms_per_step": round(saved_ms, 3),
+                      "train_step_ms": round(save_ms + saved_ms, 3)}}
 
 
 def vjp_class_flops_f32(w):

@@ -92,6 +92,11 @@ typedef struct {
    * forces that size.  The result does not depend on it beyond fp32
    * rounding order. */
   int32_t tile;
+  /* orth_orthogonalize_vjp_batched only (must be 0 elsewhere, ignored by
+   * orth_orthogonalize_batched): 1 = the workspace holds what a preceding
+   * orth_orthogonalize_save_batched call left there for the same inputs,
+   * shapes and options, and the forward recomputation is skipped. */
+  int32_t saved;
 } orth_bjorck_opts;
 
 /*
@@ -149,9 +154,11 @@ typedef struct {
  * (wide matrices through their transpose), chained from the last step to
  * the first, then through the pre-scaling W_0 = W / ||W||_F:
  *   dL/dW = (dL/dW_0 - <dL/dW_0, W_0> W_0) / ||W||_F.
- * The forward iterates are recomputed inside the call and every X_t and E_t
- * is kept in the workspace (about T (M N + N^2) elements per M x N matrix,
- * in fp32 or bf16 per opts.compute), so the workspace query grows with T.
+ * The forward iterates are recomputed inside the call (or, with
+ * opts.saved = 1, taken from a saving forward, see below) and every X_t and
+ * E_t is kept in the workspace (about T (M N + N^2) elements per M x N
+ * matrix, in fp32 or bf16 per opts.compute), so the workspace query grows
+ * with T.
  * Matrices with N <= 64 and M <= 128 (tall orientation) use fp32 products
  * whatever opts.compute says, as the forward does.
  *
@@ -167,6 +174,29 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n,
                                    const orth_bjorck_opts* opts, void* workspace,
                                    size_t workspace_bytes, int32_t* status_dev,
                                    void* stream);
+
+/*
+ * The forward of orth_orthogonalize_batched (Appendix A.5 steps, same
+ * options and results up to fp32 rounding order) that keeps, in a
+ * vector-Jacobian workspace, every X_t and E_t that the product above needs
+ * (the training pattern: a forward that saves, a backward that reuses).  A
+ * later orth_orthogonalize_vjp_batched call with opts.saved = 1, this
+ * workspace, the same inputs (unchanged) and the same shapes and options
+ * then skips its forward recomputation (about a third of its work); several
+ * such calls may reuse one saving forward.  The workspace size is that of
+ * orth_orthogonalize_vjp_workspace_size for matrices of the same shapes
+ * (orth_orthogonalize_save_workspace_size gives it from these descriptors)
+ * and holds the saved state until the caller reuses it.
+ * Errors: those of orth_orthogonalize_vjp_batched for these options
+ * (ORTH_EUNSUPPORTED for spectral pre-scaling), ORTH_EINVAL for in == out
+ * (the product reads the input again) or opts.saved != 0.
+ */
+int orth_orthogonalize_save_workspace_size(const orth_mat* mats, int32_t n,
+                                           const orth_bjorck_opts* opts, size_t* bytes);
+int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n,
+                                    const orth_bjorck_opts* opts, void* workspace,
+                                    size_t workspace_bytes, int32_t* status_dev,
+                                    void* stream);
 
 /* Options of the exponential map. */
 typedef struct {

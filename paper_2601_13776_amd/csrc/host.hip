@@ -1316,6 +1316,7 @@ int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o)
     return fail(ORTH_EINVAL, "unknown dtype");
   if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
   if (o->tile != 0 && o->tile != 128 && o->tile != 256) return fail(ORTH_EINVAL, "tile must be 0, 128 or 256");
+  if (o->saved != 0 && o->saved != 1) return fail(ORTH_EINVAL, "saved must be 0 or 1");
   for (int i = 0; i < n; ++i) {
     const orth_vjp_mat& m = mats[i];
     char buf[160];
@@ -1347,7 +1348,7 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
                     unsigned char* ws) {
   const bool bf16 = o->compute == ORTH_COMPUTE_BF16;
   const int T = o->iters;
-  const int slots = std::max(T, 1);
+  const int slots = T + 1;   // X_0 .. X_T (a saving forward writes X_T too)
   P.bucket.resize(n);
   P.mats.resize(n);
   int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
@@ -1750,6 +1751,136 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   return ORTH_OK;
 }
 
+namespace {
+// Pre-scaling and the forward steps of a vector-Jacobian product plan, with
+// X_t and E_t of every step left in the workspace.  `to_output` also runs
+// the last update and writes X_T to the plan's output (a saving forward).
+int vjp_forward(const VjpPlan& P, unsigned char* ws, const orth_bjorck_opts* opts, int n, int32_t* status,
+                bool to_output, hipStream_t s) {
+  auto TI = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
+  const TiledMat* tm = reinterpret_cast<const TiledMat*>(ws + P.off_mats);
+  const int T = opts->iters;
+  const float beta = opts->beta;
+  double* partials = reinterpret_cast<double*>(ws + P.off_partials);
+  ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
+                                   partials, s));
+  ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s));
+  ORTH_HIP(launch_prescale_scale(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
+                                 opts->compute, s));
+  for (int t = 0; t < T; ++t) {
+    ORTH_HIP(launch_list(ws, P.off_f_gram, P.f_gram, "vjp_fwd_gram_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_gram[cls]), (int)P.t_gram[cls].size(), beta, s, 0, t));
+    if (t + 1 == T && !to_output) break;
+    ORTH_HIP(launch_list(ws, P.off_f_upd, P.f_upd, "vjp_fwd_update_f32", s, t));
+    for (int cls = 1; cls >= 0; --cls)
+      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_upd[cls]), (int)P.t_upd[cls].size(), beta, s, 0, t));
+  }
+  if (to_output)   // master[1] of every tiled matrix points at X_T (fp32)
+    ORTH_HIP(launch_writeout(tm, TI(P.off_partial_items), (int)P.partial_items.size(), 1, opts->out_dtype, s));
+  return ORTH_OK;
+}
+
+// The vector-Jacobian descriptors whose plan a saving forward shares: w is
+// the forward's input, grad_in its output (the plan's output slot) and
+// grad_out a placeholder never read by the forward part.
+int save_descs(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, std::vector<orth_vjp_mat>& vm) {
+  int rc = validate_ortho(mats, n, opts);
+  if (rc) return rc;
+  if (opts->saved) return fail(ORTH_EINVAL, "saved must be 0 for the saving forward");
+  vm.resize(n);
+  for (int i = 0; i < n; ++i) {
+    const orth_mat& m = mats[i];
+    if (m.in == m.out) {
+      char buf[160];
+      snprintf(buf, sizeof buf, "matrix %d: a saving forward cannot run in place (the VJP reads the input)", i);
+      return fail(ORTH_EINVAL, buf);
+    }
+    vm[i] = orth_vjp_mat{m.in, m.in, m.out, m.rows, m.cols, m.ld_in, m.ld_in, m.ld_out};
+  }
+  return validate_vjp(vm.data(), n, opts);
+}
+}  // namespace
+
+int orth_orthogonalize_save_workspace_size(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
+                                           size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  std::vector<orth_vjp_mat> vm;
+  int rc = save_descs(mats, n, opts, vm);
+  if (rc) return rc;
+  VjpPlan P;
+  build_vjp_plan(vm.data(), n, opts, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
+                                    size_t workspace_bytes, int32_t* status_dev, void* stream) {
+  std::vector<orth_vjp_mat> vm;
+  int rc = save_descs(mats, n, opts, vm);
+  if (rc) return rc;
+  if (n == 0) return ORTH_OK;
+  VjpPlan P;
+  build_vjp_plan(vm.data(), n, opts, P, nullptr);
+  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  if (rc) return rc;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  P = VjpPlan();
+  build_vjp_plan(vm.data(), n, opts, P, ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // statuses go to the workspace, where the saved product reads them, and
+  // are copied to the caller's array
+  int32_t* status = reinterpret_cast<int32_t*>(ws + P.off_status);
+  // X_T of a tiled matrix: the fp32 iterate (bf16 products, updated in
+  // place) or saved slot T (fp32 products)
+  for (int i = 0; i < n; ++i) {
+    TiledMat& t = P.mats[i];
+    if (t.fused) continue;
+    t.master[1] = P.bucket[i] == V_F32 ? t.master[0] + (int64_t)opts->iters * t.Mp * t.Np : t.master[0];
+  }
+  // small matrices: the forward kernel, its table in the place of the
+  // vector-Jacobian one
+  static_assert(sizeof(SmallMat) <= sizeof(SmallVjpMat), "small tables share their workspace region");
+  std::vector<SmallMat> small[2];
+  for (int k = 0; k < 2; ++k)
+    for (const SmallVjpMat& q : P.small[k]) {
+      SmallMat sm{};
+      sm.in = q.w;
+      sm.out = q.gin;
+      sm.ld_in = q.ld_w;
+      sm.ld_out = q.ld_gin;
+      sm.rows = q.rows;
+      sm.cols = q.cols;
+      sm.M = q.M;
+      sm.N = q.N;
+      sm.Mp = q.Mp;
+      sm.transposed = q.transposed;
+      sm.status_index = q.status_index;
+      small[k].push_back(sm);
+    }
+  TableImage img;
+  put(img, P.off_mats, P.mats);
+  for (int k = 0; k < 2; ++k) put(img, P.off_small[k], small[k]);
+  put(img, P.off_partial_items, P.partial_items);
+  put(img, P.off_scale_items, P.scale_items);
+  put(img, P.off_f_gram, P.f_gram);
+  put(img, P.off_f_upd, P.f_upd);
+  for (int cls = 0; cls < 2; ++cls) {
+    put(img, P.off_t_gram[cls], P.t_gram[cls]);
+    put(img, P.off_t_upd[cls], P.t_upd[cls]);
+  }
+  rc = upload_tables(img, ws, s);
+  if (rc) return rc;
+  for (int k = 0; k < 2; ++k)
+    ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[k]), (int)small[k].size(),
+                                 k ? 64 : 32, P.small_max_mp[k], opts->iters, opts->beta, opts->prescale, 0,
+                                 opts->in_dtype, opts->out_dtype, status, s));
+  rc = vjp_forward(P, ws, opts, n, status, true, s);
+  if (rc) return rc;
+  if (status_dev) ORTH_HIP(hipMemcpyAsync(status_dev, status, sizeof(int32_t) * n, hipMemcpyDeviceToDevice, s));
+  return ORTH_OK;
+}
+
 int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* opts,
                                           size_t* bytes) {
   if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
@@ -1774,7 +1905,10 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   P = VjpPlan();
   build_vjp_plan(mats, n, opts, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
+  // with saved iterates the statuses of the saving forward are in the
+  // workspace; the small-matrix kernel refreshes its own
+  int32_t* status =
+      status_dev && !opts->saved ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
   TableImage img;
   put(img, P.off_mats, P.mats);
@@ -1808,20 +1942,11 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
     ORTH_HIP(launch_bjorck_small_vjp(reinterpret_cast<const SmallVjpMat*>(ws + P.off_small[k]),
                                      (int)P.small[k].size(), k ? 64 : 32, P.small_max_mp[k], T, beta,
                                      opts->prescale, opts->in_dtype, opts->out_dtype, status, s));
-  ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
-                                   partials, s));
-  ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s));
-  ORTH_HIP(launch_prescale_scale(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
-                                 opts->compute, s));
-  // forward recomputation, saving X_t and E_t (X_T itself is never needed)
-  for (int t = 0; t < T; ++t) {
-    ORTH_HIP(launch_list(ws, P.off_f_gram, P.f_gram, "vjp_fwd_gram_f32", s, t));
-    for (int cls = 1; cls >= 0; --cls)
-      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_gram[cls]), (int)P.t_gram[cls].size(), beta, s, 0, t));
-    if (t + 1 == T) break;
-    ORTH_HIP(launch_list(ws, P.off_f_upd, P.f_upd, "vjp_fwd_update_f32", s, t));
-    for (int cls = 1; cls >= 0; --cls)
-      ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_upd[cls]), (int)P.t_upd[cls].size(), beta, s, 0, t));
+  // forward recomputation, saving X_t and E_t (X_T itself is never
+  // needed), unless a saving forward left them in the workspace
+  if (!opts->saved) {
+    rc = vjp_forward(P, ws, opts, n, status, false, s);
+    if (rc) return rc;
   }
   // gradient recurrence, last step first
   ORTH_HIP(launch_vjp_load_grad(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->out_dtype, s));
@@ -1842,6 +1967,8 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   }
   ORTH_HIP(launch_vjp_writeout(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                opts->prescale, status, s));
+  if (opts->saved && status_dev)
+    ORTH_HIP(hipMemcpyAsync(status_dev, status, sizeof(int32_t) * n, hipMemcpyDeviceToDevice, s));
   return ORTH_OK;
 }
 

@@ -22,7 +22,8 @@ ORTH_CHECK_GRAM, ORTH_CHECK_CONV, ORTH_CHECK_CONV_ADJOINT = 0, 1, 2
 
 EXPORTED = [
     "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched",
-    "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched", "orth_aoc_param_shapes",
+    "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched",
+    "orth_orthogonalize_save_workspace_size", "orth_orthogonalize_save_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
     "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched", "orth_conv_apply",
     "orth_exp_map_workspace_size", "orth_exp_map_batched", "orth_conv_exp_workspace_size", "orth_conv_exp_batched",
@@ -46,7 +47,8 @@ class orth_mat(ctypes.Structure):
 class orth_bjorck_opts(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("beta", ctypes.c_float), ("prescale", ctypes.c_int32),
                 ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("compute", ctypes.c_int32),
-                ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p), ("tile", ctypes.c_int32)]
+                ("power_iters", ctypes.c_int32), ("u", ctypes.c_void_p), ("tile", ctypes.c_int32),
+                ("saved", ctypes.c_int32)]
 
 
 class orth_vjp_mat(ctypes.Structure):
@@ -106,6 +108,8 @@ def lib():
         L.orth_orthogonalize_batched.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
         L.orth_orthogonalize_vjp_workspace_size.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), P(sz)]
         L.orth_orthogonalize_vjp_batched.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
+        L.orth_orthogonalize_save_workspace_size.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), P(sz)]
+        L.orth_orthogonalize_save_batched.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
         L.orth_aoc_param_shapes.argtypes = [P(orth_conv_geom)] + [P(i32)] * 5
         L.orth_build_conv_kernels_workspace_size.argtypes = [P(orth_conv_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_batched.argtypes = [P(orth_conv_desc), i32, i32, vp, sz, vp]
@@ -175,7 +179,7 @@ def _mats(ins, outs):
     return arr
 
 
-def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile=0):
+def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile=0, saved=0):
     in_dt = _dtype_code(ins[0]) if ins else ORTH_F32
     out_dt = _dtype_code(outs[0]) if outs else ORTH_F32
     for a, b in zip(ins, outs):
@@ -191,7 +195,7 @@ def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile
             raise ValueError(f"spectral pre-scaling needs u: a contiguous float32 tensor of {need} values "
                              "(min(rows, cols) per matrix, packed in batch order)")
         uptr = u.data_ptr()
-    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp, power_iters, uptr, tile)
+    return orth_bjorck_opts(iters, beta, pres, in_dt, out_dt, comp, power_iters, uptr, tile, saved)
 
 
 def orth_orthogonalize_workspace_size(ins, iters, beta=0.5, prescale="frobenius", compute="f32", outs=None,
@@ -240,18 +244,22 @@ def _vjp_mats(ws, gouts, gins):
 
 
 def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, prescale="frobenius", compute="f32",
-                                   status=None, workspace=None, stream=None, tile=0):
+                                   status=None, workspace=None, stream=None, tile=0, saved=False):
     """dL/dW into grads_in[i] for L depending on ws[i] through
     orth_orthogonalize_batched with the same options, given grads_out[i] =
     dL/d(output) (see include/orth.h).  grads_in share the dtype of ws,
-    grads_out that of the forward outputs.  Returns the workspace tensor."""
+    grads_out that of the forward outputs.  saved=True takes the forward
+    iterates from `workspace`, which orth_orthogonalize_save_batched filled
+    for the same ws and options.  Returns the workspace tensor."""
+    if saved and workspace is None:
+        raise ValueError("saved=True needs the workspace of orth_orthogonalize_save_batched")
     if len(ws) != len(grads_out) or len(ws) != len(grads_in):
         raise ValueError("ws, grads_out and grads_in must have the same length")
     for w, gi in zip(ws, grads_in):
         if w.dtype != gi.dtype:
             raise TypeError("grads_in must have the dtype of ws")
     mats = _vjp_mats(ws, grads_out, grads_in)
-    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile, saved=1 if saved else 0)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_vjp_workspace_size")
@@ -264,6 +272,27 @@ def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, pre
                                               status.data_ptr() if status is not None else None, _stream(stream))
     _check(rc, "orth_orthogonalize_vjp_batched")
     return wsp
+
+
+def orth_orthogonalize_save_batched(ins, outs, iters, beta=0.5, prescale="frobenius", compute="f32", status=None,
+                                    workspace=None, stream=None, tile=0):
+    """orth_orthogonalize_batched that also keeps, in the returned workspace,
+    the forward iterates that orth_orthogonalize_vjp_batched(..., saved=True,
+    workspace=<it>) reuses (see include/orth.h).  outs must not be ins."""
+    mats = _mats(ins, outs)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, tile=tile)
+    n = ctypes.c_size_t()
+    _check(lib().orth_orthogonalize_save_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
+           "orth_orthogonalize_save_workspace_size")
+    device = ins[0].device if ins else torch.device("cuda")
+    ws, nbytes = _workspace(n.value, device, workspace)
+    if status is not None and (status.dtype != torch.int32 or status.numel() < len(ins)):
+        raise ValueError("status must be an int32 tensor with one slot per matrix")
+    rc = lib().orth_orthogonalize_save_batched(mats, len(ins), ctypes.byref(opts),
+                                               ws.data_ptr() if ws is not None else None, nbytes,
+                                               status.data_ptr() if status is not None else None, _stream(stream))
+    _check(rc, "orth_orthogonalize_save_batched")
+    return ws
 
 
 def orth_orthogonalize_vjp_workspace_size(ws, iters, beta=0.5, prescale="frobenius", compute="f32",

@@ -205,6 +205,46 @@ def _vjp_ws(L, shapes, iters=5, compute=0, dt=0, prescale=1, beta=0.5, alias=Non
     return rc, n.value
 
 
+def test_save_workspace_matches_vjp(L):
+    """A saving forward fills a vector-Jacobian workspace: its size query
+    equals the VJP's for the same shapes and options, in every bucket
+    (fused small, fp32 tiles, bf16 tiles of both classes)."""
+    shapes = [(16, 8), (100, 70), (300, 200), (2048, 1024), (8, 16)]
+    for compute, dt in ((0, 0), (1, 1), (1, 0)):
+        for iters in (0, 1, 6):
+            opts = orth.orth_bjorck_opts(iters, 0.5, 1, dt, dt, compute, 1, None, 0)
+            n = ctypes.c_size_t()
+            assert L.orth_orthogonalize_save_workspace_size(_mats(shapes), len(shapes), ctypes.byref(opts),
+                                                            ctypes.byref(n)) == orth.ORTH_OK
+            rc, v = _vjp_ws(L, shapes, iters=iters, compute=compute, dt=dt)
+            assert rc == orth.ORTH_OK and n.value == v, (compute, dt, iters)
+
+
+def test_save_and_saved_flag_errors(L):
+    n = ctypes.c_size_t()
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0, 1, None, 0, 1)     # saved = 1: not for the forward
+    assert L.orth_orthogonalize_save_workspace_size(_mats([(64, 32)]), 1, ctypes.byref(opts),
+                                                    ctypes.byref(n)) == orth.ORTH_EINVAL
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0, 1, None, 0, 2)     # saved must be 0 or 1
+    rc, _ = _vjp_ws(L, [(64, 32)])
+    assert rc == orth.ORTH_OK
+    assert L.orth_orthogonalize_vjp_workspace_size(_vjp_mats([(64, 32)]), 1, ctypes.byref(opts),
+                                                   ctypes.byref(n)) == orth.ORTH_EINVAL
+    inplace = (orth.orth_mat * 1)()
+    inplace[0] = orth.orth_mat(0x10000, 0x10000, 64, 32, 32, 32)
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0, 1, None, 0)
+    assert L.orth_orthogonalize_save_workspace_size(inplace, 1, ctypes.byref(opts), ctypes.byref(n)) \
+        == orth.ORTH_EINVAL
+    assert L.orth_orthogonalize_save_batched(inplace, 1, ctypes.byref(opts), None, 0, None, None) == orth.ORTH_EINVAL
+    spectral = orth.orth_bjorck_opts(3, 0.5, 2, 0, 0, 0, 1, 0x1000, 0)
+    assert L.orth_orthogonalize_save_workspace_size(_mats([(64, 32)]), 1, ctypes.byref(spectral),
+                                                    ctypes.byref(n)) == orth.ORTH_EUNSUPPORTED
+    # too small a workspace: rejected before anything is enqueued
+    rc, need = _vjp_ws(L, [(64, 32)], iters=3)
+    assert L.orth_orthogonalize_save_batched(_mats([(64, 32)]), 1, ctypes.byref(opts), 0x100000, need - 1, None,
+                                             None) == orth.ORTH_EWORKSPACE
+
+
 def test_vjp_workspace_grows_with_saved_steps(L):
     """The VJP keeps X_t and E_t of every step: fp32 products hold
     T (2 M N + N^2) fp32 values beside a few fixed buffers (X_t also

@@ -237,6 +237,45 @@ def test_conv_vjp_bf16_storage():
         assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= 1e-2
 
 
+@pytest.mark.parametrize("compute,iters,tile", [("f32", 0, 0), ("f32", 7, 0), ("bf16", 6, 128), ("bf16", 6, 256)])
+def test_saving_forward_and_saved_vjp(compute, iters, tile):
+    """orth_orthogonalize_save_batched gives the forward's outputs and
+    statuses; the VJP that takes its workspace (saved=True) gives the
+    gradients of the recomputing VJP bit for bit, twice in a row (the saved
+    iterates are left intact), including a zero matrix."""
+    print(f"[saved vjp] compute={compute} iters={iters} tile={tile}", flush=True)
+    shapes = [(16, 8), (8, 16), (100, 50), (300, 200), (256, 128), (1024, 1024), (40, 40)]
+    st = stored(240, shapes, dtype="bf16" if compute == "bf16" else "f32")
+    st[-1] = np.zeros_like(st[-1])
+    gouts = upstream(241, shapes)
+    ws = [to_dev(s) for s in st]
+    ref_out = [torch.empty(w.shape, device=DEV) for w in ws]
+    got_out = [torch.full(w.shape, float("nan"), device=DEV) for w in ws]
+    st_ref = torch.full((len(ws),), -1, dtype=torch.int32, device=DEV)
+    st_got = torch.full((len(ws),), -1, dtype=torch.int32, device=DEV)
+    orth.orth_orthogonalize_batched(ws, ref_out, iters, compute=compute, status=st_ref, tile=tile)
+    tape = orth.orth_orthogonalize_save_batched(ws, got_out, iters, compute=compute, status=st_got, tile=tile)
+    gos = [torch.from_numpy(g).to(DEV) for g in gouts]
+    g_ref = [torch.empty(w.shape, dtype=w.dtype, device=DEV) for w in ws]
+    orth.orth_orthogonalize_vjp_batched(ws, gos, g_ref, iters, compute=compute, tile=tile)
+    g_got = [[torch.full(w.shape, float("nan"), dtype=w.dtype, device=DEV) for w in ws] for _ in range(2)]
+    st_vjp = torch.full((len(ws),), -1, dtype=torch.int32, device=DEV)
+    for k, g in enumerate(g_got):
+        orth.orth_orthogonalize_vjp_batched(ws, gos, g, iters, compute=compute, tile=tile, workspace=tape,
+                                            saved=True, status=st_vjp if k else None)
+    torch.cuda.synchronize()
+    assert np.array_equal(st_got.cpu().numpy(), st_ref.cpu().numpy())
+    assert np.array_equal(st_vjp.cpu().numpy(), st_ref.cpu().numpy())
+    assert st_got.cpu().numpy()[-1] == 1
+    for a, b, shape in zip(got_out[:-1], ref_out[:-1], shapes):
+        # same arithmetic in both plans (tile lists differ only in order)
+        assert checks.relative_difference(to_f64(a), to_f64(b)) <= 1e-6, shape
+    assert torch.equal(got_out[-1], ref_out[-1]) and not torch.any(got_out[-1] != 0)
+    for g in g_got:
+        for a, b, shape in zip(g, g_ref, shapes):
+            assert torch.equal(a, b), shape
+
+
 def test_layer_vjp_chain():
     """Raw parameters -> kernel gradient -> raw-parameter gradients, all on
     the GPU (Björck forward, composition VJP, Björck VJP), against the
