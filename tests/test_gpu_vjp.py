@@ -244,7 +244,7 @@ def test_saving_forward_and_saved_vjp(compute, iters, tile):
     gradients of the recomputing VJP bit for bit, twice in a row (the saved
     iterates are left intact), including a zero matrix."""
     print(f"[saved vjp] compute={compute} iters={iters} tile={tile}", flush=True)
-    shapes = [(16, 8), (8, 16), (100, 50), (300, 200), (256, 128), (1024, 1024), (40, 40)]
+    shapes = [(16, 8), (8, 16), (100, 50), (300, 200), (200, 300), (256, 128), (1024, 1024), (40, 40)]
     st = stored(240, shapes, dtype="bf16" if compute == "bf16" else "f32")
     st[-1] = np.zeros_like(st[-1])
     gouts = upstream(241, shapes)
@@ -274,6 +274,23 @@ def test_saving_forward_and_saved_vjp(compute, iters, tile):
     for g in g_got:
         for a, b, shape in zip(g, g_ref, shapes):
             assert torch.equal(a, b), shape
+
+
+def test_saving_forward_bf16_output_and_strides():
+    """The saving forward writes bf16 outputs and honours leading dimensions
+    (strided views) like the plain forward."""
+    shapes = [(300, 200), (200, 300), (64, 48)]
+    st = stored(242, shapes)
+    ws = [to_dev(s) for s in st]
+    big = [torch.full((r, c + 24), float("nan"), dtype=torch.bfloat16, device=DEV) for r, c in shapes]
+    got = [b[:, 8:8 + c] for b, (r, c) in zip(big, shapes)]
+    ref = [torch.empty(r, c, dtype=torch.bfloat16, device=DEV) for r, c in shapes]
+    orth.orth_orthogonalize_batched(ws, ref, 6)
+    orth.orth_orthogonalize_save_batched(ws, got, 6)
+    torch.cuda.synchronize()
+    for g, r, b, (rows, cols) in zip(got, ref, big, shapes):
+        assert checks.relative_difference(to_f64(g), to_f64(r)) <= 1e-2 ** 2, (rows, cols)
+        assert torch.all(torch.isnan(b[:, :8].float())) and torch.all(torch.isnan(b[:, 8 + cols:].float()))
 
 
 def test_layer_vjp_chain():
