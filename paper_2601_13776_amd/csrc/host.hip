@@ -76,7 +76,11 @@ void timing_begin(const char* name, hipStream_t s) {
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   TimingRec r{name, pool_event(), nullptr};
-  if (r.a) hipEventRecord(r.a, s);
+  // a failed record leaves the pair incomplete, which the read reports
+  if (r.a && hipEventRecord(r.a, s) != hipSuccess) {
+    g_event_pool.push_back(r.a);
+    r.a = nullptr;
+  }
   g_pending.push_back(r);
 }
 
@@ -86,7 +90,10 @@ void timing_end(const char* name, hipStream_t s) {
   for (auto it = g_pending.rbegin(); it != g_pending.rend(); ++it) {
     if (it->b == nullptr && it->name == name) {
       it->b = pool_event();
-      if (it->b) hipEventRecord(it->b, s);
+      if (it->b && hipEventRecord(it->b, s) != hipSuccess) {
+        g_event_pool.push_back(it->b);
+        it->b = nullptr;
+      }
       break;
     }
   }
