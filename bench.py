@@ -218,15 +218,20 @@ def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, d
                 "frac": round(ach / peak, 4), "traffic": measured_traffic(dom, w.name),
                 "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(cf_ / launches)}
-    # The training pattern: a forward that keeps its iterates in the VJP
-    # workspace (orth_orthogonalize_save_batched) and a VJP that reuses them
-    # instead of recomputing the forward steps.
-    def save_step():
+    # The training pattern: a parametrization step that keeps its iterates
+    # and tap grids in the VJP workspaces (orth_orthogonalize_save_batched,
+    # orth_build_conv_kernels_save_batched) and VJPs that reuse them instead
+    # of recomputing the forward steps.
+    klayers = [dict(geom=L["geom"], rko=L["rko"], proj=L["proj"], kernel=L["kernel"]) for L in layers]
+
+    def save_step():   # the parametrization step, keeping what the VJP needs
         orth.orth_orthogonalize_save_batched(ins, outs, w.iters, compute=compute, status=status, workspace=bws)
+        if klayers:
+            orth.orth_build_conv_kernels_save_batched(klayers, workspace=cws)
 
     def saved_step():
         if vlayers:
-            orth.orth_build_conv_kernels_vjp_batched(vlayers, workspace=cws)
+            orth.orth_build_conv_kernels_vjp_batched(vlayers, workspace=cws, saved=True)
         orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, compute=compute, status=status,
                                             workspace=bws, saved=True)
 

@@ -322,7 +322,8 @@ typedef struct {
  * kernel gradient G to dT[a][b] = G[a][b] P + G[next] (I - P) and gives
  * dP = sum_taps T^T (G[a][b] - G[next]), with "next" the neighbouring tap
  * along the block's direction; P = V V^T gives dV = (dP + dP^T) V.  The
- * forward taps are recomputed inside the call.  Chain with
+ * forward taps are recomputed inside the call (see the saving composition
+ * below for the alternative).  Chain with
  * orth_orthogonalize_vjp_batched for the gradient with respect to the raw
  * parameters.  dtype is the storage type of every tensor; arithmetic is fp32.
  * Errors as orth_build_conv_kernels_batched.  grad_* must not overlap the
@@ -333,6 +334,26 @@ int orth_build_conv_kernels_vjp_workspace_size(const orth_conv_vjp_desc* descs, 
 int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t n,
                                         int32_t dtype, void* workspace,
                                         size_t workspace_bytes, void* stream);
+
+/*
+ * The composition of orth_build_conv_kernels_batched (Appendix B.1, same
+ * kernels up to fp32 rounding order) that leaves, in a composition-VJP
+ * workspace, the projectors and the input tap grid of every block step, so
+ * that orth_build_conv_kernels_vjp_saved_batched (the product above without
+ * its forward recomputation) can follow for the same layers, factors
+ * (unchanged) and dtype, as often as needed.  The workspace size is that of
+ * orth_build_conv_kernels_vjp_workspace_size for the same geometries
+ * (orth_build_conv_kernels_save_workspace_size gives it from these
+ * descriptors).  Errors as orth_build_conv_kernels_batched.
+ */
+int orth_build_conv_kernels_save_workspace_size(const orth_conv_desc* descs, int32_t n,
+                                                int32_t dtype, size_t* bytes);
+int orth_build_conv_kernels_save_batched(const orth_conv_desc* descs, int32_t n,
+                                         int32_t dtype, void* workspace,
+                                         size_t workspace_bytes, void* stream);
+int orth_build_conv_kernels_vjp_saved_batched(const orth_conv_vjp_desc* descs, int32_t n,
+                                              int32_t dtype, void* workspace,
+                                              size_t workspace_bytes, void* stream);
 
 /* Application of an explicit kernel (forward or transposed convolution). */
 typedef struct {

@@ -816,6 +816,15 @@ struct ConvVjpPlan {
   int64_t rko_max = 0, grad_max = 0;
   size_t off_proj = 0, off_last_dp = 0, off_dv = 0, off_rko_taps = 0, off_grad_taps = 0, off_rko_grad = 0;
   std::vector<size_t> off_fwd_gemm, off_bwd_gemm, off_fwd_comb, off_bwd_comb;
+  // saving forward only: the last block step into a k x k grid (G[0]) and
+  // its scatter to the OIHW kernel
+  std::vector<GemmList> save_gemm;
+  std::vector<std::vector<TapItem>> save_comb;
+  std::vector<TapItem> save_scatter;
+  std::vector<int64_t> save_max;
+  int64_t scatter_max = 0;
+  std::vector<size_t> off_save_gemm, off_save_comb;
+  size_t off_save_scatter = 0;
   size_t table_bytes = 0, total_bytes = 0;
 };
 
@@ -836,8 +845,10 @@ int validate_conv_vjp_descs(const orth_conv_vjp_desc* d, int32_t n, int32_t dtyp
 // every tile of an M x N output for the fp32 tile GEMM
 void gemm_tiles(const GemmItem& proto, GemmList& out) { out.add_all(proto); }
 
+// kernels: the layers' kernel outputs for a saving forward (nullptr
+// otherwise; the layout does not depend on it)
 void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, ConvVjpPlan& P,
-                         unsigned char* ws) {
+                         unsigned char* ws, const void* const* kernels = nullptr) {
   const size_t esz = dtype == ORTH_BF16 ? 2 : 4;
   int max_kp = 1;
   for (int i = 0; i < n; ++i) max_kp = std::max(max_kp, d[i].geom.k - d[i].geom.stride + 1);
@@ -848,6 +859,9 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
   P.bwd_comb.assign(n_phase, {});
   P.fwd_max.assign(n_phase, 0);
   P.bwd_max.assign(n_phase, 0);
+  P.save_gemm.assign(n_phase, {});
+  P.save_comb.assign(n_phase, {});
+  P.save_max.assign(n_phase, 0);
 
   // Two passes: the first (ws == nullptr inside) only counts table entries;
   // buffers follow the tables, so table sizes must be known first.
@@ -864,12 +878,17 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
       P.off_bwd_gemm.resize(n_phase);
       P.off_fwd_comb.resize(n_phase);
       P.off_bwd_comb.resize(n_phase);
+      P.off_save_gemm.resize(n_phase);
+      P.off_save_comb.resize(n_phase);
       for (int ph = 0; ph < n_phase; ++ph) {
         P.off_fwd_gemm[ph] = A.take(GemmList::bound(P.fwd_gemm[ph].size()));
         P.off_bwd_gemm[ph] = A.take(GemmList::bound(P.bwd_gemm[ph].size()));
         P.off_fwd_comb[ph] = A.take(sizeof(TapItem) * P.fwd_comb[ph].size());
         P.off_bwd_comb[ph] = A.take(sizeof(TapItem) * P.bwd_comb[ph].size());
+        P.off_save_gemm[ph] = A.take(GemmList::bound(P.save_gemm[ph].size()));
+        P.off_save_comb[ph] = A.take(sizeof(TapItem) * P.save_comb[ph].size());
       }
+      P.off_save_scatter = A.take(sizeof(TapItem) * P.save_scatter.size());
       P.table_bytes = align_up(A.off);
       P.proj_items.clear();
       P.last_dp.clear();
@@ -882,7 +901,10 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
         P.bwd_gemm[ph].clear();
         P.fwd_comb[ph].clear();
         P.bwd_comb[ph].clear();
+        P.save_gemm[ph].clear();
+        P.save_comb[ph].clear();
       }
+      P.save_scatter.clear();
     }
     auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 && ws) ? ws + off : nullptr; };
     auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
@@ -956,6 +978,31 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
           P.fwd_comb[ph].push_back(TapItem{Ts[q], Y, Ts[q + 1], nullptr, og, c, gh, gw, v, 0});
           P.fwd_max[ph] = std::max<int64_t>(P.fwd_max[ph], (int64_t)(gh + v) * (gw + 1 - v) * tap);
         }
+        // saving forward: the last block step into the k x k grid G[0],
+        // then the grid (or, without blocks, the s x s RKO taps) to OIHW
+        if (nq) {
+          const int q = nq - 1;
+          int gh, gw, v;
+          in_grid(q, gh, gw, v);
+          const int ph = gphase(q);
+          GemmItem gi{};
+          gi.A = Ts[q];
+          gi.B = Pm + (size_t)q * c * c;
+          gi.C = Y ? Y : G[1];
+          gi.lda = gi.ldb = gi.ldc = c;
+          gi.M = gh * gw * og;
+          gi.N = c;
+          gi.K = c;
+          gi.epi = EPI_STORE;
+          gemm_tiles(gi, P.save_gemm[ph]);
+          P.save_comb[ph].push_back(TapItem{Ts[q], gi.C, G[0], nullptr, og, c, gh, gw, v, 0});
+          P.save_max[ph] = std::max<int64_t>(P.save_max[ph], (int64_t)(gh + v) * (gw + 1 - v) * tap);
+        }
+        void* kslice = kernels ? static_cast<unsigned char*>(const_cast<void*>(kernels[li])) +
+                                     (size_t)grp * og * c * k * k * esz
+                               : nullptr;
+        P.save_scatter.push_back(TapItem{nq ? G[0] : Ts[0], nullptr, kslice, nullptr, og, c, k, k, 0, 0});
+        P.scatter_max = std::max<int64_t>(P.scatter_max, (int64_t)k * k * tap);
         // gradient, last step first
         int cur = 0;
         P.grad_taps.push_back(TapItem{gk, nullptr, G[0], nullptr, og, c, k, k, 0, 0});
@@ -2049,18 +2096,20 @@ int orth_build_conv_kernels_vjp_workspace_size(const orth_conv_vjp_desc* descs, 
   return ORTH_OK;
 }
 
-int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void* workspace,
-                                        size_t workspace_bytes, void* stream) {
-  int rc = validate_conv_vjp_descs(descs, n, dtype);
-  if (rc) return rc;
+namespace {
+// mode 0: vector-Jacobian product with the forward recomputed; 1: the same
+// from the tap grids and projectors a saving forward left in the workspace;
+// 2: the saving forward (kernels[] receive the composed kernels)
+int conv_vjp_run(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                 size_t workspace_bytes, void* stream, int mode, const void* const* kernels) {
   if (n == 0) return ORTH_OK;
   ConvVjpPlan P;
   build_conv_vjp_plan(descs, n, dtype, P, nullptr);
-  rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
+  int rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = ConvVjpPlan();
-  build_conv_vjp_plan(descs, n, dtype, P, ws);
+  build_conv_vjp_plan(descs, n, dtype, P, ws, kernels);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int n_phase = (int)P.fwd_gemm.size();
 
@@ -2071,20 +2120,33 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
   put(img, P.off_rko_taps, P.rko_taps);
   put(img, P.off_grad_taps, P.grad_taps);
   put(img, P.off_rko_grad, P.rko_grad);
+  put(img, P.off_save_scatter, P.save_scatter);
   for (int ph = 0; ph < n_phase; ++ph) {
     put(img, P.off_fwd_gemm[ph], P.fwd_gemm[ph]);
     put(img, P.off_bwd_gemm[ph], P.bwd_gemm[ph]);
     put(img, P.off_fwd_comb[ph], P.fwd_comb[ph]);
     put(img, P.off_bwd_comb[ph], P.bwd_comb[ph]);
+    put(img, P.off_save_gemm[ph], P.save_gemm[ph]);
+    put(img, P.off_save_comb[ph], P.save_comb[ph]);
   }
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
   auto TI = [&](size_t off) { return reinterpret_cast<const TapItem*>(ws + off); };
-  ORTH_HIP(launch_tap_items(0, TI(P.off_rko_taps), (int)P.rko_taps.size(), dtype, P.rko_max, s));
-  ORTH_HIP(launch_list(ws, P.off_proj, P.proj_items, "conv_vjp_projector", s));
-  for (int ph = 0; ph < n_phase; ++ph) {
-    ORTH_HIP(launch_list(ws, P.off_fwd_gemm[ph], P.fwd_gemm[ph], "conv_vjp_tap_gemm", s));
-    ORTH_HIP(launch_tap_items(3, TI(P.off_fwd_comb[ph]), (int)P.fwd_comb[ph].size(), dtype, P.fwd_max[ph], s));
+  if (mode != 1) {
+    // forward: RKO taps, projectors, the block steps (keeping every input grid)
+    ORTH_HIP(launch_tap_items(0, TI(P.off_rko_taps), (int)P.rko_taps.size(), dtype, P.rko_max, s));
+    ORTH_HIP(launch_list(ws, P.off_proj, P.proj_items, "conv_vjp_projector", s));
+    for (int ph = 0; ph < n_phase; ++ph) {
+      ORTH_HIP(launch_list(ws, P.off_fwd_gemm[ph], P.fwd_gemm[ph], "conv_vjp_tap_gemm", s));
+      if (mode == 2) ORTH_HIP(launch_list(ws, P.off_save_gemm[ph], P.save_gemm[ph], "conv_vjp_tap_gemm", s));
+      ORTH_HIP(launch_tap_items(3, TI(P.off_fwd_comb[ph]), (int)P.fwd_comb[ph].size(), dtype, P.fwd_max[ph], s));
+      if (mode == 2)
+        ORTH_HIP(launch_tap_items(3, TI(P.off_save_comb[ph]), (int)P.save_comb[ph].size(), dtype, P.save_max[ph], s));
+    }
+  }
+  if (mode == 2) {
+    ORTH_HIP(launch_tap_items(2, TI(P.off_save_scatter), (int)P.save_scatter.size(), dtype, P.scatter_max, s));
+    return ORTH_OK;
   }
   ORTH_HIP(launch_tap_items(1, TI(P.off_grad_taps), (int)P.grad_taps.size(), dtype, P.grad_max, s));
   for (int ph = n_phase - 1; ph >= 0; --ph) {
@@ -2095,6 +2157,64 @@ int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t
   ORTH_HIP(launch_list(ws, P.off_dv, P.dv_items, "conv_vjp_factor_grad", s));
   ORTH_HIP(launch_tap_items(2, TI(P.off_rko_grad), (int)P.rko_grad.size(), dtype, P.rko_max, s));
   return ORTH_OK;
+}
+
+// The vector-Jacobian descriptors whose plan a saving composition shares:
+// the gradient fields hold placeholders that the forward never touches.
+int conv_save_descs(const orth_conv_desc* d, int32_t n, int32_t dtype, std::vector<orth_conv_vjp_desc>& vd,
+                    std::vector<const void*>& kernels) {
+  int rc = validate_conv_descs(d, n, dtype);
+  if (rc) return rc;
+  vd.resize(n);
+  kernels.resize(n);
+  for (int i = 0; i < n; ++i) {
+    vd[i] = orth_conv_vjp_desc{};
+    vd[i].geom = d[i].geom;
+    vd[i].rko = d[i].rko;
+    vd[i].proj = d[i].proj;
+    vd[i].grad_kernel = d[i].kernel;
+    vd[i].grad_rko = const_cast<void*>(d[i].rko);
+    vd[i].grad_proj = const_cast<void*>(d[i].proj);
+    kernels[i] = d[i].kernel;
+  }
+  return validate_conv_vjp_descs(vd.data(), n, dtype);
+}
+}  // namespace
+
+int orth_build_conv_kernels_vjp_batched(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  const int rc = validate_conv_vjp_descs(descs, n, dtype);
+  if (rc) return rc;
+  return conv_vjp_run(descs, n, dtype, workspace, workspace_bytes, stream, 0, nullptr);
+}
+
+int orth_build_conv_kernels_vjp_saved_batched(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype,
+                                              void* workspace, size_t workspace_bytes, void* stream) {
+  const int rc = validate_conv_vjp_descs(descs, n, dtype);
+  if (rc) return rc;
+  return conv_vjp_run(descs, n, dtype, workspace, workspace_bytes, stream, 1, nullptr);
+}
+
+int orth_build_conv_kernels_save_workspace_size(const orth_conv_desc* descs, int32_t n, int32_t dtype,
+                                                size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  std::vector<orth_conv_vjp_desc> vd;
+  std::vector<const void*> kernels;
+  const int rc = conv_save_descs(descs, n, dtype, vd, kernels);
+  if (rc) return rc;
+  ConvVjpPlan P;
+  build_conv_vjp_plan(vd.data(), n, dtype, P, nullptr);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_build_conv_kernels_save_batched(const orth_conv_desc* descs, int32_t n, int32_t dtype, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  std::vector<orth_conv_vjp_desc> vd;
+  std::vector<const void*> kernels;
+  const int rc = conv_save_descs(descs, n, dtype, vd, kernels);
+  if (rc) return rc;
+  return conv_vjp_run(vd.data(), n, dtype, workspace, workspace_bytes, stream, 2, kernels.data());
 }
 
 int orth_conv_apply(const orth_conv_apply_args* a, void* stream) {

@@ -25,7 +25,9 @@ EXPORTED = [
     "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched",
     "orth_orthogonalize_save_workspace_size", "orth_orthogonalize_save_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
-    "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched", "orth_conv_apply",
+    "orth_build_conv_kernels_vjp_workspace_size", "orth_build_conv_kernels_vjp_batched",
+    "orth_build_conv_kernels_save_workspace_size", "orth_build_conv_kernels_save_batched",
+    "orth_build_conv_kernels_vjp_saved_batched", "orth_conv_apply",
     "orth_exp_map_workspace_size", "orth_exp_map_batched", "orth_conv_exp_workspace_size", "orth_conv_exp_batched",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
     "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
@@ -116,6 +118,9 @@ def lib():
         L.orth_build_conv_kernel.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp, sz, vp]
         L.orth_build_conv_kernels_vjp_workspace_size.argtypes = [P(orth_conv_vjp_desc), i32, i32, P(sz)]
         L.orth_build_conv_kernels_vjp_batched.argtypes = [P(orth_conv_vjp_desc), i32, i32, vp, sz, vp]
+        L.orth_build_conv_kernels_save_workspace_size.argtypes = [P(orth_conv_desc), i32, i32, P(sz)]
+        L.orth_build_conv_kernels_save_batched.argtypes = [P(orth_conv_desc), i32, i32, vp, sz, vp]
+        L.orth_build_conv_kernels_vjp_saved_batched.argtypes = [P(orth_conv_vjp_desc), i32, i32, vp, sz, vp]
         L.orth_conv_apply.argtypes = [P(orth_conv_apply_args), vp]
         L.orth_exp_map_workspace_size.argtypes = [P(orth_mat), i32, P(orth_exp_opts), P(sz)]
         L.orth_exp_map_batched.argtypes = [P(orth_mat), i32, P(orth_exp_opts), vp, sz, vp, vp]
@@ -352,12 +357,16 @@ def orth_build_conv_kernel(rko, proj, cin, cout, k, stride, dilation, groups, ke
         workspace, stream)
 
 
-def orth_build_conv_kernels_vjp_batched(layers, workspace=None, stream=None):
+def orth_build_conv_kernels_vjp_batched(layers, workspace=None, stream=None, saved=False):
     """layers: list of dicts with geom, rko, proj (or None), grad_kernel,
     grad_rko and grad_proj (or None) tensors (contiguous, one dtype).
-    Writes dL/d rko and dL/d proj given dL/d kernel."""
+    Writes dL/d rko and dL/d proj given dL/d kernel.  saved=True skips the
+    forward recomputation: `workspace` holds what
+    orth_build_conv_kernels_save_batched left for the same layers."""
     if not layers:
         return None
+    if saved and workspace is None:
+        raise ValueError("saved=True needs the workspace of orth_build_conv_kernels_save_batched")
     dt = _dtype_code(layers[0]["grad_kernel"])
     arr = (orth_conv_vjp_desc * len(layers))()
     for i, L in enumerate(layers):
@@ -372,9 +381,33 @@ def orth_build_conv_kernels_vjp_batched(layers, workspace=None, stream=None):
     _check(lib().orth_build_conv_kernels_vjp_workspace_size(arr, len(layers), dt, ctypes.byref(n)),
            "orth_build_conv_kernels_vjp_workspace_size")
     ws, nbytes = _workspace(n.value, layers[0]["grad_kernel"].device, workspace)
-    rc = lib().orth_build_conv_kernels_vjp_batched(arr, len(layers), dt, ws.data_ptr() if ws is not None else None,
-                                                   nbytes, _stream(stream))
+    fn = lib().orth_build_conv_kernels_vjp_saved_batched if saved else lib().orth_build_conv_kernels_vjp_batched
+    rc = fn(arr, len(layers), dt, ws.data_ptr() if ws is not None else None, nbytes, _stream(stream))
     _check(rc, "orth_build_conv_kernels_vjp_batched")
+    return ws
+
+
+def orth_build_conv_kernels_save_batched(layers, workspace=None, stream=None):
+    """orth_build_conv_kernels_batched that also keeps, in the returned
+    (composition-VJP) workspace, what orth_build_conv_kernels_vjp_batched(...,
+    saved=True, workspace=<it>) reuses.  layers as for
+    orth_build_conv_kernels_batched."""
+    if not layers:
+        return None
+    dt = _dtype_code(layers[0]["kernel"])
+    for L in layers:
+        for key in ("rko", "proj", "kernel"):
+            t = L.get(key)
+            if t is not None and (not t.is_contiguous() or _dtype_code(t) != dt):
+                raise ValueError(f"{key} must be contiguous and of the kernel's dtype")
+    descs = _conv_descs(layers)
+    n = ctypes.c_size_t()
+    _check(lib().orth_build_conv_kernels_save_workspace_size(descs, len(layers), dt, ctypes.byref(n)),
+           "orth_build_conv_kernels_save_workspace_size")
+    ws, nbytes = _workspace(n.value, layers[0]["kernel"].device, workspace)
+    rc = lib().orth_build_conv_kernels_save_batched(descs, len(layers), dt, ws.data_ptr() if ws is not None else None,
+                                                    nbytes, _stream(stream))
+    _check(rc, "orth_build_conv_kernels_save_batched")
     return ws
 
 

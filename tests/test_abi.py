@@ -245,6 +245,29 @@ def test_save_and_saved_flag_errors(L):
                                              None) == orth.ORTH_EWORKSPACE
 
 
+def test_conv_save_workspace_matches_vjp(L):
+    """A saving composition fills a composition-VJP workspace: its size
+    query equals the VJP's for the same geometries and dtype."""
+    geoms = [(16, 16, 3, 1, 1, 1), (16, 32, 2, 2, 1, 1), (32, 32, 3, 1, 1, 4), (6, 6, 5, 2, 3, 3), (8, 8, 1, 1, 1, 1)]
+    fwd = (orth.orth_conv_desc * len(geoms))()
+    vjp = (orth.orth_conv_vjp_desc * len(geoms))()
+    for i, g in enumerate(geoms):
+        base = 0x100000 * (i + 1)
+        has_proj = g[2] > g[3]
+        fwd[i] = orth.orth_conv_desc(orth.orth_conv_geom(*g), base, base + 0x10000 if has_proj else None, base + 0x20000)
+        vjp[i] = orth.orth_conv_vjp_desc(orth.orth_conv_geom(*g), base, base + 0x10000 if has_proj else None,
+                                         base + 0x30000, base + 0x40000, base + 0x50000 if has_proj else None)
+    for dt in (0, 1):
+        a, b = ctypes.c_size_t(), ctypes.c_size_t()
+        assert L.orth_build_conv_kernels_save_workspace_size(fwd, len(geoms), dt, ctypes.byref(a)) == orth.ORTH_OK
+        assert L.orth_build_conv_kernels_vjp_workspace_size(vjp, len(geoms), dt, ctypes.byref(b)) == orth.ORTH_OK
+        assert a.value == b.value > 0
+    bad = (orth.orth_conv_desc * 1)()
+    bad[0] = orth.orth_conv_desc(orth.orth_conv_geom(16, 16, 3, 1, 1, 1), 0x1000, None, 0x3000)   # proj missing
+    n = ctypes.c_size_t()
+    assert L.orth_build_conv_kernels_save_workspace_size(bad, 1, 0, ctypes.byref(n)) == orth.ORTH_EINVAL
+
+
 def test_vjp_workspace_grows_with_saved_steps(L):
     """The VJP keeps X_t and E_t of every step: fp32 products hold
     T (2 M N + N^2) fp32 values beside a few fixed buffers (X_t also

@@ -293,6 +293,46 @@ def test_saving_forward_bf16_output_and_strides():
         assert torch.all(torch.isnan(b[:, :8].float())) and torch.all(torch.isnan(b[:, 8 + cols:].float()))
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_saving_composition_and_saved_conv_vjp(dtype):
+    """orth_build_conv_kernels_save_batched composes the kernels of
+    orth_build_conv_kernels_batched; the composition VJP from its workspace
+    (saved=True) equals the recomputing one bit for bit, twice in a row."""
+    print(f"[saved conv vjp] {dtype}", flush=True)
+    items = [(geom, *conv_factors(geom, 600 + i)) for i, geom in enumerate(CONV_GEOMS)]
+    t = lambda a: torch.from_numpy(a).to(DEV).to(dtype).contiguous()
+    fwd_ref, fwd_got = [], []
+    for geom, rko, proj, dk in items:
+        cin, cout, k = geom[0], geom[1], geom[2]
+        shape = (cout, cin // geom[5], k, k)
+        fwd_ref.append(dict(geom=geom, rko=t(rko), proj=t(proj) if proj is not None else None,
+                            kernel=torch.empty(shape, dtype=dtype, device=DEV)))
+        fwd_got.append(dict(geom=geom, rko=fwd_ref[-1]["rko"], proj=fwd_ref[-1]["proj"],
+                            kernel=torch.full(shape, float("nan"), dtype=dtype, device=DEV)))
+    orth.orth_build_conv_kernels_batched(fwd_ref)
+    tape = orth.orth_build_conv_kernels_save_batched(fwd_got)
+    ref = conv_vjp_gpu(items, dtype)
+    got = []
+    for _ in range(2):
+        layers = []
+        for (geom, rko, proj, dk), F in zip(items, fwd_got):
+            layers.append(dict(geom=geom, rko=F["rko"], proj=F["proj"], grad_kernel=t(dk),
+                               grad_rko=torch.full(rko.shape, float("nan"), dtype=dtype, device=DEV),
+                               grad_proj=torch.full(proj.shape, float("nan"), dtype=dtype, device=DEV)
+                               if proj is not None else None))
+        orth.orth_build_conv_kernels_vjp_batched(layers, workspace=tape, saved=True)
+        got.append(layers)
+    torch.cuda.synchronize()
+    for a, b, (geom, *_) in zip(fwd_got, fwd_ref, items):
+        tol = 1e-6 if dtype == torch.float32 else 1e-2
+        assert checks.relative_difference(to_f64(a["kernel"]), to_f64(b["kernel"])) <= tol, geom
+    for layers in got:
+        for L, R, (geom, *_) in zip(layers, ref, items):
+            assert torch.equal(L["grad_rko"], R["grad_rko"]), geom
+            if R["grad_proj"] is not None:
+                assert torch.equal(L["grad_proj"], R["grad_proj"]), geom
+
+
 def test_layer_vjp_chain():
     """Raw parameters -> kernel gradient -> raw-parameter gradients, all on
     the GPU (Björck forward, composition VJP, Björck VJP), against the
