@@ -118,6 +118,18 @@ def test_imagenet_conv_vjp_full_size():
     print("[imagenet conv vjp] all 16 layers", flush=True)
     orth.orth_build_conv_kernels_vjp_batched(layers)
     torch.cuda.synchronize()
+    # the training pattern: saving composition, then the saved VJP (same
+    # workspace layout), bit for bit the recomputing VJP
+    fw = [dict(geom=g, rko=L["rko"], proj=L["proj"],
+               kernel=torch.empty(g[1], g[0] // g[5], g[2], g[2], device=DEV)) for (g, *_), L in zip(items, layers)]
+    tape = orth.orth_build_conv_kernels_save_batched(fw)
+    saved = [dict(L, grad_rko=torch.empty_like(L["grad_rko"]), grad_proj=torch.empty_like(L["grad_proj"]))
+             for L in layers]
+    orth.orth_build_conv_kernels_vjp_batched(saved, workspace=tape, saved=True)
+    torch.cuda.synchronize()
+    for a, b in zip(saved, layers):
+        assert torch.equal(a["grad_rko"], b["grad_rko"]) and torch.equal(a["grad_proj"], b["grad_proj"])
+    del tape, saved
     for li in (0, 4):                  # widths 128 and 256
         print(f"[imagenet conv vjp] oracle layer {li}", flush=True)
         geom, rko, proj, dk = items[li]
@@ -177,6 +189,18 @@ def test_stress_vjp_full_size():
     torch.cuda.synchronize()
     print("[stress vjp] done", flush=True)
     assert np.all(status.cpu().numpy() == 0)
+    # the training pattern in the same workspace: a saving forward, then the
+    # VJP from its iterates gives the same gradients bit for bit
+    outs_fwd = [torch.empty(s, device=DEV) for s in shapes]
+    orth.orth_orthogonalize_save_batched(ins, outs_fwd, w.iters, compute="bf16", workspace=ws)
+    gsaved = [torch.empty_like(t) for t in ins]
+    orth.orth_orthogonalize_vjp_batched(ins, gouts, gsaved, w.iters, compute="bf16", workspace=ws, saved=True)
+    torch.cuda.synchronize()
+    print("[stress vjp] saved done", flush=True)
+    for i in (0, 63, 64, 4159):
+        assert torch.equal(gsaved[i], gins[i]), i
+    assert all(torch.equal(a, b) for a, b in zip(gsaved, gins))
+    del gsaved, outs_fwd
     for g in gins[:64]:
         assert bool(torch.isfinite(g.float()).all())
     for i in list(range(64, 4160, 257)):
