@@ -85,7 +85,11 @@ def allocate_outputs(w, ins, torch, dev, out_dtype):
 
 # traffic records: profiles/traffic_<kernel>_<workload>.md
 # the traffic depends on the kernel and on the tile order the host planner builds
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2601_13776_amd", "csrc", f) for f in ("bjorck_bf16.hip", "tile_order.h")]
+def kernel_sources(kernel_name):
+    """Sources whose change invalidates a traffic record: the kernel and the
+    planner code that orders its tiles."""
+    files = ("bjorck_bf16.hip", "tile_order.h") if "bf16" in kernel_name else ("gemm_f32.hip", "host.hip")
+    return [os.path.join(ROOT, "paper_2601_13776_amd", "csrc", f) for f in files]
 
 
 def measured_traffic(kernel_name, workload):
@@ -102,7 +106,7 @@ def measured_traffic(kernel_name, workload):
     fields = dict(re.findall(r"^- (\w+): (\S+)$", text, flags=re.M))
     try:
         h = hashlib.sha256()
-        for f in KERNEL_SOURCES:
+        for f in kernel_sources(kernel_name):
             h.update(open(f, "rb").read())
         src_hash = h.hexdigest()
         if fields.get("kernel") != kernel_name or fields.get("workload") != workload \
