@@ -496,8 +496,8 @@ def main():
                     help="also run one plain 1 GiB device copy (for HBM counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(matrices would be distributed across GPUs by size; see DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(the independent matrices would be distributed across GPUs by size)", file=sys.stderr)
         sys.exit(2)
 
     import torch

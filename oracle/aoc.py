@@ -5,9 +5,9 @@ The paper builds an explicit orthogonal k x k kernel as
     AOC = RKO ⊛ K_BCOP
 
 where ⊛ is the block-convolution (kernel-on-kernel) operator: the kernel of
-the composition of two convolutions.  The AOC details are deferred to a paper
-that is not available here, so this module fixes one reading that is provably
-orthogonal (every reading is listed in the design doc):
+the composition of two convolutions.  The paper defers the AOC details to a
+companion paper, so this module fixes one reading that is provably
+orthogonal:
 
 * c = cin / groups channels per group, k' = k - s + 1 (valid iff k >= s).
 * RKO factor: an s x s kernel with stride s whose (cout/g) x (c s^2)
