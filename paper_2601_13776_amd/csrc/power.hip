@@ -51,21 +51,53 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
   // rows and columns start 16-byte aligned: runs of 8 elements are loaded
   // with one 16-byte (bf16) or two (fp32) vector loads
   const bool vec = vec8_ok(d.in, d.ld_in, in_dtype);
-  if (!it.coldot) {
+  if (!it.coldot && vec) {
+    // out[r] = sum_c W[r][c] in[c]: a wave per row, lanes along the row in
+    // 8-element runs; the vector goes through LDS one chunk of columns at a
+    // time, so that the 64 rows of the block share each load of it
+    constexpr int CH = 2048;
+    __shared__ double vin[CH];
+    const int cols8 = d.cols / 8 * 8;
+    double acc[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) acc[k] = 0.0;
+    for (int cb = 0; cb < cols8; cb += CH) {
+      const int cn = cols8 - cb < CH ? cols8 - cb : CH;
+      __syncthreads();   // the previous chunk's reads are done
+      for (int j = threadIdx.x; j < cn; j += 256) vin[j] = in[cb + j];
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int r = it.block * 64 + wave + 4 * k;
+        if (r < d.rows) {
+          const int64_t row = (int64_t)r * d.ld_in + cb;
+          for (int c0 = lane * 8; c0 < cn; c0 += 512) {
+            float w[8];
+            load8_f32(d.in, row + c0, in_dtype, w);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[k] += (double)w[q] * vin[c0 + q];
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int r = it.block * 64 + wave + 4 * k;
+      if (r < d.rows) {
+        const int64_t row = (int64_t)r * d.ld_in;
+        for (int c = cols8 + lane; c < d.cols; c += 64) acc[k] += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
+        const double t = wave_sum(acc[k]);
+        if (lane == 0) out[r] = t;
+      }
+    }
+  } else if (!it.coldot) {
     // out[r] = sum_c W[r][c] in[c]: a wave per row, lanes along the row
-    const int cols8 = vec ? d.cols / 8 * 8 : 0;
     for (int i = wave; i < 64; i += 4) {
       const int r = it.block * 64 + i;
       if (r >= d.rows) break;
       double acc = 0.0;
       const int64_t row = (int64_t)r * d.ld_in;
-      for (int c0 = lane * 8; c0 < cols8; c0 += 512) {
-        float w[8];
-        load8_f32(d.in, row + c0, in_dtype, w);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc += (double)w[q] * in[c0 + q];
-      }
-      for (int c = cols8 + lane; c < d.cols; c += 64) acc += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
+      for (int c = lane; c < d.cols; c += 64) acc += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
       acc = wave_sum(acc);
       if (lane == 0) out[r] = acc;
     }
