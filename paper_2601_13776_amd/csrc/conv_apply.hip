@@ -263,7 +263,10 @@ constexpr int HALO_CB = 8, HALO_BNP = 64, HALO_MAXE = 24;
 
 // 64 output rows x BN pixels per workgroup; each wave 32 rows x BN / 2
 // pixels (NI accumulators)
-template <bool TR, int KS, int BN, bool KBF16>
+// VECA (forward conv, fp32 kernel with rows of a multiple of four elements):
+// each chunk's kernel tile is loaded as 16-byte vectors along the kernel
+// rows, with the offsets computed once per workgroup.
+template <bool TR, int KS, int BN, bool KBF16, bool VECA>
 __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloGeom Hg,
                                                               const void* __restrict__ kern,
                                                               const float* __restrict__ x, float* __restrict__ y) {
@@ -332,10 +335,23 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
     }
     boff[i] = off;
   }
-  // kernel elements of this thread: e = tid + i 256 over 64 rows x KCH
-  int aoff[MAXA];
+  // VECA: float4 f = tid + j 256 of the 64 x KCH tile: global offset (-1:
+  // row past the end), column within the chunk, LDS offset
+  constexpr int Q4 = KCH / 4, NV = (64 * Q4 + 255) / 256;
+  int vgo[VECA ? NV : 1], vcol[VECA ? NV : 1], vlo[VECA ? NV : 1];
+  if constexpr (VECA) {
 #pragma unroll
-  for (int i = 0; i < MAXA; ++i) {
+    for (int j = 0; j < NV; ++j) {
+      const int f = tid + j * 256, row = f / Q4, c4 = f - row * Q4;
+      vgo[j] = f < 64 * Q4 && row0 + row < G.rows ? (grp * G.og + row0 + row) * G.red + c4 * 4 : -1;
+      vcol[j] = c4 * 4;
+      vlo[j] = f < 64 * Q4 ? row * AP + c4 * 4 : -1;
+    }
+  }
+  // kernel elements of this thread: e = tid + i 256 over 64 rows x KCH
+  int aoff[VECA ? 1 : MAXA];
+#pragma unroll
+  for (int i = 0; i < (VECA ? 0 : MAXA); ++i) {
     aoff[i] = -1;
     const int e = tid + i * 256;
     if (e >= 64 * KCH) continue;
@@ -361,25 +377,54 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
     const char* xq = reinterpret_cast<const char*>(x + (int64_t)ch0 * cplane);
     // raw bits first, widened at the LDS store: a conversion inside the
     // guarded load would make every load wait for its data
-    uint32_t ra[MAXA];
+    uint32_t ra[VECA ? 1 : MAXA];
+    float4 va[VECA ? NV : 1];
     float rb[HALO_MAXE];
+    if constexpr (VECA) {
+      const int lim = nvalid >= CB ? KCH : nvalid * KK;   // valid columns of this chunk
+      const float* kf = reinterpret_cast<const float*>(kq);
 #pragma unroll
-    for (int i = 0; i < MAXA; ++i) {
-      const int e = tid + i * 256, col = e - (e / KCH) * KCH;
-      uint32_t v = 0;
-      if (aoff[i] >= 0 && col / KK < nvalid) {
-        const uint32_t bo = (uint32_t)aoff[i] * (uint32_t)kes;
-        if constexpr (KBF16)
-          v = *reinterpret_cast<const uint16_t*>(kq + bo);
-        else
-          v = *reinterpret_cast<const uint32_t*>(kq + bo);
+      for (int j = 0; j < NV; ++j) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        const int col = vcol[j];
+        if (vgo[j] >= 0) {
+          const float* p = kf + (uint32_t)vgo[j];
+          if (col + 4 <= lim) {
+            v = *reinterpret_cast<const float4*>(p);
+          } else {
+            if (col < lim) v.x = p[0];
+            if (col + 1 < lim) v.y = p[1];
+            if (col + 2 < lim) v.z = p[2];
+          }
+        }
+        va[j] = v;
       }
-      ra[i] = v;
-    }
-    // materialize the raw values after the guarded loads (otherwise the
-    // widening shift is moved into each guarded block, where it waits)
 #pragma unroll
-    for (int i = 0; i < MAXA; ++i) asm volatile("" : "+v"(ra[i]));
+      for (int j = 0; j < NV; ++j) {
+        asm volatile("" : "+v"(va[j].x));
+        asm volatile("" : "+v"(va[j].y));
+        asm volatile("" : "+v"(va[j].z));
+        asm volatile("" : "+v"(va[j].w));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MAXA; ++i) {
+        const int e = tid + i * 256, col = e - (e / KCH) * KCH;
+        uint32_t v = 0;
+        if (aoff[i] >= 0 && col / KK < nvalid) {
+          const uint32_t bo = (uint32_t)aoff[i] * (uint32_t)kes;
+          if constexpr (KBF16)
+            v = *reinterpret_cast<const uint16_t*>(kq + bo);
+          else
+            v = *reinterpret_cast<const uint32_t*>(kq + bo);
+        }
+        ra[i] = v;
+      }
+      // materialize the raw values after the guarded loads (otherwise the
+      // widening shift is moved into each guarded block, where it waits)
+#pragma unroll
+      for (int i = 0; i < MAXA; ++i) asm volatile("" : "+v"(ra[i]));
+    }
 #pragma unroll
     for (int i = 0; i < HALO_MAXE; ++i) {
       const int r = srow0 + i * rpp;
@@ -387,10 +432,16 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
       if (boff[i] >= 0 && r < nvalid * RC) v = *reinterpret_cast<const float*>(xq + (uint32_t)boff[i] * 4u);
       rb[i] = v;
     }
+    if constexpr (VECA) {
 #pragma unroll
-    for (int i = 0; i < MAXA; ++i) {
-      const int e = tid + i * 256;
-      if (e < 64 * KCH) As[(e / KCH) * AP + e % KCH] = __uint_as_float(KBF16 ? ra[i] << 16 : ra[i]);
+      for (int j = 0; j < NV; ++j)
+        if (vlo[j] >= 0) *reinterpret_cast<float4*>(&As[vlo[j]]) = va[j];
+    } else {
+#pragma unroll
+      for (int i = 0; i < MAXA; ++i) {
+        const int e = tid + i * 256;
+        if (e < 64 * KCH) As[(e / KCH) * AP + e % KCH] = __uint_as_float(KBF16 ? ra[i] << 16 : ra[i]);
+      }
     }
 #pragma unroll
     for (int i = 0; i < HALO_MAXE; ++i) {
@@ -442,21 +493,27 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
   }
 }
 
-template <bool TR, int KS, bool KBF16>
+template <bool TR, int KS, bool KBF16, bool VECA>
 hipError_t launch_halo_k(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
                          hipStream_t s) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipError_t e = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16, VECA>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16>), grid, dim3(256), lds, s, G, Hg, a->kernel,
-                     a->x, a->y);
+  hipLaunchKernelGGL((conv_apply_halo_kernel<TR, KS, HALO_BNP, KBF16, VECA>), grid, dim3(256), lds, s, G, Hg,
+                     a->kernel, a->x, a->y);
   return hipGetLastError();
 }
 template <bool TR, int KS>
 hipError_t launch_halo(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
                        hipStream_t s) {
-  return G.kdtype == ORTH_BF16 ? launch_halo_k<TR, KS, true>(G, Hg, grid, lds, a, s)
-                               : launch_halo_k<TR, KS, false>(G, Hg, grid, lds, a, s);
+  if (G.kdtype == ORTH_BF16) return launch_halo_k<TR, KS, true, false>(G, Hg, grid, lds, a, s);
+  // 16-byte kernel loads: forward conv, rows of a multiple of four floats,
+  // a 16-byte aligned kernel
+  if constexpr (!TR)
+    if (G.red % 4 == 0 && (reinterpret_cast<uintptr_t>(a->kernel) & 15) == 0)
+      return launch_halo_k<TR, KS, false, true>(G, Hg, grid, lds, a, s);
+  return launch_halo_k<TR, KS, false, false>(G, Hg, grid, lds, a, s);
 }
 
 }  // namespace
