@@ -263,9 +263,11 @@ constexpr int HALO_CB = 8, HALO_BNP = 64, HALO_MAXE = 24;
 
 // 64 output rows x BN pixels per workgroup; each wave 32 rows x BN / 2
 // pixels (NI accumulators)
-// VECA (forward conv, fp32 kernel with rows of a multiple of four elements):
-// each chunk's kernel tile is loaded as 16-byte vectors along the kernel
-// rows, with the offsets computed once per workgroup.
+// VECA (fp32 kernel, rows of a multiple of four elements): each chunk's
+// kernel tile is loaded as 16-byte vectors, with the offsets computed once
+// per workgroup.  Forward: along the kernel rows.  Transposed: the chunk's
+// channels o each hold the tile's 64 rows x k^2 taps contiguously
+// (K[o][i][tap]), read as one run per o and scattered to the LDS rows.
 template <bool TR, int KS, int BN, bool KBF16, bool VECA>
 __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloGeom Hg,
                                                               const void* __restrict__ kern,
@@ -337,15 +339,26 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
   }
   // VECA: float4 f = tid + j 256 of the 64 x KCH tile: global offset (-1:
   // row past the end), column within the chunk, LDS offset
-  constexpr int Q4 = KCH / 4, NV = (64 * Q4 + 255) / 256;
+  // (transposed: f over CB runs of 64 KK floats; vcol = element within the
+  // run, vlo = the run's channel o; elim = valid elements of a run)
+  constexpr int Q4 = KCH / 4, NV = (64 * Q4 + 255) / 256, QR = 64 * KK / 4;
   int vgo[VECA ? NV : 1], vcol[VECA ? NV : 1], vlo[VECA ? NV : 1];
-  if constexpr (VECA) {
+  const int elim = TR ? (G.rows - row0 < 64 ? G.rows - row0 : 64) * KK : 0;
+  if constexpr (VECA && !TR) {
 #pragma unroll
     for (int j = 0; j < NV; ++j) {
       const int f = tid + j * 256, row = f / Q4, c4 = f - row * Q4;
       vgo[j] = f < 64 * Q4 && row0 + row < G.rows ? (grp * G.og + row0 + row) * G.red + c4 * 4 : -1;
       vcol[j] = c4 * 4;
       vlo[j] = f < 64 * Q4 ? row * AP + c4 * 4 : -1;
+    }
+  } else if constexpr (VECA && TR) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int f = tid + j * 256, o = f / QR, w4 = f - o * QR;
+      vgo[j] = f < 64 * Q4 ? ((grp * G.og + o) * G.c + row0) * KK + w4 * 4 : -1;
+      vcol[j] = w4 * 4;
+      vlo[j] = o;
     }
   }
   // kernel elements of this thread: e = tid + i 256 over 64 rows x KCH
@@ -381,13 +394,15 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
     float4 va[VECA ? NV : 1];
     float rb[HALO_MAXE];
     if constexpr (VECA) {
-      const int lim = nvalid >= CB ? KCH : nvalid * KK;   // valid columns of this chunk
+      // valid elements of this thread's runs: forward, the chunk's valid
+      // columns; transposed, the rows that exist (channels checked apart)
+      const int lim = TR ? elim : (nvalid >= CB ? KCH : nvalid * KK);
       const float* kf = reinterpret_cast<const float*>(kq);
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
         float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
         const int col = vcol[j];
-        if (vgo[j] >= 0) {
+        if (vgo[j] >= 0 && (!TR || vlo[j] < nvalid)) {
           const float* p = kf + (uint32_t)vgo[j];
           if (col + 4 <= lim) {
             v = *reinterpret_cast<const float4*>(p);
@@ -432,10 +447,22 @@ __global__ __launch_bounds__(256) void conv_apply_halo_kernel(ApplyGeom G, HaloG
       if (boff[i] >= 0 && r < nvalid * RC) v = *reinterpret_cast<const float*>(xq + (uint32_t)boff[i] * 4u);
       rb[i] = v;
     }
-    if constexpr (VECA) {
+    if constexpr (VECA && !TR) {
 #pragma unroll
       for (int j = 0; j < NV; ++j)
         if (vlo[j] >= 0) *reinterpret_cast<float4*>(&As[vlo[j]]) = va[j];
+    } else if constexpr (VECA && TR) {
+      // element e of channel o's run is row e / KK, tap e % KK
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        if (vgo[j] < 0) continue;
+        const float w[4] = {va[j].x, va[j].y, va[j].z, va[j].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = vcol[j] + q, row = e / KK;
+          As[row * AP + vlo[j] * KK + (e - row * KK)] = w[q];
+        }
+      }
     } else {
 #pragma unroll
       for (int i = 0; i < MAXA; ++i) {
@@ -508,11 +535,11 @@ template <bool TR, int KS>
 hipError_t launch_halo(const ApplyGeom& G, const HaloGeom& Hg, dim3 grid, size_t lds, const orth_conv_apply_args* a,
                        hipStream_t s) {
   if (G.kdtype == ORTH_BF16) return launch_halo_k<TR, KS, true, false>(G, Hg, grid, lds, a, s);
-  // 16-byte kernel loads: forward conv, rows of a multiple of four floats,
-  // a 16-byte aligned kernel
-  if constexpr (!TR)
-    if (G.red % 4 == 0 && (reinterpret_cast<uintptr_t>(a->kernel) & 15) == 0)
-      return launch_halo_k<TR, KS, false, true>(G, Hg, grid, lds, a, s);
+  // 16-byte kernel loads: runs of a multiple of four floats, a 16-byte
+  // aligned kernel
+  const int64_t run = TR ? (int64_t)G.c * G.k * G.k : G.red;   // elements between consecutive runs
+  if (run % 4 == 0 && (reinterpret_cast<uintptr_t>(a->kernel) & 15) == 0)
+    return launch_halo_k<TR, KS, false, true>(G, Hg, grid, lds, a, s);
   return launch_halo_k<TR, KS, false, false>(G, Hg, grid, lds, a, s);
 }
 
