@@ -99,6 +99,80 @@ void timing_end(const char* name, hipStream_t s) {
   }
 }
 
+// ------------------------------------------------------- side streams ----
+// Independent parts of one call (the small-matrix kernels beside the tiled
+// path) run on side streams.  They fork from the caller's stream once the
+// call's tables are uploaded (an event recorded there, waited on by each
+// side stream) and join back (an event per side stream, waited on by the
+// caller's stream) before anything that reads their results, so the
+// caller sees one stream.  Side streams have the default priority.  Every
+// host thread keeps its own per device, so the records and waits of one
+// call are issued in order by one thread; they live until the process ends.
+namespace {
+constexpr int kSides = 2;
+struct SideSet {
+  hipStream_t st[kSides] = {};
+  hipEvent_t fork = nullptr;
+  hipEvent_t join[kSides] = {};
+};
+
+hipError_t side_set(SideSet** out) {
+  thread_local std::map<int, SideSet> sets;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  SideSet& S = sets[dev];
+  if (!S.fork) {
+    SideSet n;
+    for (int i = 0; i < kSides && e == hipSuccess; ++i) e = hipStreamCreateWithFlags(&n.st[i], hipStreamNonBlocking);
+    for (int i = 0; i < kSides && e == hipSuccess; ++i)
+      e = hipEventCreateWithFlags(&n.join[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&n.fork, hipEventDisableTiming);
+    if (e != hipSuccess) return e;
+    S = n;
+  }
+  *out = &S;
+  return hipSuccess;
+}
+
+// The fork and join of one call.  side(i) is the caller's stream until
+// fork() has succeeded; a fork that an error path leaves open is joined by
+// the destructor, so no side work outlives the caller's view of the call.
+class Fork {
+ public:
+  explicit Fork(hipStream_t s) : s_(s) {}
+  Fork(const Fork&) = delete;
+  Fork& operator=(const Fork&) = delete;
+  ~Fork() {
+    if (forked_) (void)join();
+  }
+  hipError_t fork() {
+    hipError_t e = side_set(&S_);
+    if (e == hipSuccess) e = hipEventRecord(S_->fork, s_);
+    for (int i = 0; i < kSides && e == hipSuccess; ++i) e = hipStreamWaitEvent(S_->st[i], S_->fork, 0);
+    forked_ = e == hipSuccess;
+    return e;
+  }
+  hipStream_t side(int i) const { return forked_ ? S_->st[i] : s_; }
+  hipError_t join() {
+    if (!forked_) return hipSuccess;
+    forked_ = false;
+    hipError_t first = hipSuccess;
+    for (int i = 0; i < kSides; ++i) {
+      hipError_t e = hipEventRecord(S_->join[i], S_->st[i]);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s_, S_->join[i], 0);
+      if (first == hipSuccess) first = e;
+    }
+    return first;
+  }
+
+ private:
+  hipStream_t s_;
+  SideSet* S_ = nullptr;
+  bool forked_ = false;
+};
+}  // namespace
+
 // ------------------------------------------------- descriptor staging ----
 // Descriptor tables are built on the host and copied into the caller's
 // workspace (the regions that each call's layout reserves for them).  The copy source is a pinned staging buffer from a
@@ -1764,6 +1838,16 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   const int nt = (int)P.tiled.size();
   const bool bf16 = opts->compute == ORTH_COMPUTE_BF16;
   const int iters = opts->iters;
+  // the small-matrix kernels (one size class per side stream) run beside
+  // the tiled path, which leaves most compute units idle between its
+  // launches on small batches
+  Fork fk(s);
+  if (nt > 0 && (!P.small[0].empty() || !P.small[1].empty())) ORTH_HIP(fk.fork());
+  for (int b = 0; b < 2; ++b)
+    ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
+                                 b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale,
+                                 opts->prescale == ORTH_PRESCALE_SPECTRAL ? opts->power_iters : 0, opts->in_dtype,
+                                 opts->out_dtype, status, fk.side(b)));
   if (nt > 0) {
     double* partials = reinterpret_cast<double*>(ws + P.off_partials);
     ORTH_HIP(launch_prescale_partial(tm, T(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
@@ -1797,11 +1881,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
     ORTH_HIP(launch_writeout(tm, T(P.off_writeout_items), (int)P.writeout_items.size(), bf16 ? 0 : (iters & 1),
                              opts->out_dtype, s));
   }
-  for (int b = 0; b < 2; ++b)
-    ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
-                                 b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale,
-                                 opts->prescale == ORTH_PRESCALE_SPECTRAL ? opts->power_iters : 0, opts->in_dtype,
-                                 opts->out_dtype, status, s));
+  ORTH_HIP(fk.join());
   return ORTH_OK;
 }
 
@@ -1925,12 +2005,16 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   }
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
+  // small matrices on side streams beside the tiled forward
+  Fork fk(s);
+  if (!P.partial_items.empty() && (!small[0].empty() || !small[1].empty())) ORTH_HIP(fk.fork());
   for (int k = 0; k < 2; ++k)
     ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[k]), (int)small[k].size(),
                                  k ? 64 : 32, P.small_max_mp[k], opts->iters, opts->beta, opts->prescale, 0,
-                                 opts->in_dtype, opts->out_dtype, status, s));
+                                 opts->in_dtype, opts->out_dtype, status, fk.side(k)));
   rc = vjp_forward(P, ws, opts, n, status, true, s);
   if (rc) return rc;
+  ORTH_HIP(fk.join());
   if (status_dev) ORTH_HIP(hipMemcpyAsync(status_dev, status, sizeof(int32_t) * n, hipMemcpyDeviceToDevice, s));
   return ORTH_OK;
 }
@@ -1991,11 +2075,14 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   const int T = opts->iters;
   const float beta = opts->beta;
   double* partials = reinterpret_cast<double*>(ws + P.off_partials);
-  // small matrices: the whole product per workgroup
+  // small matrices: the whole product per workgroup, on side streams
+  // beside the tiled matrices' steps
+  Fork fk(s);
+  if (!P.partial_items.empty() && (!P.small[0].empty() || !P.small[1].empty())) ORTH_HIP(fk.fork());
   for (int k = 0; k < 2; ++k)
     ORTH_HIP(launch_bjorck_small_vjp(reinterpret_cast<const SmallVjpMat*>(ws + P.off_small[k]),
                                      (int)P.small[k].size(), k ? 64 : 32, P.small_max_mp[k], T, beta,
-                                     opts->prescale, opts->in_dtype, opts->out_dtype, status, s));
+                                     opts->prescale, opts->in_dtype, opts->out_dtype, status, fk.side(k)));
   // forward recomputation, saving X_t and E_t (X_T itself is never
   // needed), unless a saving forward left them in the workspace
   if (!opts->saved) {
@@ -2021,6 +2108,7 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   }
   ORTH_HIP(launch_vjp_writeout(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                opts->prescale, status, s));
+  ORTH_HIP(fk.join());
   if (opts->saved && status_dev)
     ORTH_HIP(hipMemcpyAsync(status_dev, status, sizeof(int32_t) * n, hipMemcpyDeviceToDevice, s));
   return ORTH_OK;
