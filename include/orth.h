@@ -20,7 +20,12 @@
  *   input cannot occur; degenerate matrices are reported per matrix (see
  *   orth_orthogonalize_batched).
  * - Work is asynchronous on `stream` (a hipStream_t, NULL = the legacy
- *   default stream).  Nothing synchronizes inside a call.
+ *   default stream).  Nothing synchronizes inside a call.  The Björck
+ *   entry points may run the small matrices of a batch on side streams
+ *   that fork from `stream` and join back into it within the call (event
+ *   record and wait; default priority; per calling thread and device,
+ *   created on first use and kept until the process ends), so the caller
+ *   still sees all of a call's work ordered on `stream`.
  * - bfloat16 is the raw 16-bit pattern (same layout as torch.bfloat16);
  *   conversions to bfloat16 round to nearest, ties to even.
  * - orth_last_error() returns a thread-local message for the last failing

@@ -118,6 +118,59 @@ def test_bf16_mixed_batch(tile):
             assert abs(checks.gram_deviation(got) - checks.gram_deviation(ref)) <= ORTH_BF16, shape
 
 
+def test_concurrent_calls_two_threads():
+    """Two host threads, each on a stream of its own, run mixed batches
+    (small matrices on the library's side streams, tiled ones on the
+    caller's stream) at the same time, three calls each; every result is
+    bit-identical to the same call made alone, which matches the oracle."""
+    import threading
+
+    print("[concurrent] two threads x 3 calls", flush=True)
+    jobs = [(stored(111, SMALL + TILED_F32), "f32", 12),
+            (stored(112, [(256, 128), (384, 200), (1024, 512), (64, 32), (32, 32), (100, 50)], dtype="bf16"),
+             "bf16", 20)]
+    alone = []
+    for st_list, comp, iters in jobs:
+        outs, status = gpu_orthogonalize(st_list, iters, compute=comp)
+        assert np.all(status == 0)
+        alone.append([o.clone() for o in outs])
+    # the fp32 batch made alone against the oracle
+    for s, o in zip(oracle_inputs(jobs[0][0]), alone[0]):
+        assert checks.relative_difference(to_f64(o), bjorck.bjorck(s, 12)) <= REL_F32
+    ins = [[to_dev(s) for s in st_list] for st_list, _, _ in jobs]
+    results = [[None] * 3 for _ in jobs]
+    errors = []
+    torch.cuda.synchronize()
+
+    def run(j):
+        try:
+            stream = torch.cuda.Stream()
+            _, comp, iters = jobs[j]
+            with torch.cuda.stream(stream):
+                for rep in range(3):
+                    outs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in ins[j]]
+                    status = torch.full((len(outs),), -1, dtype=torch.int32, device=DEV)
+                    orth.orth_orthogonalize_batched(ins[j], outs, iters, compute=comp, status=status)
+                    results[j][rep] = (outs, status)
+            stream.synchronize()
+        except Exception as e:  # re-raised by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=run, args=(j,)) for j in range(len(jobs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for j in range(len(jobs)):
+        for rep in range(3):
+            outs, status = results[j][rep]
+            assert np.all(status.cpu().numpy() == 0), (j, rep)
+            for a, b in zip(alone[j], outs):
+                assert torch.equal(a, b), (j, rep, tuple(a.shape))
+
+
 @pytest.mark.parametrize("tile", [0, 256])
 def test_bf16_converged_all(tile):
     shapes = [(256, 256), (1024, 1024), (512, 256)]
