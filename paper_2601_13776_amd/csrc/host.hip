@@ -116,18 +116,28 @@ struct SideSet {
   hipEvent_t join[kSides] = {};
 };
 
-hipError_t side_set(SideSet** out) {
+// The side set of the device that runs the caller's stream `s` (created
+// with that device current, which is restored afterwards).
+hipError_t side_set(hipStream_t s, SideSet** out) {
   thread_local std::map<int, SideSet> sets;
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  hipDevice_t dev = 0;
+  hipError_t e = hipStreamGetDevice(s, &dev);
   if (e != hipSuccess) return e;
   SideSet& S = sets[dev];
   if (!S.fork) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    if (e != hipSuccess) return e;
     SideSet n;
     for (int i = 0; i < kSides && e == hipSuccess; ++i) e = hipStreamCreateWithFlags(&n.st[i], hipStreamNonBlocking);
     for (int i = 0; i < kSides && e == hipSuccess; ++i)
       e = hipEventCreateWithFlags(&n.join[i], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&n.fork, hipEventDisableTiming);
+    if (cur != dev) {
+      const hipError_t r = hipSetDevice(cur);
+      if (e == hipSuccess) e = r;
+    }
     if (e != hipSuccess) return e;
     S = n;
   }
@@ -147,7 +157,7 @@ class Fork {
     if (forked_) (void)join();
   }
   hipError_t fork() {
-    hipError_t e = side_set(&S_);
+    hipError_t e = side_set(s_, &S_);
     if (e == hipSuccess) e = hipEventRecord(S_->fork, s_);
     for (int i = 0; i < kSides && e == hipSuccess; ++i) e = hipStreamWaitEvent(S_->st[i], S_->fork, 0);
     forked_ = e == hipSuccess;
