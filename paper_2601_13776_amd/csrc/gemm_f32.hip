@@ -242,7 +242,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     if (lane == 0) atomicMax(reinterpret_cast<unsigned int*>(g->red), __float_as_uint(m));
     return;
   }
-  if (j >= N) return;
+  // update tiles stage their transposed copy through LDS with every lane
+  if (j >= N && epi != EPI_UPDATE) return;
   float* C = static_cast<float*>(g->C) + g->c_step * st;
   const int64_t ldc = g->ldc;
   if (epi == EPI_STORE) {
@@ -290,13 +291,40 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     float* dst2 = g->dst2 ? g->dst2 + g->d2_step * st : nullptr;
     const int64_t lds_ = g->ld_src, ld2 = g->ld2;
     const float beta = g->beta;
+    float v[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = ibase + acc_row(r, lane);
-      if (i < M) {
-        const float v = src[(int64_t)i * lds_ + j] + beta * acc[r];
-        C[(int64_t)i * ldc + j] = v;
-        if (dst2) dst2[(int64_t)j * ld2 + i] = v;
+      v[r] = 0.f;
+      if (i < M && j < N) {
+        v[r] = src[(int64_t)i * lds_ + j] + beta * acc[r];
+        C[(int64_t)i * ldc + j] = v[r];
+      }
+    }
+    if (dst2) {
+      // the wave's 32 x 32 block transposed through LDS (its own 32 x 33
+      // region of As, free after the last k-step's barrier), so that every
+      // row of the copy is written as 16-byte pieces
+      float* Tt = &As[0][0] + wave * (32 * 33);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Tt[(lane & 31) * 33 + acc_row(r, lane)] = v[r];
+      __syncthreads();
+      const int jbase = col0 + wn * 32;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = q * 64 + lane;
+        const int jj = e >> 3, c4 = (e & 7) * 4;
+        const int gj = jbase + jj, gi = ibase + c4;
+        if (gj >= N) continue;
+        const float* t = Tt + jj * 33 + c4;
+        float* d = dst2 + (int64_t)gj * ld2 + gi;
+        if (gi + 4 <= M && (reinterpret_cast<uintptr_t>(d) & 15) == 0) {
+          *reinterpret_cast<float4*>(d) = make_float4(t[0], t[1], t[2], t[3]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (gi + k < M) d[k] = t[k];
+        }
       }
     }
   }
