@@ -475,7 +475,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=wl.WORKLOAD_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--prescale", default="frobenius", choices=["frobenius", "spectral"],
@@ -572,7 +572,10 @@ def main():
     tiled = [n for n in names if n.startswith("bjorck_bf16") or n in ("bjorck_gram_f32", "bjorck_update_f32")]
     roof = None
     if tiled:
-        dom = max(tiled, key=lambda n: ktimes[n][0])
+        # the fp32 path times its Gram and update launches separately, with
+        # equal flops and times within a few percent of each other: report
+        # the update launches, which carry the iterate's HBM traffic
+        dom = "bjorck_update_f32" if "bjorck_update_f32" in tiled else max(tiled, key=lambda n: ktimes[n][0])
         tot_ms, launches = ktimes[dom]
         if dom.startswith("bjorck_bf16"):
             flops = class_flops(w, dom) * args.steps
