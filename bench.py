@@ -137,6 +137,32 @@ def class_flops(w, kernel_name):
     return out
 
 
+def executed_flops(w, kernel_name, iters=None):
+    """Flops the MFMA pipes execute in the named tiled Björck kernel per
+    parametrization step: a Gram launch computes only the upper tiles of the
+    symmetric E = I - X^T X (tn (tn + 1) / 2 tiles of B x B over Mp), an
+    update launch every tile of X E (tm tn tiles over Np), both on the tile
+    grid the planner pads to.  The algorithmic count (class_flops) charges
+    the dense 2 m n^2 for the Gram instead."""
+    T = w.iters if iters is None else iters
+    shapes = [(max(r, c), min(r, c)) for r, c in w.matrix_shapes()]
+    big = sum(-(-m // 256) * -(-n // 256) for m, n in shapes if n >= 1024) >= 4 * 256
+    out = 0
+    for m, n in shapes:
+        if n <= 64 and m <= 128:
+            continue
+        if w.dtype == "bf16":
+            cls = 256 if n >= 1024 and big else 128
+            if not kernel_name.endswith(str(cls)):
+                continue
+        else:
+            cls = 64
+        mp, np_ = -(-m // cls) * cls, -(-n // cls) * cls
+        tm, tn = mp // cls, np_ // cls
+        out += T * (tn * (tn + 1) // 2 * 2 * cls * cls * mp + tm * tn * 2 * cls * cls * np_)
+    return out
+
+
 def vjp_flops(w):
     """Algorithmic flops of one vector-Jacobian product of the whole
     workload: the forward recomputation (a Gram and an update product per
@@ -305,12 +331,9 @@ def vjp_cpu_baseline(w, budget_s=25.0):
     ref_f = ref_s[0] * ref_s[1] * min(ref_s)
     total = sum(per_shape.get(s, per_shape[ref_s] * s[0] * s[1] * min(s) / ref_f) * len(idx)
                 for s, idx in by_shape.items())
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
-    return {"value": w.n_layers / total, "unit": "layers/s", "cores": threads, "kind": "oracle",
+    cores, model, blas = host_info()
+    return {"value": w.n_layers / total, "unit": "layers/s", "cores": cores, "kind": "oracle",
+            "cpu_model": model, "blas": blas,
             "sample": f"float64 numpy oracle VJP (Björck only), timed {'+'.join(desc)} at T={t_s} and scaled to "
                       f"T={w.iters} by (10T-2) and by matrix count (estimated full backward {total:.1f} s)",
             "est_step_s": total}
@@ -428,47 +451,89 @@ def run_expo(w, ins, steps, torch, orth, dev, terms=12, conv_terms=6):
     return out or None
 
 
-def cpu_baseline(w, budget_s=25.0):
-    """Time the float64 oracle on a bounded sample of the workload and scale
-    to the whole workload."""
-    from oracle import bjorck
+def host_info():
+    """Cores this process may run on, the CPU model and the BLAS library
+    (name, version, threads) that NumPy calls."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = {}
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = {"library": i.get("internal_api"), "version": i.get("version"),
+                        "threads": i.get("num_threads"), "file": os.path.basename(i.get("filepath", ""))}
+                break
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        pass
+    return len(os.sched_getaffinity(0)), model, blas
+
+
+def cpu_sample(w):
+    """The matrices the CPU legs time, per shape: for the stress batch two
+    of the 64 4096^2 matrices (0 and 63) and all 4096 32^2 ones; otherwise
+    every matrix of shapes up to 1024 x 1024 and two of each larger shape."""
     shapes = w.matrix_shapes()
-    # group matrices by shape; time one matrix of each big shape and a batch of
-    # each small shape, until the time budget is used
     by_shape = {}
-    for i, s in enumerate(shapes):
-        by_shape.setdefault(s, []).append(i)
-    per_shape = {}
-    t_start = time.perf_counter()
-    sample_desc = []
-    for s, idx in sorted(by_shape.items(), key=lambda kv: kv[0][0] * kv[0][1]):
-        n_take = 1 if s[0] * s[1] >= 512 * 512 else min(len(idx), 64)
+    for i, s_ in enumerate(shapes):
+        by_shape.setdefault(s_, []).append(i)
+    take = {}
+    for s_, idx in by_shape.items():
+        take[s_] = idx if s_[0] * s_[1] <= 1024 * 1024 else [idx[0], idx[-1]] if len(idx) > 1 else idx
+    return by_shape, take
+
+
+def plain_f32_bjorck(w32, iters, beta=0.5):
+    """The Björck step (App. A.5) in plain NumPy float32 (BLAS sgemm),
+    Frobenius pre-scaling, smaller Gram: the 'plain CPU fp32' baseline."""
+    x = w32 if w32.shape[0] >= w32.shape[1] else w32.T
+    x = x / np.float32(np.sqrt(np.sum(x * x, dtype=np.float64)))
+    b = np.float32(beta)
+    for _ in range(iters):
+        x = (1 + b) * x - b * (x @ (x.T @ x))
+    return x if w32.shape[0] >= w32.shape[1] else x.T
+
+
+def cpu_baseline(w):
+    """Time the float64 oracle (and a plain float32 NumPy run of the same
+    formula) on a bounded sample of the workload, scaled by matrix count to
+    the whole Björck step (labelled extrapolated when a shape was sampled)."""
+    from oracle import bjorck
+    cores, model, blas = host_info()
+    by_shape, take = cpu_sample(w)
+    per64, per32, desc = {}, {}, []
+    extrapolated = False
+    for s_, idx in sorted(by_shape.items(), key=lambda kv: kv[0][0] * kv[0][1]):
+        sel = take[s_]
+        mats = [wl.as_f64(wl.stored_matrix(w, i, *s_)) for i in sel]
         t0 = time.perf_counter()
-        for i in idx[:n_take]:
-            bjorck.bjorck(wl.as_f64(wl.stored_matrix(w, i, *s)), w.iters)
-        dt = (time.perf_counter() - t0) / n_take
-        per_shape[s] = dt
-        sample_desc.append(f"{n_take}x{s[0]}x{s[1]}")
-        if time.perf_counter() - t_start > budget_s:
-            break
-    # shapes not sampled (budget exhausted): scale by flops from the largest sampled shape
-    ref_s = max(per_shape, key=lambda s: s[0] * s[1] * min(s))
-    ref_f = ref_s[0] * ref_s[1] * min(ref_s)
-    total = 0.0
-    for s, idx in by_shape.items():
-        t = per_shape.get(s, per_shape[ref_s] * s[0] * s[1] * min(s) / ref_f)
-        total += t * len(idx)
-    value = w.n_layers / total
-    return {"value": value, "unit": "layers/s", "cores": threads, "kind": "oracle",
-            "sample": f"float64 numpy oracle, T={w.iters}, timed {'+'.join(sample_desc)} and scaled by matrix "
-                      f"count to all {len(shapes)} matrices (estimated full-step {total:.1f} s; "
-                      f"{platform.processor() or platform.machine()})",
-            "est_step_s": total}
+        for m in mats:
+            bjorck.bjorck(m, w.iters)
+        per64[s_] = (time.perf_counter() - t0) / len(sel)
+        m32 = [m.astype(np.float32) for m in mats]
+        t0 = time.perf_counter()
+        for m in m32:
+            plain_f32_bjorck(m, w.iters)
+        per32[s_] = (time.perf_counter() - t0) / len(sel)
+        desc.append(f"{len(sel)}/{len(idx)}x{s_[0]}x{s_[1]}")
+        extrapolated |= len(sel) < len(idx)
+    tot64 = sum(per64[s_] * len(idx) for s_, idx in by_shape.items())
+    tot32 = sum(per32[s_] * len(idx) for s_, idx in by_shape.items())
+    label = "extrapolated by matrix count" if extrapolated else "every matrix timed"
+    return {"value": w.n_layers / tot64, "unit": "layers/s", "cores": cores, "kind": "oracle",
+            "sample": f"float64 NumPy oracle, Björck T={w.iters} with Frobenius pre-scaling of the workload's "
+                      f"matrices: timed {'+'.join(desc)} (timed/total x shape), {label} to the whole "
+                      f"{len(w.matrix_shapes())}-matrix step ({tot64:.1f} s)",
+            "est_step_s": round(tot64, 3), "cpu_model": model, "blas": blas,
+            "plain_cpu_fp32": {"value": w.n_layers / tot32, "unit": "layers/s", "est_step_s": round(tot32, 3),
+                               "kind": "plain NumPy float32 (BLAS sgemm), same formula and sample"}}
 
 
 def main():
@@ -565,6 +630,12 @@ def main():
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     bjorck_tflops = bjorck_flops / (t_bjorck_ms / 1e3) / 1e12 if t_bjorck_ms > 0 else None
     step_tflops = bjorck_flops / (ms_per_step / 1e3) / 1e12
+    # executed flops of the tiled launches (upper-triangle Gram tiles) plus
+    # the small matrices' dense count
+    small_flops = wl.algorithmic_bjorck_flops([s_ for s_ in shapes if min(s_) <= 64 and max(s_) <= 128], w.iters)
+    tiled_exec = sum(executed_flops(w, n) for n in ("bjorck_bf16_128", "bjorck_bf16_256")) if w.dtype == "bf16" \
+        else executed_flops(w, "")
+    bjorck_exec_tflops = (tiled_exec + small_flops) / (t_bjorck_ms / 1e3) / 1e12 if t_bjorck_ms > 0 else None
 
     # roofline of the dominant kernel: algorithmic flops of its launches in
     # the timed region over its measured time (= per-launch average / average
@@ -586,6 +657,15 @@ def main():
                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom, w.name),
                 "avg_launch_ms": round(tot_ms / launches, 4),
                 "algorithmic_flops_per_launch": int(flops / launches)}
+        if dom.startswith("bjorck_bf16"):
+            # what the MFMA pipes execute: the Gram launches skip the lower
+            # tiles of the symmetric E, so the executed rate is below the
+            # algorithmic one
+            ex = executed_flops(w, dom) * args.steps
+            ex_ach = ex / (tot_ms / 1e3) / 1e12
+            roof["executed"] = {"achieved": round(ex_ach, 1), "frac": round(ex_ach / peak, 4),
+                                "flops_per_launch": int(ex / launches),
+                                "note": "upper-triangle Gram tiles plus full update tiles, padded tile grid"}
 
     power = None
     if args.prescale == "spectral" and "power_dot" in ktimes:
@@ -641,6 +721,9 @@ def main():
                    "prescale": args.prescale},
         "bjorck_tflops_algorithmic": round(bjorck_tflops, 1) if bjorck_tflops else None,
         "bjorck_pct_peak": round(100 * bjorck_tflops / peak, 2) if bjorck_tflops else None,
+        "bjorck_tflops_executed": round(bjorck_exec_tflops, 1) if bjorck_exec_tflops else None,
+        "bjorck_pct_peak_executed": round(100 * bjorck_exec_tflops / peak, 2) if bjorck_exec_tflops else None,
+        "t_bjorck_ms": round(t_bjorck_ms, 3),
         "step_tflops_algorithmic": round(step_tflops, 1),
         "kernel_ms_per_step": {n: round(ktimes[n][0] / args.steps, 4) for n in names},
         "roofline": roof, "cpu_baseline": cpu,

@@ -20,7 +20,15 @@
  *   input cannot occur; degenerate matrices are reported per matrix (see
  *   orth_orthogonalize_batched).
  * - Work is asynchronous on `stream` (a hipStream_t, NULL = the legacy
- *   default stream).  Nothing synchronizes inside a call.  The Björck
+ *   default stream).  A call's descriptor tables are copied into its
+ *   workspace (hipMemcpyAsync on `stream`) from pinned host staging
+ *   buffers that the library keeps for the life of the process: a buffer
+ *   is reused only once its last copy has completed, and a new one is
+ *   allocated (pinned host memory, never device memory) when none is
+ *   idle.  The host blocks in one case only: when 64 calls' copies are
+ *   still in flight, a call waits for the oldest of them.  Because the
+ *   staging buffers are reused, a call's copies must not be captured into
+ *   a HIP graph that is replayed after later calls.  The Björck
  *   entry points may run the small matrices of a batch on side streams
  *   that fork from `stream` and join back into it within the call (event
  *   record and wait; default priority; per calling thread and device,

@@ -15,7 +15,7 @@ same matrix; the grouping only changes rounding.
 
 Pins (tests/test_oracle_pins.py): P1 closed form through the SVD, P2
 convergence, P3 orthogonal input, P4 scale invariance, and a hand-derived
-golden value (tests/golden/bjorck_diag2.json).
+golden value (tests/golden/bjorck_hand.json).
 """
 
 import numpy as np
@@ -73,15 +73,6 @@ def bjorck(w, iters, beta=0.5, prescale="frobenius", return_status=False):
     if return_status:
         return w, status
     return w
-
-
-def scalar_map_iterate(x, iters, beta=0.5):
-    """f^iters(x) for the scalar map f(x) = (1+beta) x - beta x^3 that the
-    matrix iteration applies to every singular value independently."""
-    x = np.asarray(x, dtype=np.float64)
-    for _ in range(iters):
-        x = (1.0 + beta) * x - beta * x ** 3
-    return x
 
 
 def iterations_to_converge(w, tol=1e-5, beta=0.5, max_iters=200):

@@ -39,3 +39,23 @@ def conv_adjoint_norm_ratios(kernel, y, in_hw, stride=1, dilation=1, groups=1):
     num = np.sqrt(np.sum(x.reshape(n, -1) ** 2, axis=1))
     den = np.sqrt(np.sum(np.asarray(y, dtype=np.float64).reshape(n, -1) ** 2, axis=1))
     return num / den
+
+
+def tile_relative_differences(a, b, tile=256):
+    """||a_T - b_T||_F / ||b_T||_F for every tile x tile block T of the
+    matrices (ragged blocks at the right and bottom edges included; a block
+    whose reference is all zero reports ||a_T||_F).  Returned as a
+    (row blocks, column blocks) array, so that an error confined to a few
+    blocks stands out against the whole-matrix relative difference."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    if a.shape != b.shape:
+        raise ValueError("shapes differ")
+    rows, cols = b.shape
+    nr, nc = -(-rows // tile), -(-cols // tile)
+    out = np.zeros((nr, nc))
+    for i in range(nr):
+        for j in range(nc):
+            out[i, j] = relative_difference(a[i * tile:(i + 1) * tile, j * tile:(j + 1) * tile],
+                                            b[i * tile:(i + 1) * tile, j * tile:(j + 1) * tile])
+    return out

@@ -4,6 +4,8 @@
 // enqueues anything; the library allocates no device memory.
 #include <algorithm>
 #include <climits>
+#include <cstdarg>
+#include <cstdlib>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -29,6 +31,36 @@ static int fail(int code, const std::string& msg) {
     hipError_t e_ = (call);                                                             \
     if (e_ != hipSuccess) return fail(ORTH_EHIP, std::string(#call) + ": " + hipGetErrorString(e_)); \
   } while (0)
+
+// ------------------------------------------------------ diagnostics ----
+// Two environment switches, read once per process:
+//   ORTH_LOG=1        every entry point prints its plan to stderr (matrices
+//                     per bucket, work-table sizes, workspace layout);
+//   ORTH_LOG=2        also every kernel launch (name and stream);
+//   ORTH_DEBUG_SYNC=1 every kernel launch is followed by a synchronization
+//                     of its stream, and a failing launch or kernel is
+//                     printed with its name (the call still returns the
+//                     error at its next HIP check).
+static int env_level(const char* name) {
+  const char* v = std::getenv(name);
+  return v && *v ? std::atoi(v) : 0;
+}
+int log_level() {
+  static const int lvl = env_level("ORTH_LOG");
+  return lvl;
+}
+static bool debug_sync() {
+  static const bool on = env_level("ORTH_DEBUG_SYNC") > 0;
+  return on;
+}
+void log_line(const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  std::fprintf(stderr, "[orth] %s\n", buf);
+}
 
 // ------------------------------------------------------------ timing ----
 namespace {
@@ -73,6 +105,7 @@ int drain_timing_locked() {
 }  // namespace
 
 void timing_begin(const char* name, hipStream_t s) {
+  if (log_level() >= 2) log_line("launch %s on stream %p", name, (void*)s);
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   TimingRec r{name, pool_event(), nullptr};
@@ -85,6 +118,14 @@ void timing_begin(const char* name, hipStream_t s) {
 }
 
 void timing_end(const char* name, hipStream_t s) {
+  if (debug_sync()) {
+    hipError_t e = hipPeekAtLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess)
+      log_line("ORTH_DEBUG_SYNC: %s failed: %s", name, hipGetErrorString(e));
+    else if (log_level() >= 2)
+      log_line("ORTH_DEBUG_SYNC: %s done", name);
+  }
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   for (auto it = g_pending.rbegin(); it != g_pending.rend(); ++it) {
@@ -185,17 +226,29 @@ class Fork {
 
 // ------------------------------------------------- descriptor staging ----
 // Descriptor tables are built on the host and copied into the caller's
-// workspace (the regions that each call's layout reserves for them).  The copy source is a pinned staging buffer from a
-// small ring; an event recorded after each copy guards reuse of the buffer.
+// workspace (the regions that each call's layout reserves for them).  The
+// copy source is a pinned staging buffer from a process-wide pool.  A
+// buffer is taken only when the copy that last read it has completed
+// (hipEventQuery, which does not block); when no idle buffer is large
+// enough a new one is allocated (pinned host memory).  Buffers are never
+// freed while the pool is below kStageMax buffers, so a call neither
+// frees memory nor waits.  With kStageMax copies still in flight (that
+// many calls enqueued ahead of the device), a call waits for the oldest
+// one (and replaces its buffer if it is too small): the one point where
+// the host blocks, documented at the boundary.
 namespace {
 struct StageSlot {
   void* buf = nullptr;
   size_t cap = 0;
   hipEvent_t done = nullptr;
+  uint64_t seq = 0;          // order of last use (oldest = smallest)
 };
+constexpr size_t kStageMax = 64;
 std::mutex g_smu;
-StageSlot g_stage[4];
-int g_stage_next = 0;
+std::vector<StageSlot> g_stage;
+uint64_t g_stage_seq = 0;
+
+bool slot_idle(const StageSlot& sl) { return !sl.done || hipEventQuery(sl.done) == hipSuccess; }
 }  // namespace
 
 // Host image of a call's tables: the spans that put() fills (workspace
@@ -231,27 +284,48 @@ struct TableImage {
 static int upload_tables(const TableImage& img, void* dst, hipStream_t s) {
   if (img.data.empty()) return ORTH_OK;
   std::lock_guard<std::mutex> lk(g_smu);
-  StageSlot& sl = g_stage[g_stage_next];
-  g_stage_next = (g_stage_next + 1) % 4;
-  if (sl.done) ORTH_HIP(hipEventSynchronize(sl.done));
   const size_t total = img.data.size();
-  if (sl.cap < total) {
-    if (sl.buf) ORTH_HIP(hipHostFree(sl.buf));
-    sl.buf = nullptr;
+  // the smallest idle buffer that fits
+  StageSlot* sl = nullptr;
+  for (auto& c : g_stage)
+    if (c.cap >= total && (!sl || c.cap < sl->cap) && slot_idle(c)) sl = &c;
+  if (!sl) {
     size_t cap = std::max<size_t>(total, 1 << 16);
     cap = (cap + 4095) & ~size_t(4095);
-    ORTH_HIP(hipHostMalloc(&sl.buf, cap, hipHostMallocDefault));
-    sl.cap = cap;
+    if (g_stage.size() < kStageMax) {
+      StageSlot n;
+      ORTH_HIP(hipHostMalloc(&n.buf, cap, hipHostMallocDefault));
+      n.cap = cap;
+      const hipError_t e = hipEventCreateWithFlags(&n.done, hipEventDisableTiming);
+      if (e != hipSuccess) {
+        (void)hipHostFree(n.buf);
+        return fail(ORTH_EHIP, std::string("hipEventCreateWithFlags: ") + hipGetErrorString(e));
+      }
+      g_stage.push_back(n);
+      sl = &g_stage.back();
+    } else {
+      // every buffer is in flight: wait for the oldest copy
+      sl = &*std::min_element(g_stage.begin(), g_stage.end(),
+                              [](const StageSlot& a, const StageSlot& b) { return a.seq < b.seq; });
+      ORTH_HIP(hipEventSynchronize(sl->done));
+      if (sl->cap < total) {
+        ORTH_HIP(hipHostFree(sl->buf));
+        sl->buf = nullptr;
+        sl->cap = 0;
+        ORTH_HIP(hipHostMalloc(&sl->buf, cap, hipHostMallocDefault));
+        sl->cap = cap;
+      }
+    }
   }
-  if (!sl.done) ORTH_HIP(hipEventCreateWithFlags(&sl.done, hipEventDisableTiming));
-  std::memcpy(sl.buf, img.data.data(), total);
+  sl->seq = ++g_stage_seq;
+  std::memcpy(sl->buf, img.data.data(), total);
   size_t at = 0;
   for (const auto& sp : img.spans) {
-    ORTH_HIP(hipMemcpyAsync(static_cast<unsigned char*>(dst) + sp.first, static_cast<unsigned char*>(sl.buf) + at,
+    ORTH_HIP(hipMemcpyAsync(static_cast<unsigned char*>(dst) + sp.first, static_cast<unsigned char*>(sl->buf) + at,
                             sp.second, hipMemcpyHostToDevice, s));
     at += sp.second;
   }
-  ORTH_HIP(hipEventRecord(sl.done, s));
+  ORTH_HIP(hipEventRecord(sl->done, s));
   return ORTH_OK;
 }
 
@@ -399,6 +473,28 @@ struct OrthoPlan {
   size_t off_partials = 0, off_inv = 0, off_status = 0;
   size_t table_bytes = 0, total_bytes = 0;
 };
+
+// ORTH_LOG plan dump of an orthogonalization call
+void log_ortho_plan(const char* entry, const OrthoPlan& P, const orth_bjorck_opts* o) {
+  if (log_level() < 1) return;
+  int cnt[5] = {0, 0, 0, 0, 0};
+  for (const auto& q : P.mp) ++cnt[q.bucket];
+  log_line("%s: %zu matrices (fused small N<=32: %d, N<=64: %d; tiled fp32: %d; bf16 128-tiles: %d, 256-tiles: %d), "
+           "T=%d beta=%g prescale=%d compute=%s",
+           entry, P.mp.size(), cnt[SMALL32], cnt[SMALL64], cnt[TILED_F32], cnt[TILED_BF16_128], cnt[TILED_BF16_256],
+           o->iters, o->beta, o->prescale, o->compute == ORTH_COMPUTE_BF16 ? "bf16" : "f32");
+  for (int cls = 0; cls < 2; ++cls)
+    if (!P.tabs[cls][TAB_GRAM].empty())
+      log_line("%s: bf16 %d-tiles per step: %zu Gram + %zu update", entry, cls ? 256 : 128,
+               P.tabs[cls][TAB_GRAM].size(), P.tabs[cls][TAB_UPDATE].size());
+  if (P.f32_gram.size())
+    log_line("%s: fp32 64-tiles per step: %zu Gram + %zu update", entry, P.f32_gram.size(), P.f32_update[0].size());
+  log_line("%s: workspace %zu bytes (tables %zu)", entry, P.total_bytes, P.table_bytes);
+  if (log_level() >= 3)
+    for (size_t i = 0; i < P.mp.size(); ++i)
+      log_line("%s:   matrix %zu: %d x %d (tall), padded %d x %d, bucket %d%s", entry, i, P.mp[i].M, P.mp[i].N,
+               P.mp[i].Mp, P.mp[i].Np, P.mp[i].bucket, P.mp[i].transposed ? ", transposed" : "");
+}
 
 int validate_ortho(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o) {
   if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
@@ -1439,6 +1535,15 @@ struct VjpPlan {
   size_t table_bytes = 0, total_bytes = 0;
 };
 
+void log_vjp_plan(const char* entry, const VjpPlan& P, int n) {
+  if (log_level() < 1) return;
+  log_line("%s: %d matrices (fused small: %zu + %zu), bf16 tiles per step: 128 %zu/%zu/%zu/%zu, 256 %zu/%zu/%zu/%zu "
+           "(Gram/update/S/gradient update), fp32 64-tiles %zu/%zu/%zu/%zu; workspace %zu bytes (tables %zu)",
+           entry, n, P.small[0].size(), P.small[1].size(), P.t_gram[0].size(), P.t_upd[0].size(), P.t_s[0][0].size(),
+           P.t_yu[0][0].size(), P.t_gram[1].size(), P.t_upd[1].size(), P.t_s[1][0].size(), P.t_yu[1][0].size(),
+           P.f_gram.size(), P.f_upd.size(), P.b_s[0].size(), P.b_upd[0].size(), P.total_bytes, P.table_bytes);
+}
+
 int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o) {
   if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
   if (n > 0 && !mats) return fail(ORTH_EINVAL, "mats is NULL");
@@ -1823,6 +1928,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = OrthoPlan();
   build_ortho_plan(mats, n, opts, P, ws, true);
+  log_ortho_plan("orth_orthogonalize_batched", P, opts);
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
@@ -1971,6 +2077,7 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = VjpPlan();
   build_vjp_plan(vm.data(), n, opts, P, ws);
+  log_vjp_plan("orth_orthogonalize_save_batched", P, n);
   hipStream_t s = static_cast<hipStream_t>(stream);
   // statuses go to the workspace, where the saved product reads them, and
   // are copied to the caller's array
@@ -2052,6 +2159,7 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = VjpPlan();
   build_vjp_plan(mats, n, opts, P, ws);
+  log_vjp_plan("orth_orthogonalize_vjp_batched", P, n);
   hipStream_t s = static_cast<hipStream_t>(stream);
   // with saved iterates the statuses of the saving forward are in the
   // workspace; the small-matrix kernel refreshes its own
@@ -2159,6 +2267,13 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = ConvPlan();
   build_conv_plan(descs, n, dtype, P, ws);
+  if (log_level() >= 1) {
+    size_t tiles = P.proj_items.size();
+    for (const auto& g : P.phase_gemm) tiles += g.size();
+    log_line("orth_build_conv_kernels_batched: %d layers, %zu groups, %zu block steps, %zu fp32 64-tiles; "
+             "workspace %zu bytes (tables %zu)", n, P.groups.size(), P.phase_gemm.size(), tiles, P.total_bytes,
+             P.table_bytes);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   TableImage img;
@@ -2208,6 +2323,9 @@ int conv_vjp_run(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = ConvVjpPlan();
   build_conv_vjp_plan(descs, n, dtype, P, ws, kernels);
+  if (log_level() >= 1)
+    log_line("composition VJP (mode %d): %d layers, %zu block steps; workspace %zu bytes (tables %zu)", mode, n,
+             P.fwd_gemm.size(), P.total_bytes, P.table_bytes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int n_phase = (int)P.fwd_gemm.size();
 

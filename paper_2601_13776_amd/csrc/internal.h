@@ -265,9 +265,14 @@ struct LaunchCtx {
   hipStream_t stream;
 };
 
-// Timing hooks around every launch (no-ops unless timing is enabled).
+// Hooks around every launch: per-kernel event timing when enabled, the
+// launch trace of ORTH_LOG=2 and the per-launch synchronization of
+// ORTH_DEBUG_SYNC=1.
 void timing_begin(const char* name, hipStream_t s);
 void timing_end(const char* name, hipStream_t s);
+// ORTH_LOG level (0 when unset) and one stderr line prefixed "[orth] ".
+int log_level();
+void log_line(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 
 // Kernel launchers (defined next to their kernels).
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,

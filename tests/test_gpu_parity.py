@@ -12,6 +12,7 @@ Tolerances (stated by the target):
 """
 
 import math
+import os
 
 import numpy as np
 import pytest
@@ -377,9 +378,63 @@ def test_workload_mixed_gds19():
 
 
 def test_workload_cifar_stack12():
+    """Every layer of the CIFAR-like stack (fp32, T = 15; all 54 factors in
+    one call, all 12 kernels in one call) against the oracle's whole chain
+    from the raw parameters: kernels up to 256 channels in full, the
+    512-wide ones on sampled output channels (K = R ⊛ B is linear in R row
+    by row, App. B.1).  Then the same at T_conv: max |G - I| of all 54
+    factors within the fp32 bound, and norm preservation of a circular conv
+    input at every width."""
     w = wl.WORKLOADS["cifar_stack12"]
-    st, outs, kernels = run_workload_layers(w, w.iters)
-    for li, (layer, (a, b)) in enumerate(zip(w.layers, wl.layer_matrix_ranges(w))):
-        if li in (0, 2, 4, 8, 11):
-            ref = oracle_layer(w, layer, st, a, w.iters)
-            assert checks.relative_difference(to_f64(kernels[li]), ref) <= REL_F32, li
+    st_all = oracle_inputs(wl.all_matrices(w))
+    T_conv = t_conv(st_all)
+    for iters in (w.iters, T_conv):
+        print(f"[cifar] T = {iters}", flush=True)
+        st, outs, kernels = run_workload_layers(w, iters)
+        for li, (layer, (a, b)) in enumerate(zip(w.layers, wl.layer_matrix_ranges(w))):
+            fac = [bjorck.bjorck(m, iters) for m in st_all[a:b]]
+            got = to_f64(kernels[li])
+            if layer.cout <= 256:
+                ref = aoc.aoc_kernel(fac[0][None], np.stack(fac[1:])[None], layer.cin, layer.cout, layer.k,
+                                     layer.stride, layer.dilation, layer.groups)
+                rel = checks.relative_difference(got, ref)
+            else:
+                rows = sorted({0, 63, 64, 200, 255, 256, 383, 448, layer.cout - 1})
+                ref = aoc.compose_group(fac[0][rows], fac[1:], layer.c, layer.k, layer.stride)
+                rel = checks.relative_difference(got[rows], ref)
+            assert rel <= REL_F32, (li, iters, rel)
+        if iters == T_conv:
+            for i, o in enumerate(outs):
+                assert checks.gram_deviation(to_f64(o)) <= ORTH_F32, i
+            for li in (0, 2, 3, 4, 8, 11):
+                # stride-2 transitions (cout = 2 cin) map onto fewer output
+                # values: their rows are orthonormal, so the transposed conv
+                # preserves the norm (an input on the output grid)
+                layer = w.layers[li]
+                geom = (layer.cin, layer.cout, layer.k, layer.stride, layer.dilation, layer.groups)
+                adjoint = layer.stride > 1
+                shape = (2, layer.cout, 8, 8) if adjoint else (2, layer.cin, 16, 16)
+                x = wl.check_batch(w, shape)
+                r = orth.orth_check_norm_conv(kernels[li], geom, to_dev(x), adjoint=adjoint).cpu().numpy()
+                assert np.max(np.abs(r - 1)) <= 1e-5, (li, r)
+
+
+def test_diagnostic_switches():
+    """ORTH_LOG=2 prints every call's plan and every launch; ORTH_DEBUG_SYNC=1
+    synchronizes after each launch and reports it done.  Run in a child
+    process (the switches are read once per process)."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import sys, torch; sys.path.insert(0, %r); sys.path.insert(0, %r)\n"
+            "from gpu_util import gpu_orthogonalize\n"
+            "from test_gpu_parity import stored\n"
+            "outs, status = gpu_orthogonalize(stored(5, [(300, 200), (40, 20)]), 3)\n"
+            "assert (status == 0).all()\n" % (root, os.path.join(root, "tests")))
+    env = dict(os.environ, ORTH_LOG="2", ORTH_DEBUG_SYNC="1")
+    p = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
+    assert p.returncode == 0, p.stderr[-2000:]
+    err = p.stderr
+    assert "[orth] orth_orthogonalize_batched: 2 matrices" in err, err[-2000:]
+    assert "[orth] launch bjorck_gram_f32" in err and "[orth] ORTH_DEBUG_SYNC: bjorck_gram_f32 done" in err
+    assert "failed" not in err

@@ -354,3 +354,26 @@ def test_param_shapes():
     assert aoc.param_shapes(64, 128, 3, 2, 1, 1) == (128, 256, 2, 64, 32)
     assert aoc.param_shapes(128, 512, 2, 2, 1, 1) == (512, 512, 0, 128, 64)
     assert aoc.param_shapes(256, 256, 3, 1, 1, 4) == (64, 64, 4, 64, 32)
+
+
+def test_tile_relative_differences_localizes_errors():
+    """The per-tile check used by the bf16 parity tests: one wrong 32 x 32
+    sub-block of a 2000 x 1100 matrix moves the whole-matrix relative
+    difference by about 3% but the difference of its 256-tile by about
+    18%; ragged edge tiles are covered; an exact copy gives zeros."""
+    rng = np.random.default_rng(3)
+    b = rng.standard_normal((2000, 1100))
+    assert np.all(checks.tile_relative_differences(b.copy(), b) == 0)
+    a = b.copy()
+    a[512 + 64:512 + 96, 256 + 32:256 + 64] = rng.standard_normal((32, 32))
+    t = checks.tile_relative_differences(a, b)
+    assert t.shape == (8, 5)
+    assert checks.relative_difference(a, b) < 0.04
+    assert t[2, 1] > 0.15 and np.count_nonzero(t) == 1
+    # the ragged bottom-right tile (208 x 76) is its own block
+    a = b.copy()
+    a[-1, -1] += 1.0
+    t = checks.tile_relative_differences(a, b)
+    assert np.count_nonzero(t) == 1 and t[7, 4] > 0
+    ref = np.linalg.norm(b[1792:, 1024:])
+    assert abs(t[7, 4] - 1.0 / ref) < 1e-12
