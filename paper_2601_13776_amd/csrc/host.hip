@@ -1883,41 +1883,13 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
 }
 }  // namespace
 
-}  // namespace orth
-
-using namespace orth;
-
-// ================================================================== C ABI =
-extern "C" {
-
-const char* orth_status_string(int status) {
-  switch (status) {
-    case ORTH_OK: return "ok";
-    case ORTH_EINVAL: return "invalid argument";
-    case ORTH_EUNSUPPORTED: return "unsupported configuration";
-    case ORTH_EWORKSPACE: return "workspace missing, too small or misaligned";
-    case ORTH_EHIP: return "HIP runtime error";
-    default: return "unknown status";
-  }
-}
-
-const char* orth_last_error(void) { return g_last_error.c_str(); }
-
-int32_t orth_version(void) { return 100; }
-
-int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
-                                      size_t* bytes) {
-  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
-  int rc = validate_ortho(mats, n, opts);
-  if (rc) return rc;
-  OrthoPlan P;
-  build_ortho_plan(mats, n, opts, P, nullptr, true);
-  *bytes = P.total_bytes;
-  return ORTH_OK;
-}
-
-int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
-                               size_t workspace_bytes, int32_t* status_dev, void* stream) {
+// The orthogonalization of one batch, enqueued on `s` into the workspace
+// `workspace` (at least `workspace_bytes`, checked here).  `side_streams`
+// lets the small-matrix kernels run on the calling thread's side streams;
+// `upload` copies the descriptor tables (nullptr: the pinned staging pool).
+int ortho_enqueue(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
+                  size_t workspace_bytes, int32_t* status_dev, hipStream_t s, bool side_streams,
+                  TableUploader upload, const char* entry) {
   int rc = validate_ortho(mats, n, opts);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
@@ -1928,8 +1900,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   P = OrthoPlan();
   build_ortho_plan(mats, n, opts, P, ws, true);
-  log_ortho_plan("orth_orthogonalize_batched", P, opts);
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  log_ortho_plan(entry, P, opts);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
   TableImage img;
@@ -1946,7 +1917,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   put(img, P.off_f32_update[1], P.f32_update[1]);
   put(img, P.off_power[0], P.power[0]);
   put(img, P.off_power[1], P.power[1]);
-  rc = upload_tables(img, ws, s);
+  rc = upload ? upload(img.data.data(), img.spans.data(), img.spans.size(), ws, s) : upload_tables(img, ws, s);
   if (rc) return rc;
 
   auto T = [&](size_t off) { return reinterpret_cast<const TileItem*>(ws + off); };
@@ -1958,7 +1929,7 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   // the tiled path, which leaves most compute units idle between its
   // launches on small batches
   Fork fk(s);
-  if (nt > 0 && (!P.small[0].empty() || !P.small[1].empty())) ORTH_HIP(fk.fork());
+  if (side_streams && nt > 0 && (!P.small[0].empty() || !P.small[1].empty())) ORTH_HIP(fk.fork());
   for (int b = 0; b < 2; ++b)
     ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[b]), (int)P.small[b].size(),
                                  b ? 64 : 32, P.max_mp[b], iters, opts->beta, opts->prescale,
@@ -1999,6 +1970,45 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorc
   }
   ORTH_HIP(fk.join());
   return ORTH_OK;
+}
+
+}  // namespace orth
+
+using namespace orth;
+
+// ================================================================== C ABI =
+extern "C" {
+
+const char* orth_status_string(int status) {
+  switch (status) {
+    case ORTH_OK: return "ok";
+    case ORTH_EINVAL: return "invalid argument";
+    case ORTH_EUNSUPPORTED: return "unsupported configuration";
+    case ORTH_EWORKSPACE: return "workspace missing, too small or misaligned";
+    case ORTH_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* orth_last_error(void) { return g_last_error.c_str(); }
+
+int32_t orth_version(void) { return 100; }
+
+int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
+                                      size_t* bytes) {
+  if (!bytes) return fail(ORTH_EINVAL, "bytes is NULL");
+  int rc = validate_ortho(mats, n, opts);
+  if (rc) return rc;
+  OrthoPlan P;
+  build_ortho_plan(mats, n, opts, P, nullptr, true);
+  *bytes = P.total_bytes;
+  return ORTH_OK;
+}
+
+int orth_orthogonalize_batched(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
+                               size_t workspace_bytes, int32_t* status_dev, void* stream) {
+  return ortho_enqueue(mats, n, opts, workspace, workspace_bytes, status_dev, static_cast<hipStream_t>(stream), true,
+                       nullptr, "orth_orthogonalize_batched");
 }
 
 namespace {

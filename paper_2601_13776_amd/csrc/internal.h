@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "../../include/orth.h"
 
 namespace orth {
@@ -273,6 +275,19 @@ void timing_end(const char* name, hipStream_t s);
 // ORTH_LOG level (0 when unset) and one stderr line prefixed "[orth] ".
 int log_level();
 void log_line(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+
+// Copies a call's descriptor tables into its workspace `dst` on stream s:
+// n_spans spans (workspace offset, bytes) whose bytes lie back to back in
+// `data`.  Returns an orth_status.
+typedef int (*TableUploader)(const unsigned char* data, const std::pair<size_t, size_t>* spans, size_t n_spans,
+                             void* dst, hipStream_t s);
+// The orthogonalization of one batch (validation, planning, table upload
+// and every launch) on stream s into `workspace`; side_streams lets the
+// small-matrix kernels run on the calling thread's side streams; upload
+// nullptr copies the tables from the library's pinned staging pool.
+int ortho_enqueue(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts, void* workspace,
+                  size_t workspace_bytes, int32_t* status_dev, hipStream_t s, bool side_streams,
+                  TableUploader upload, const char* entry);
 
 // Kernel launchers (defined next to their kernels).
 hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, int iters, float beta,
