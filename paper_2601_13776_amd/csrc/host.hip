@@ -26,6 +26,7 @@ static int fail(int code, const std::string& msg) {
   g_last_error = msg;
   return code;
 }
+int report_error(int code, const char* msg) { return fail(code, msg); }
 #define ORTH_HIP(call)                                                                  \
   do {                                                                                  \
     hipError_t e_ = (call);                                                             \

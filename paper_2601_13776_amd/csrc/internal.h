@@ -272,6 +272,8 @@ struct LaunchCtx {
 // ORTH_DEBUG_SYNC=1.
 void timing_begin(const char* name, hipStream_t s);
 void timing_end(const char* name, hipStream_t s);
+// Sets the calling thread's last-error message and returns `code`.
+int report_error(int code, const char* msg);
 // ORTH_LOG level (0 when unset) and one stderr line prefixed "[orth] ".
 int log_level();
 void log_line(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
