@@ -144,6 +144,31 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n,
                                size_t workspace_bytes, int32_t* status_dev,
                                void* stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same
+ * orthogonalization as orth_orthogonalize_batched, same arguments and
+ * results, with the library's own device scratch in place of the
+ * workspace.  The scratch is a fixed array of ORTH_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) that each GPU the library runs on holds until the process ends.
+ * A batch whose orth_orthogonalize_workspace_size exceeds it fails with
+ * ORTH_EWORKSPACE before anything is enqueued.  The call allocates
+ * nothing: no device memory, no pinned staging (the descriptor tables are
+ * copied from pageable host memory, which HIP may perform synchronously,
+ * so the host can wait for earlier work on `stream`), no side streams
+ * (every kernel runs on `stream`).  All calls on one GPU share its scratch,
+ * which keeps the last call's contents (nothing in it needs to start at
+ * zero): calls that overlap on one GPU (other streams or threads without
+ * an ordering between them) race and must be serialized by the caller.
+ * status_dev as for orth_orthogonalize_batched (NULL: the statuses stay in
+ * the scratch).  Errors: those of orth_orthogonalize_batched, and
+ * ORTH_EWORKSPACE for a batch larger than the scratch.
+ */
+#define ORTH_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int orth_orthogonalize_batched_noalloc(const orth_mat* mats, int32_t n,
+                                       const orth_bjorck_opts* opts,
+                                       int32_t* status_dev, void* stream);
+
 /* One matrix of a Björck vector-Jacobian product. */
 typedef struct {
   const void* w;         /* device, the raw parameter W the forward call was

@@ -19,9 +19,10 @@ ORTH_F32, ORTH_BF16 = 0, 1
 ORTH_COMPUTE_F32, ORTH_COMPUTE_BF16 = 0, 1
 ORTH_PRESCALE_NONE, ORTH_PRESCALE_FROBENIUS, ORTH_PRESCALE_SPECTRAL = 0, 1, 2
 ORTH_CHECK_GRAM, ORTH_CHECK_CONV, ORTH_CHECK_CONV_ADJOINT = 0, 1, 2
+ORTH_NOALLOC_SCRATCH_BYTES = 64 << 20   # the allocation-free entry point's device scratch per GPU
 
 EXPORTED = [
-    "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched",
+    "orth_orthogonalize_workspace_size", "orth_orthogonalize_batched", "orth_orthogonalize_batched_noalloc",
     "orth_orthogonalize_vjp_workspace_size", "orth_orthogonalize_vjp_batched",
     "orth_orthogonalize_save_workspace_size", "orth_orthogonalize_save_batched", "orth_aoc_param_shapes",
     "orth_build_conv_kernels_workspace_size", "orth_build_conv_kernels_batched", "orth_build_conv_kernel",
@@ -108,6 +109,7 @@ def lib():
         P = ctypes.POINTER
         L.orth_orthogonalize_workspace_size.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), P(sz)]
         L.orth_orthogonalize_batched.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
+        L.orth_orthogonalize_batched_noalloc.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), vp, vp]
         L.orth_orthogonalize_vjp_workspace_size.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), P(sz)]
         L.orth_orthogonalize_vjp_batched.argtypes = [P(orth_vjp_mat), i32, P(orth_bjorck_opts), vp, sz, vp, vp]
         L.orth_orthogonalize_save_workspace_size.argtypes = [P(orth_mat), i32, P(orth_bjorck_opts), P(sz)]
@@ -236,6 +238,22 @@ def orth_orthogonalize_batched(ins, outs, iters, beta=0.5, prescale="frobenius",
                                           status.data_ptr() if status is not None else None, _stream(stream))
     _check(rc, "orth_orthogonalize_batched")
     return ws
+
+
+def orth_orthogonalize_batched_noalloc(ins, outs, iters, beta=0.5, prescale="frobenius", compute="f32",
+                                       status=None, stream=None, power_iters=1, u=None, tile=0):
+    """orth_orthogonalize_batched without a workspace: the library's own
+    device scratch (ORTH_NOALLOC_SCRATCH_BYTES per GPU) holds the iterates,
+    so neither the library nor this binding allocates anything.  Calls on
+    one GPU share the scratch and must not overlap."""
+    mats = _mats(ins, outs)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u, tile)
+    if status is not None and (status.dtype != torch.int32 or status.numel() < len(ins)):
+        raise ValueError("status must be an int32 tensor with one slot per matrix")
+    rc = lib().orth_orthogonalize_batched_noalloc(mats, len(ins), ctypes.byref(opts),
+                                                  status.data_ptr() if status is not None else None,
+                                                  _stream(stream))
+    _check(rc, "orth_orthogonalize_batched_noalloc")
 
 
 def _vjp_mats(ws, gouts, gins):

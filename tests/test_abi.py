@@ -158,6 +158,25 @@ def test_workspace_errors_before_launch(L):
     assert L.orth_orthogonalize_batched(None, 0, ctypes.byref(opts), None, 0, None, None) == orth.ORTH_OK
 
 
+def test_noalloc_errors_before_the_device(L):
+    """The allocation-free entry point validates like the workspace one and
+    rejects a batch larger than its fixed scratch with ORTH_EWORKSPACE, all
+    on the host (no GPU here)."""
+    opts = orth.orth_bjorck_opts(3, 0.5, 1, 0, 0, 0)
+    assert L.orth_orthogonalize_batched_noalloc(None, 0, ctypes.byref(opts), None, None) == orth.ORTH_OK
+    assert L.orth_orthogonalize_batched_noalloc(_mats([(0, 4)]), 1, ctypes.byref(opts), None, None) \
+        == orth.ORTH_EINVAL
+    bad = orth.orth_bjorck_opts(3, 0.75, 1, 0, 0, 0)
+    assert L.orth_orthogonalize_batched_noalloc(_mats([(8, 4)]), 1, ctypes.byref(bad), None, None) \
+        == orth.ORTH_EINVAL
+    big = [(4096, 2048)]
+    rc, need = _ws_size(L, big)
+    assert rc == 0 and need > orth.ORTH_NOALLOC_SCRATCH_BYTES
+    assert L.orth_orthogonalize_batched_noalloc(_mats(big), 1, ctypes.byref(opts), None, None) \
+        == orth.ORTH_EWORKSPACE
+    assert b"holds 67108864" in L.orth_last_error()
+
+
 def test_conv_validation(L):
     d = (orth.orth_conv_desc * 1)()
     d[0] = orth.orth_conv_desc(orth.orth_conv_geom(4, 4, 3, 2, 2, 1), 0x1000, 0x2000, 0x3000)
