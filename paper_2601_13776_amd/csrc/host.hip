@@ -588,22 +588,19 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     std::vector<int> gm = members, um = members;
     std::stable_sort(gm.begin(), gm.end(), [&](int a, int b) { return P.mp[a].Mp > P.mp[b].Mp; });
     std::stable_sort(um.begin(), um.end(), [&](int a, int b) { return P.mp[a].Np > P.mp[b].Np; });
-    for (int k = 0; k < (int)members.size(); ++k) {
-      std::vector<TileItem> gt, ut, unused;
-      const MatPlan& qg = P.mp[gm[k]];
-      bf16_matrix_tiles(tiled_of[gm[k]], qg.Mp / tsz, qg.Np / tsz, gt, unused);
-      const MatPlan& qu = P.mp[um[k]];
-      unused.clear();
-      bf16_matrix_tiles(tiled_of[um[k]], qu.Mp / tsz, qu.Np / tsz, unused, ut);
-      for (int par = 0; par < 2; ++par) {
-        for (TileItem t : gt) {
-          t.flags = par ? TILE_PARITY : 0;
-          g[par].push_back(t);
-        }
-        for (TileItem t : ut) {
-          t.flags = TILE_UPDATE | (par ? TILE_PARITY : 0);
-          u[par].push_back(t);
-        }
+    std::vector<std::pair<int, int>> gram_mats;
+    for (int i : gm) gram_mats.push_back({tiled_of[i], P.mp[i].Np / tsz});
+    const std::vector<TileItem> gt = bf16_gram_tiles(gram_mats);
+    std::vector<TileItem> ut;
+    for (int i : um) bf16_update_tiles(tiled_of[i], P.mp[i].Mp / tsz, P.mp[i].Np / tsz, ut);
+    for (int par = 0; par < 2; ++par) {
+      for (TileItem t : gt) {
+        t.flags = par ? TILE_PARITY : 0;
+        g[par].push_back(t);
+      }
+      for (TileItem t : ut) {
+        t.flags = TILE_UPDATE | (par ? TILE_PARITY : 0);
+        u[par].push_back(t);
       }
     }
     // dispatched in the order bf16_matrix_tiles builds (tile_order.h)
@@ -1672,15 +1669,10 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
     std::vector<int> gm = bf16_members[cls], um = bf16_members[cls];
     std::stable_sort(gm.begin(), gm.end(), [&](int a, int c) { return P.mats[a].Mp > P.mats[c].Mp; });
     std::stable_sort(um.begin(), um.end(), [&](int a, int c) { return P.mats[a].Np > P.mats[c].Np; });
-    std::vector<TileItem> unused;
-    for (int i : gm) {
-      unused.clear();
-      bf16_matrix_tiles(i, P.mats[i].Mp / tsz, P.mats[i].Np / tsz, tg[cls], unused);
-    }
-    for (int i : um) {
-      unused.clear();
-      bf16_matrix_tiles(i, P.mats[i].Mp / tsz, P.mats[i].Np / tsz, unused, tu[cls]);
-    }
+    std::vector<std::pair<int, int>> gram_mats;
+    for (int i : gm) gram_mats.push_back({i, P.mats[i].Np / tsz});
+    tg[cls] = bf16_gram_tiles(gram_mats);
+    for (int i : um) bf16_update_tiles(i, P.mats[i].Mp / tsz, P.mats[i].Np / tsz, tu[cls]);
   }
   for (int cls = 0; cls < 2; ++cls) {
     P.t_gram[cls] = tg[cls];
