@@ -89,3 +89,94 @@ def iterations_to_converge_scaled(w, scale, tol=1e-5, beta=0.5, max_iters=400):
             return t
         s = (1.0 + beta) * s - beta * s ** 3
     return None
+
+
+def spectral_prescale_vjp(w, u, power_iters, grad_w0):
+    """dL/dW of W_0 = W / sigma(W) (spectral_prescale) given dL/dW_0, the
+    cached vector u held constant (it is state carried between parameter
+    steps, not a function of this step's W).
+
+    With X the tall orientation, G_0 = dL/dX_0 and sigma = max(sigma_hat,
+    ||X||_F / sqrt(N)):
+
+        dL/dX = G_0 / sigma + c d(sigma)/dX,   c = -<G_0, X> / sigma^2.
+
+    Frobenius branch (sigma_hat < ||X||_F / sqrt(N), ties go to sigma_hat
+    as in the forward's max): d(sigma)/dX = X / (||X||_F sqrt(N)).
+    Power-iteration branch: sigma_hat = |y| / |x| with x = X v, y = X^T x
+    and v = v_{q-1} the vector before the last step; every earlier vector
+    v_k = y_k / |y_k| depends on X as well, down to the constant v_0.  The
+    chain rule through one step, written out with a = |y|, b = |x|:
+
+        last step:  yh = c y / (a b),  gx = -c a x / b^3 + X yh,
+                    dL/dX += x yh^T + gx v^T,   dL/dv = X^T gx;
+        earlier:    gy = (dL/dv_k - <dL/dv_k, v_k> v_k) / |y_k|,
+                    dL/dX += x_k gy^T + (X gy) v_{k-1}^T,
+                    dL/dv_{k-1} = X^T X gy.
+
+    Zero matrix: zero gradient; non-finite: all NaN (the forward's
+    statuses)."""
+    w = np.asarray(w, dtype=np.float64)
+    rows, cols = w.shape
+    n = min(rows, cols)
+    g0 = np.asarray(grad_w0, dtype=np.float64)
+    if not np.all(np.isfinite(w)):
+        return np.full(w.shape, np.nan)
+    fro = np.sqrt(np.sum(w * w))
+    if fro == 0.0:
+        return np.zeros(w.shape)
+    tall = rows >= cols
+    X = w if tall else w.T
+    G = g0 if tall else g0.T
+    u = np.asarray(u, dtype=np.float64).reshape(n)
+    nv = np.sqrt(np.sum(u * u))
+    v = u / nv if (nv > 0 and np.isfinite(nv)) else np.full(n, 1.0 / np.sqrt(n))
+    # forward power iteration, keeping every vector
+    vs, xs, ys = [v], [], []
+    sigma_hat = 0.0
+    for _ in range(power_iters):
+        x = X @ vs[-1]
+        y = X.T @ x
+        ny = np.sqrt(np.sum(y * y))
+        if ny == 0.0:
+            sigma_hat = 0.0
+            xs, ys = [], []
+            break
+        xs.append(x)
+        ys.append(y)
+        sigma_hat = ny / np.sqrt(np.sum(x * x))
+        vs.append(y / ny)
+    floor = fro / np.sqrt(n)
+    sigma = max(sigma_hat, floor)
+    c = -float(np.sum(G * X)) / sigma ** 2
+    out = G / sigma
+    if sigma_hat >= floor and xs:
+        q = len(xs)
+        x, y = xs[-1], ys[-1]
+        a, b = np.sqrt(np.sum(y * y)), np.sqrt(np.sum(x * x))
+        yh = c * y / (a * b)
+        gx = -c * a * x / b ** 3 + X @ yh
+        out = out + np.outer(x, yh) + np.outer(gx, vs[q - 1])
+        gv = X.T @ gx
+        for k in range(q - 1, 0, -1):           # v_k = y_k / |y_k| (step k, 1-based)
+            yk, vk = ys[k - 1], vs[k]
+            gy = (gv - np.sum(gv * vk) * vk) / np.sqrt(np.sum(yk * yk))
+            xg = X @ gy
+            out = out + np.outer(xs[k - 1], gy) + np.outer(xg, vs[k - 1])
+            gv = X.T @ xg
+    else:
+        out = out + c * X / (fro * np.sqrt(n))
+    return out if tall else out.T
+
+
+def bjorck_spectral_vjp(w, u, grad_out, iters, power_iters=1, beta=0.5):
+    """dL/dW for L depending on W through bjorck_spectral(W, u, iters,
+    power_iters, beta)[0], given dL/d(output) = grad_out, u constant."""
+    from . import bjorck_grad as _bg
+    w0, _, _, status = spectral_prescale(w, u, power_iters)
+    if status == _bj.STATUS_NONFINITE:
+        return np.full(np.shape(w), np.nan)
+    if status == _bj.STATUS_ZERO:
+        return np.zeros(np.shape(w))
+    g0 = _bg.bjorck_vjp(w0, grad_out, iters, beta, prescale="none")
+    return spectral_prescale_vjp(w, u, power_iters, g0)

@@ -30,7 +30,7 @@ REL_F32 = 1e-5
 ORTH_F32 = 1e-5
 ORTH_BF16 = 3e-3
 BF16_REL = 1e-2
-TILE_REL_BF16 = 2e-2
+TILE_REL_BF16 = 1e-2
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 

@@ -9,7 +9,14 @@ S4  the wide case is the transpose of the tall case;
 S5  the point of the step: from a good cached vector, spectral scaling
     needs fewer Björck iterations than Frobenius scaling, about
     log_1.5(||W||_F / sigma) fewer on the workload's matrices;
-S6  statuses, and planted mistakes that the pins catch.
+S6  statuses, and planted mistakes that the pins catch;
+S7  the vector-Jacobian product through the pre-scaling (cached vector held
+    constant): central finite differences of the oracle forward in both
+    branches of the max, every Jacobian entry on tiny matrices; torch
+    autograd through an independent float64 torch forward of the power
+    steps and the iteration; the statuses; planted mistakes (the earlier
+    power steps' dependence on W dropped, the other branch's derivative)
+    that the finite differences catch.
 """
 
 import json
@@ -171,3 +178,133 @@ def test_workload_shapes_step_saving():
         assert dev(spec) <= max(dev(frob), 1e-12), (i, shapes[i], k, dev(spec), dev(frob))
         saved.append(k)
     assert min(saved) >= 2 and max(saved) >= 5
+
+
+# ------------------------------------------------------------------ S7 ---
+def fd_spectral(w, u, y, d, iters, q, h=1e-6):
+    f = lambda x: spectral.bjorck_spectral(x, u, iters, q)[0]
+    return float(np.sum(y * (f(w + h * d) - f(w - h * d)))) / (2 * h)
+
+
+def frobenius_branch_case(rng, n=5):
+    """A matrix whose power-iteration estimate from the cached vector stays
+    below ||W||_F / sqrt(N): the cached vector lies on a small singular
+    direction of a matrix with one large singular value."""
+    w = np.diag([4.0] + [1.0] * (n - 1)) + 0.01 * rng.standard_normal((n, n))
+    u = np.zeros(n)
+    u[1] = 1.0
+    return w, u
+
+
+@pytest.mark.parametrize("shape,q", [((7, 4), 1), ((7, 4), 3), ((4, 7), 2), ((6, 6), 1), ((6, 6), 4), ((9, 1), 2)])
+def test_spectral_vjp_directional_fd(shape, q):
+    w = RNG.standard_normal(shape)
+    u = RNG.standard_normal(min(shape))
+    y = RNG.standard_normal(shape)
+    _, _, sigma, _ = spectral.spectral_prescale(w, u, q)
+    assert sigma > np.linalg.norm(w) / np.sqrt(min(shape))   # power-iteration branch
+    g = spectral.bjorck_spectral_vjp(w, u, y, 5, q)
+    for _ in range(3):
+        d = RNG.standard_normal(shape)
+        fd = fd_spectral(w, u, y, d, 5, q)
+        assert abs(float(np.sum(g * d)) - fd) <= 1e-7 * max(1.0, abs(fd))
+
+
+@pytest.mark.parametrize("q", [1, 2])
+def test_spectral_vjp_frobenius_branch_fd(q):
+    w, u = frobenius_branch_case(RNG)
+    _, _, sigma, _ = spectral.spectral_prescale(w, u, q)
+    assert sigma == np.linalg.norm(w) / np.sqrt(5)
+    y = RNG.standard_normal(w.shape)
+    g = spectral.bjorck_spectral_vjp(w, u, y, 4, q)
+    for _ in range(3):
+        d = RNG.standard_normal(w.shape)
+        fd = fd_spectral(w, u, y, d, 4, q)
+        assert abs(float(np.sum(g * d)) - fd) <= 1e-7 * max(1.0, abs(fd))
+
+
+def test_spectral_vjp_full_jacobian_fd():
+    w = RNG.standard_normal((3, 2))
+    u = RNG.standard_normal(2)
+    y = RNG.standard_normal((3, 2))
+    g = spectral.bjorck_spectral_vjp(w, u, y, 3, 2)
+    fd = np.zeros(w.shape)
+    for i in range(3):
+        for j in range(2):
+            e = np.zeros(w.shape)
+            e[i, j] = 1.0
+            fd[i, j] = fd_spectral(w, u, y, e, 3, 2)
+    assert np.max(np.abs(g - fd)) <= 1e-8 * max(1.0, np.max(np.abs(fd)))
+
+
+def torch_spectral_forward(w, u, iters, q, beta=0.5):
+    """Power steps and iteration written with torch ops (test-local)."""
+    import torch
+    tall = w.shape[0] >= w.shape[1]
+    x_mat = w if tall else w.mT
+    v = u / torch.linalg.vector_norm(u)
+    for _ in range(q):
+        x = x_mat @ v
+        y = x_mat.mT @ x
+        sig = torch.linalg.vector_norm(y) / torch.linalg.vector_norm(x)
+        v = y / torch.linalg.vector_norm(y)
+    floor = torch.linalg.matrix_norm(w) / min(w.shape) ** 0.5
+    z = w / (sig if sig >= floor else floor)
+    for _ in range(iters):
+        z = (1 + beta) * z - beta * (z @ z.mT @ z)
+    return z
+
+
+@pytest.mark.parametrize("shape,q,branch", [((12, 5), 2, "power"), ((5, 12), 3, "power"), ((8, 8), 1, "power"),
+                                            ((5, 5), 2, "frobenius")])
+def test_spectral_vjp_matches_torch_autograd(shape, q, branch):
+    import torch
+    if branch == "power":
+        w = RNG.standard_normal(shape)
+        u = RNG.standard_normal(min(shape))
+    else:
+        w, u = frobenius_branch_case(RNG)
+    y = RNG.standard_normal(w.shape)
+    wt = torch.tensor(w, dtype=torch.float64, requires_grad=True)
+    out = torch_spectral_forward(wt, torch.tensor(u, dtype=torch.float64), 6, q)
+    (out * torch.tensor(y)).sum().backward()
+    g = spectral.bjorck_spectral_vjp(w, u, y, 6, q)
+    assert np.max(np.abs(g - wt.grad.numpy())) <= 1e-10 * max(1.0, np.max(np.abs(g)))
+
+
+def test_spectral_vjp_statuses():
+    u = np.ones(3)
+    y = RNG.standard_normal((4, 3))
+    assert np.all(spectral.bjorck_spectral_vjp(np.zeros((4, 3)), u, y, 3, 1) == 0)
+    bad = RNG.standard_normal((4, 3))
+    bad[1, 2] = np.inf
+    assert np.all(np.isnan(spectral.bjorck_spectral_vjp(bad, u, y, 3, 1)))
+    # a zero cached vector starts from ones, as in the forward
+    w = RNG.standard_normal((4, 3))
+    g0 = spectral.bjorck_spectral_vjp(w, np.zeros(3), y, 3, 2)
+    g1 = spectral.bjorck_spectral_vjp(w, np.ones(3), y, 3, 2)
+    assert np.array_equal(g0, g1)
+
+
+def test_planted_spectral_vjp_mistakes():
+    """Treating the earlier power steps' vectors as constants, or taking the
+    Frobenius branch's derivative where sigma_hat is the maximum, both
+    fail the finite differences."""
+    w = RNG.standard_normal((6, 4))
+    u = RNG.standard_normal(4)
+    y = RNG.standard_normal((6, 4))
+    d = RNG.standard_normal((6, 4))
+    fd = fd_spectral(w, u, y, d, 4, 3)
+    good = float(np.sum(spectral.bjorck_spectral_vjp(w, u, y, 4, 3) * d))
+    assert abs(good - fd) <= 1e-7 * max(1.0, abs(fd))
+    # only the last power step differentiated: q = 3 seen as one step from v_2
+    w0, v, sigma, _ = spectral.spectral_prescale(w, u, 2)
+    from oracle import bjorck_grad
+    g0 = bjorck_grad.bjorck_vjp(spectral.spectral_prescale(w, u, 3)[0], y, 4, prescale="none")
+    last_only = spectral.spectral_prescale_vjp(w, v, 1, g0)
+    assert abs(float(np.sum(last_only * d)) - fd) > 1e-4 * max(1.0, abs(fd))
+    # Frobenius branch's derivative in the power-iteration branch
+    n = 4
+    c = -float(np.sum(g0 * w)) / spectral.spectral_prescale(w, u, 3)[2] ** 2
+    wrong = g0 / spectral.spectral_prescale(w, u, 3)[2] + c * w / (np.linalg.norm(w) * np.sqrt(n))
+    assert abs(float(np.sum(wrong * d)) - fd) > 1e-4 * max(1.0, abs(fd))
