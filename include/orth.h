@@ -192,6 +192,20 @@ typedef struct {
  * (wide matrices through their transpose), chained from the last step to
  * the first, then through the pre-scaling W_0 = W / ||W||_F:
  *   dL/dW = (dL/dW_0 - <dL/dW_0, W_0> W_0) / ||W||_F.
+ * Spectral pre-scaling (App. A.5; the estimate W_0 = W / sigma with sigma =
+ * max(sigma_hat, ||W||_F / sqrt(N)) of orth_orthogonalize_batched): the
+ * cached vector is state, not a function of W, and is held constant; with
+ * G_0 = dL/dX_0 (tall orientation) and c = -<G_0, X_0> / sigma,
+ *   floor branch:  dL/dX = G_0 / sigma + c X / (||X||_F sqrt(N)),
+ *   power branch:  dL/dX = G_0 / sigma + the 2q rank-1 terms of the chain
+ *                  rule through the q power steps (each step's vectors
+ *                  depend on W; only the starting vector is constant).
+ * opts.u then holds the cached vectors as the differentiated forward call
+ * found them (before it wrote its new estimates back); they are read, never
+ * written.  With opts.saved = 1 they are not read: the saving forward kept
+ * the power steps and a copy of its starting vectors in the workspace.
+ * power_iters may be at most 16 here (the workspace keeps every step's
+ * vectors and the backward adds 2q rank-1 terms to every element).
  * The forward iterates are recomputed inside the call (or, with
  * opts.saved = 1, taken from a saving forward, see below) and every X_t and
  * E_t is kept in the workspace (about T (M N + N^2) elements per M x N
@@ -202,9 +216,10 @@ typedef struct {
  *
  * status_dev: optional, as for the forward (1: zero matrix -> zero gradient;
  * 2: non-finite input -> NaN gradient).
- * Returns ORTH_EINVAL for the argument errors of the forward call, iters >
- * 4096, or aliasing other than the two allowed above; ORTH_EUNSUPPORTED for
- * spectral pre-scaling (its derivative is not provided).
+ * Returns ORTH_EINVAL for the argument errors of the forward call (u may
+ * be NULL with opts.saved = 1), iters > 4096, or aliasing other than the
+ * two allowed above; ORTH_EUNSUPPORTED for spectral pre-scaling with more
+ * than 16 power steps.
  */
 int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n,
                                           const orth_bjorck_opts* opts, size_t* bytes);
@@ -225,9 +240,13 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n,
  * orth_orthogonalize_vjp_workspace_size for matrices of the same shapes
  * (orth_orthogonalize_save_workspace_size gives it from these descriptors)
  * and holds the saved state until the caller reuses it.
+ * Spectral pre-scaling: the cached vectors are read and the new estimates
+ * written back as by orth_orthogonalize_batched; the vectors this call
+ * started from are copied into the workspace for the saved product.
  * Errors: those of orth_orthogonalize_vjp_batched for these options
- * (ORTH_EUNSUPPORTED for spectral pre-scaling), ORTH_EINVAL for in == out
- * (the product reads the input again) or opts.saved != 0.
+ * (ORTH_EUNSUPPORTED for spectral pre-scaling with more than 16 power
+ * steps), ORTH_EINVAL for in == out (the product reads the input again) or
+ * opts.saved != 0.
  */
 int orth_orthogonalize_save_workspace_size(const orth_mat* mats, int32_t n,
                                            const orth_bjorck_opts* opts, size_t* bytes);

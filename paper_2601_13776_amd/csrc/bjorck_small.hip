@@ -135,6 +135,140 @@ __device__ double spectral_sigma(const float* X, const SmallMat& d, int power_it
   return fmax(sig, sqrt(tot) / sqrt((double)N));
 }
 
+// The power steps of spectral_sigma for a vector-Jacobian product: from the
+// cached vector the differentiated forward started from, every step's
+// vectors kept in d.pst (v_0 .. v_q, then x_1 .. x_q, then y_1 .. y_q, fp64)
+// and the cached vector left untouched.  Returns sigma_hat.
+template <int NP, int NWAVES>
+__device__ double spectral_keep(const float* X, const SmallVjpMat& d, int q, double* red) {
+  constexpr int XP = NP + 1, NTHR = 64 * NWAVES;
+  __shared__ double v[NP], y[NP], x[128];
+  const int tid = threadIdx.x, M = d.M, N = d.N;
+  double* V = d.pst;
+  double* Xs = V + (int64_t)(q + 1) * N;
+  double* Ys = Xs + (int64_t)q * M;
+  double ss = 0.0;
+  for (int j = tid; j < N; j += NTHR) {
+    const double u = d.u[j];
+    ss += u * u;
+  }
+  const double nu = sqrt(block_sum<NWAVES>(ss, red));
+  const bool ok = nu > 0.0 && isfinite(nu);
+  for (int j = tid; j < N; j += NTHR) {
+    v[j] = ok ? d.u[j] / nu : 1.0 / sqrt((double)N);
+    V[j] = v[j];
+  }
+  __syncthreads();
+  double sig = 0.0;
+  for (int k = 1; k <= q; ++k) {
+    for (int i = tid; i < M; i += NTHR) {
+      double a = 0.0;
+      for (int j = 0; j < N; ++j) a += (double)X[i * XP + j] * v[j];
+      x[i] = a;
+      Xs[(int64_t)(k - 1) * M + i] = a;
+    }
+    __syncthreads();
+    for (int j = tid; j < N; j += NTHR) {
+      double a = 0.0;
+      for (int i = 0; i < M; ++i) a += (double)X[i * XP + j] * x[i];
+      y[j] = a;
+      Ys[(int64_t)(k - 1) * N + j] = a;
+    }
+    __syncthreads();
+    double sx = 0.0, sy = 0.0;
+    for (int i = tid; i < M; i += NTHR) sx += x[i] * x[i];
+    for (int j = tid; j < N; j += NTHR) sy += y[j] * y[j];
+    const double nx = sqrt(block_sum<NWAVES>(sx, red));
+    const double ny = sqrt(block_sum<NWAVES>(sy, red));
+    if (ny == 0.0) {   // uniform: the floor of the max is the scale
+      sig = 0.0;
+      break;
+    }
+    sig = ny / nx;
+    for (int j = tid; j < N; j += NTHR) {
+      v[j] = y[j] / ny;
+      V[(int64_t)k * N + j] = v[j];
+    }
+    __syncthreads();
+  }
+  return sig;
+}
+
+// The backward through the power steps (the power-iteration branch of the
+// max): the 2q rank-1 pairs (a: M values, b: N values) of dL/dX, written
+// after the kept vectors in d.pst.  X holds X_0 = X / sigma; c = -<G_0, X_0>
+// / sigma.  With a = |y_q|, b = |x_q|: yh = c y_q / (a b), gx = -c a x_q /
+// b^3 + X yh give x_q yh^T + gx v_{q-1}^T; then gv = X^T gx and for
+// k = q-1 .. 1: gy = (gv - <gv, v_k> v_k) / |y_k| gives x_k gy^T +
+// (X gy) v_{k-1}^T, and gv = X^T X gy.
+template <int NP, int NWAVES>
+__device__ void spectral_small_bwd(const float* X, const SmallVjpMat& d, int q, double sigma, double c,
+                                   double* red) {
+  constexpr int XP = NP + 1, NTHR = 64 * NWAVES;
+  __shared__ double vn[NP], vm[128];
+  const int tid = threadIdx.x, M = d.M, N = d.N;
+  const double* V = d.pst;
+  const double* Xs = V + (int64_t)(q + 1) * N;
+  const double* Ys = Xs + (int64_t)q * M;
+  double* pair = d.pst + (int64_t)(q + 1) * N + (int64_t)q * (M + N);
+  const int64_t ps = (int64_t)M + N;
+  const double* x = Xs + (int64_t)(q - 1) * M;
+  const double* y = Ys + (int64_t)(q - 1) * N;
+  double sx = 0.0, sy = 0.0;
+  for (int i = tid; i < M; i += NTHR) sx += x[i] * x[i];
+  for (int j = tid; j < N; j += NTHR) sy += y[j] * y[j];
+  const double bn = sqrt(block_sum<NWAVES>(sx, red));
+  const double a = sqrt(block_sum<NWAVES>(sy, red));
+  for (int j = tid; j < N; j += NTHR) {
+    vn[j] = c * y[j] / (a * bn);
+    pair[M + j] = vn[j];                          // pair 0: (x_q, yh)
+    pair[ps + M + j] = V[(int64_t)(q - 1) * N + j];   // pair 1's b: v_{q-1}
+  }
+  __syncthreads();
+  const double xs = -c * a / (bn * bn * bn);
+  for (int i = tid; i < M; i += NTHR) {
+    double t = 0.0;
+    for (int j = 0; j < N; ++j) t += (double)X[i * XP + j] * vn[j];
+    vm[i] = xs * x[i] + sigma * t;                // gx
+    pair[i] = x[i];
+    pair[ps + i] = vm[i];
+  }
+  __syncthreads();
+  for (int k = q - 1; k >= 1; --k) {
+    // gv = X^T (gx or X gy) into vn
+    for (int j = tid; j < N; j += NTHR) {
+      double t = 0.0;
+      for (int i = 0; i < M; ++i) t += (double)X[i * XP + j] * vm[i];
+      vn[j] = sigma * t;
+    }
+    __syncthreads();
+    const double* vk = V + (int64_t)k * N;
+    const double* yk = Ys + (int64_t)(k - 1) * N;
+    double sd = 0.0, sk = 0.0;
+    for (int j = tid; j < N; j += NTHR) {
+      sd += vn[j] * vk[j];
+      sk += yk[j] * yk[j];
+    }
+    const double dv = block_sum<NWAVES>(sd, red);
+    const double nk = sqrt(block_sum<NWAVES>(sk, red));
+    double* p = pair + (int64_t)(2 * (q - k)) * ps;
+    for (int j = tid; j < N; j += NTHR) {
+      vn[j] = (vn[j] - dv * vk[j]) / nk;          // gy
+      p[M + j] = vn[j];
+      p[ps + M + j] = V[(int64_t)(k - 1) * N + j];
+    }
+    for (int i = tid; i < M; i += NTHR) p[i] = Xs[(int64_t)(k - 1) * M + i];
+    __syncthreads();
+    for (int i = tid; i < M; i += NTHR) {
+      double t = 0.0;
+      for (int j = 0; j < N; ++j) t += (double)X[i * XP + j] * vn[j];
+      vm[i] = sigma * t;                          // X gy
+      p[ps + i] = vm[i];
+    }
+    __syncthreads();
+  }
+}
+
 template <int NP, int NWAVES>
 __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMat* __restrict__ mats, int iters,
                                                                   float beta, int prescale, int power_iters,
@@ -254,7 +388,8 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_kernel(const SmallMa
 template <int NP, int NWAVES>
 __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const SmallVjpMat* __restrict__ mats,
                                                                       int iters, float beta, int prescale,
-                                                                      int in_dtype, int gout_dtype,
+                                                                      int power_iters, int in_dtype,
+                                                                      int gout_dtype,
                                                                       int32_t* __restrict__ status) {
   constexpr int NT = NP / 32;
   constexpr int XP = NP + 1;
@@ -288,6 +423,7 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
   for (int w = 0; w < NWAVES; ++w) tot += red[w];
   int st = ORTH_MAT_OK;
   float scale = 1.f;
+  double sig_hat = 0.0, sigma = 0.0;
   if (bad_any) {
     st = ORTH_MAT_NONFINITE;
     scale = __builtin_nanf("");
@@ -296,6 +432,10 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
     scale = 0.f;
   } else if (prescale == ORTH_PRESCALE_FROBENIUS) {
     scale = (float)(1.0 / sqrt(tot));
+  } else if (prescale == ORTH_PRESCALE_SPECTRAL) {
+    sig_hat = spectral_keep<NP, NWAVES>(X, d, power_iters, red);
+    sigma = fmax(sig_hat, sqrt(tot) / sqrt((double)N));
+    scale = (float)(1.0 / sigma);
   }
   if (tid == 0 && status) status[d.status_index] = st;
   for (int idx = tid; idx < Mp * NP; idx += NTHR) {
@@ -426,14 +566,31 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
 
   // -- pre-scaling derivative (X holds X_0 here) in the caller's layout
   float dot = 0.f;
-  if (prescale == ORTH_PRESCALE_FROBENIUS && st == ORTH_MAT_OK) {
+  double dotd = 0.0;
+  if (prescale != ORTH_PRESCALE_NONE && st == ORTH_MAT_OK) {
     double a = 0.0;
     for (int idx = tid; idx < M * N; idx += NTHR) {
       const int r = idx / N, c = idx - (idx / N) * N;
       a += (double)Y[r * XP + c] * (double)X[r * XP + c];
     }
-    dot = (float)block_sum<NWAVES>(a, red);
+    dotd = block_sum<NWAVES>(a, red);
+    dot = (float)dotd;
   }
+  // spectral pre-scaling: dL/dX = Y_0 / sigma - <Y_0, X_0> X_0 / (||X||_F
+  // sqrt(N)) when the floor is the max, else Y_0 / sigma plus the rank-1
+  // pairs of the power steps
+  int npair = 0;
+  float xcoef = 0.f;
+  if (prescale == ORTH_PRESCALE_SPECTRAL && st == ORTH_MAT_OK) {
+    const double fro = sqrt(tot);
+    if (power_iters > 0 && sig_hat > 0.0 && sig_hat >= fro / sqrt((double)N)) {
+      spectral_small_bwd<NP, NWAVES>(X, d, power_iters, sigma, -dotd / sigma, red);
+      npair = 2 * power_iters;
+    } else {
+      xcoef = (float)(-dotd / (fro * sqrt((double)N)));
+    }
+  }
+  const double* pairs = npair ? d.pst + (int64_t)(power_iters + 1) * N + (int64_t)power_iters * (M + N) : nullptr;
   for (int idx = tid; idx < M * N; idx += NTHR) {
     const int r = idx / N, c = idx - (idx / N) * N;
     float v;
@@ -443,7 +600,11 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
       v = 0.f;
     else if (prescale == ORTH_PRESCALE_FROBENIUS)
       v = scale * (Y[r * XP + c] - dot * X[r * XP + c]);
-    else
+    else if (prescale == ORTH_PRESCALE_SPECTRAL) {
+      double a = 0.0;
+      for (int p = 0; p < npair; ++p) a += pairs[p * (M + N) + r] * pairs[p * (M + N) + M + c];
+      v = scale * Y[r * XP + c] + xcoef * X[r * XP + c] + (float)a;
+    } else
       v = Y[r * XP + c];
     const int64_t dst = d.transposed ? (int64_t)c * d.ld_gin + r : (int64_t)r * d.ld_gin + c;
     store_from_f32(d.gin, dst, in_dtype, v);
@@ -473,7 +634,8 @@ hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, 
 }
 
 hipError_t launch_bjorck_small_vjp(const SmallVjpMat* mats, int n, int np, int max_mp, int iters, float beta,
-                                   int prescale, int in_dtype, int gout_dtype, int32_t* status, hipStream_t s) {
+                                   int prescale, int power_iters, int in_dtype, int gout_dtype, int32_t* status,
+                                   hipStream_t s) {
   if (n <= 0) return hipSuccess;
   // X and Y (max_mp rows), E and S' (np rows), pitch np + 1: at most 99.8 KB
   const size_t lds = (size_t)(2 * max_mp + 2 * np) * (np + 1) * sizeof(float);
@@ -484,13 +646,13 @@ hipError_t launch_bjorck_small_vjp(const SmallVjpMat* mats, int n, int np, int m
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e == hipSuccess)
       hipLaunchKernelGGL((bjorck_small_vjp_kernel<32, 1>), dim3(n), dim3(64), lds, s, mats, iters, beta, prescale,
-                         in_dtype, gout_dtype, status);
+                         power_iters, in_dtype, gout_dtype, status);
   } else {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&bjorck_small_vjp_kernel<64, 4>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e == hipSuccess)
       hipLaunchKernelGGL((bjorck_small_vjp_kernel<64, 4>), dim3(n), dim3(256), lds, s, mats, iters, beta, prescale,
-                         in_dtype, gout_dtype, status);
+                         power_iters, in_dtype, gout_dtype, status);
   }
   if (e == hipSuccess) e = hipGetLastError();
   timing_end("bjorck_small_vjp", s);

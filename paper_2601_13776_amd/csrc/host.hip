@@ -3,6 +3,7 @@
 // include/orth.h.  Every entry point validates everything before it
 // enqueues anything; the library allocates no device memory.
 #include <algorithm>
+#include <array>
 #include <climits>
 #include <cstdarg>
 #include <cstdlib>
@@ -1526,6 +1527,13 @@ struct VjpPlan {
   std::vector<SmallVjpMat> small[2];  // N <= 32, N <= 64 (fused kernel)
   int small_max_mp[2] = {0, 0};
   size_t off_small[2] = {0, 0};
+  // spectral pre-scaling: power-step items, the backward's table of the
+  // same matrices with its own vectors, and the copy of the cached vectors
+  // a saving forward keeps for its saved product
+  std::vector<PowerItem> power[2];
+  std::vector<TiledMat> bw;
+  size_t off_power[2] = {0, 0}, off_bw = 0, off_u0 = 0;
+  size_t u_floats = 0;
   size_t off_mats = 0, off_partial_items = 0, off_scale_items = 0;
   size_t off_f_gram = 0, off_f_upd = 0, off_b_s[2] = {}, off_b_upd[2] = {};
   size_t off_t_gram[2] = {}, off_t_upd[2] = {}, off_t_s[2][2] = {}, off_t_yu[2][2] = {};
@@ -1542,6 +1550,8 @@ void log_vjp_plan(const char* entry, const VjpPlan& P, int n) {
            P.f_gram.size(), P.f_upd.size(), P.b_s[0].size(), P.b_upd[0].size(), P.total_bytes, P.table_bytes);
 }
 
+constexpr int kVjpMaxPowerIters = 16;
+
 int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o) {
   if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
   if (n > 0 && !mats) return fail(ORTH_EINVAL, "mats is NULL");
@@ -1549,10 +1559,16 @@ int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o)
   if (o->iters < 0) return fail(ORTH_EINVAL, "iters must be >= 0");
   if (o->iters > 4096) return fail(ORTH_EINVAL, "iters must be <= 4096");
   if (!(o->beta > 0.f && o->beta <= 0.5f)) return fail(ORTH_EINVAL, "beta must lie in (0, 0.5]");
-  if (o->prescale == ORTH_PRESCALE_SPECTRAL)
-    return fail(ORTH_EUNSUPPORTED, "the vector-Jacobian product supports no spectral pre-scaling");
-  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS)
+  if (o->prescale != ORTH_PRESCALE_NONE && o->prescale != ORTH_PRESCALE_FROBENIUS &&
+      o->prescale != ORTH_PRESCALE_SPECTRAL)
     return fail(ORTH_EINVAL, "unknown prescale mode");
+  if (o->prescale == ORTH_PRESCALE_SPECTRAL) {
+    if (o->power_iters < 1 || o->power_iters > 1024) return fail(ORTH_EINVAL, "power_iters must lie in [1, 1024]");
+    if (o->power_iters > kVjpMaxPowerIters)
+      return fail(ORTH_EUNSUPPORTED, "the vector-Jacobian product through spectral pre-scaling takes at most 16 "
+                                     "power steps");
+    if (!o->u && !o->saved) return fail(ORTH_EINVAL, "spectral pre-scaling needs the cached vectors u");
+  }
   if ((o->in_dtype != ORTH_F32 && o->in_dtype != ORTH_BF16) || (o->out_dtype != ORTH_F32 && o->out_dtype != ORTH_BF16))
     return fail(ORTH_EINVAL, "unknown dtype");
   if (o->compute != ORTH_COMPUTE_F32 && o->compute != ORTH_COMPUTE_BF16) return fail(ORTH_EINVAL, "unknown compute mode");
@@ -1590,9 +1606,11 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
   const bool bf16 = o->compute == ORTH_COMPUTE_BF16;
   const int T = o->iters;
   const int slots = T + 1;   // X_0 .. X_T (a saving forward writes X_T too)
+  const bool spectral = o->prescale == ORTH_PRESCALE_SPECTRAL;
+  const int pq = spectral ? o->power_iters : 0;
   P.bucket.resize(n);
   P.mats.resize(n);
-  int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0;
+  int64_t n_part = 0, n_scale = 0, n_fg = 0, n_fu = 0, n_pw[2] = {0, 0};
   std::vector<TileItem> tg[2], tu[2];
   std::vector<int> bf16_members[2];
   std::vector<std::pair<int, int>> dims(n);
@@ -1661,6 +1679,10 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
     } else {
       bf16_members[b == V_BF16_256 ? 1 : 0].push_back(i);
     }
+    if (spectral) {
+      n_pw[0] += (t.M + 63) / 64;
+      n_pw[1] += (t.N + 63) / 64;
+    }
   }
   // bf16 tile lists, longest tiles first (Gram and S' tiles run over Mp,
   // update tiles over Np)
@@ -1705,25 +1727,59 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       P.off_t_yu[cls][par] = A.take(sizeof(TileItem) * P.t_yu[cls][par].size());
     }
   }
+  for (int h = 0; h < 2; ++h) P.off_power[h] = A.take(sizeof(PowerItem) * n_pw[h]);
+  P.off_bw = A.take(spectral ? sizeof(TiledMat) * n : 0);
   P.table_bytes = align_up(A.off);
   P.off_partials = A.take(sizeof(double) * n_part);
   P.off_inv = A.take(sizeof(float) * n);
   P.off_dot = A.take(sizeof(double) * n);
   P.off_status = A.take(sizeof(int32_t) * n);
+  if (spectral)
+    for (int i = 0; i < n; ++i) P.u_floats += std::min(mats[i].rows, mats[i].cols);
+  P.off_u0 = A.take(sizeof(float) * P.u_floats);
 
   auto dev = [&](size_t off) -> unsigned char* { return ws ? ws + off : nullptr; };
   // saved X_t and E_t of the fused small matrices, pitch np
+  // offsets of every matrix's cached vector in the packed array
+  std::vector<int64_t> u_off(n + 1, 0);
+  for (int i = 0; i < n; ++i) u_off[i + 1] = u_off[i] + (spectral ? std::min(mats[i].rows, mats[i].cols) : 0);
+  const float* u_src = o->saved ? reinterpret_cast<const float*>(dev(P.off_u0)) : o->u;
   for (int k = 0; k < 2; ++k)
     for (SmallVjpMat& q : P.small[k]) {
       const int np = q.np;
       q.save = reinterpret_cast<float*>(dev(A.take((size_t)T * ((size_t)q.Mp * np + (size_t)np * np) * 4)));
+      if (spectral) {
+        // the start vector (the caller's u, or the saving forward's copy of
+        // it), the power steps' vectors and the 2q rank-1 pairs
+        q.u = u_src ? u_src + u_off[q.status_index] : nullptr;
+        const size_t nd = (size_t)(pq + 1) * q.N + (size_t)pq * (q.M + q.N) + (size_t)2 * pq * (q.M + q.N);
+        q.pst = reinterpret_cast<double*>(dev(A.take(sizeof(double) * nd)));
+      }
     }
+  std::vector<std::array<double*, 3>> bw_vec(n, {nullptr, nullptr, nullptr});
   for (int i = 0; i < n; ++i) {
     TiledMat& t = P.mats[i];
     if (t.fused) continue;
     const int64_t xe = (int64_t)t.Mp * t.Np, ee = (int64_t)t.Np * t.Np;
     t.inv_norm = reinterpret_cast<float*>(dev(P.off_inv)) + i;
     t.dot = reinterpret_cast<double*>(dev(P.off_dot)) + i;
+    if (spectral) {
+      auto dbl = [&](size_t cnt) { return reinterpret_cast<double*>(dev(A.take(sizeof(double) * cnt))); };
+      t.u = o->u ? const_cast<float*>(o->u) + u_off[i] : nullptr;
+      t.pv = dbl(t.N);
+      t.px = dbl(t.M);
+      t.py = dbl(t.N);
+      t.sig = dbl(1);
+      t.pq = pq;
+      t.pst = dbl((size_t)(pq + 1) * t.N + (size_t)pq * (t.M + t.N));
+      t.sb = dbl(SB_SLOTS);
+      t.pair = dbl((size_t)2 * pq * (t.M + t.N));
+      bw_vec[i] = {dbl(t.N), dbl(t.M), dbl(t.N)};
+      // X v is a row product of W for a tall input and a column product for
+      // a wide one; X^T x the other way round
+      for (int b = 0; b < (t.M + 63) / 64; ++b) P.power[0].push_back(PowerItem{i, b, t.transposed, 0});
+      for (int b = 0; b < (t.N + 63) / 64; ++b) P.power[1].push_back(PowerItem{i, b, !t.transposed, 1});
+    }
     for (int a = 0; a < (t.rows + 63) / 64; ++a)
       for (int b = 0; b < (t.cols + 63) / 64; ++b) P.partial_items.push_back(TileItem{i, a, b, 0});
     for (int a = 0; a < t.Mp / 64; ++a)
@@ -1867,6 +1923,14 @@ void build_vjp_plan(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts*
       }
   }
   P.total_bytes = align_up(A.off);
+  if (spectral) {
+    P.bw = P.mats;
+    for (int i = 0; i < n; ++i) {
+      P.bw[i].pv = bw_vec[i][0];
+      P.bw[i].px = bw_vec[i][1];
+      P.bw[i].py = bw_vec[i][2];
+    }
+  }
   longest_first(P.f_gram);
   longest_first(P.f_upd);
   for (int par = 0; par < 2; ++par) {
@@ -2017,7 +2081,21 @@ int vjp_forward(const VjpPlan& P, unsigned char* ws, const orth_bjorck_opts* opt
   double* partials = reinterpret_cast<double*>(ws + P.off_partials);
   ORTH_HIP(launch_prescale_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                    partials, s));
-  ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s));
+  if (opts->prescale == ORTH_PRESCALE_SPECTRAL) {
+    // the power steps, every step's vectors kept for the backward
+    ORTH_HIP(launch_power_init(tm, n, s));
+    ORTH_HIP(launch_power_keep(tm, n, 0, s));
+    for (int k = 1; k <= opts->power_iters; ++k) {
+      for (int h = 0; h < 2; ++h)
+        ORTH_HIP(launch_power_dot(tm, reinterpret_cast<const PowerItem*>(ws + P.off_power[h]),
+                                  (int)P.power[h].size(), opts->in_dtype, s));
+      ORTH_HIP(launch_power_normalize(tm, n, s));
+      ORTH_HIP(launch_power_keep(tm, n, k, s));
+    }
+  }
+  // a saving forward hands the new estimate back; the recomputation inside
+  // a vector-Jacobian product leaves the cached vectors alone
+  ORTH_HIP(launch_prescale_finish(tm, n, partials, opts->prescale, status, s, to_output ? 1 : 0));
   ORTH_HIP(launch_prescale_scale(tm, TI(P.off_scale_items), (int)P.scale_items.size(), opts->in_dtype,
                                  opts->compute, s));
   for (int t = 0; t < T; ++t) {
@@ -2110,11 +2188,15 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
       sm.Mp = q.Mp;
       sm.transposed = q.transposed;
       sm.status_index = q.status_index;
+      sm.u = const_cast<float*>(q.u);
       small[k].push_back(sm);
     }
   TableImage img;
   put(img, P.off_mats, P.mats);
   for (int k = 0; k < 2; ++k) put(img, P.off_small[k], small[k]);
+  put(img, P.off_power[0], P.power[0]);
+  put(img, P.off_power[1], P.power[1]);
+  put(img, P.off_bw, P.bw);
   put(img, P.off_partial_items, P.partial_items);
   put(img, P.off_scale_items, P.scale_items);
   put(img, P.off_f_gram, P.f_gram);
@@ -2125,12 +2207,17 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   }
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
+  // spectral: the cached vectors as this call found them, for the saved
+  // product (this call writes the new estimates back into u)
+  if (opts->prescale == ORTH_PRESCALE_SPECTRAL && P.u_floats)
+    ORTH_HIP(hipMemcpyAsync(ws + P.off_u0, opts->u, sizeof(float) * P.u_floats, hipMemcpyDeviceToDevice, s));
   // small matrices on side streams beside the tiled forward
   Fork fk(s);
   if (!P.partial_items.empty() && (!small[0].empty() || !small[1].empty())) ORTH_HIP(fk.fork());
   for (int k = 0; k < 2; ++k)
     ORTH_HIP(launch_bjorck_small(reinterpret_cast<const SmallMat*>(ws + P.off_small[k]), (int)small[k].size(),
-                                 k ? 64 : 32, P.small_max_mp[k], opts->iters, opts->beta, opts->prescale, 0,
+                                 k ? 64 : 32, P.small_max_mp[k], opts->iters, opts->beta, opts->prescale,
+                                 opts->prescale == ORTH_PRESCALE_SPECTRAL ? opts->power_iters : 0,
                                  opts->in_dtype, opts->out_dtype, status, fk.side(k)));
   rc = vjp_forward(P, ws, opts, n, status, true, s);
   if (rc) return rc;
@@ -2172,6 +2259,9 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   TableImage img;
   put(img, P.off_mats, P.mats);
   for (int k = 0; k < 2; ++k) put(img, P.off_small[k], P.small[k]);
+  put(img, P.off_power[0], P.power[0]);
+  put(img, P.off_power[1], P.power[1]);
+  put(img, P.off_bw, P.bw);
   put(img, P.off_partial_items, P.partial_items);
   put(img, P.off_scale_items, P.scale_items);
   put(img, P.off_f_gram, P.f_gram);
@@ -2203,7 +2293,9 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   for (int k = 0; k < 2; ++k)
     ORTH_HIP(launch_bjorck_small_vjp(reinterpret_cast<const SmallVjpMat*>(ws + P.off_small[k]),
                                      (int)P.small[k].size(), k ? 64 : 32, P.small_max_mp[k], T, beta,
-                                     opts->prescale, opts->in_dtype, opts->out_dtype, status, fk.side(k)));
+                                     opts->prescale,
+                                     opts->prescale == ORTH_PRESCALE_SPECTRAL ? opts->power_iters : 0,
+                                     opts->in_dtype, opts->out_dtype, status, fk.side(k)));
   // forward recomputation, saving X_t and E_t (X_T itself is never
   // needed), unless a saving forward left them in the workspace
   if (!opts->saved) {
@@ -2222,11 +2314,16 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
       ORTH_HIP(launch_bf16_tiles(cls, tm, TI(P.off_t_yu[cls][par]), (int)P.t_yu[cls][par].size(), beta, s, 1, t));
   }
   // derivative of the pre-scaling, in the caller's layout
-  if (opts->prescale == ORTH_PRESCALE_FROBENIUS) {
+  if (opts->prescale != ORTH_PRESCALE_NONE) {
     ORTH_HIP(launch_vjp_dot_partial(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                     partials, s));
     ORTH_HIP(launch_vjp_dot_finish(tm, n, partials, s));
   }
+  if (opts->prescale == ORTH_PRESCALE_SPECTRAL)
+    ORTH_HIP(launch_spec_bwd(tm, reinterpret_cast<const TiledMat*>(ws + P.off_bw), n,
+                             reinterpret_cast<const PowerItem*>(ws + P.off_power[0]), (int)P.power[0].size(),
+                             reinterpret_cast<const PowerItem*>(ws + P.off_power[1]), (int)P.power[1].size(),
+                             opts->power_iters, opts->in_dtype, status, s));
   ORTH_HIP(launch_vjp_writeout(tm, TI(P.off_partial_items), (int)P.partial_items.size(), opts->in_dtype,
                                opts->prescale, status, s));
   ORTH_HIP(fk.join());

@@ -113,7 +113,18 @@ struct TiledMat {
   double* px;                // X v (M)
   double* py;                // X^T X v (N)
   double* sig;               // sigma_hat
+  // Spectral pre-scaling in a vector-Jacobian product: the vectors of every
+  // power step (v_0 .. v_q at pst, then x_1 .. x_q, then y_1 .. y_q), the
+  // backward scalars (SB_* slots) and the 2q rank-1 pairs (a: M values, then
+  // b: N values, each pair M + N apart) that the power steps add to dL/dX.
+  double* pst;
+  double* sb;
+  double* pair;
+  int32_t pq;                // power steps q
 };
+
+// Slots of TiledMat::sb.
+enum { SB_FRO = 0, SB_SIGMA = 1, SB_BRANCH = 2, SB_DSCALE = 3, SB_C = 4, SB_SLOTS = 8 };
 
 struct TileItem {
   int32_t mat;
@@ -155,6 +166,11 @@ struct SmallVjpMat {
   int32_t status_index;
   int32_t np;                // LDS columns: 32 or 64
   float* save;
+  // spectral pre-scaling: the cached vector the differentiated forward
+  // started from (read only) and fp64 storage for the power steps' vectors
+  // and the rank-1 pairs of the backward
+  const float* u;
+  double* pst;
 };
 
 // One batched power-iteration work item: 64 outputs of a matrix-vector
@@ -296,15 +312,25 @@ hipError_t launch_bjorck_small(const SmallMat* mats, int n, int np, int max_mp, 
                                int prescale, int power_iters, int in_dtype, int out_dtype, int32_t* status,
                                hipStream_t s);
 hipError_t launch_bjorck_small_vjp(const SmallVjpMat* mats, int n, int np, int max_mp, int iters, float beta,
-                                   int prescale, int in_dtype, int gout_dtype, int32_t* status, hipStream_t s);
+                                   int prescale, int power_iters, int in_dtype, int gout_dtype, int32_t* status,
+                                   hipStream_t s);
 hipError_t launch_power_init(const TiledMat* mats, int n_mats, hipStream_t s);
+// vector-Jacobian product through spectral pre-scaling: the forward's power
+// vectors kept per step, then the backward through the steps (bw: the same
+// matrices with pv / px / py pointing at the backward's vectors)
+hipError_t launch_power_keep(const TiledMat* mats, int n_mats, int k, hipStream_t s);
+hipError_t launch_spec_bwd(const TiledMat* mats, const TiledMat* bw, int n_mats, const PowerItem* items0,
+                           int n_items0, const PowerItem* items1, int n_items1, int q, int in_dtype,
+                           const int32_t* status, hipStream_t s);
 hipError_t launch_power_dot(const TiledMat* mats, const PowerItem* items, int n_items, int in_dtype,
                             hipStream_t s);
 hipError_t launch_power_normalize(const TiledMat* mats, int n_mats, hipStream_t s);
 hipError_t launch_prescale_partial(const TiledMat* mats, const TileItem* items, int n_items,
                                    int in_dtype, double* partials, hipStream_t s);
+// write_u = 0: the spectral estimate is not handed back (a vector-Jacobian
+// product's recomputation); matrices with sb record ||W||_F and the scale
 hipError_t launch_prescale_finish(const TiledMat* mats, int n_mats, const double* partials,
-                                  int prescale, int32_t* status, hipStream_t s);
+                                  int prescale, int32_t* status, hipStream_t s, int write_u = 1);
 hipError_t launch_prescale_scale(const TiledMat* mats, const TileItem* items, int n_items,
                                  int in_dtype, int compute, hipStream_t s);
 hipError_t launch_writeout(const TiledMat* mats, const TileItem* items, int n_items,

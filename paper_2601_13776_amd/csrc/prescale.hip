@@ -75,7 +75,8 @@ __global__ __launch_bounds__(256) void prescale_partial_kernel(const TiledMat* _
 
 __global__ __launch_bounds__(256) void prescale_finish_kernel(const TiledMat* __restrict__ mats,
                                                               const double* __restrict__ partials,
-                                                              int prescale, int32_t* __restrict__ status) {
+                                                              int prescale, int32_t* __restrict__ status,
+                                                              int write_u) {
   __shared__ double red[4];
   const TiledMat& d = mats[blockIdx.x];
   if (d.fused) return;   // pre-scaled inside the fused small-matrix kernel
@@ -98,6 +99,10 @@ __global__ __launch_bounds__(256) void prescale_finish_kernel(const TiledMat* __
       // both terms are lower bounds of the largest singular value
       const double sigma = fmax(*d.sig, sqrt(tot) / sqrt((double)d.N));
       inv = (float)(1.0 / sigma);
+      if (d.sb) {
+        d.sb[SB_FRO] = sqrt(tot);
+        d.sb[SB_SIGMA] = sigma;
+      }
     }
     *d.inv_norm = inv;
     if (status) status[d.status_index] = st;
@@ -105,7 +110,7 @@ __global__ __launch_bounds__(256) void prescale_finish_kernel(const TiledMat* __
   }
   __syncthreads();
   // spectral: hand the new estimate back (a degenerate matrix keeps the old one)
-  if (prescale == ORTH_PRESCALE_SPECTRAL && st_sh == ORTH_MAT_OK)
+  if (prescale == ORTH_PRESCALE_SPECTRAL && st_sh == ORTH_MAT_OK && write_u)
     for (int j = threadIdx.x; j < d.N; j += 256) d.u[j] = (float)d.pv[j];
 }
 
@@ -224,10 +229,11 @@ hipError_t launch_prescale_partial(const TiledMat* mats, const TileItem* items, 
 }
 
 hipError_t launch_prescale_finish(const TiledMat* mats, int n_mats, const double* partials, int prescale,
-                                  int32_t* status, hipStream_t s) {
+                                  int32_t* status, hipStream_t s, int write_u) {
   if (n_mats <= 0) return hipSuccess;
   timing_begin("prescale_finish", s);
-  hipLaunchKernelGGL(prescale_finish_kernel, dim3(n_mats), dim3(256), 0, s, mats, partials, prescale, status);
+  hipLaunchKernelGGL(prescale_finish_kernel, dim3(n_mats), dim3(256), 0, s, mats, partials, prescale, status,
+                     write_u);
   hipError_t e = hipGetLastError();
   timing_end("prescale_finish", s);
   return e;

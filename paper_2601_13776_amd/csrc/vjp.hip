@@ -9,7 +9,11 @@
 //   writeout    : the derivative of W_0 = W / ||W||_F,
 //                   dL/dW = inv (Y_0 - <Y_0, W_0> W_0),  W_0 = inv W,
 //                 (Y_0 itself without pre-scaling), in the caller's layout;
-//                 zero for a zero matrix and NaN for a non-finite one
+//                 zero for a zero matrix and NaN for a non-finite one.
+//                 Spectral pre-scaling, W_0 = W / sigma, inv = 1 / sigma:
+//                   dL/dW = inv (Y_0 - dscale W) + sum_p a_p b_p^T
+//                 with dscale and the rank-1 pairs (tall orientation) from
+//                 the backward through the power steps (power.hip).
 //
 // HBM-bound; the transposed (wide) case goes through an LDS tile so that
 // both sides are accessed with coalesced rows.
@@ -154,8 +158,17 @@ __global__ __launch_bounds__(256) void vjp_writeout_kernel(const TiledMat* __res
   const float* gy = d.gy[d.gy_final];
   const int st = status[d.status_index];
   const float inv = *d.inv_norm;
-  const bool frob = prescale == ORTH_PRESCALE_FROBENIUS;
-  const float dscale = frob && st == ORTH_MAT_OK ? (float)(*d.dot) * inv : 0.f;
+  const bool spec = prescale == ORTH_PRESCALE_SPECTRAL;
+  const bool frob = prescale == ORTH_PRESCALE_FROBENIUS || spec;   // a term in W
+  const float dscale = st != ORTH_MAT_OK ? 0.f : spec ? (float)d.sb[SB_DSCALE] : (float)(*d.dot) * inv;
+  // rank-1 pairs of the power-iteration branch
+  const int npair = spec && st == ORTH_MAT_OK && d.sb[SB_BRANCH] != 0.0 ? 2 * d.pq : 0;
+  const int64_t pstride = (int64_t)d.M + d.N;
+  auto rank1 = [&](int ti, int tj) {   // tall row, tall column
+    double a = 0.0;
+    for (int p = 0; p < npair; ++p) a += d.pair[p * pstride + ti] * d.pair[p * pstride + d.M + tj];
+    return (float)a;
+  };
   if (!d.transposed && R + TB <= d.rows && C + TB <= d.cols && vec8_ok(d.in, d.ld_in, in_dtype) &&
       vec8_ok(d.out, d.ld_out, in_dtype) && vec8_ok(gy, d.Np, ORTH_F32)) {
 #pragma unroll
@@ -174,6 +187,8 @@ __global__ __launch_bounds__(256) void vjp_writeout_kernel(const TiledMat* __res
 #pragma unroll
           for (int i = 0; i < 8; ++i) v[i] = inv * (v[i] - dscale * w[i]);
         }
+        if (npair)
+          for (int i = 0; i < 8; ++i) v[i] += rank1(r, c + i);
       }
       store8_f32(d.out, (int64_t)r * d.ld_out + c, in_dtype, v);
     }
@@ -192,6 +207,7 @@ __global__ __launch_bounds__(256) void vjp_writeout_kernel(const TiledMat* __res
     } else if (frob) {
       const float w = load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype);
       v = inv * (tile[x][y] - dscale * w);
+      if (npair) v += d.transposed ? rank1(c, r) : rank1(r, c);
     } else {
       v = tile[x][y];
     }

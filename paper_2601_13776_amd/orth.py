@@ -186,7 +186,7 @@ def _mats(ins, outs):
     return arr
 
 
-def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile=0, saved=0):
+def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile=0, saved=0, need_u=True):
     in_dt = _dtype_code(ins[0]) if ins else ORTH_F32
     out_dt = _dtype_code(outs[0]) if outs else ORTH_F32
     for a, b in zip(ins, outs):
@@ -196,7 +196,7 @@ def _opts(ins, outs, iters, beta, prescale, compute, power_iters=1, u=None, tile
             "spectral": ORTH_PRESCALE_SPECTRAL}[prescale]
     comp = {"f32": ORTH_COMPUTE_F32, "bf16": ORTH_COMPUTE_BF16}[compute]
     uptr = None
-    if pres == ORTH_PRESCALE_SPECTRAL and ins:
+    if pres == ORTH_PRESCALE_SPECTRAL and ins and (need_u or u is not None):
         need = sum(min(t.shape[0], t.shape[1]) for t in ins)
         if u is None or u.dtype != torch.float32 or not u.is_contiguous() or u.numel() < need:
             raise ValueError(f"spectral pre-scaling needs u: a contiguous float32 tensor of {need} values "
@@ -267,13 +267,16 @@ def _vjp_mats(ws, gouts, gins):
 
 
 def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, prescale="frobenius", compute="f32",
-                                   status=None, workspace=None, stream=None, tile=0, saved=False):
+                                   status=None, workspace=None, stream=None, tile=0, saved=False, power_iters=1,
+                                   u=None):
     """dL/dW into grads_in[i] for L depending on ws[i] through
     orth_orthogonalize_batched with the same options, given grads_out[i] =
     dL/d(output) (see include/orth.h).  grads_in share the dtype of ws,
     grads_out that of the forward outputs.  saved=True takes the forward
     iterates from `workspace`, which orth_orthogonalize_save_batched filled
-    for the same ws and options.  Returns the workspace tensor."""
+    for the same ws and options.  prescale="spectral": u holds the cached
+    vectors as the differentiated forward found them (read only; not needed
+    with saved=True).  Returns the workspace tensor."""
     if saved and workspace is None:
         raise ValueError("saved=True needs the workspace of orth_orthogonalize_save_batched")
     if len(ws) != len(grads_out) or len(ws) != len(grads_in):
@@ -282,7 +285,8 @@ def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, pre
         if w.dtype != gi.dtype:
             raise TypeError("grads_in must have the dtype of ws")
     mats = _vjp_mats(ws, grads_out, grads_in)
-    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile, saved=1 if saved else 0)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute, power_iters, u, tile=tile, saved=1 if saved else 0,
+                 need_u=not saved)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_vjp_workspace_size")
@@ -298,12 +302,12 @@ def orth_orthogonalize_vjp_batched(ws, grads_out, grads_in, iters, beta=0.5, pre
 
 
 def orth_orthogonalize_save_batched(ins, outs, iters, beta=0.5, prescale="frobenius", compute="f32", status=None,
-                                    workspace=None, stream=None, tile=0):
+                                    workspace=None, stream=None, tile=0, power_iters=1, u=None):
     """orth_orthogonalize_batched that also keeps, in the returned workspace,
     the forward iterates that orth_orthogonalize_vjp_batched(..., saved=True,
     workspace=<it>) reuses (see include/orth.h).  outs must not be ins."""
     mats = _mats(ins, outs)
-    opts = _opts(ins, outs, iters, beta, prescale, compute, tile=tile)
+    opts = _opts(ins, outs, iters, beta, prescale, compute, power_iters, u, tile=tile)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_save_workspace_size(mats, len(ins), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_save_workspace_size")
@@ -319,10 +323,10 @@ def orth_orthogonalize_save_batched(ins, outs, iters, beta=0.5, prescale="froben
 
 
 def orth_orthogonalize_vjp_workspace_size(ws, iters, beta=0.5, prescale="frobenius", compute="f32",
-                                          grads_out=None, tile=0):
+                                          grads_out=None, tile=0, power_iters=1):
     grads_out = ws if grads_out is None else grads_out
     mats = _vjp_mats(ws, grads_out, ws)
-    opts = _opts(ws, grads_out, iters, beta, prescale, compute, tile=tile)
+    opts = _opts(ws, grads_out, iters, beta, prescale, compute, power_iters, tile=tile, need_u=False)
     n = ctypes.c_size_t()
     _check(lib().orth_orthogonalize_vjp_workspace_size(mats, len(ws), ctypes.byref(opts), ctypes.byref(n)),
            "orth_orthogonalize_vjp_workspace_size")

@@ -255,7 +255,7 @@ def test_save_and_saved_flag_errors(L):
     assert L.orth_orthogonalize_save_workspace_size(inplace, 1, ctypes.byref(opts), ctypes.byref(n)) \
         == orth.ORTH_EINVAL
     assert L.orth_orthogonalize_save_batched(inplace, 1, ctypes.byref(opts), None, 0, None, None) == orth.ORTH_EINVAL
-    spectral = orth.orth_bjorck_opts(3, 0.5, 2, 0, 0, 0, 1, 0x1000, 0)
+    spectral = orth.orth_bjorck_opts(3, 0.5, 2, 0, 0, 0, 17, 0x1000, 0)   # over 16 power steps
     assert L.orth_orthogonalize_save_workspace_size(_mats([(64, 32)]), 1, ctypes.byref(spectral),
                                                     ctypes.byref(n)) == orth.ORTH_EUNSUPPORTED
     # too small a workspace: rejected before anything is enqueued
@@ -359,11 +359,32 @@ def test_spectral_validation(L, q, u, code):
     assert rc == code
 
 
-def test_vjp_rejects_spectral(L):
-    opts = orth.orth_bjorck_opts(5, 0.5, orth.ORTH_PRESCALE_SPECTRAL, 0, 0, 0, 1, 0x1000)
+def test_vjp_spectral_validation(L):
+    """The VJP through spectral pre-scaling takes 1..16 power steps, needs the
+    cached vectors unless it reuses a saving forward's workspace, and its
+    workspace grows with the number of power steps."""
     n = ctypes.c_size_t()
-    rc = L.orth_orthogonalize_vjp_workspace_size(_vjp_mats([(64, 32)]), 1, ctypes.byref(opts), ctypes.byref(n))
-    assert rc == orth.ORTH_EUNSUPPORTED
+    mats = _vjp_mats([(64, 32), (300, 200)])
+
+    def size(q, u, saved=0):
+        opts = orth.orth_bjorck_opts(5, 0.5, orth.ORTH_PRESCALE_SPECTRAL, 0, 0, 0, q, u, 0, saved)
+        rc = L.orth_orthogonalize_vjp_workspace_size(mats, 2, ctypes.byref(opts), ctypes.byref(n))
+        return rc, n.value
+
+    rc1, n1 = size(1, 0x1000)
+    rc3, n3 = size(3, 0x1000)
+    assert rc1 == rc3 == orth.ORTH_OK and n3 > n1
+    assert size(17, 0x1000)[0] == orth.ORTH_EUNSUPPORTED
+    assert size(0, 0x1000)[0] == orth.ORTH_EINVAL
+    assert size(1, None)[0] == orth.ORTH_EINVAL
+    assert size(1, None, saved=1) == (orth.ORTH_OK, n1)
+    # the saving forward lays out the same workspace
+    opts = orth.orth_bjorck_opts(5, 0.5, orth.ORTH_PRESCALE_SPECTRAL, 0, 0, 0, 1, 0x1000)
+    arr = (orth.orth_mat * 2)()
+    arr[0] = orth.orth_mat(0x1000, 0x2000, 64, 32, 32, 32)
+    arr[1] = orth.orth_mat(0x3000, 0x4000, 300, 200, 200, 200)
+    assert L.orth_orthogonalize_save_workspace_size(arr, 2, ctypes.byref(opts), ctypes.byref(n)) == orth.ORTH_OK
+    assert n.value == n1
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -362,3 +362,133 @@ def test_layer_vjp_chain():
     got_p = np.stack([to_f64(t) for t in gins[g:]]).reshape(ref_p.shape)
     assert checks.relative_difference(got_r, ref_r) <= REL_F32
     assert checks.relative_difference(got_p, ref_p) <= REL_F32
+
+
+# ------------------------------------------- spectral pre-scaling (f1 x f2) --
+
+def cached_vectors(seed, shapes):
+    rng = np.random.default_rng(seed)
+    return [rng.standard_normal(min(s)).astype(np.float32) for s in shapes]
+
+
+def spectral_vjp(st, gouts, us, iters, q, compute="f32", tile=0):
+    ws = [to_dev(s) for s in st]
+    gos = [torch.from_numpy(g).to(DEV) for g in gouts]
+    gis = [torch.empty(w.shape, dtype=w.dtype, device=DEV) for w in ws]
+    u = torch.from_numpy(np.concatenate(us)).to(DEV)
+    u_before = u.clone()
+    status = torch.full((len(ws),), -1, dtype=torch.int32, device=DEV)
+    orth.orth_orthogonalize_vjp_batched(ws, gos, gis, iters, compute=compute, status=status, tile=tile,
+                                        prescale="spectral", power_iters=q, u=u)
+    torch.cuda.synchronize()
+    assert torch.equal(u, u_before), "the vector-Jacobian product must not write the cached vectors"
+    return gis, status.cpu().numpy()
+
+
+SPEC_SHAPES_F32 = [(16, 8), (8, 16), (40, 40), (128, 64), (100, 50), (65, 65), (200, 130), (130, 300), (512, 256)]
+
+
+@pytest.mark.parametrize("q", [1, 3])
+def test_vjp_spectral_f32_mixed_batch(q):
+    """Spectral pre-scaling from cached vectors (held constant) through q
+    power steps: small (fused kernel) and tiled matrices, tall and wide,
+    against oracle.spectral.bjorck_spectral_vjp."""
+    from oracle import spectral
+    print(f"[vjp spectral f32] q={q}", flush=True)
+    st = stored(221, SPEC_SHAPES_F32)
+    gouts = upstream(222, SPEC_SHAPES_F32)
+    us = cached_vectors(223, SPEC_SHAPES_F32)
+    gis, status = spectral_vjp(st, gouts, us, 8, q)
+    assert np.all(status == 0)
+    for s, g, u, o, shape in zip(st, gouts, us, gis, SPEC_SHAPES_F32):
+        ref = spectral.bjorck_spectral_vjp(wl.as_f64(s), u.astype(np.float64), g.astype(np.float64), 8, q)
+        rel = checks.relative_difference(to_f64(o), ref)
+        assert rel <= REL_F32, (shape, q, rel)
+
+
+def test_vjp_spectral_floor_branch():
+    """Cached vectors on a small singular direction: the power estimate stays
+    below ||W||_F / sqrt(N), the floor sets the scale and its derivative
+    applies (fused and tiled matrices).  Singular values near 1.5 and 1
+    keep the largest one of W_0 below sqrt(3) under the floor's scale."""
+    from oracle import spectral
+    rng = np.random.default_rng(224)
+    shapes = [(48, 40), (200, 130)]
+    st, us = [], []
+    for r, c in shapes:
+        w = 0.001 * rng.standard_normal((r, c))
+        w[np.arange(c), np.arange(c)] += 1.0
+        w[0, 0] = 1.5
+        st.append(w.astype(np.float32))
+        u = np.zeros(c, dtype=np.float32)
+        u[1] = 1.0
+        us.append(u)
+    gouts = upstream(225, shapes)
+    for s, u in zip(st, us):
+        _, _, sigma, _ = spectral.spectral_prescale(s.astype(np.float64), u.astype(np.float64), 1)
+        floor = np.sqrt(np.sum(s.astype(np.float64) ** 2)) / np.sqrt(min(s.shape))
+        assert abs(sigma - floor) <= 1e-12 * floor
+    gis, status = spectral_vjp(st, gouts, us, 6, 1)
+    assert np.all(status == 0)
+    for s, g, u, o in zip(st, gouts, us, gis):
+        ref = spectral.bjorck_spectral_vjp(s.astype(np.float64), u.astype(np.float64), g.astype(np.float64), 6, 1)
+        assert checks.relative_difference(to_f64(o), ref) <= REL_F32, s.shape
+
+
+SPEC_SHAPES_BF16 = [(128, 64), (64, 100), (256, 128), (300, 700), (1024, 512), (512, 512)]
+
+
+@pytest.mark.parametrize("q", [1, 2])
+def test_vjp_spectral_bf16_mixed_batch(q):
+    from oracle import spectral
+    print(f"[vjp spectral bf16] q={q}", flush=True)
+    st = stored(226, SPEC_SHAPES_BF16, "bf16")
+    gouts = upstream(227, SPEC_SHAPES_BF16)
+    us = cached_vectors(228, SPEC_SHAPES_BF16)
+    gis, status = spectral_vjp(st, gouts, us, 20, q, compute="bf16")
+    assert np.all(status == 0)
+    for s, g, u, o, shape in zip(st, gouts, us, gis, SPEC_SHAPES_BF16):
+        ref = spectral.bjorck_spectral_vjp(wl.as_f64(s), u.astype(np.float64), g.astype(np.float64), 20, q)
+        rel = checks.relative_difference(to_f64(o), ref)
+        bound = REL_BF16_SQUARE if shape[0] == shape[1] else REL_BF16_RECT
+        assert rel <= bound, (shape, q, rel)
+
+
+def test_vjp_spectral_saved_and_statuses():
+    """The training pattern with spectral pre-scaling: the saving forward
+    gives the outputs and new cached vectors of orth_orthogonalize_batched,
+    and the VJP from its workspace (no cached vectors passed) equals the
+    recomputing VJP given the vectors the forward started from, bit for
+    bit; a zero matrix gets a zero gradient."""
+    shapes = [(40, 20), (96, 96), (300, 200), (130, 64)]
+    st = stored(229, shapes)
+    st[1][:] = 0
+    ins = [to_dev(s) for s in st]
+    us = cached_vectors(230, shapes)
+    u0 = torch.from_numpy(np.concatenate(us)).to(DEV)
+    gouts = [torch.from_numpy(g).to(DEV) for g in upstream(231, shapes)]
+    # plain forward
+    u_a = u0.clone()
+    outs_a = [torch.empty(s, device=DEV) for s in shapes]
+    orth.orth_orthogonalize_batched(ins, outs_a, 7, prescale="spectral", power_iters=2, u=u_a)
+    # saving forward, then the saved VJP
+    u_b = u0.clone()
+    outs_b = [torch.empty(s, device=DEV) for s in shapes]
+    status = torch.full((len(shapes),), -1, dtype=torch.int32, device=DEV)
+    tape = orth.orth_orthogonalize_save_batched(ins, outs_b, 7, prescale="spectral", power_iters=2, u=u_b,
+                                                status=status)
+    g_saved = [torch.empty_like(t) for t in ins]
+    orth.orth_orthogonalize_vjp_batched(ins, gouts, g_saved, 7, prescale="spectral", power_iters=2,
+                                        workspace=tape, saved=True)
+    # recomputing VJP from the vectors the forward started from
+    g_rec = [torch.empty_like(t) for t in ins]
+    orth.orth_orthogonalize_vjp_batched(ins, gouts, g_rec, 7, prescale="spectral", power_iters=2, u=u0.clone())
+    torch.cuda.synchronize()
+    assert list(status.cpu().numpy()) == [0, 1, 0, 0]
+    # same arithmetic in both plans (tile lists differ only in order)
+    assert torch.allclose(u_a, u_b, rtol=1e-6, atol=1e-7)
+    for a, b, shape in zip(outs_a, outs_b, shapes):
+        assert checks.relative_difference(to_f64(a), to_f64(b)) <= 1e-6, shape
+    for a, b in zip(g_saved, g_rec):
+        assert torch.equal(a, b)
+    assert bool((g_rec[1] == 0).all())
