@@ -10,7 +10,9 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <list>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -331,6 +333,79 @@ static int upload_tables(const TableImage& img, void* dst, hipStream_t s) {
   return ORTH_OK;
 }
 
+// ----------------------------------------------------------- plan cache ---
+// The plans of recent calls, keyed by the exact argument values that
+// determine them (descriptors, options, workspace address): a call that
+// repeats an earlier one (a training loop) skips the host planning, which
+// costs from tens of microseconds to tens of milliseconds.  The descriptor
+// tables are still copied into the workspace on every call, so nothing
+// depends on the workspace's contents between calls.  ORTH_PLAN_CACHE=0
+// turns the cache off.
+namespace {
+struct PlanKey {
+  std::string k;
+  template <typename T>
+  void add(const T& v) {
+    k.append(reinterpret_cast<const char*>(&v), sizeof(T));
+  }
+  void add_bytes(const void* p, size_t n) {
+    if (n) k.append(static_cast<const char*>(p), n);
+  }
+  void add_opts(const orth_bjorck_opts* o) {
+    add(o->iters);
+    add(o->beta);
+    add(o->prescale);
+    add(o->in_dtype);
+    add(o->out_dtype);
+    add(o->compute);
+    add(o->power_iters);
+    add(o->u);
+    add(o->tile);
+    add(o->saved);
+  }
+};
+
+bool plan_cache_on() {
+  static const bool on = [] {
+    const char* v = std::getenv("ORTH_PLAN_CACHE");
+    return !(v && *v && std::atoi(v) == 0);
+  }();
+  return on;
+}
+
+template <typename Plan>
+class PlanCache {
+ public:
+  // build fills a plan; seal_plan(Plan&) seals its GEMM lists so that the
+  // cached plan is never modified again
+  template <typename Build>
+  std::shared_ptr<const Plan> get(const std::string& key, Build&& build) {
+    if (plan_cache_on()) {
+      std::lock_guard<std::mutex> lk(mu_);
+      for (auto it = lru_.begin(); it != lru_.end(); ++it)
+        if (it->first == key) {
+          lru_.splice(lru_.begin(), lru_, it);
+          return lru_.front().second;
+        }
+    }
+    auto p = std::make_shared<Plan>();
+    build(*p);
+    seal_plan(*p);
+    if (plan_cache_on()) {
+      std::lock_guard<std::mutex> lk(mu_);
+      lru_.emplace_front(key, p);
+      if (lru_.size() > kEntries) lru_.pop_back();
+    }
+    return p;
+  }
+
+ private:
+  static constexpr size_t kEntries = 4;
+  std::mutex mu_;
+  std::list<std::pair<std::string, std::shared_ptr<const Plan>>> lru_;
+};
+}  // namespace
+
 // ------------------------------------------------------------ layout ----
 namespace {
 constexpr size_t kAlign = 256;
@@ -415,11 +490,19 @@ struct GemmList {
   size_t bytes() const { return items_bytes() + align_up(tiles.size() * sizeof(GemmTile)); }
 };
 
-void put(TableImage& img, size_t off, GemmList& g) {
+// Tiles of the products added whole, and the k-major tiles moved to the
+// end: a list is sealed once its plan is complete, before any upload.
+void seal(GemmList& g) {
   g.finalize();
   g.partition_km();
+}
+void put(TableImage& img, size_t off, const GemmList& g) {
   img.add(off, g.items.data(), g.items.size() * sizeof(GemmItem));
   img.add(off + g.items_bytes(), g.tiles.data(), g.tiles.size() * sizeof(GemmTile));
+}
+void put(TableImage& img, size_t off, GemmList& g) {
+  seal(g);
+  put(img, off, static_cast<const GemmList&>(g));
 }
 
 // Longest reductions first (stable: a product's tiles keep their order), so
@@ -496,6 +579,12 @@ void log_ortho_plan(const char* entry, const OrthoPlan& P, const orth_bjorck_opt
     for (size_t i = 0; i < P.mp.size(); ++i)
       log_line("%s:   matrix %zu: %d x %d (tall), padded %d x %d, bucket %d%s", entry, i, P.mp[i].M, P.mp[i].N,
                P.mp[i].Mp, P.mp[i].Np, P.mp[i].bucket, P.mp[i].transposed ? ", transposed" : "");
+}
+
+void seal_plan(OrthoPlan& P) {
+  seal(P.f32_gram);
+  seal(P.f32_update[0]);
+  seal(P.f32_update[1]);
 }
 
 int validate_ortho(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o) {
@@ -838,6 +927,11 @@ struct ConvPlan {
   size_t table_bytes = 0, total_bytes = 0;
 };
 
+void seal_plan(ConvPlan& P) {
+  seal(P.proj_items);
+  for (auto& g : P.phase_gemm) seal(g);
+}
+
 int validate_conv_descs(const orth_conv_desc* d, int32_t n, int32_t dtype) {
   if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
   if (n > 0 && !d) return fail(ORTH_EINVAL, "descs is NULL");
@@ -1006,6 +1100,15 @@ struct ConvVjpPlan {
   size_t off_save_scatter = 0;
   size_t table_bytes = 0, total_bytes = 0;
 };
+
+void seal_plan(ConvVjpPlan& P) {
+  seal(P.proj_items);
+  seal(P.last_dp);
+  seal(P.dv_items);
+  for (auto& g : P.fwd_gemm) seal(g);
+  for (auto& g : P.bwd_gemm) seal(g);
+  for (auto& g : P.save_gemm) seal(g);
+}
 
 int validate_conv_vjp_descs(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype) {
   if (n < 0) return fail(ORTH_EINVAL, "n must be >= 0");
@@ -1550,6 +1653,15 @@ void log_vjp_plan(const char* entry, const VjpPlan& P, int n) {
            P.f_gram.size(), P.f_upd.size(), P.b_s[0].size(), P.b_upd[0].size(), P.total_bytes, P.table_bytes);
 }
 
+void seal_plan(VjpPlan& P) {
+  seal(P.f_gram);
+  seal(P.f_upd);
+  for (int par = 0; par < 2; ++par) {
+    seal(P.b_s[par]);
+    seal(P.b_upd[par]);
+  }
+}
+
 constexpr int kVjpMaxPowerIters = 16;
 
 int validate_vjp(const orth_vjp_mat* mats, int32_t n, const orth_bjorck_opts* o) {
@@ -1950,13 +2062,17 @@ int ortho_enqueue(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
   int rc = validate_ortho(mats, n, opts);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
-  OrthoPlan P;
-  build_ortho_plan(mats, n, opts, P, nullptr, true);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  static PlanCache<OrthoPlan> cache;
+  PlanKey key;
+  key.add(n);
+  key.add_bytes(mats, sizeof(orth_mat) * n);
+  key.add_opts(opts);
+  key.add(ws);
+  const auto Pp = cache.get(key.k, [&](OrthoPlan& P) { build_ortho_plan(mats, n, opts, P, ws, true); });
+  const OrthoPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = OrthoPlan();
-  build_ortho_plan(mats, n, opts, P, ws, true);
   log_ortho_plan(entry, P, opts);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
 
@@ -2151,13 +2267,17 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   int rc = save_descs(mats, n, opts, vm);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
-  VjpPlan P;
-  build_vjp_plan(vm.data(), n, opts, P, nullptr);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  static PlanCache<VjpPlan> cache;
+  PlanKey key;
+  key.add(n);
+  key.add_bytes(vm.data(), sizeof(orth_vjp_mat) * n);
+  key.add_opts(opts);
+  key.add(ws);
+  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(vm.data(), n, opts, P, ws); });
+  const VjpPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = VjpPlan();
-  build_vjp_plan(vm.data(), n, opts, P, ws);
   log_vjp_plan("orth_orthogonalize_save_batched", P, n);
   hipStream_t s = static_cast<hipStream_t>(stream);
   // statuses go to the workspace, where the saved product reads them, and
@@ -2165,8 +2285,9 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   int32_t* status = reinterpret_cast<int32_t*>(ws + P.off_status);
   // X_T of a tiled matrix: the fp32 iterate (bf16 products, updated in
   // place) or saved slot T (fp32 products)
+  std::vector<TiledMat> fwd_mats = P.mats;
   for (int i = 0; i < n; ++i) {
-    TiledMat& t = P.mats[i];
+    TiledMat& t = fwd_mats[i];
     if (t.fused) continue;
     t.master[1] = P.bucket[i] == V_F32 ? t.master[0] + (int64_t)opts->iters * t.Mp * t.Np : t.master[0];
   }
@@ -2192,7 +2313,7 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
       small[k].push_back(sm);
     }
   TableImage img;
-  put(img, P.off_mats, P.mats);
+  put(img, P.off_mats, fwd_mats);
   for (int k = 0; k < 2; ++k) put(img, P.off_small[k], small[k]);
   put(img, P.off_power[0], P.power[0]);
   put(img, P.off_power[1], P.power[1]);
@@ -2242,13 +2363,17 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   int rc = validate_vjp(mats, n, opts);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
-  VjpPlan P;
-  build_vjp_plan(mats, n, opts, P, nullptr);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  static PlanCache<VjpPlan> cache;
+  PlanKey key;
+  key.add(n);
+  key.add_bytes(mats, sizeof(orth_vjp_mat) * n);
+  key.add_opts(opts);
+  key.add(ws);
+  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(mats, n, opts, P, ws); });
+  const VjpPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = VjpPlan();
-  build_vjp_plan(mats, n, opts, P, ws);
   log_vjp_plan("orth_orthogonalize_vjp_batched", P, n);
   hipStream_t s = static_cast<hipStream_t>(stream);
   // with saved iterates the statuses of the saving forward are in the
@@ -2360,13 +2485,17 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
   int rc = validate_conv_descs(descs, n, dtype);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
-  ConvPlan P;
-  build_conv_plan(descs, n, dtype, P, nullptr);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  static PlanCache<ConvPlan> cache;
+  PlanKey key;
+  key.add(n);
+  key.add(dtype);
+  key.add_bytes(descs, sizeof(orth_conv_desc) * n);
+  key.add(ws);
+  const auto Pp = cache.get(key.k, [&](ConvPlan& P) { build_conv_plan(descs, n, dtype, P, ws); });
+  const ConvPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = ConvPlan();
-  build_conv_plan(descs, n, dtype, P, ws);
   if (log_level() >= 1) {
     size_t tiles = P.proj_items.size();
     for (const auto& g : P.phase_gemm) tiles += g.size();
@@ -2416,13 +2545,19 @@ namespace {
 int conv_vjp_run(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void* workspace,
                  size_t workspace_bytes, void* stream, int mode, const void* const* kernels) {
   if (n == 0) return ORTH_OK;
-  ConvVjpPlan P;
-  build_conv_vjp_plan(descs, n, dtype, P, nullptr);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  static PlanCache<ConvVjpPlan> cache;
+  PlanKey key;
+  key.add(n);
+  key.add(dtype);
+  key.add(mode);
+  key.add_bytes(descs, sizeof(orth_conv_vjp_desc) * n);
+  key.add_bytes(kernels, kernels ? sizeof(void*) * n : 0);
+  key.add(ws);
+  const auto Pp = cache.get(key.k, [&](ConvVjpPlan& P) { build_conv_vjp_plan(descs, n, dtype, P, ws, kernels); });
+  const ConvVjpPlan& P = *Pp;
   int rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = ConvVjpPlan();
-  build_conv_vjp_plan(descs, n, dtype, P, ws, kernels);
   if (log_level() >= 1)
     log_line("composition VJP (mode %d): %d layers, %zu block steps; workspace %zu bytes (tables %zu)", mode, n,
              P.fwd_gemm.size(), P.total_bytes, P.table_bytes);
@@ -2564,13 +2699,11 @@ int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* o
   int rc = validate_exp(mats, n, opts);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
   ExpPlan P;
-  build_exp_plan(mats, n, opts, P, nullptr);
+  build_exp_plan(mats, n, opts, P, ws);
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = ExpPlan();
-  build_exp_plan(mats, n, opts, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* status = status_dev ? status_dev : reinterpret_cast<int32_t*>(ws + P.off_status);
   TableImage img;
@@ -2620,13 +2753,11 @@ int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dt
   int rc = validate_conv_exp(descs, n, dtype);
   if (rc) return rc;
   if (n == 0) return ORTH_OK;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
   ExpPlan P;
-  build_conv_exp_plan(descs, n, dtype, P, nullptr);
+  build_conv_exp_plan(descs, n, dtype, P, ws);
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  P = ExpPlan();
-  build_conv_exp_plan(descs, n, dtype, P, ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
   TableImage img;
   put(img, P.off_items, P.items);
