@@ -411,6 +411,13 @@ namespace {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+// Base address a plan is laid out from: the workspace, or (sizing only, or
+// a missing workspace that the call then rejects) a stand-in that is never
+// dereferenced, so that the planners' address arithmetic never starts from
+// a null pointer.
+inline unsigned char* plan_base(void* ws) {
+  return ws ? static_cast<unsigned char*>(ws) : reinterpret_cast<unsigned char*>(uintptr_t(1) << 44);
+}
 
 struct Arena {
   size_t off = 0;
@@ -1188,7 +1195,8 @@ void build_conv_vjp_plan(const orth_conv_vjp_desc* d, int32_t n, int32_t dtype, 
       }
       P.save_scatter.clear();
     }
-    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 && ws) ? ws + off : nullptr; };
+    // (pass 0 lays out from the stand-in base: its addresses are discarded)
+    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 ? ws : plan_base(nullptr)) + off; };
     auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
 
     for (int li = 0; li < n; ++li) {
@@ -1550,7 +1558,8 @@ void build_conv_exp_plan(const orth_conv_exp_desc* d, int32_t n, int32_t dtype, 
       P.scatter.clear();
       for (auto& s : P.steps) s.clear();
     }
-    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 && ws) ? ws + off : nullptr; };
+    // (pass 0 lays out from the stand-in base: its addresses are discarded)
+    auto dev = [&](size_t off) -> unsigned char* { return (pass == 1 ? ws : plan_base(nullptr)) + off; };
     auto fbuf = [&](int64_t elems) { return reinterpret_cast<float*>(dev(A.take((size_t)elems * 4))); };
     for (int li = 0; li < n; ++li) {
       const orth_conv_exp_desc& L = d[li];
@@ -2069,7 +2078,7 @@ int ortho_enqueue(const orth_mat* mats, int32_t n, const orth_bjorck_opts* opts,
   key.add_bytes(mats, sizeof(orth_mat) * n);
   key.add_opts(opts);
   key.add(ws);
-  const auto Pp = cache.get(key.k, [&](OrthoPlan& P) { build_ortho_plan(mats, n, opts, P, ws, true); });
+  const auto Pp = cache.get(key.k, [&](OrthoPlan& P) { build_ortho_plan(mats, n, opts, P, plan_base(ws), true); });
   const OrthoPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
@@ -2173,7 +2182,7 @@ int orth_orthogonalize_workspace_size(const orth_mat* mats, int32_t n, const ort
   int rc = validate_ortho(mats, n, opts);
   if (rc) return rc;
   OrthoPlan P;
-  build_ortho_plan(mats, n, opts, P, nullptr, true);
+  build_ortho_plan(mats, n, opts, P, plan_base(nullptr), true);
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2256,7 +2265,7 @@ int orth_orthogonalize_save_workspace_size(const orth_mat* mats, int32_t n, cons
   int rc = save_descs(mats, n, opts, vm);
   if (rc) return rc;
   VjpPlan P;
-  build_vjp_plan(vm.data(), n, opts, P, nullptr);
+  build_vjp_plan(vm.data(), n, opts, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2274,7 +2283,7 @@ int orth_orthogonalize_save_batched(const orth_mat* mats, int32_t n, const orth_
   key.add_bytes(vm.data(), sizeof(orth_vjp_mat) * n);
   key.add_opts(opts);
   key.add(ws);
-  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(vm.data(), n, opts, P, ws); });
+  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(vm.data(), n, opts, P, plan_base(ws)); });
   const VjpPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
@@ -2353,7 +2362,7 @@ int orth_orthogonalize_vjp_workspace_size(const orth_vjp_mat* mats, int32_t n, c
   int rc = validate_vjp(mats, n, opts);
   if (rc) return rc;
   VjpPlan P;
-  build_vjp_plan(mats, n, opts, P, nullptr);
+  build_vjp_plan(mats, n, opts, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2370,7 +2379,7 @@ int orth_orthogonalize_vjp_batched(const orth_vjp_mat* mats, int32_t n, const or
   key.add_bytes(mats, sizeof(orth_vjp_mat) * n);
   key.add_opts(opts);
   key.add(ws);
-  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(mats, n, opts, P, ws); });
+  const auto Pp = cache.get(key.k, [&](VjpPlan& P) { build_vjp_plan(mats, n, opts, P, plan_base(ws)); });
   const VjpPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
@@ -2475,7 +2484,7 @@ int orth_build_conv_kernels_workspace_size(const orth_conv_desc* descs, int32_t 
   int rc = validate_conv_descs(descs, n, dtype);
   if (rc) return rc;
   ConvPlan P;
-  build_conv_plan(descs, n, dtype, P, nullptr);
+  build_conv_plan(descs, n, dtype, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2492,7 +2501,7 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
   key.add(dtype);
   key.add_bytes(descs, sizeof(orth_conv_desc) * n);
   key.add(ws);
-  const auto Pp = cache.get(key.k, [&](ConvPlan& P) { build_conv_plan(descs, n, dtype, P, ws); });
+  const auto Pp = cache.get(key.k, [&](ConvPlan& P) { build_conv_plan(descs, n, dtype, P, plan_base(ws)); });
   const ConvPlan& P = *Pp;
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
@@ -2533,7 +2542,7 @@ int orth_build_conv_kernels_vjp_workspace_size(const orth_conv_vjp_desc* descs, 
   const int rc = validate_conv_vjp_descs(descs, n, dtype);
   if (rc) return rc;
   ConvVjpPlan P;
-  build_conv_vjp_plan(descs, n, dtype, P, nullptr);
+  build_conv_vjp_plan(descs, n, dtype, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2554,7 +2563,8 @@ int conv_vjp_run(const orth_conv_vjp_desc* descs, int32_t n, int32_t dtype, void
   key.add_bytes(descs, sizeof(orth_conv_vjp_desc) * n);
   key.add_bytes(kernels, kernels ? sizeof(void*) * n : 0);
   key.add(ws);
-  const auto Pp = cache.get(key.k, [&](ConvVjpPlan& P) { build_conv_vjp_plan(descs, n, dtype, P, ws, kernels); });
+  const auto Pp =
+      cache.get(key.k, [&](ConvVjpPlan& P) { build_conv_vjp_plan(descs, n, dtype, P, plan_base(ws), kernels); });
   const ConvVjpPlan& P = *Pp;
   int rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
@@ -2654,7 +2664,7 @@ int orth_build_conv_kernels_save_workspace_size(const orth_conv_desc* descs, int
   const int rc = conv_save_descs(descs, n, dtype, vd, kernels);
   if (rc) return rc;
   ConvVjpPlan P;
-  build_conv_vjp_plan(vd.data(), n, dtype, P, nullptr);
+  build_conv_vjp_plan(vd.data(), n, dtype, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2689,7 +2699,7 @@ int orth_exp_map_workspace_size(const orth_mat* mats, int32_t n, const orth_exp_
   const int rc = validate_exp(mats, n, opts);
   if (rc) return rc;
   ExpPlan P;
-  build_exp_plan(mats, n, opts, P, nullptr);
+  build_exp_plan(mats, n, opts, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2701,7 +2711,7 @@ int orth_exp_map_batched(const orth_mat* mats, int32_t n, const orth_exp_opts* o
   if (n == 0) return ORTH_OK;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   ExpPlan P;
-  build_exp_plan(mats, n, opts, P, ws);
+  build_exp_plan(mats, n, opts, P, plan_base(ws));
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -2743,7 +2753,7 @@ int orth_conv_exp_workspace_size(const orth_conv_exp_desc* descs, int32_t n, int
   const int rc = validate_conv_exp(descs, n, dtype);
   if (rc) return rc;
   ExpPlan P;
-  build_conv_exp_plan(descs, n, dtype, P, nullptr);
+  build_conv_exp_plan(descs, n, dtype, P, plan_base(nullptr));
   *bytes = P.total_bytes;
   return ORTH_OK;
 }
@@ -2755,7 +2765,7 @@ int orth_conv_exp_batched(const orth_conv_exp_desc* descs, int32_t n, int32_t dt
   if (n == 0) return ORTH_OK;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   ExpPlan P;
-  build_conv_exp_plan(descs, n, dtype, P, ws);
+  build_conv_exp_plan(descs, n, dtype, P, plan_base(ws));
   rc = check_workspace(workspace, workspace_bytes, P.total_bytes);
   if (rc) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
