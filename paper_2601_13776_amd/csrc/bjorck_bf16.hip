@@ -12,7 +12,9 @@
 //            upper tile E[k-block, J] is read transposed.  The epilogue
 //            updates the fp32 iterate in place (each tile reads and writes
 //            only its own elements) and emits the next bf16 copy (ping-pong:
-//            other tiles still read the current one).
+//            other tiles still read the current one); the last two k-steps
+//            already load the first two 32-row chunks of the iterate in
+//            place of the loads that would only re-read a k-step.
 //
 // Every work item names its matrix, tile, mode (Gram or update) and
 // ping-pong parity, so one launch can cover any mix of tiles.
@@ -33,6 +35,8 @@
 // fences keep LDS reads and loads interleaved with MFMAs.  Work items come
 // from a table whose order the host chooses so that concurrently running
 // tiles share operand panels through the caches.
+#include <type_traits>
+
 #include "internal.h"
 
 namespace orth {
@@ -174,6 +178,26 @@ struct Operand {
 #pragma unroll
     for (int i = 0; i < NBLK; ++i) dma16(b + off[i], lds + (i * NW + wave) * 512);
   }
+  // the same loads, or (pf: a k-step past the end, whose loads only keep
+  // the wait counts) 1 KB pieces q0 + i of an epilogue prefetch: a piece is
+  // RPP rows of TN fp32 values starting at row RPP q of chunk base pfb (row
+  // stride pfr bytes), 4 values per lane
+  template <int TN>
+  __device__ __forceinline__ void issue_pf(uint16_t* lds, int k0, int wave, int lane, bool pf, const char* pfb,
+                                           int64_t pfr, int q0) const {
+    constexpr int RPP = 256 / TN;
+    const char* b = base + (TRANS ? (int64_t)k0 * ld * 2 : (int64_t)k0 * 2);
+    // both addresses are formed and one is kept by a mask (a uniform
+    // condition would otherwise become a branch inside the scheduled k-step)
+    const uint64_t keep = pf ? ~0ull : 0ull;
+#pragma unroll
+    for (int i = 0; i < NBLK; ++i) {
+      const uint64_t a = reinterpret_cast<uint64_t>(b + off[i]);
+      const uint64_t p = reinterpret_cast<uint64_t>(pfb) +
+                         (uint64_t)(((q0 + i) * RPP + lane / (TN / 4)) * pfr + (lane % (TN / 4)) * 16);
+      dma16(reinterpret_cast<const char*>((a & ~keep) | (p & keep)), lds + (i * NW + wave) * 512);
+    }
+  }
   // fragment f of sub-step kk (16 k) from LDS stage `lds`
   __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int f, int kk) const {
     if (!TRANS) {
@@ -211,11 +235,22 @@ struct Tile {
 // branching: the barrier's partial wait relies on this k-step's A loads
 // being the newest in flight (skipped, they would let the next k-step's B
 // loads pass the barrier unfinished).
-template <int BM, int BN, int WM, int WN, bool AT, bool BT>
+// Epilogue prefetch of an update tile: in the last two k-steps of its final
+// K loop the loads would re-read a valid k-step (see kloop); instead they
+// fetch the first two 32-row chunks of this wave's part of the fp32
+// iterate, A loads the first pieces and B loads the rest of a chunk.  The
+// chunk of k-step kt (kt + 2 - nk = 0 or 1) lands in that k-step's free A
+// buffer and its B buffer (blocks (i * 4 + wave), as the operand loads).
+struct Prefetch {
+  const char* base = nullptr;   // the wave's part of the iterate (wave-uniform)
+  int64_t row = 0;              // bytes between iterate rows
+};
+
+template <int BM, int BN, int WM, int WN, bool AT, bool BT, bool PF = false>
 __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32], const uint16_t* A, int64_t lda,
                                       const uint16_t* B, int64_t ldb, int kb, int ke, uint16_t* sA0, uint16_t* sB0,
                                       uint16_t* sA1, uint16_t* sB1, uint16_t* sX, int wave, int lane, int wm,
-                                      int wn) {
+                                      int wn, Prefetch pf = Prefetch()) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int MI = T::MI, NI = T::NI, BK = T::BK;
   const int nk = (ke - kb) / BK;
@@ -254,8 +289,13 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
   auto kstep = [&](uint16_t* ca, uint16_t* cb, uint16_t* na, uint16_t* nb, uint16_t* sa, int kt) {
     const int kn2 = kb + (kt + 2 < nk ? kt + 2 : nk - 1) * BK;
     constexpr bool BIG = NM >= 16;   // 256-tiles: loads and reads spread over the sub-step
+    const bool pfk = PF && kt + 2 >= nk;
+    const char* pfb = PF ? pf.base + (pfk ? (int64_t)(kt + 2 - nk) * 32 * pf.row : 0) : nullptr;
     lds_settle();
-    oa.issue(sa, kn2, wave);
+    if constexpr (PF)
+      oa.template issue_pf<BN / WN>(sa, kn2, wave, lane, pfk, pfb, pf.row, 0);
+    else
+      oa.issue(sa, kn2, wave);
     if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(1, ca, cb, 1);
     mma(0);
@@ -285,7 +325,10 @@ __device__ __forceinline__ void kloop(f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
     __builtin_amdgcn_s_waitcnt((NA & 15) | (7 << 4) | ((NA >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    ob.issue(cb, kn2, wave);
+    if constexpr (PF)
+      ob.template issue_pf<BN / WN>(cb, kn2, wave, lane, pfk, pfb, pf.row, NA);
+    else
+      ob.issue(cb, kn2, wave);
     if constexpr (!BIG) __builtin_amdgcn_sched_barrier(0);
     rd(0, na, nb, 0);
     mma(1);
@@ -373,12 +416,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
   // row panel I of P times the symmetric matrix Q (upper tiles stored) at
   // column panel J: below tile J the stored tiles Q[k-block, J] are read
   // transposed, from tile J on the stored rows Q[J, k] directly
-  auto panel_times_sym = [&](const uint16_t* P, const uint16_t* Q) {
+  // (PF: the final K loop prefetches the iterate for the epilogue)
+  auto panel_times_sym = [&](const uint16_t* P, const uint16_t* Q, auto pf_tag, Prefetch pf) {
+    constexpr bool PF = decltype(pf_tag)::value;
     const int ksplit = it.tj * BN;
     kloop<BM, BN, WM, WN, false, true>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN, Np, 0,
                                        ksplit, sA0, sB0, sA1, sB1, sX, wave, lane, wm, wn);
-    kloop<BM, BN, WM, WN, false, false>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN * Np, Np,
-                                        ksplit, Np, sA0, sB0, sA1, sB1, sX, wave, lane, wm, wn);
+    kloop<BM, BN, WM, WN, false, false, PF>(acc, P + (int64_t)it.ti * BM * Np, Np, Q + (int64_t)it.tj * BN * Np,
+                                            Np, ksplit, Np, sA0, sB0, sA1, sB1, sX, wave, lane, wm, wn, pf);
   };
   // column panels I of P and J of Q, k over all Mp rows: P[:, I]^T Q[:, J]
   auto cols_t_cols = [&](const uint16_t* P, const uint16_t* Q) {
@@ -386,12 +431,24 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
                                       sB0, sA1, sB1, sX, wave, lane, wm, wn);
   };
 
+  // forward update tiles: this wave's part of the fp32 iterate, prefetched
+  // by the final K loop (a k-step's A loads carry half a chunk, its B loads
+  // the other half; the loop has at least two k-steps: BN / BK >= 2)
+  static_assert(32 * TN / 256 / 2 == BM * BK * 2 / 1024 / T::NW && BM == BN && BN / BK >= 2,
+                "an update tile's k-step loads must cover one 32-row chunk of its iterate");
+  Prefetch pf;
+  if (!VJP && MODE == 1) {
+    pf.base = reinterpret_cast<const char*>(d->master[0] + (int64_t)(it.ti * BM + wm * TM) * Np + it.tj * BN +
+                                            wn * TN);
+    pf.row = (int64_t)Np * 4;
+  }
+
   const uint16_t* Y = nullptr;
   if constexpr (!VJP) {
     if (MODE == 0)
       cols_t_cols(X, X);            // Gram tile of I - X^T X
     else
-      panel_times_sym(X, Ep);       // update tile of X E
+      panel_times_sym(X, Ep, std::true_type(), pf);   // update tile of X E
   } else {
     Y = static_cast<const uint16_t*>(d->yc[parity]);
     const uint16_t* S = static_cast<const uint16_t*>(d->s);
@@ -399,43 +456,121 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
       cols_t_cols(X, Y);            // S tile: X^T Y + Y^T X
       cols_t_cols(Y, X);
     } else {
-      panel_times_sym(Y, Ep);       // Y E + X S' with S' = -(X^T Y + Y^T X)
-      panel_times_sym(X, S);
+      panel_times_sym(Y, Ep, std::false_type(), pf);   // Y E + X S' with S' = -(X^T Y + Y^T X)
+      panel_times_sym(X, S, std::false_type(), pf);
     }
   }
 
   // ------------------------------------------------------------ epilogue --
-  // Each wave stages its accumulators 32 rows at a time through a private
-  // fp32 LDS buffer (32 x TN, 16-byte chunks XOR-swizzled so that the two
-  // half-waves, which hold rows 4 apart, hit disjoint banks) and writes its
-  // outputs as coalesced 8- or 16-byte vectors along rows.
-  float* buf;
-  if (BM == 256)
-    buf = reinterpret_cast<float*>((wave < 2 ? sA0 : sB0) + (wave & 1) * (32 * TN * 2));
-  else
-    buf = reinterpret_cast<float*>(wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1);
-  // update tiles: each wave's fp32 iterate chunk (32 x TN) is prefetched by
-  // direct-to-LDS loads into a second private buffer, so that the loads of
-  // chunk mi + 1 fly while chunk mi is written (no registers held)
-  uint16_t* mbuf;
-  if (BM == 256)
-    mbuf = (wave < 2 ? sA1 : sB1) + (wave & 1) * (32 * TN * 2);
-  else
-    mbuf = (wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1) + 32 * TN * 2;
-  auto bidx = [&](int r, int c) {  // float index of element (r, c) of the staging buffer
+  float* Xm = VJP ? d->gy[0] : d->master[0];   // the fp32 iterate an update tile advances
+  const int gi0 = it.ti * BM + wm * TM;  // first global row of this wave
+  const int gj0 = it.tj * BN + wn * TN;  // first global column
+  uint16_t* Xo = static_cast<uint16_t*>(VJP ? d->yc[parity ^ 1] : d->xc[parity ^ 1]) + (VJP ? 0 : xoff);
+  if (!VJP && MODE == 1) {
+    // Update tiles advance the fp32 iterate in place and emit its next bf16
+    // copy.  Chunks 0 and 1 (32 rows each) of this wave's part of the
+    // iterate were loaded by the final K loop's last two k-steps, into
+    // those k-steps' free A buffers (A rotates through sX, sA0, sA1) and
+    // their B buffers (sB0, sB1 alternately): piece q (1 KB: 256 / TN rows,
+    // 4 values per lane) of chunk c sits in block q * 4 + wave of the A
+    // buffer (q < NQ / 2) or of the B buffer (the rest).  Chunk mi + 2 goes
+    // into chunk mi's blocks once they are read.  The accumulators are
+    // staged 16 rows at a time in the last k-step's A buffer, the one
+    // buffer left free.
+    const int nkf = (Np - it.tj * BN) / BK;
+    auto abuf = [&](int t) { const int r = t % 3; return r == 0 ? sX : r == 1 ? sA0 : sA1; };
+    auto cbuf = [&](int t) { const int r = t % 3; return r == 0 ? sA0 : r == 1 ? sA1 : sX; };
+    constexpr int NQ = 32 * TN / 256;   // pieces per chunk
+    uint16_t* pa[2] = {abuf(nkf - 2), abuf(nkf - 1)};
+    uint16_t* pb[2] = {(nkf - 2) & 1 ? sB1 : sB0, (nkf - 1) & 1 ? sB1 : sB0};
+    float* sbuf = reinterpret_cast<float*>(cbuf(nkf - 1) + wave * (16 * TN * 2));
+    auto piece = [&](int mi, int q) {
+      return q < NQ / 2 ? pa[mi & 1] + (q * 4 + wave) * 512 : pb[mi & 1] + ((q - NQ / 2) * 4 + wave) * 512;
+    };
+    auto bidx = [&](int r, int c) {     // float index of element (r, c) of sbuf (16-byte chunks swizzled)
+      return r * TN + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 2) + (c & 3);
+    };
+    const int col = lane & 31;
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi) {
+      const int gi = gi0 + mi * 32;
+      if (mi >= 2) {
+        // this chunk's pieces went out during chunk mi - 2; issued after them
+        // are that chunk's second-half stores, chunk mi - 1's stores and
+        // perhaps chunk mi + 1's pieces: at least 3 NQ operations (more than
+        // 63 do not fit the counter: then 63)
+        constexpr int NEWER = 3 * NQ < 63 ? 3 * NQ : 63;
+        __builtin_amdgcn_s_waitcnt((NEWER & 15) | (7 << 4) | (15 << 8) | ((NEWER >> 4) << 14));
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // this half's iterate values; once both halves are read, chunk
+        // mi + 2 goes into their blocks
+        float4 mpre[NQ / 2];
+#pragma unroll
+        for (int q = 0; q < NQ / 2; ++q)
+          mpre[q] = *reinterpret_cast<const float4*>(piece(mi, h * NQ / 2 + q) + lane * 8);
+        if (h == 1 && mi + 2 < MI) {
+          lds_settle();
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            const int e4 = q * 64 + lane;
+            const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
+            dma16(Xm + (int64_t)(gi + 64 + r) * Np + gj0 + c, piece(mi, q));
+          }
+        }
+        // accumulator rows 16 h .. 16 h + 15 of the chunk -> sbuf
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+          for (int r = 8 * h; r < 8 * h + 8; ++r)
+            sbuf[bidx(acc_row(r, lane) - 16 * h, ni * 32 + col)] = acc[mi][ni][r];
+        // row-major pass: 4 consecutive columns per lane
+#pragma unroll
+        for (int q = h * NQ / 2; q < (h + 1) * NQ / 2; ++q) {
+          const int e4 = q * 64 + lane;
+          const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
+          float4 v = *reinterpret_cast<const float4*>(&sbuf[bidx(r - 16 * h, c)]);
+          const int64_t off = (int64_t)(gi + r) * Np + gj0 + c;
+          const float4 m = mpre[q - h * NQ / 2];
+          v.x = m.x + beta * v.x;
+          v.y = m.y + beta * v.y;
+          v.z = m.z + beta * v.z;
+          v.w = m.w + beta * v.w;
+          *reinterpret_cast<float4*>(Xm + off) = v;
+          *reinterpret_cast<uint2*>(Xo + off) = pack4_bf16(v.x, v.y, v.z, v.w);
+        }
+      }
+    }
+    return;
+  }
+  // Other tiles: each wave stages its accumulators through a private fp32
+  // LDS buffer (rows of TN floats, 16-byte chunks XOR-swizzled so that the
+  // two half-waves, which hold rows 4 apart, hit disjoint banks) and writes
+  // its outputs as coalesced 8- or 16-byte vectors along rows.
+  auto bidx = [&](int r, int c) {  // float index of element (r, c) of a staging buffer
     return r * TN + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 2) + (c & 3);
   };
   const int col = lane & 31;
-  const int gi0 = it.ti * BM + wm * TM;  // first global row of this wave
-  const int gj0 = it.tj * BN + wn * TN;  // first global column
+  constexpr int NQ = 32 * TN / 256;        // 1 KB pieces (4 columns per lane) of a 32-row chunk
   // Gram-like tiles write E (or S' in VJP mode) with the identity (or
-  // none) subtracted from; update-like tiles advance the fp32 iterate (or
-  // gradient iterate) in place and emit its next bf16 copy
+  // none) subtracted from; gradient-update tiles advance the fp32 gradient
+  // iterate in place and emit its next bf16 copy, each wave's iterate chunk
+  // (32 x TN) loaded by direct-to-LDS loads into a second private buffer,
+  // chunk mi + 1 in flight while chunk mi is written.  The accumulators are
+  // staged 32 rows at a time (every buffer is free after the loop).
+  float* buf;
+  uint16_t* mbuf;
+  if (BM == 256) {
+    buf = reinterpret_cast<float*>((wave < 2 ? sA0 : sB0) + (wave & 1) * (32 * TN * 2));
+    mbuf = (wave < 2 ? sA1 : sB1) + (wave & 1) * (32 * TN * 2);
+  } else {
+    buf = reinterpret_cast<float*>(wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1);
+    mbuf = (wave == 0 ? sA0 : wave == 1 ? sB0 : wave == 2 ? sA1 : sB1) + 32 * TN * 2;
+  }
   uint16_t* E = static_cast<uint16_t*>(VJP ? d->s : d->e) + (VJP ? 0 : eoff);
-  float* Xm = VJP ? d->gy[0] : d->master[0];
-  uint16_t* Xo = static_cast<uint16_t*>(VJP ? d->yc[parity ^ 1] : d->xc[parity ^ 1]) + (VJP ? 0 : xoff);
   constexpr float DELTA = VJP ? 0.f : 1.f;
-  constexpr int NQ = 32 * TN / 256;        // 4-column groups per lane and chunk
+  const bool upd = VJP && MODE == 1;
   // chunk mi of the iterate into mbuf, row-major (TN floats per row): load q
   // of a lane covers the same (row, 4 columns) that its row-major pass reads
   auto load_chunk = [&](int mi) {
@@ -446,19 +581,19 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
       dma16(Xm + (int64_t)(gi0 + mi * 32 + r) * Np + gj0 + c, mbuf + q * 512);
     }
   };
-  if (MODE == 1) load_chunk(0);
+  if (upd) load_chunk(0);
 #pragma unroll
   for (int mi = 0; mi < MI; ++mi) {
     const int gi = gi0 + mi * 32;
     float4 mpre[NQ];
-    if (MODE == 1) {
+    if (upd) {
       // this chunk's iterate from LDS, then the next chunk's loads
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
       for (int q = 0; q < NQ; ++q)
         mpre[q] = *reinterpret_cast<const float4*>(mbuf + q * 512 + lane * 8);
       if (mi + 1 < MI) {
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        lds_settle();
         load_chunk(mi + 1);
       }
     }
@@ -474,7 +609,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
       const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
       float4 v = *reinterpret_cast<const float4*>(&buf[bidx(r, c)]);
       const int64_t off = (int64_t)(gi + r) * Np + gj0 + c;
-      if (MODE == 0) {
+      if (!upd) {
         const int dg = (gi + r) - (gj0 + c);   // the diagonal hits column c + dg
         v.x = (dg == 0 ? DELTA : 0.f) - v.x;
         v.y = (dg == 1 ? DELTA : 0.f) - v.y;
