@@ -12,6 +12,7 @@ X5  planted mistakes.
 """
 
 import math
+import zlib
 
 import numpy as np
 import pytest
@@ -20,6 +21,15 @@ from scipy.linalg import expm
 from oracle import conv, expo, spectral
 
 RNG = np.random.default_rng(20260115)
+
+
+@pytest.fixture(autouse=True)
+def _rng_per_test(request):
+    """Each test draws from a generator seeded by its own name, so that its
+    inputs do not depend on which tests ran before it in the process (a
+    parallel run deals tests to workers in any order)."""
+    global RNG
+    RNG = np.random.default_rng([20260115, zlib.crc32(request.node.name.encode())])
 
 
 def trunc_bound(norm, p):

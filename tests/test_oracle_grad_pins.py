@@ -15,6 +15,8 @@ G6  planted mistakes (a dropped term, a missing symmetrization, a flipped
     sign) that each fail one of the pins above.
 """
 
+import zlib
+
 import numpy as np
 import pytest
 import torch
@@ -24,10 +26,40 @@ from oracle import aoc, aoc_grad, bjorck, bjorck_grad
 RNG = np.random.default_rng(20260113)
 
 
+@pytest.fixture(autouse=True)
+def _rng_per_test(request):
+    """Each test draws from a generator seeded by its own name, so that its
+    inputs do not depend on which tests ran before it in the process (a
+    parallel run deals tests to workers in any order)."""
+    global RNG
+    RNG = np.random.default_rng([20260113, zlib.crc32(request.node.name.encode())])
+
+
+EPS = np.finfo(np.float64).eps
+
+
 def fd_directional(f, w, y, d, h=1e-5):
-    """<Y, (f(W + h D) - f(W - h D)) / 2h>: the directional derivative of
-    L = <Y, f(W)> along D, by central differences."""
-    return float(np.sum(y * (f(w + h * d) - f(w - h * d)))) / (2 * h)
+    """The directional derivative of L = <Y, f(W)> along D by central
+    differences at steps h and h/2, combined so that their second-order
+    truncation terms cancel, and a bound on its error: the two central
+    differences' gap (three quarters of the step-h truncation term, far
+    above the combination's) plus the rounding of the function values (a
+    few machine epsilons of their absolute sums, over the step).  Returns
+    (estimate, error bound)."""
+    v = {t: y * f(w + t * d) for t in (h, -h, h / 2, -h / 2)}
+    d1 = float(np.sum(v[h] - v[-h])) / (2 * h)
+    d2 = float(np.sum(v[h / 2] - v[-h / 2])) / h
+    rounding = 8 * EPS * max(float(np.sum(np.abs(a))) for a in v.values()) / h
+    return (4 * d2 - d1) / 3, abs(d2 - d1) + rounding
+
+
+def assert_fd(gd, fd_err, rel):
+    """<G, D> agrees with the finite difference to `rel` (relative) beyond
+    the difference's own error bound, which must itself be small enough for
+    the check to mean something."""
+    fd, err = fd_err
+    assert err <= 1e-5 * max(1.0, abs(fd)), (fd, err)
+    assert abs(gd - fd) <= rel * max(1.0, abs(fd)) + err, (gd, fd, err)
 
 
 # ----------------------------------------------------------------- G1 ---
@@ -37,13 +69,11 @@ def test_bjorck_vjp_full_jacobian_fd(shape, iters):
     y = RNG.standard_normal(shape)
     g = bjorck_grad.bjorck_vjp(w, y, iters)
     f = lambda x: bjorck.bjorck(x, iters)
-    fd = np.zeros(shape)
     for i in range(shape[0]):
         for j in range(shape[1]):
             e = np.zeros(shape)
             e[i, j] = 1.0
-            fd[i, j] = fd_directional(f, w, y, e)
-    assert np.max(np.abs(g - fd)) <= 1e-8 * max(1.0, np.max(np.abs(fd)))
+            assert_fd(g[i, j], fd_directional(f, w, y, e), 1e-8)
 
 
 @pytest.mark.parametrize("shape,iters,beta,prescale", [
@@ -62,8 +92,7 @@ def test_bjorck_vjp_directional_fd(shape, iters, beta, prescale):
     f = lambda x: bjorck.bjorck(x, iters, beta, prescale)
     for _ in range(4):
         d = RNG.standard_normal(shape)
-        fd = fd_directional(f, w, y, d)
-        assert abs(float(np.sum(g * d)) - fd) <= 1e-7 * max(1.0, abs(fd))
+        assert_fd(float(np.sum(g * d)), fd_directional(f, w, y, d), 1e-7)
 
 
 # ----------------------------------------------------------------- G2 ---
@@ -181,8 +210,7 @@ def test_compose_vjp_fd_in_projectors(geom):
     f = lambda p: aoc.aoc_kernel(rko, p, *geom)
     for _ in range(3):
         dirn = RNG.standard_normal(proj.shape)
-        fd = fd_directional(f, proj, dk, dirn)
-        assert abs(float(np.sum(dproj * dirn)) - fd) <= 1e-8 * max(1.0, abs(fd))
+        assert_fd(float(np.sum(dproj * dirn)), fd_directional(f, proj, dk, dirn), 1e-8)
 
 
 @pytest.mark.parametrize("geom", GEOMS)
@@ -195,15 +223,13 @@ def test_layer_vjp_fd_and_scale_invariance(geom):
     g_rko, g_proj = aoc_grad.aoc_layer_vjp(raw_rko, raw_proj, *geom, iters, dk)
     f_r = lambda r: aoc.aoc_layer(r, raw_proj, *geom, iters)
     dirn = RNG.standard_normal(raw_rko.shape)
-    fd = fd_directional(f_r, raw_rko, dk, dirn)
-    assert abs(float(np.sum(g_rko * dirn)) - fd) <= 1e-7 * max(1.0, abs(fd))
+    assert_fd(float(np.sum(g_rko * dirn)), fd_directional(f_r, raw_rko, dk, dirn), 1e-7)
     for j in range(g):
         assert abs(float(np.sum(g_rko[j] * raw_rko[j]))) <= 1e-11 * max(1.0, np.linalg.norm(g_rko[j]))
     if g_proj is not None:
         f_p = lambda p: aoc.aoc_layer(raw_rko, p, *geom, iters)
         dirn = RNG.standard_normal(raw_proj.shape)
-        fd = fd_directional(f_p, raw_proj, dk, dirn)
-        assert abs(float(np.sum(g_proj * dirn)) - fd) <= 1e-7 * max(1.0, abs(fd))
+        assert_fd(float(np.sum(g_proj * dirn)), fd_directional(f_p, raw_proj, dk, dirn), 1e-7)
         for j in range(g):
             for t in range(raw_proj.shape[1]):
                 assert abs(float(np.sum(g_proj[j, t] * raw_proj[j, t]))) <= \
