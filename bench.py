@@ -456,11 +456,19 @@ def host_info():
     (name, version, threads) that NumPy calls."""
     model = platform.processor() or platform.machine()
     try:
+        fields = {}
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
-                    break
+                if not line.strip():
+                    break          # the first processor's block
+                k, _, v = line.partition(":")
+                fields[k.strip()] = v.strip()
+        if "model name" in fields:
+            # a virtualized host may report only the vendor line; the family
+            # and model numbers still name the part
+            model = fields["model name"]
+            if "cpu family" in fields and "model" in fields:
+                model += f" (family {fields['cpu family']}, model {fields['model']})"
     except OSError:
         pass
     blas = {}
@@ -531,8 +539,8 @@ def cpu_baseline(w):
             "sample": f"float64 NumPy oracle, Björck T={w.iters} with Frobenius pre-scaling of the workload's "
                       f"matrices: timed {'+'.join(desc)} (timed/total x shape), {label} to the whole "
                       f"{len(w.matrix_shapes())}-matrix step ({tot64:.1f} s)",
-            "est_step_s": round(tot64, 3), "cpu_model": model, "blas": blas,
-            "plain_cpu_fp32": {"value": w.n_layers / tot32, "unit": "layers/s", "est_step_s": round(tot32, 3),
+            "est_step_s": float(f"{tot64:.4g}"), "cpu_model": model, "blas": blas,
+            "plain_cpu_fp32": {"value": w.n_layers / tot32, "unit": "layers/s", "est_step_s": float(f"{tot32:.4g}"),
                                "kind": "plain NumPy float32 (BLAS sgemm), same formula and sample"}}
 
 
