@@ -119,6 +119,45 @@ def test_bf16_mixed_batch(tile):
             assert abs(checks.gram_deviation(got) - checks.gram_deviation(ref)) <= ORTH_BF16, shape
 
 
+# K-loop lengths of the bf16 tile kernel: with 64-deep k-steps, a Gram tile
+# runs Mp / 64 k-steps and an update tile tj * T / 64 (stored-tile part)
+# plus (Np - tj * T) / 64 (the rest) for tile size T, always even; the loop
+# runs whole six-step periods and a remainder of 0, 2 or 4 k-steps, each a
+# different stretch of straight-line code with its own buffer rotation and
+# wait counts.  These shapes give every remainder in each kind of loop, for
+# both tile sizes, and the results are checked whole and per block.
+KLOOP_SHAPES = {256: [(1536, 1024), (1280, 1280), (1024, 1024), (1024, 1792)],
+                128: [(384, 200), (256, 128), (512, 256), (640, 384), (768, 768)]}
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+def test_bf16_k_loop_remainders(tile):
+    shapes = KLOOP_SHAPES[tile]
+    print(f"[bf16 k-loop remainders] tile={tile} shapes={shapes}", flush=True)
+    for m, n in shapes:   # the shapes above do span every remainder
+        mp, np_ = -(-max(m, n) // tile) * tile, -(-min(m, n) // tile) * tile
+        assert min(m, n) > 64 and (tile == 128 or min(m, n) >= 1024)
+        assert (mp // 64) % 2 == 0 and (np_ // 64) % 2 == 0
+    gram = {(-(-max(m, n) // tile) * tile // 64) % 6 for m, n in shapes}
+    upd = set()
+    for m, n in shapes:
+        np_ = -(-min(m, n) // tile) * tile
+        for tj in range(np_ // tile):
+            upd |= {(tj * tile // 64) % 6, ((np_ - tj * tile) // 64) % 6}
+    assert gram == {0, 2, 4} and upd == {0, 2, 4}, (gram, upd)
+    st = stored(131 + tile, shapes, dtype="bf16")
+    x64 = oracle_inputs(st)
+    iters = 8
+    outs, status = gpu_orthogonalize(st, iters, compute="bf16", tile=tile)
+    assert np.all(status == 0)
+    for s, o, shape in zip(x64, outs, shapes):
+        ref = bjorck.bjorck(s, iters)
+        got = to_f64(o)
+        assert checks.relative_difference(got, ref) <= BF16_REL, shape
+        tiles = checks.tile_relative_differences(got, ref, tile)
+        assert tiles.max() <= BF16_REL, (shape, tiles.max(), np.unravel_index(np.argmax(tiles), tiles.shape))
+
+
 def test_concurrent_calls_two_threads():
     """Two host threads, each on a stream of its own, run mixed batches
     (small matrices on the library's side streams, tiled ones on the
