@@ -81,6 +81,22 @@ def test_p3_orthogonal_input(n):
     np.testing.assert_allclose(bjorck.bjorck(q, 10), c * q, rtol=0, atol=1e-13)
 
 
+@pytest.mark.parametrize("rows,cols,iters", [(40, 7, 9), (7, 40, 9), (33, 1, 3), (64, 64, 12)])
+def test_p3_reflected_factor_is_kept(rows, cols, iters):
+    """P3 (orthogonal factor): for W = Q D with Q the first n columns of a
+    Householder reflection and D diagonal, the iteration keeps Q:
+    Bjorck(Q D) = Q Bjorck(D), the reference the extreme-shape GPU tests
+    use (tests/reflected.py), checked against the oracle on the dense W."""
+    import reflected
+    v, d = reflected.factors(rows * 1000 + cols, rows, cols)
+    w = reflected.matrix(v, d, rows, cols)
+    q = reflected.lift(v, np.eye(len(d)))
+    assert np.abs(q.T @ q - np.eye(len(d))).max() <= 1e-14      # orthonormal columns
+    ref = reflected.lift(v, bjorck.bjorck(np.diag(d), iters))
+    got = bjorck.bjorck(w, iters)
+    np.testing.assert_allclose(got, ref if rows >= cols else ref.T, rtol=0, atol=1e-13)
+
+
 def test_p4_scale_invariance():
     rng = np.random.default_rng(5)
     w = rand(rng, 24, 12)
