@@ -68,6 +68,25 @@ __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 // differ in bits 1-2 and in bits 2-3, which keeps both cases conflict free.
 __device__ __forceinline__ int swt(int k) { return (0xCA60 >> ((k & 3) * 4)) & 15; }
 
+// Global-memory accesses of the epilogues.  The kernel takes its data
+// pointers from the descriptor table, and the compiler cannot prove that
+// a pointer loaded from memory points to global memory, so plain accesses
+// through it become FLAT instructions, which count against the LDS counter
+// as well: every wait for an LDS result (the staging buffer's reads) would
+// then also wait for the epilogue's stores in flight.
+// (The address-space attribute takes effect on vector-extension types,
+// not on HIP's float4 / uint2 classes.)
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) f32x4v g_f32x4;
+typedef __attribute__((address_space(1))) u32x2v g_u32x2;
+__device__ __forceinline__ float4 gload4(const float* p) {
+  const f32x4v v = *(const g_f32x4*)(p);
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void gstore4(float* p, float4 v) { *(g_f32x4*)(p) = f32x4v{v.x, v.y, v.z, v.w}; }
+__device__ __forceinline__ void gstore2(uint16_t* p, uint2 v) { *(g_u32x2*)(p) = u32x2v{v.x, v.y}; }
+
 // 16-byte direct global -> LDS load of every lane (gfx950
 // global_load_lds_dwordx4): lane l's bytes land at lds + 16 l.  Kept in a
 // plain device function: used directly in a kernel template, the builtin
@@ -473,8 +492,12 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
     // those k-steps' free A buffers (A rotates through sX, sA0, sA1) and
     // their B buffers (sB0, sB1 alternately): piece q (1 KB: 256 / TN rows,
     // 4 values per lane) of chunk c sits in block q * 4 + wave of the A
-    // buffer (q < NQ / 2) or of the B buffer (the rest).  Chunk mi + 2 goes
-    // into chunk mi's blocks once they are read.  The accumulators are
+    // buffer (q < NQ / 2) or of the B buffer (the rest).  On 256-tiles
+    // chunk 2 is loaded into registers as the epilogue starts and chunk 3
+    // as chunk 2 starts (both at once would spill), in the same 4-column
+    // pieces per lane as the stores; loads into LDS would make the compiler
+    // wait for them before every access of the staging buffer, as it
+    // cannot tell the run-time-chosen buffers apart.  The accumulators are
     // staged 16 rows at a time in the last k-step's A buffer, the one
     // buffer left free.
     const int nkf = (Np - it.tj * BN) / BK;
@@ -491,34 +514,30 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
       return r * TN + ((((c >> 2) ^ (((r >> 2) & 1) << 3))) << 2) + (c & 3);
     };
     const int col = lane & 31;
+    static_assert(MI <= 4, "chunks past the fourth have no registers");
+    constexpr int MR = MI > 2 ? MI - 2 : 1;   // chunks read into registers
+    float4 mreg[MR][NQ];
+    auto load_reg = [&](int j) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int e4 = q * 64 + lane;
+        const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
+        mreg[j][q] = gload4(Xm + (int64_t)(gi0 + (j + 2) * 32 + r) * Np + gj0 + c);
+      }
+    };
+    if (MI > 2) load_reg(0);
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi) {
       const int gi = gi0 + mi * 32;
-      if (mi >= 2) {
-        // this chunk's pieces went out during chunk mi - 2; issued after them
-        // are that chunk's second-half stores, chunk mi - 1's stores and
-        // perhaps chunk mi + 1's pieces: at least 3 NQ operations (more than
-        // 63 do not fit the counter: then 63)
-        constexpr int NEWER = 3 * NQ < 63 ? 3 * NQ : 63;
-        __builtin_amdgcn_s_waitcnt((NEWER & 15) | (7 << 4) | (15 << 8) | ((NEWER >> 4) << 14));
-      }
+      if (mi == 2 && MI > 3) load_reg(1);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        // this half's iterate values; once both halves are read, chunk
-        // mi + 2 goes into their blocks
+        // this half's iterate values
         float4 mpre[NQ / 2];
 #pragma unroll
         for (int q = 0; q < NQ / 2; ++q)
-          mpre[q] = *reinterpret_cast<const float4*>(piece(mi, h * NQ / 2 + q) + lane * 8);
-        if (h == 1 && mi + 2 < MI) {
-          lds_settle();
-#pragma unroll
-          for (int q = 0; q < NQ; ++q) {
-            const int e4 = q * 64 + lane;
-            const int r = e4 / (TN / 4), c = (e4 % (TN / 4)) * 4;
-            dma16(Xm + (int64_t)(gi + 64 + r) * Np + gj0 + c, piece(mi, q));
-          }
-        }
+          mpre[q] = mi < 2 ? *reinterpret_cast<const float4*>(piece(mi, h * NQ / 2 + q) + lane * 8)
+                           : mreg[mi < 2 ? 0 : mi - 2][h * NQ / 2 + q];
         // accumulator rows 16 h .. 16 h + 15 of the chunk -> sbuf
 #pragma unroll
         for (int ni = 0; ni < NI; ++ni)
@@ -537,8 +556,8 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
           v.y = m.y + beta * v.y;
           v.z = m.z + beta * v.z;
           v.w = m.w + beta * v.w;
-          *reinterpret_cast<float4*>(Xm + off) = v;
-          *reinterpret_cast<uint2*>(Xo + off) = pack4_bf16(v.x, v.y, v.z, v.w);
+          gstore4(Xm + off, v);
+          gstore2(Xo + off, pack4_bf16(v.x, v.y, v.z, v.w));
         }
       }
     }
@@ -615,15 +634,15 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void bjorck_bf16_kernel(const Tile
         v.y = (dg == 1 ? DELTA : 0.f) - v.y;
         v.z = (dg == 2 ? DELTA : 0.f) - v.z;
         v.w = (dg == 3 ? DELTA : 0.f) - v.w;
-        *reinterpret_cast<uint2*>(E + off) = pack4_bf16(v.x, v.y, v.z, v.w);
+        gstore2(E + off, pack4_bf16(v.x, v.y, v.z, v.w));
       } else {
         const float4 m = mpre[q];
         v.x = m.x + beta * v.x;
         v.y = m.y + beta * v.y;
         v.z = m.z + beta * v.z;
         v.w = m.w + beta * v.w;
-        *reinterpret_cast<float4*>(Xm + off) = v;
-        *reinterpret_cast<uint2*>(Xo + off) = pack4_bf16(v.x, v.y, v.z, v.w);
+        gstore4(Xm + off, v);
+        gstore2(Xo + off, pack4_bf16(v.x, v.y, v.z, v.w));
       }
     }
   }
