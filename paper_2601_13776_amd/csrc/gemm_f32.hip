@@ -88,8 +88,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         if (dt == ORTH_F32) {
           const float* p = static_cast<const float*>(P) + (int64_t)gr * ld + gk;
           if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-            const uint4 x = reinterpret_cast<const uint4*>(p)[0];
-            const uint4 y = reinterpret_cast<const uint4*>(p)[1];
+            const uint4 x = gld_u32x4(p);
+            const uint4 y = gld_u32x4(p + 4);
             dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
             dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
             return;
@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         } else {
           const uint16_t* p = static_cast<const uint16_t*>(P) + (int64_t)gr * ld + gk;
           if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-            const uint4 x = *reinterpret_cast<const uint4*>(p);
+            const uint4 x = gld_u32x4(p);
             dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
             packed = true;
             return;
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         uint32_t v = 0;
         if (gr < rows_lim && gk + q < K) {
           const int64_t idx = tr ? (int64_t)(gk + q) * ld + gr : (int64_t)gr * ld + gk + q;
-          v = dt == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(P)[idx] : static_cast<const uint32_t*>(P)[idx];
+          v = dt == ORTH_BF16 ? (uint32_t)gld_u16(P, idx) : gld_u32(P, idx);
         }
         dst[q] = v;
       }
@@ -124,8 +124,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         if (dt == ORTH_F32) {
           const float* p = static_cast<const float*>(P) + (int64_t)gk * ld + gr;
           if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-            const uint4 x = reinterpret_cast<const uint4*>(p)[0];
-            const uint4 y = reinterpret_cast<const uint4*>(p)[1];
+            const uint4 x = gld_u32x4(p);
+            const uint4 y = gld_u32x4(p + 4);
             dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
             dst[4] = y.x; dst[5] = y.y; dst[6] = y.z; dst[7] = y.w;
             return;
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         } else {
           const uint16_t* p = static_cast<const uint16_t*>(P) + (int64_t)gk * ld + gr;
           if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-            const uint4 x = *reinterpret_cast<const uint4*>(p);
+            const uint4 x = gld_u32x4(p);
             dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
             packed = true;
             return;
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         uint32_t v = 0;
         if (gk < K && gr + q < rows_lim) {
           const int64_t idx = (int64_t)gk * ld + gr + q;
-          v = dt == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(P)[idx] : static_cast<const uint32_t*>(P)[idx];
+          v = dt == ORTH_BF16 ? (uint32_t)gld_u16(P, idx) : gld_u32(P, idx);
         }
         dst[q] = v;
       }
@@ -260,8 +260,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       const int i = ibase + acc_row(r, lane);
       if (i < M) {
         const float v = (i == j ? 1.f : 0.f) - acc[r];
-        C[(int64_t)i * ldc + j] = v;
-        if (mirror) C[(int64_t)j * ldc + i] = v;
+        gst_f32(C, (int64_t)i * ldc + j, v);
+        if (mirror) gst_f32(C, (int64_t)j * ldc + i, v);
       }
     }
   } else if (epi == EPI_SERIES) {
@@ -273,8 +273,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       const int i = ibase + acc_row(r, lane);
       if (i < M) {
         const float v = beta * acc[r];
-        C[(int64_t)i * ldc + j] = v;
-        dst2[(int64_t)i * ld2 + j] += v;   // each element belongs to one item of the launch
+        gst_f32(C, (int64_t)i * ldc + j, v);
+        // each element belongs to one item of the launch
+        gst_f32(dst2, (int64_t)i * ld2 + j, gld_f32(dst2, (int64_t)i * ld2 + j) + v);
       }
     }
   } else if (epi == EPI_NEG) {
@@ -282,8 +283,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
     for (int r = 0; r < 16; ++r) {
       const int i = ibase + acc_row(r, lane);
       if (i < M) {
-        C[(int64_t)i * ldc + j] = -acc[r];
-        if (mirror) C[(int64_t)j * ldc + i] = -acc[r];
+        gst_f32(C, (int64_t)i * ldc + j, -acc[r]);
+        if (mirror) gst_f32(C, (int64_t)j * ldc + i, -acc[r]);
       }
     }
   } else {  // EPI_UPDATE
@@ -297,8 +298,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
       const int i = ibase + acc_row(r, lane);
       v[r] = 0.f;
       if (i < M && j < N) {
-        v[r] = src[(int64_t)i * lds_ + j] + beta * acc[r];
-        C[(int64_t)i * ldc + j] = v[r];
+        v[r] = gld_f32(src, (int64_t)i * lds_ + j) + beta * acc[r];
+        gst_f32(C, (int64_t)i * ldc + j, v[r]);
       }
     }
     if (dst2) {
@@ -319,11 +320,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmItem* __restric
         const float* t = Tt + jj * 33 + c4;
         float* d = dst2 + (int64_t)gj * ld2 + gi;
         if (gi + 4 <= M && (reinterpret_cast<uintptr_t>(d) & 15) == 0) {
-          *reinterpret_cast<float4*>(d) = make_float4(t[0], t[1], t[2], t[3]);
+          gst_f32x4(d, make_float4(t[0], t[1], t[2], t[3]));
         } else {
 #pragma unroll
           for (int k = 0; k < 4; ++k)
-            if (gi + k < M) d[k] = t[k];
+            if (gi + k < M) gst_f32(d, k, t[k]);
         }
       }
     }

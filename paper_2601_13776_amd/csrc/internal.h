@@ -23,15 +23,47 @@ __device__ inline uint16_t f32_to_bf16(float f) {
   u += 0x7fffu + ((u >> 16) & 1u);
   return static_cast<uint16_t>(u >> 16);
 }
+// ---------------------------------------------------------------------------
+// Global-memory accesses.  Kernels take their data pointers from descriptor
+// tables, and the compiler cannot prove that a pointer loaded from memory
+// addresses global memory: plain accesses through it become FLAT
+// instructions, which count against the LDS counter as well, so every wait
+// for an LDS result also waits for the global loads and stores in flight.
+// These helpers access through global-address-space pointers (the attribute
+// takes effect on scalar and vector-extension types, not on HIP's vector
+// classes).  Every pointer passed to them must address global memory.
+// ---------------------------------------------------------------------------
+#define ORTH_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t orth_u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t orth_u32x2 __attribute__((ext_vector_type(2)));
+typedef float orth_f32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float gld_f32(const void* p, int64_t i) { return ((const ORTH_GLOBAL float*)p)[i]; }
+__device__ __forceinline__ uint32_t gld_u32(const void* p, int64_t i) { return ((const ORTH_GLOBAL uint32_t*)p)[i]; }
+__device__ __forceinline__ uint16_t gld_u16(const void* p, int64_t i) { return ((const ORTH_GLOBAL uint16_t*)p)[i]; }
+__device__ __forceinline__ uint4 gld_u32x4(const void* p) {
+  const orth_u32x4 v = *(const ORTH_GLOBAL orth_u32x4*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 gld_f32x4(const void* p) {
+  const orth_f32x4 v = *(const ORTH_GLOBAL orth_f32x4*)p;
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void gst_f32(void* p, int64_t i, float v) { ((ORTH_GLOBAL float*)p)[i] = v; }
+__device__ __forceinline__ void gst_u16(void* p, int64_t i, uint16_t v) { ((ORTH_GLOBAL uint16_t*)p)[i] = v; }
+__device__ __forceinline__ void gst_f32x4(void* p, float4 v) {
+  *(ORTH_GLOBAL orth_f32x4*)p = orth_f32x4{v.x, v.y, v.z, v.w};
+}
+__device__ __forceinline__ void gst_u32x4(void* p, uint4 v) { *(ORTH_GLOBAL orth_u32x4*)p = orth_u32x4{v.x, v.y, v.z, v.w}; }
+__device__ __forceinline__ void gst_u32x2(void* p, uint2 v) { *(ORTH_GLOBAL orth_u32x2*)p = orth_u32x2{v.x, v.y}; }
+
 __device__ inline float load_as_f32(const void* p, int64_t idx, int dtype) {
-  return dtype == ORTH_BF16 ? bf16_to_f32(static_cast<const uint16_t*>(p)[idx])
-                            : static_cast<const float*>(p)[idx];
+  return dtype == ORTH_BF16 ? bf16_to_f32(gld_u16(p, idx)) : gld_f32(p, idx);
 }
 __device__ inline void store_from_f32(void* p, int64_t idx, int dtype, float v) {
   if (dtype == ORTH_BF16)
-    static_cast<uint16_t*>(p)[idx] = f32_to_bf16(v);
+    gst_u16(p, idx, f32_to_bf16(v));
   else
-    static_cast<float*>(p)[idx] = v;
+    gst_f32(p, idx, v);
 }
 
 // Runs of 8 consecutive elements moved as 16-byte vectors (one for bf16,
@@ -43,7 +75,7 @@ __device__ inline bool vec8_ok(const void* p, int64_t ld, int dtype) {
 }
 __device__ inline void load8_f32(const void* p, int64_t idx, int dtype, float (&v)[8]) {
   if (dtype == ORTH_BF16) {
-    const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + idx);
+    const uint4 q = gld_u32x4(static_cast<const uint16_t*>(p) + idx);
     const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -51,8 +83,8 @@ __device__ inline void load8_f32(const void* p, int64_t idx, int dtype, float (&
       v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
     }
   } else {
-    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + idx);
-    const float4 b = *reinterpret_cast<const float4*>(static_cast<const float*>(p) + idx + 4);
+    const float4 a = gld_f32x4(static_cast<const float*>(p) + idx);
+    const float4 b = gld_f32x4(static_cast<const float*>(p) + idx + 4);
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   }
@@ -65,10 +97,10 @@ __device__ inline uint4 pack8_bf16(const float (&v)[8]) {
 }
 __device__ inline void store8_f32(void* p, int64_t idx, int dtype, const float (&v)[8]) {
   if (dtype == ORTH_BF16) {
-    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + idx) = pack8_bf16(v);
+    gst_u32x4(static_cast<uint16_t*>(p) + idx, pack8_bf16(v));
   } else {
-    *reinterpret_cast<float4*>(static_cast<float*>(p) + idx) = make_float4(v[0], v[1], v[2], v[3]);
-    *reinterpret_cast<float4*>(static_cast<float*>(p) + idx + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    gst_f32x4(static_cast<float*>(p) + idx, make_float4(v[0], v[1], v[2], v[3]));
+    gst_f32x4(static_cast<float*>(p) + idx + 4, make_float4(v[4], v[5], v[6], v[7]));
   }
 }
 
