@@ -63,7 +63,7 @@ __device__ inline void load_tall(float* dst, const void* src, int64_t ld, int tr
       w[u] = 0;
       if (idx < total && r < M && c < N) {
         const int64_t e = transposed ? (int64_t)c * ld + r : (int64_t)r * ld + c;
-        w[u] = dtype == ORTH_BF16 ? (uint32_t) static_cast<const uint16_t*>(src)[e] : static_cast<const uint32_t*>(src)[e];
+        w[u] = dtype == ORTH_BF16 ? (uint32_t)gld_u16(src, e) : gld_u32(src, e);
       }
     }
     float v[U];
@@ -501,8 +501,8 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
   auto save_step = [&](int t) {
     float* xs = d.save + t * step_floats;
     float* es = xs + (int64_t)Mp * NP;
-    for (int idx = tid; idx < Mp * NP; idx += NTHR) xs[idx] = X[(idx / NP) * XP + idx % NP];
-    for (int idx = tid; idx < NP * NP; idx += NTHR) es[idx] = E[(idx / NP) * XP + idx % NP];
+    for (int idx = tid; idx < Mp * NP; idx += NTHR) gst_f32(xs, idx, X[(idx / NP) * XP + idx % NP]);
+    for (int idx = tid; idx < NP * NP; idx += NTHR) gst_f32(es, idx, E[(idx / NP) * XP + idx % NP]);
   };
   // (X and E are contiguous in the slot: 16-byte loads, U of them in
   // flight per thread before their LDS stores)
@@ -515,7 +515,7 @@ __global__ __launch_bounds__(64 * NWAVES) void bjorck_small_vjp_kernel(const Sma
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int q = base + u * NTHR + tid;
-        if (q < total) v[u] = src[q];
+        if (q < total) v[u] = gld_f32x4(src + q);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {

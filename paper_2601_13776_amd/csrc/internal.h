@@ -40,6 +40,7 @@ typedef float orth_f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float gld_f32(const void* p, int64_t i) { return ((const ORTH_GLOBAL float*)p)[i]; }
 __device__ __forceinline__ uint32_t gld_u32(const void* p, int64_t i) { return ((const ORTH_GLOBAL uint32_t*)p)[i]; }
 __device__ __forceinline__ uint16_t gld_u16(const void* p, int64_t i) { return ((const ORTH_GLOBAL uint16_t*)p)[i]; }
+__device__ __forceinline__ double gld_f64(const void* p, int64_t i) { return ((const ORTH_GLOBAL double*)p)[i]; }
 __device__ __forceinline__ uint4 gld_u32x4(const void* p) {
   const orth_u32x4 v = *(const ORTH_GLOBAL orth_u32x4*)p;
   return make_uint4(v.x, v.y, v.z, v.w);
@@ -50,6 +51,7 @@ __device__ __forceinline__ float4 gld_f32x4(const void* p) {
 }
 __device__ __forceinline__ void gst_f32(void* p, int64_t i, float v) { ((ORTH_GLOBAL float*)p)[i] = v; }
 __device__ __forceinline__ void gst_u16(void* p, int64_t i, uint16_t v) { ((ORTH_GLOBAL uint16_t*)p)[i] = v; }
+__device__ __forceinline__ void gst_f64(void* p, int64_t i, double v) { ((ORTH_GLOBAL double*)p)[i] = v; }
 __device__ __forceinline__ void gst_f32x4(void* p, float4 v) {
   *(ORTH_GLOBAL orth_f32x4*)p = orth_f32x4{v.x, v.y, v.z, v.w};
 }

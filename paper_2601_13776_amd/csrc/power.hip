@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
     for (int cb = 0; cb < cols8; cb += CH) {
       const int cn = cols8 - cb < CH ? cols8 - cb : CH;
       __syncthreads();   // the previous chunk's reads are done
-      for (int j = threadIdx.x; j < cn; j += 256) vin[j] = in[cb + j];
+      for (int j = threadIdx.x; j < cn; j += 256) vin[j] = gld_f64(in, cb + j);
       __syncthreads();
 #pragma unroll
       for (int k = 0; k < 16; ++k) {
@@ -86,9 +86,10 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
       const int r = it.block * 64 + wave + 4 * k;
       if (r < d.rows) {
         const int64_t row = (int64_t)r * d.ld_in;
-        for (int c = cols8 + lane; c < d.cols; c += 64) acc[k] += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
+        for (int c = cols8 + lane; c < d.cols; c += 64)
+          acc[k] += (double)load_as_f32(d.in, row + c, in_dtype) * gld_f64(in, c);
         const double t = wave_sum(acc[k]);
-        if (lane == 0) out[r] = t;
+        if (lane == 0) gst_f64(out, r, t);
       }
     }
   } else if (!it.coldot) {
@@ -98,9 +99,9 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
       if (r >= d.rows) break;
       double acc = 0.0;
       const int64_t row = (int64_t)r * d.ld_in;
-      for (int c = lane; c < d.cols; c += 64) acc += (double)load_as_f32(d.in, row + c, in_dtype) * in[c];
+      for (int c = lane; c < d.cols; c += 64) acc += (double)load_as_f32(d.in, row + c, in_dtype) * gld_f64(in, c);
       acc = wave_sum(acc);
-      if (lane == 0) out[r] = acc;
+      if (lane == 0) gst_f64(out, r, acc);
     }
   } else if (vec && (d.cols - it.block * 64 >= 64 || d.cols % 8 == 0)) {
     // out[c] = sum_r W[r][c] in[r] over this item's 64 columns: eight lanes
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
       for (int r = wave * 8 + rsub; r < d.rows; r += 32) {
         float w[8];
         load8_f32(d.in, (int64_t)r * d.ld_in + c0, in_dtype, w);
-        const double x = in[r];
+        const double x = gld_f64(in, r);
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[q] += (double)w[q] * x;
       }
@@ -129,17 +130,18 @@ __global__ __launch_bounds__(256) void power_dot_kernel(const TiledMat* __restri
       for (int q = 0; q < 8; ++q) colsum[wave][cg * 8 + q] = acc[q];
     __syncthreads();
     const int c = it.block * 64 + lane;
-    if (wave == 0 && c < d.cols) out[c] = ((colsum[0][lane] + colsum[1][lane]) + colsum[2][lane]) + colsum[3][lane];
+    if (wave == 0 && c < d.cols)
+      gst_f64(out, c, ((colsum[0][lane] + colsum[1][lane]) + colsum[2][lane]) + colsum[3][lane]);
   } else {
     // out[c] = sum_r W[r][c] in[r]: lanes along 64 columns, waves interleave rows
     const int c = it.block * 64 + lane;
     double acc = 0.0;
     if (c < d.cols)
       for (int r = wave; r < d.rows; r += 4)
-        acc += (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype) * in[r];
+        acc += (double)load_as_f32(d.in, (int64_t)r * d.ld_in + c, in_dtype) * gld_f64(in, r);
     part[wave][lane] = acc;
     __syncthreads();
-    if (wave == 0 && c < d.cols) out[c] = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+    if (wave == 0 && c < d.cols) gst_f64(out, c, ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]);
   }
 }
 

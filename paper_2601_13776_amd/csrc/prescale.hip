@@ -161,12 +161,12 @@ __global__ __launch_bounds__(256) void prescale_scale_kernel(const TiledMat* __r
     const int a = e / TB, b = e % TB;
     const int64_t off = (int64_t)(R + a) * d.Np + C + b;
     const float v = tile[a][b];
-    master[off] = v;
+    gst_f32(master, off, v);
     // bf16 products: the bf16 copy; fp32 products: the transposed iterate
     // xt[(C + a)][(R + b)] = tile[b][a] (each only where the plan has one)
-    if (compute == ORTH_COMPUTE_BF16 && d.xc[0]) static_cast<uint16_t*>(d.xc[0])[off] = f32_to_bf16(v);
+    if (compute == ORTH_COMPUTE_BF16 && d.xc[0]) gst_u16(d.xc[0], off, f32_to_bf16(v));
     if (compute != ORTH_COMPUTE_BF16 && d.xt)
-      static_cast<float*>(d.xt)[(int64_t)(C + a) * d.Mp + R + b] = tile[b][a];
+      gst_f32(d.xt, (int64_t)(C + a) * d.Mp + R + b, tile[b][a]);
   }
 }
 
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) void writeout_kernel(const TiledMat* __restric
     for (int e = threadIdx.x; e < TB * TB; e += 256) {
       const int r = R + e / TB, c = C + e % TB;
       if (r < d.rows && c < d.cols)
-        store_from_f32(d.out, (int64_t)r * d.ld_out + c, out_dtype, master[(int64_t)r * d.Np + c]);
+        store_from_f32(d.out, (int64_t)r * d.ld_out + c, out_dtype, gld_f32(master, (int64_t)r * d.Np + c));
     }
     return;
   }
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(256) void writeout_kernel(const TiledMat* __restric
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int a = e / TB, b = e % TB;
     const int tr = C + a, tc = R + b;  // tall row / col
-    tile[a][b] = (tr < d.Mp && tc < d.Np) ? master[(int64_t)tr * d.Np + tc] : 0.f;
+    tile[a][b] = (tr < d.Mp && tc < d.Np) ? gld_f32(master, (int64_t)tr * d.Np + tc) : 0.f;
   }
   __syncthreads();
   for (int e = threadIdx.x; e < TB * TB; e += 256) {

@@ -31,12 +31,12 @@ __device__ inline void caller_tile(const TiledMat& d, const float* y, int R, int
     const int a = e / TB, b = e % TB;
     if (!d.transposed) {
       const int r = R + a, c = C + b;
-      tile[a][b] = (r < d.Mp && c < d.Np) ? y[(int64_t)r * d.Np + c] : 0.f;
+      tile[a][b] = (r < d.Mp && c < d.Np) ? gld_f32(y, (int64_t)r * d.Np + c) : 0.f;
     } else {
       // caller (R + b, C + a) is tall (C + a, R + b): rows of the tall
       // buffer are read along b
       const int tr = C + a, tc = R + b;
-      tile[b][a] = (tr < d.Mp && tc < d.Np) ? y[(int64_t)tr * d.Np + tc] : 0.f;
+      tile[b][a] = (tr < d.Mp && tc < d.Np) ? gld_f32(y, (int64_t)tr * d.Np + tc) : 0.f;
     }
   }
   __syncthreads();
@@ -81,11 +81,11 @@ __global__ __launch_bounds__(256) void vjp_load_grad_kernel(const TiledMat* __re
   for (int e = threadIdx.x; e < TB * TB; e += 256) {
     const int a = e / TB, b = e % TB;
     const int64_t off = (int64_t)(R + a) * d.Np + C + b;
-    y[off] = tile[a][b];
-    if (yc) yc[off] = f32_to_bf16(tile[a][b]);
+    gst_f32(y, off, tile[a][b]);
+    if (yc) gst_u16(yc, off, f32_to_bf16(tile[a][b]));
     // fp32 products: the transpose too, Np x Mp (consecutive threads along
     // a, so its rows are written coalesced)
-    if (yt) yt[(int64_t)(C + a) * d.Mp + R + b] = tile[b][a];
+    if (yt) gst_f32(yt, (int64_t)(C + a) * d.Mp + R + b, tile[b][a]);
   }
 }
 
