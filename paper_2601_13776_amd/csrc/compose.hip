@@ -63,22 +63,6 @@ __global__ __launch_bounds__(256) void compose_combine_kernel(const ComposeGroup
   }
 }
 
-// kernel[group * cout_g + o][i][a][b] = taps[a][b][o][i]
-__global__ __launch_bounds__(256) void compose_scatter_kernel(const ComposeGroup* __restrict__ groups, int dtype) {
-  const ComposeGroup& g = groups[blockIdx.y];
-  const int k = g.k, c = g.c, og = g.cout_g;
-  const int64_t tap = (int64_t)og * c;
-  const int64_t total = (int64_t)k * k * tap;
-  const float* T = g.taps[g.cur];
-  const int64_t base = (int64_t)g.group * og * c * k * k;
-  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int b = (int)(e % k);
-    const int a = (int)((e / k) % k);
-    const int64_t oi = e / ((int64_t)k * k);
-    store_from_f32(g.kernel, base + e, dtype, T[(int64_t)(a * k + b) * tap + oi]);
-  }
-}
-
 unsigned grid_x(int64_t max_elems) {
   int64_t b = (max_elems + 255) / 256;
   if (b < 1) b = 1;
@@ -108,14 +92,5 @@ hipError_t launch_compose_combine(const ComposeGroup* groups, const CombineItem*
   return e;
 }
 
-hipError_t launch_compose_scatter(const ComposeGroup* groups, int n_groups, int dtype, int64_t max_elems,
-                                  hipStream_t s) {
-  if (n_groups <= 0) return hipSuccess;
-  timing_begin("compose_scatter", s);
-  hipLaunchKernelGGL(compose_scatter_kernel, dim3(grid_x(max_elems), n_groups), dim3(256), 0, s, groups, dtype);
-  hipError_t e = hipGetLastError();
-  timing_end("compose_scatter", s);
-  return e;
-}
 
 }  // namespace orth

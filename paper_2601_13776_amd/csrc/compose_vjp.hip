@@ -53,16 +53,14 @@ __global__ __launch_bounds__(256) void tap_layout_kernel(const TapItem* __restri
         tile[t][m] = load_as_f32(it.a, (m0 + m) * T + t0 + t, dtype);
       }
       __syncthreads();
-      float* out = static_cast<float*>(it.out);
       for (int j = threadIdx.x; j < tn * TM; j += 256) {
         const int t = j >> 6, m = j & 63;
-        if (m < mn) out[(int64_t)(t0 + t) * M + m0 + m] = tile[t][m];
+        if (m < mn) gst_f32(it.out, (int64_t)(t0 + t) * M + m0 + m, tile[t][m]);
       }
     } else {
-      const float* a = static_cast<const float*>(it.a);
       for (int j = threadIdx.x; j < tn * TM; j += 256) {
         const int t = j >> 6, m = j & 63;
-        if (m < mn) tile[t][m] = a[(int64_t)(t0 + t) * M + m0 + m];
+        if (m < mn) tile[t][m] = gld_f32(it.a, (int64_t)(t0 + t) * M + m0 + m);
       }
       __syncthreads();
       for (int j = threadIdx.x; j < mn * tn; j += 256) {
@@ -132,12 +130,13 @@ unsigned grid_x(int64_t max_elems) {
 }  // namespace
 
 hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dtype, int64_t max_elems,
-                            hipStream_t s) {
+                            hipStream_t s, const char* name) {
   if (n_items <= 0) return hipSuccess;
   static const char* names[5] = {"conv_vjp_rko_taps", "conv_vjp_grad_taps", "conv_vjp_rko_grad",
                                  "conv_vjp_combine_fwd", "conv_vjp_combine_bwd"};
   if (kind < 0 || kind > 4) return hipErrorInvalidValue;
-  timing_begin(names[kind], s);
+  if (!name) name = names[kind];
+  timing_begin(name, s);
   // the layout kernels take a 64 x 64 tile per grid-stride step
   const dim3 grid(kind <= 2 ? grid_x((max_elems + 15) / 16) : grid_x(max_elems), n_items);
   switch (kind) {
@@ -148,7 +147,7 @@ hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dty
     default: hipLaunchKernelGGL(combine_bwd_kernel, grid, dim3(256), 0, s, items); break;
   }
   hipError_t e = hipGetLastError();
-  timing_end(names[kind], s);
+  timing_end(name, s);
   return e;
 }
 

@@ -929,7 +929,8 @@ struct ConvPlan {
   std::vector<std::vector<CombineItem>> phase_comb;
   std::vector<int64_t> phase_max_elems;
   int64_t init_max = 0, scatter_max = 0;
-  size_t off_groups = 0, off_proj_items = 0;
+  std::vector<TapItem> scatter;                 // final taps -> OIHW kernel, per group
+  size_t off_groups = 0, off_proj_items = 0, off_scatter = 0;
   std::vector<size_t> off_phase_gemm, off_phase_comb;
   size_t table_bytes = 0, total_bytes = 0;
 };
@@ -1002,6 +1003,7 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
     P.off_phase_gemm[ph] = A.take(GemmList::bound(n_pg[ph]));
     P.off_phase_comb[ph] = A.take(sizeof(CombineItem) * n_pc[ph]);
   }
+  P.off_scatter = A.take(sizeof(TapItem) * n_groups);
   P.table_bytes = align_up(A.off);
 
   for (auto& t : tmp) {
@@ -1073,6 +1075,11 @@ void build_conv_plan(const orth_conv_desc* d, int32_t n, int32_t dtype, ConvPlan
     }
     G.cur = cur;
     P.groups.push_back(G);
+    // kernel[group * og + o][i][a][b] = taps[a k + b][o][i]: the group's
+    // slice of the OIHW kernel is the [og c][k k] transpose of its final taps
+    P.scatter.push_back(TapItem{G.taps[cur], nullptr,
+                                static_cast<unsigned char*>(L.kernel) + (size_t)t.group * og * c * k * k * esz,
+                                nullptr, og, c, k, k, 0, 0});
   }
   P.total_bytes = align_up(A.off);
   for (int ph = 0; ph < n_phase; ++ph) longest_first(P.phase_gemm[ph]);
@@ -2521,6 +2528,7 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
     put(img, P.off_phase_gemm[ph], P.phase_gemm[ph]);
     put(img, P.off_phase_comb[ph], P.phase_comb[ph]);
   }
+  put(img, P.off_scatter, P.scatter);
   rc = upload_tables(img, ws, s);
   if (rc) return rc;
   const ComposeGroup* G = reinterpret_cast<const ComposeGroup*>(ws + P.off_groups);
@@ -2532,7 +2540,8 @@ int orth_build_conv_kernels_batched(const orth_conv_desc* descs, int32_t n, int3
     ORTH_HIP(launch_compose_combine(G, reinterpret_cast<const CombineItem*>(ws + P.off_phase_comb[ph]),
                                     (int)P.phase_comb[ph].size(), P.phase_max_elems[ph], s));
   }
-  ORTH_HIP(launch_compose_scatter(G, ng, dtype, P.scatter_max, s));
+  ORTH_HIP(launch_tap_items(2, reinterpret_cast<const TapItem*>(ws + P.off_scatter), (int)P.scatter.size(), dtype,
+                            P.scatter_max, s, "compose_scatter"));
   return ORTH_OK;
 }
 

@@ -386,14 +386,13 @@ hipError_t launch_compose_init(const ComposeGroup* groups, int n_groups, int dty
                                hipStream_t s);
 hipError_t launch_compose_combine(const ComposeGroup* groups, const CombineItem* items, int n_items,
                                   int64_t max_elems, hipStream_t s);
-hipError_t launch_compose_scatter(const ComposeGroup* groups, int n_groups, int dtype,
-                                  int64_t max_elems, hipStream_t s);
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // kind: 0 taps from the RKO matrix, 1 taps from an OIHW kernel gradient,
-// 2 RKO gradient (or any OIHW tensor) from taps, 3 forward combine,
-// 4 adjoint combine
+// 2 RKO gradient (or any OIHW tensor: the composed kernel) from taps,
+// 3 forward combine, 4 adjoint combine; name: the timing name (default:
+// the kind's role in the composition VJP)
 hipError_t launch_tap_items(int kind, const TapItem* items, int n_items, int dtype, int64_t max_elems,
-                            hipStream_t s);
+                            hipStream_t s, const char* name = nullptr);
 
 // Exponentials (expo.hip).  One item per matrix or conv layer.
 struct ExpItem {

@@ -317,12 +317,8 @@ hipError_t launch_compose_combine(const ComposeGroup*, const CombineItem* items,
   table(items, n, "launch_compose_combine");
   return launched();
 }
-hipError_t launch_compose_scatter(const ComposeGroup* groups, int n, int, int64_t, hipStream_t) {
-  table(groups, n, "launch_compose_scatter");
-  return launched();
-}
 hipError_t launch_fill_f32(float*, int64_t, float, hipStream_t) { return launched(); }
-hipError_t launch_tap_items(int, const TapItem* items, int n, int, int64_t, hipStream_t) {
+hipError_t launch_tap_items(int, const TapItem* items, int n, int, int64_t, hipStream_t, const char*) {
   table(items, n, "launch_tap_items");
   return launched();
 }
