@@ -132,6 +132,13 @@ typedef struct {
  *
  * status_dev: optional device array of n int32 (orth_mat_status).  A zero
  * or non-finite matrix does not fail the call.
+ * Workspace: the size depends on the output descriptors as well.  An fp32
+ * output laid out as the matrix's fp32 iterate (rows >= cols, both
+ * multiples of the tile edge: 64 for fp32 products, 128 or 256 for bf16
+ * ones (see tile); ld_out == cols; a 16-byte aligned address) serves as
+ * the iterate buffer that the last step writes, so it needs no workspace
+ * and is written during the call, not only at its end.  Query the size
+ * with the descriptors of the call.
  * Returns ORTH_EINVAL for n < 0, a NULL pointer, rows or cols < 1,
  * ld < cols, iters < 0, beta outside (0, 0.5], an unknown dtype, compute or
  * prescale mode, in == out with differing dtype/leading dim, tile not in

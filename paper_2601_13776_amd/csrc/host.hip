@@ -564,6 +564,7 @@ struct OrthoPlan {
   size_t off_power[2] = {0, 0};
   size_t off_partials = 0, off_inv = 0, off_status = 0;
   size_t table_bytes = 0, total_bytes = 0;
+  int n_out_iter = 0;   // tiled matrices whose output buffer holds the fp32 iterate
 };
 
 // ORTH_LOG plan dump of an orthogonalization call
@@ -581,7 +582,8 @@ void log_ortho_plan(const char* entry, const OrthoPlan& P, const orth_bjorck_opt
                P.tabs[cls][TAB_GRAM].size(), P.tabs[cls][TAB_UPDATE].size());
   if (P.f32_gram.size())
     log_line("%s: fp32 64-tiles per step: %zu Gram + %zu update", entry, P.f32_gram.size(), P.f32_update[0].size());
-  log_line("%s: workspace %zu bytes (tables %zu)", entry, P.total_bytes, P.table_bytes);
+  log_line("%s: workspace %zu bytes (tables %zu); outputs holding the fp32 iterate: %d", entry, P.total_bytes,
+           P.table_bytes, P.n_out_iter);
   if (log_level() >= 3)
     for (size_t i = 0; i < P.mp.size(); ++i)
       log_line("%s:   matrix %zu: %d x %d (tall), padded %d x %d, bucket %d%s", entry, i, P.mp[i].M, P.mp[i].N,
@@ -798,8 +800,20 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     part_base += pr * pc;
     const size_t elems = (size_t)q.Mp * q.Np;
     const size_t csz = bf16 ? 2 : 4;
-    t.master[0] = reinterpret_cast<float*>(dev(A.take(elems * 4)));
-    t.master[1] = bf16 ? nullptr : reinterpret_cast<float*>(dev(A.take(elems * 4)));
+    // An fp32 output with the iterate's own layout (tall, no padding, row
+    // stride Np, 16-byte aligned) serves as the fp32 buffer that the last
+    // step writes (bf16 products update their single buffer in place; fp32
+    // ones alternate two, X_T landing in slot T mod 2): no workspace for it
+    // and no write-out pass.  The pre-scaling reads the input in full
+    // before anything is written there, so in-place calls qualify too.
+    const bool out_iter = o->out_dtype == ORTH_F32 && !q.transposed && q.Mp == m.rows && q.Np == m.cols &&
+                          m.ld_out == q.Np && (reinterpret_cast<uintptr_t>(m.out) & 15) == 0;
+    const int last = bf16 ? 0 : (o->iters & 1);
+    for (int k = 0; k < (bf16 ? 1 : 2); ++k)
+      t.master[k] = out_iter && k == last ? static_cast<float*>(m.out)
+                                          : reinterpret_cast<float*>(dev(A.take(elems * 4)));
+    if (bf16) t.master[1] = nullptr;
+    P.n_out_iter += out_iter;
     t.xc[0] = bf16 ? dev(A.take(elems * 2)) : nullptr;
     t.xc[1] = bf16 ? dev(A.take(elems * 2)) : nullptr;
     t.xt = bf16 ? nullptr : dev(A.take(elems * csz));   // the bf16 Gram reads X itself
@@ -821,7 +835,7 @@ void build_ortho_plan(const orth_mat* mats, int32_t n, const orth_bjorck_opts* o
     for (int a = 0; a < pr; ++a)
       for (int b = 0; b < pc; ++b) {
         P.partial_items.push_back(TileItem{tiled_idx, a, b, 0});
-        P.writeout_items.push_back(TileItem{tiled_idx, a, b, 0});
+        if (!out_iter) P.writeout_items.push_back(TileItem{tiled_idx, a, b, 0});
       }
     for (int a = 0; a < q.Mp / 64; ++a)
       for (int b = 0; b < q.Np / 64; ++b) P.scale_items.push_back(TileItem{tiled_idx, a, b, 0});

@@ -87,8 +87,42 @@ def test_workspace_sizes(L):
     rc, big = _ws_size(L, [(4096, 4096)], compute=1, dt=1)
     # fp32 iterate + two bf16 copies (ping-pong) + bf16 E
     assert rc == 0 and 4096 * 4096 * (4 + 2 + 2 + 2) <= big < 4096 * 4096 * 11
-    rc, f32 = _ws_size(L, [(512, 256)])
-    assert rc == 0 and f32 >= 512 * 256 * (4 + 4 + 4) + 256 * 256 * 4
+    # fp32 products, output not laid out as the iterate: two fp32 iterates
+    # (ping-pong) + the transposed iterate + E
+    f32 = _ws_out(L, [(512, 256)], 0, 0, 0, ld_pad=4)
+    assert f32 >= 512 * 256 * (4 + 4 + 4) + 256 * 256 * 4
+
+
+def _ws_out(L, shapes, compute, in_dt, out_dt, iters=5, ld_pad=0, out_off=0, inplace=False):
+    arr = (orth.orth_mat * len(shapes))()
+    for i, (r, c) in enumerate(shapes):
+        src = 0x10000 + 0x4000000 * i
+        dst = src if inplace else src + 0x2000000 + out_off
+        arr[i] = orth.orth_mat(src, dst, r, c, c + (ld_pad if inplace else 0), c + ld_pad)
+    opts = orth.orth_bjorck_opts(iters, 0.5, 1, in_dt, out_dt, compute, 1, None, 0)
+    n = ctypes.c_size_t()
+    assert L.orth_orthogonalize_workspace_size(arr, len(shapes), ctypes.byref(opts), ctypes.byref(n)) == 0
+    return n.value
+
+
+def test_output_holds_iterate(L):
+    """An fp32 output laid out as the fp32 iterate (tall, no padding,
+    ld_out == cols, 16-byte aligned) serves as the buffer the last step
+    writes: exactly one fp32 iterate less workspace; any other output keeps
+    the workspace buffer (and the write-out pass)."""
+    sq = [(4096, 4096)]
+    full = _ws_out(L, sq, 1, 1, 0, ld_pad=8)
+    assert full - _ws_out(L, sq, 1, 1, 0) == 4096 * 4096 * 4
+    assert _ws_out(L, sq, 1, 1, 0, out_off=8) == full           # misaligned output
+    assert _ws_out(L, sq, 1, 1, 1) == full                      # bf16 output
+    assert _ws_out(L, [(4096, 8192)], 1, 1, 0) == _ws_out(L, [(4096, 8192)], 1, 1, 0, ld_pad=8)   # wide
+    assert _ws_out(L, [(1000, 1000)], 1, 1, 0) == _ws_out(L, [(1000, 1000)], 1, 1, 0, ld_pad=8)   # padded
+    assert _ws_out(L, [(100, 40)], 0, 0, 0) == _ws_out(L, [(100, 40)], 0, 0, 0, ld_pad=8)         # fused kernel
+    for iters in (0, 5, 6):   # fp32 products: X_T in slot T mod 2, either slot
+        full = _ws_out(L, [(512, 256)], 0, 0, 0, iters=iters, ld_pad=4)
+        assert full - _ws_out(L, [(512, 256)], 0, 0, 0, iters=iters) == 512 * 256 * 4
+        assert full - _ws_out(L, [(512, 256)], 0, 0, 0, iters=iters, inplace=True) == 512 * 256 * 4
+        assert _ws_out(L, [(512, 256)], 0, 0, 0, iters=iters, ld_pad=4, inplace=True) == full
 
 
 @pytest.mark.parametrize("kw,shapes,code", [

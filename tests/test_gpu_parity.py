@@ -265,6 +265,45 @@ def test_inplace_strided_and_bf16_out(shape):
     assert checks.relative_difference(to_f64(o), ref) <= 4e-3
 
 
+@pytest.mark.parametrize("compute,shape,iters", [("f32", (256, 128), 0), ("f32", (256, 128), 5),
+                                                 ("f32", (512, 256), 6), ("bf16", (1024, 1024), 5),
+                                                 ("bf16", (1024, 512), 0)])
+def test_output_holding_the_iterate(compute, shape, iters):
+    """fp32 outputs laid out as the fp32 iterate (no padding, ld_out = cols)
+    hold the iterate during the call: the same bits as an output with a
+    wider row stride (which keeps the workspace buffer and the write-out
+    pass), also in place, and zero or non-finite inputs still give zeros or
+    NaN there."""
+    st = stored(108, [shape] * 3)
+    st[1][:] = 0.0
+    st[2][5, 3] = np.nan
+    ins = [to_dev(a) for a in st]
+    if compute == "bf16":
+        ins = [t.to(torch.bfloat16) for t in ins]
+    plain = [torch.full(shape, 3.0, device=DEV) for _ in ins]
+    wide = [torch.full((shape[0], shape[1] + 8), 3.0, device=DEV) for _ in ins]
+    views = [w[:, :shape[1]] for w in wide]
+    for outs in (plain, views):
+        status = torch.zeros(3, dtype=torch.int32, device=DEV)
+        orth.orth_orthogonalize_batched(ins, outs, iters, compute=compute, status=status)
+        torch.cuda.synchronize()
+        assert status.tolist() == [0, 1, 2]
+    for a, b in zip(plain, views):
+        assert torch.equal(a, b) or (torch.isnan(a).all() and torch.isnan(b).all())
+    assert torch.all(plain[1] == 0) and torch.all(torch.isnan(plain[2]))
+    assert torch.all(wide[0][:, shape[1]:] == 3.0)
+    ref = bjorck.bjorck(to_f64(ins[0]), iters)
+    assert checks.relative_difference(to_f64(plain[0]), ref) <= (REL_F32 if compute == "f32" else BF16_REL)
+    # in place (fp32 input and output)
+    t = to_dev(st[0])
+    orth.orth_orthogonalize_batched([t], [t], iters, compute=compute)
+    torch.cuda.synchronize()
+    if compute == "f32":
+        assert torch.equal(t, plain[0])
+    else:   # the bf16 copies now round the fp32 input, not a bf16 one
+        assert checks.relative_difference(to_f64(t), bjorck.bjorck(st[0].astype(np.float64), iters)) <= BF16_REL
+
+
 # ------------------------------------------------------------ composition --
 
 COMPOSE_GEOMS = [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (128, 512, 2, 2, 1, 1), (32, 32, 3, 1, 1, 4),

@@ -68,8 +68,9 @@ def test_noalloc_zero_matrix_and_statuses():
 
 
 def test_noalloc_rejects_a_batch_larger_than_its_scratch():
-    ins = [torch.empty(4096, 2048, dtype=torch.bfloat16, device=DEV)]
-    outs = [torch.empty(4096, 2048, device=DEV)]
+    # bf16 copies and E alone: 96 MiB (the fp32 output holds the iterate)
+    ins = [torch.empty(4096, 4096, dtype=torch.bfloat16, device=DEV)]
+    outs = [torch.empty(4096, 4096, device=DEV)]
     need = orth.orth_orthogonalize_workspace_size(ins, 10, compute="bf16", outs=outs)
     assert need > orth.ORTH_NOALLOC_SCRATCH_BYTES
     with pytest.raises(orth.OrthError) as e:
