@@ -117,15 +117,20 @@ def measured_traffic(kernel_name, workload):
         return None
 
 
+def big_tiles(shapes):
+    """The library's choice of 256-tiles for the matrices with N >= 1024 (a
+    tall list of (M, N)): their update tiles of 256 fill four waves of the
+    256 compute units."""
+    return sum(-(-m // 256) * -(-n // 256) for m, n in shapes if n >= 1024) >= 4 * 256
+
+
 def class_flops(w, kernel_name):
     """Algorithmic Björck flops of one parametrization step that run in the
     named tiled kernel: every matrix of its size class contributes
     4 m n min(m, n) T (a Gram and an update product per iteration)."""
     out = 0
     shapes = [(max(r, c), min(r, c)) for r, c in w.matrix_shapes()]
-    # 256-tiles only when the wide matrices' update tiles fill four waves of
-    # the 256 compute units (the library's planning rule)
-    big = sum(-(-m // 256) * -(-n // 256) for m, n in shapes if n >= 1024) >= 4 * 256
+    big = big_tiles(shapes)
     for m, n in shapes:
         if n <= 64 and m <= 128:          # fused small-matrix kernel
             continue
@@ -146,7 +151,7 @@ def executed_flops(w, kernel_name, iters=None):
     the dense 2 m n^2 for the Gram instead."""
     T = w.iters if iters is None else iters
     shapes = [(max(r, c), min(r, c)) for r, c in w.matrix_shapes()]
-    big = sum(-(-m // 256) * -(-n // 256) for m, n in shapes if n >= 1024) >= 4 * 256
+    big = big_tiles(shapes)
     out = 0
     for m, n in shapes:
         if n <= 64 and m <= 128:
@@ -227,11 +232,11 @@ def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, d
     log(f"[bench] vjp timed {steps} steps")
     names = orth.orth_timing_names()
     kt = {n: orth.orth_timing_read(n) for n in names}
+    # wall time covered by the GEMM-chain launches (side streams overlap)
+    gemm_ms = orth.orth_timing_span("bjorck_", "vjp_fwd_", "vjp_s_", "vjp_update_")[0] / steps
     orth.orth_timing_enable(False)
     ms = (t1 - t0) * 1e3 / steps
     flops = vjp_flops(w)
-    gemm_ms = sum(kt[n][0] for n in names if n.startswith(("bjorck_", "vjp_fwd_", "vjp_s_", "vjp_update_")))
-    gemm_ms /= steps
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     # roofline of the dominant gradient-recurrence kernel: its class's
     # algorithmic 6 m n^2 T flops per step over its measured time
@@ -627,14 +632,15 @@ def main():
     log(f"[bench] timed {args.steps} steps")
     names = orth.orth_timing_names()
     ktimes = {n: orth.orth_timing_read(n) for n in names}
+    # wall time covered by the Björck launches (the small-matrix kernels run
+    # on side streams, beside the tiled ones)
+    t_bjorck_ms = orth.orth_timing_span("bjorck_")[0] / args.steps
     orth.orth_timing_enable(False)
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = w.n_layers / (ms_per_step / 1e3)
     shapes = w.matrix_shapes()
     bjorck_flops = wl.algorithmic_bjorck_flops(shapes, w.iters)
-    gemm_names = [n for n in names if n.startswith("bjorck_")]
-    t_bjorck_ms = sum(ktimes[n][0] for n in gemm_names) / args.steps
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     bjorck_tflops = bjorck_flops / (t_bjorck_ms / 1e3) / 1e12 if t_bjorck_ms > 0 else None
     step_tflops = bjorck_flops / (ms_per_step / 1e3) / 1e12

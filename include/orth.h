@@ -500,11 +500,16 @@ int32_t orth_version(void);
  * launch stream (off by default; process-wide; not for concurrent callers).
  * orth_timing_read synchronizes the recorded events and returns the total
  * milliseconds and launch count of the named kernel since the last reset.
+ * orth_timing_span returns the wall-clock milliseconds covered by the
+ * launches whose kernel name starts with one of the ';'-separated
+ * prefixes (the union of their intervals: launches that overlap on
+ * several streams count once) and their number, since the last reset.
  * orth_timing_names writes a ';'-separated list of the kernel names seen.
  */
 int orth_timing_enable(int32_t on);
 int orth_timing_reset(void);
 int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launches);
+int orth_timing_span(const char* prefixes, double* covered_ms, int64_t* launches);
 int orth_timing_names(char* buf, size_t buf_bytes);
 
 #ifdef __cplusplus

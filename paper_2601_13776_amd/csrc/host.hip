@@ -77,6 +77,10 @@ bool g_timing = false;
 std::vector<TimingRec> g_pending;
 std::vector<hipEvent_t> g_event_pool;
 std::map<std::string, std::pair<double, int64_t>> g_totals;
+// per name, each launch's [start, end] in ms after the reference event (the
+// first start drained since the last reset; kept out of the pool until then)
+std::map<std::string, std::vector<std::pair<double, double>>> g_spans;
+hipEvent_t g_ref = nullptr;
 
 hipEvent_t pool_event() {
   if (!g_event_pool.empty()) {
@@ -92,15 +96,21 @@ hipEvent_t pool_event() {
 int drain_timing_locked() {
   int rc = ORTH_OK;
   for (auto& r : g_pending) {
-    float ms = 0.f;
+    float ms = 0.f, at = 0.f;
     if (r.a && r.b && hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
       auto& t = g_totals[r.name];
       t.first += ms;
       t.second += 1;
+      // events of every stream share the device's clock
+      if (!g_ref) g_ref = r.a;
+      if (hipEventElapsedTime(&at, g_ref, r.a) == hipSuccess)
+        g_spans[r.name].push_back({(double)at, (double)at + ms});
+      else
+        rc = ORTH_EHIP;
     } else {
       rc = ORTH_EHIP;
     }
-    if (r.a) g_event_pool.push_back(r.a);
+    if (r.a && r.a != g_ref) g_event_pool.push_back(r.a);
     if (r.b) g_event_pool.push_back(r.b);
   }
   g_pending.clear();
@@ -2939,6 +2949,9 @@ int orth_timing_reset(void) {
   std::lock_guard<std::mutex> lk(g_tmu);
   const int rc = drain_timing_locked();
   g_totals.clear();
+  g_spans.clear();
+  if (g_ref) g_event_pool.push_back(g_ref);
+  g_ref = nullptr;
   return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
 }
 
@@ -2949,6 +2962,42 @@ int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launche
   auto it = g_totals.find(kernel_name);
   *total_ms = it == g_totals.end() ? 0.0 : it->second.first;
   *launches = it == g_totals.end() ? 0 : it->second.second;
+  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+}
+
+int orth_timing_span(const char* prefixes, double* covered_ms, int64_t* launches) {
+  if (!prefixes || !covered_ms || !launches) return fail(ORTH_EINVAL, "NULL argument");
+  std::vector<std::string> pre;
+  for (const char* p = prefixes;;) {
+    const char* q = std::strchr(p, ';');
+    const std::string one = q ? std::string(p, q) : std::string(p);
+    if (!one.empty()) pre.push_back(one);
+    if (!q) break;
+    p = q + 1;
+  }
+  std::lock_guard<std::mutex> lk(g_tmu);
+  const int rc = drain_timing_locked();
+  std::vector<std::pair<double, double>> iv;
+  for (const auto& kv : g_spans)
+    for (const auto& p : pre)
+      if (kv.first.compare(0, p.size(), p) == 0) {
+        iv.insert(iv.end(), kv.second.begin(), kv.second.end());
+        break;
+      }
+  std::sort(iv.begin(), iv.end());
+  double covered = 0.0, lo = 0.0, hi = 0.0;
+  for (size_t i = 0; i < iv.size(); ++i) {
+    if (i == 0 || iv[i].first > hi) {
+      covered += hi - lo;
+      lo = iv[i].first;
+      hi = iv[i].second;
+    } else {
+      hi = std::max(hi, iv[i].second);
+    }
+  }
+  if (!iv.empty()) covered += hi - lo;
+  *covered_ms = covered;
+  *launches = (int64_t)iv.size();
   return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
 }
 

@@ -31,7 +31,8 @@ EXPORTED = [
     "orth_build_conv_kernels_vjp_saved_batched", "orth_conv_apply",
     "orth_exp_map_workspace_size", "orth_exp_map_batched", "orth_conv_exp_workspace_size", "orth_conv_exp_batched",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
-    "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_names",
+    "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_span",
+    "orth_timing_names",
 ]
 
 
@@ -135,6 +136,7 @@ def lib():
         L.orth_last_error.restype = ctypes.c_char_p
         L.orth_timing_enable.argtypes = [i32]
         L.orth_timing_read.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
+        L.orth_timing_span.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
         L.orth_timing_names.argtypes = [ctypes.c_char_p, sz]
         for name in EXPORTED:
             if name not in ("orth_status_string", "orth_last_error"):
@@ -550,6 +552,15 @@ def orth_timing_reset():
 def orth_timing_read(name):
     ms, n = ctypes.c_double(), ctypes.c_int64()
     _check(lib().orth_timing_read(name.encode(), ctypes.byref(ms), ctypes.byref(n)), "orth_timing_read")
+    return ms.value, n.value
+
+
+def orth_timing_span(*prefixes):
+    """Wall-clock ms covered by the launches whose names start with any of
+    the prefixes (overlapping launches count once), and their number."""
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    _check(lib().orth_timing_span(";".join(prefixes).encode(), ctypes.byref(ms), ctypes.byref(n)),
+           "orth_timing_span")
     return ms.value, n.value
 
 

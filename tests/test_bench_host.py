@@ -16,12 +16,11 @@ from paper_2601_13776_amd import workloads as wl
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def tiles_counted(w, cls_name):
+def tiles_counted(w, cls_name, big):
     """Executed flops by listing every tile: Gram tiles (i <= j) over the
-    padded rows, update tiles over the padded columns."""
+    padded rows, update tiles over the padded columns (big: the matrices
+    with N >= 1024 are on 256-tiles)."""
     shapes = [(max(r, c), min(r, c)) for r, c in w.matrix_shapes()]
-    wide = [(m, n) for m, n in shapes if n >= 1024]
-    big = sum(-(-m // 256) * -(-n // 256) for m, n in wide) >= 1024
     total = 0
     for m, n in shapes:
         if n <= 64 and m <= 128:
@@ -38,11 +37,46 @@ def tiles_counted(w, cls_name):
     return total * w.iters
 
 
-@pytest.mark.parametrize("name,kernel", [("stress_4096x64_32x4096", "bjorck_bf16_256"),
-                                         ("imagenet_backbone25", "bjorck_bf16_128")])
-def test_executed_flops_match_a_tile_count(name, kernel):
+@pytest.mark.parametrize("name,kernel,big", [("stress_4096x64_32x4096", "bjorck_bf16_256", True),
+                                             ("imagenet_backbone25", "bjorck_bf16_128", False)])
+def test_executed_flops_match_a_tile_count(name, kernel, big):
     w = wl.WORKLOADS[name]
-    assert bench.executed_flops(w, kernel) == tiles_counted(w, kernel)
+    assert bench.executed_flops(w, kernel) == tiles_counted(w, kernel, big)
+
+
+def _library_uses_256(shapes, vjp):
+    """The library's own choice, read from its workspace sizes: the automatic
+    choice sizes like the forced 256-tiles and unlike the forced 128."""
+    import ctypes
+    from paper_2601_13776_amd import orth
+    L = orth.lib()
+    sizes = []
+    for tile in (0, 128, 256):
+        opts = orth.orth_bjorck_opts(5, 0.5, 1, 1, 1, 1, 1, None, tile)
+        n = ctypes.c_size_t()
+        if vjp:
+            arr = (orth.orth_vjp_mat * len(shapes))()
+            for i, (r, c) in enumerate(shapes):
+                b = 0x10000 + 0x4000000 * i
+                arr[i] = orth.orth_vjp_mat(b, b + 0x1000000, b + 0x2000000, r, c, c, c, c)
+            rc = L.orth_orthogonalize_vjp_workspace_size(arr, len(shapes), ctypes.byref(opts), ctypes.byref(n))
+        else:
+            arr = (orth.orth_mat * len(shapes))()
+            for i, (r, c) in enumerate(shapes):
+                b = 0x10000 + 0x4000000 * i
+                arr[i] = orth.orth_mat(b, b + 0x2000000, r, c, c, c)
+            rc = L.orth_orthogonalize_workspace_size(arr, len(shapes), ctypes.byref(opts), ctypes.byref(n))
+        assert rc == 0
+        sizes.append(n.value)
+    assert sizes[1] != sizes[2]
+    return sizes[0] == sizes[2]
+
+
+@pytest.mark.parametrize("name", ["stress_4096x64_32x4096", "imagenet_backbone25"])
+def test_bench_tile_rule_matches_the_library(name):
+    shapes = wl.WORKLOADS[name].matrix_shapes()
+    tall = [(max(r, c), min(r, c)) for r, c in shapes]
+    assert bench.big_tiles(tall) == _library_uses_256(shapes, vjp=False) == _library_uses_256(shapes, vjp=True)
 
 
 def test_stress_flop_counts():

@@ -119,6 +119,41 @@ def test_bf16_mixed_batch(tile):
             assert abs(checks.gram_deviation(got) - checks.gram_deviation(ref)) <= ORTH_BF16, shape
 
 
+def test_bf16_two_tile_classes_and_timing_span():
+    """A batch with both bf16 tile classes (the N >= 1024 matrices forced to
+    256-tiles): the same bits as each class's matrices orthogonalized in
+    calls of their own, the oracle's result on a sampled large matrix, and
+    a timing span (the union of the launches' intervals) between the longer
+    class's kernel time and the sum of both."""
+    shapes = [(2048, 2048)] * 4 + [(512, 256), (256, 512), (384, 384), (1000, 130)] * 2
+    st = stored(109, shapes, dtype="bf16")
+    ins = [to_dev(a) for a in st]
+    iters = 6
+    print("[bf16 two classes] combined call", flush=True)
+    orth.orth_timing_enable(True)
+    orth.orth_timing_reset()
+    both = [torch.empty(t.shape, device=DEV) for t in ins]
+    orth.orth_orthogonalize_batched(ins, both, iters, compute="bf16", tile=256)
+    torch.cuda.synchronize()
+    t256, n256 = orth.orth_timing_read("bjorck_bf16_256")
+    t128, n128 = orth.orth_timing_read("bjorck_bf16_128")
+    span, n = orth.orth_timing_span("bjorck_bf16_")
+    orth.orth_timing_enable(False)
+    orth.orth_timing_reset()
+    assert n256 == n128 == 2 * iters and n == n256 + n128
+    assert max(t256, t128) * 0.999 <= span <= (t256 + t128) * 1.001
+    print("[bf16 two classes] classes apart", flush=True)
+    for part in ([0, 1, 2, 3], list(range(4, len(shapes)))):
+        outs = [torch.empty(ins[i].shape, device=DEV) for i in part]
+        orth.orth_orthogonalize_batched([ins[i] for i in part], outs, iters, compute="bf16", tile=256)
+        torch.cuda.synchronize()
+        for i, o in zip(part, outs):
+            assert torch.equal(o, both[i]), shapes[i]
+    ref = bjorck.bjorck(oracle_inputs([st[3]])[0], iters)
+    assert checks.relative_difference(to_f64(both[3]), ref) <= BF16_REL
+    assert checks.tile_relative_differences(to_f64(both[3]), ref, 256).max() <= BF16_REL
+
+
 # K-loop lengths of the bf16 tile kernel: with 64-deep k-steps, a Gram tile
 # runs Mp / 64 k-steps and an update tile tj * T / 64 (stored-tile part)
 # plus (Np - tj * T) / 64 (the rest) for tile size T, always even; the loop
