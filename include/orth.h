@@ -81,7 +81,9 @@ typedef struct {
   const void* in;   /* device, rows x cols, leading dim ld_in, opts.in_dtype */
   void* out;        /* device, rows x cols, leading dim ld_out, opts.out_dtype.
                        May equal `in` (in-place) when dtypes and leading
-                       dims agree; otherwise the two must not overlap. */
+                       dims agree; otherwise the two must not overlap, and
+                       no output may overlap another matrix's input or
+                       output (an output can be written during the call). */
   int32_t rows, cols;   /* >= 1 */
   int64_t ld_in, ld_out;
 } orth_mat;
