@@ -221,6 +221,9 @@ def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, d
         vstep()
         torch.cuda.synchronize()
         log(f"[bench] vjp warmup {i + 1}/{warmup}")
+    # events only around the GEMM-chain launches (each timed launch costs a
+    # few microseconds of stream time)
+    orth.orth_timing_filter("bjorck_", "vjp_fwd_", "vjp_s_", "vjp_update_")
     orth.orth_timing_enable(True)
     orth.orth_timing_reset()
     torch.cuda.synchronize()
@@ -235,6 +238,7 @@ def run_vjp(w, ins, outs, layers, status, compute, steps, warmup, torch, orth, d
     # wall time covered by the GEMM-chain launches (side streams overlap)
     gemm_ms = orth.orth_timing_span("bjorck_", "vjp_fwd_", "vjp_s_", "vjp_update_")[0] / steps
     orth.orth_timing_enable(False)
+    orth.orth_timing_filter()
     ms = (t1 - t0) * 1e3 / steps
     flops = vjp_flops(w)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -376,6 +380,7 @@ def run_conv_apply(w, layers, batch, steps, torch, orth, dev):
             orth.orth_conv_apply(L["kernel"], L["geom"], yt, transposed=True)
     one()
     torch.cuda.synchronize()
+    orth.orth_timing_filter("conv_apply")
     orth.orth_timing_enable(True)
     orth.orth_timing_reset()
     t0 = time.perf_counter()
@@ -385,6 +390,7 @@ def run_conv_apply(w, layers, batch, steps, torch, orth, dev):
     t1 = time.perf_counter()
     kt = {n: orth.orth_timing_read(n) for n in ("conv_apply", "conv_apply_transposed")}
     orth.orth_timing_enable(False)
+    orth.orth_timing_filter()
     flops = sum(j[3] for j in jobs)
     out = {"batch": batch, "first_layer_hw": APPLY_HW[w.name], "ms_per_pass": round((t1 - t0) * 1e3 / steps, 3),
            "algorithmic_flops_per_direction": flops}
@@ -436,6 +442,7 @@ def run_expo(w, ins, steps, torch, orth, dev, terms=12, conv_terms=6):
     for name, fn, flops, kname, count in jobs:
         fn()
         torch.cuda.synchronize()
+        orth.orth_timing_filter(kname)
         orth.orth_timing_enable(True)
         orth.orth_timing_reset()
         t0 = time.perf_counter()
@@ -445,6 +452,7 @@ def run_expo(w, ins, steps, torch, orth, dev, terms=12, conv_terms=6):
         t1 = time.perf_counter()
         kt = orth.orth_timing_read(kname)
         orth.orth_timing_enable(False)
+        orth.orth_timing_filter()
         ms = (t1 - t0) * 1e3 / steps
         kms = kt[0] / steps
         ach = flops / (kms / 1e3) / 1e12
@@ -621,6 +629,10 @@ def main():
         log(f"[bench] warmup {i + 1}/{args.warmup}")
     assert int(status.max().item()) == 0, "a matrix was reported degenerate"
 
+    # events only around the Björck launches, which the rates and the
+    # roofline need (each timed launch costs a few microseconds of stream
+    # time, which would otherwise inflate the small workloads' step)
+    orth.orth_timing_filter("bjorck_", *(("power_",) if args.prescale == "spectral" else ()))
     orth.orth_timing_enable(True)
     orth.orth_timing_reset()
     torch.cuda.synchronize()
@@ -636,6 +648,7 @@ def main():
     # on side streams, beside the tiled ones)
     t_bjorck_ms = orth.orth_timing_span("bjorck_")[0] / args.steps
     orth.orth_timing_enable(False)
+    orth.orth_timing_filter()
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = w.n_layers / (ms_per_step / 1e3)

@@ -507,8 +507,12 @@ int32_t orth_version(void);
  * prefixes (the union of their intervals: launches that overlap on
  * several streams count once) and their number, since the last reset.
  * orth_timing_names writes a ';'-separated list of the kernel names seen.
+ * orth_timing_filter limits the timing to launches whose kernel name starts
+ * with one of the ';'-separated prefixes (NULL or "": every launch); each
+ * timed launch adds two event records to its stream (a few microseconds).
  */
 int orth_timing_enable(int32_t on);
+int orth_timing_filter(const char* prefixes);
 int orth_timing_reset(void);
 int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launches);
 int orth_timing_span(const char* prefixes, double* covered_ms, int64_t* launches);

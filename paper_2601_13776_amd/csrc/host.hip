@@ -81,6 +81,27 @@ std::map<std::string, std::pair<double, int64_t>> g_totals;
 // first start drained since the last reset; kept out of the pool until then)
 std::map<std::string, std::vector<std::pair<double, double>>> g_spans;
 hipEvent_t g_ref = nullptr;
+std::vector<std::string> g_filter;   // name prefixes of the launches to time (empty: all)
+
+bool timed_locked(const char* name) {
+  if (g_filter.empty()) return true;
+  for (const auto& p : g_filter)
+    if (std::strncmp(name, p.c_str(), p.size()) == 0) return true;
+  return false;
+}
+
+std::vector<std::string> split_prefixes(const char* prefixes) {
+  std::vector<std::string> out;
+  if (!prefixes) return out;
+  for (const char* p = prefixes;;) {
+    const char* q = std::strchr(p, ';');
+    const std::string one = q ? std::string(p, q) : std::string(p);
+    if (!one.empty()) out.push_back(one);
+    if (!q) break;
+    p = q + 1;
+  }
+  return out;
+}
 
 hipEvent_t pool_event() {
   if (!g_event_pool.empty()) {
@@ -122,6 +143,7 @@ void timing_begin(const char* name, hipStream_t s) {
   if (log_level() >= 2) log_line("launch %s on stream %p", name, (void*)s);
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
+  if (!timed_locked(name)) return;
   TimingRec r{name, pool_event(), nullptr};
   // a failed record leaves the pair incomplete, which the read reports
   if (r.a && hipEventRecord(r.a, s) != hipSuccess) {
@@ -142,6 +164,7 @@ void timing_end(const char* name, hipStream_t s) {
   }
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
+  if (!timed_locked(name)) return;
   for (auto it = g_pending.rbegin(); it != g_pending.rend(); ++it) {
     if (it->b == nullptr && it->name == name) {
       it->b = pool_event();
@@ -2965,16 +2988,15 @@ int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launche
   return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
 }
 
+int orth_timing_filter(const char* prefixes) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_filter = split_prefixes(prefixes);
+  return ORTH_OK;
+}
+
 int orth_timing_span(const char* prefixes, double* covered_ms, int64_t* launches) {
   if (!prefixes || !covered_ms || !launches) return fail(ORTH_EINVAL, "NULL argument");
-  std::vector<std::string> pre;
-  for (const char* p = prefixes;;) {
-    const char* q = std::strchr(p, ';');
-    const std::string one = q ? std::string(p, q) : std::string(p);
-    if (!one.empty()) pre.push_back(one);
-    if (!q) break;
-    p = q + 1;
-  }
+  const std::vector<std::string> pre = split_prefixes(prefixes);
   std::lock_guard<std::mutex> lk(g_tmu);
   const int rc = drain_timing_locked();
   std::vector<std::pair<double, double>> iv;

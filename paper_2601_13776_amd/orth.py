@@ -31,8 +31,8 @@ EXPORTED = [
     "orth_build_conv_kernels_vjp_saved_batched", "orth_conv_apply",
     "orth_exp_map_workspace_size", "orth_exp_map_batched", "orth_conv_exp_workspace_size", "orth_conv_exp_batched",
     "orth_check_workspace_size", "orth_check_norm", "orth_status_string", "orth_last_error",
-    "orth_version", "orth_timing_enable", "orth_timing_reset", "orth_timing_read", "orth_timing_span",
-    "orth_timing_names",
+    "orth_version", "orth_timing_enable", "orth_timing_filter", "orth_timing_reset", "orth_timing_read",
+    "orth_timing_span", "orth_timing_names",
 ]
 
 
@@ -136,6 +136,7 @@ def lib():
         L.orth_last_error.restype = ctypes.c_char_p
         L.orth_timing_enable.argtypes = [i32]
         L.orth_timing_read.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
+        L.orth_timing_filter.argtypes = [ctypes.c_char_p]
         L.orth_timing_span.argtypes = [ctypes.c_char_p, P(ctypes.c_double), P(ctypes.c_int64)]
         L.orth_timing_names.argtypes = [ctypes.c_char_p, sz]
         for name in EXPORTED:
@@ -543,6 +544,12 @@ def orth_check_norm_conv(kernel, geom, x, adjoint=False, workspace=None, stream=
 
 def orth_timing_enable(on=True):
     _check(lib().orth_timing_enable(1 if on else 0), "orth_timing_enable")
+
+
+def orth_timing_filter(*prefixes):
+    """Time only launches whose kernel names start with one of the prefixes
+    (none: every launch)."""
+    _check(lib().orth_timing_filter(";".join(prefixes).encode()), "orth_timing_filter")
 
 
 def orth_timing_reset():
