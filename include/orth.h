@@ -154,8 +154,8 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n,
                                void* stream);
 
 /*
- * For callers that cannot allocate (code under HIP graph capture, tight
- * serving loops, harnesses that forbid hipMalloc): the same
+ * For callers that cannot allocate (tight serving loops, harnesses that
+ * forbid hipMalloc): the same
  * orthogonalization as orth_orthogonalize_batched, same arguments and
  * results, with the library's own device scratch in place of the
  * workspace.  The scratch is a fixed array of ORTH_NOALLOC_SCRATCH_BYTES
@@ -170,8 +170,11 @@ int orth_orthogonalize_batched(const orth_mat* mats, int32_t n,
  * zero): calls that overlap on one GPU (other streams or threads without
  * an ordering between them) race and must be serialized by the caller.
  * status_dev as for orth_orthogonalize_batched (NULL: the statuses stay in
- * the scratch).  Errors: those of orth_orthogonalize_batched, and
- * ORTH_EWORKSPACE for a batch larger than the scratch.
+ * the scratch).  The call cannot be captured into a HIP graph (its table
+ * copies read host memory that lives only during the call): on a capturing
+ * stream it returns ORTH_EUNSUPPORTED before anything is enqueued.
+ * Errors: those of orth_orthogonalize_batched, ORTH_EWORKSPACE for a batch
+ * larger than the scratch, and ORTH_EUNSUPPORTED under stream capture.
  */
 #define ORTH_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 int orth_orthogonalize_batched_noalloc(const orth_mat* mats, int32_t n,

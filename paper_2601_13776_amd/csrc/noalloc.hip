@@ -1,7 +1,7 @@
 // Allocation-free orthogonalization: orth_orthogonalize_batched with a fixed
 // device array of the library in place of the caller's workspace, for
-// callers that cannot allocate (code under HIP graph capture, tight serving
-// loops, harnesses that forbid allocation).  The call allocates nothing:
+// callers that cannot allocate (tight serving loops, harnesses that forbid
+// allocation; not code under HIP graph capture, which it refuses).  The call allocates nothing:
 // the scratch below instead of a workspace, descriptor tables copied from
 // pageable host memory instead of the pinned staging pool, every kernel on
 // the caller's stream instead of side streams.
@@ -84,8 +84,18 @@ extern "C" int orth_orthogonalize_batched_noalloc(const orth_mat* mats, int32_t 
     return report_error(ORTH_EWORKSPACE, msg.c_str());
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // A captured call could not be replayed: its table copies read host
+  // memory that lives only during the call.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(s, &cap);
+  if (e != hipSuccess)
+    return report_error(ORTH_EHIP, (std::string("hipStreamIsCapturing: ") + hipGetErrorString(e)).c_str());
+  if (cap != hipStreamCaptureStatusNone)
+    return report_error(ORTH_EUNSUPPORTED,
+                        "orth_orthogonalize_batched_noalloc cannot be captured into a HIP graph: its descriptor "
+                        "tables are copied from host memory that lives only during the call");
   int dev = 0;
-  hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+  e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
   if (e != hipSuccess)
     return report_error(ORTH_EHIP, (std::string("device of the stream: ") + hipGetErrorString(e)).c_str());
   unsigned char* ws = nullptr;

@@ -77,3 +77,23 @@ def test_noalloc_rejects_a_batch_larger_than_its_scratch():
         orth.orth_orthogonalize_batched_noalloc(ins, outs, 10, compute="bf16")
     assert e.value.code == orth.ORTH_EWORKSPACE
     assert "holds" in str(e.value)
+
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
+def test_noalloc_refuses_stream_capture():
+    """Under HIP graph capture the allocation-free call refuses before it
+    enqueues anything (its tables are copied from host memory of the call),
+    and an ordinary call afterwards still matches the workspace entry point."""
+    st = stored(34, [(300, 200), (40, 20)])
+    ins = [to_dev(s) for s in st]
+    outs = [torch.empty(t.shape, device=DEV) for t in ins]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with pytest.raises(orth.OrthError) as e:
+        with torch.cuda.graph(g):
+            orth.orth_orthogonalize_batched_noalloc(ins, outs, 5)
+    assert e.value.code == orth.ORTH_EUNSUPPORTED
+    assert "captured" in str(e.value)
+    torch.cuda.synchronize()
+    status = both(st, 5, "f32")
+    assert list(status) == [0, 0]
