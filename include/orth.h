@@ -27,8 +27,10 @@
  *   allocated (pinned host memory, never device memory) when none is
  *   idle.  The host blocks in one case only: when 64 calls' copies are
  *   still in flight, a call waits for the oldest of them.  Because the
- *   staging buffers are reused, a call's copies must not be captured into
- *   a HIP graph that is replayed after later calls.  The Björck
+ *   staging buffers are reused, a captured copy would read whatever later
+ *   calls left there: every call that copies tables returns
+ *   ORTH_EUNSUPPORTED on a capturing stream (HIP graph capture), before
+ *   anything is enqueued.  The Björck
  *   entry points may run the small matrices of a batch on side streams
  *   that fork from `stream` and join back into it within the call (event
  *   record and wait; default priority; per calling thread and device,

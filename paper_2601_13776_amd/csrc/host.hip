@@ -320,6 +320,14 @@ struct TableImage {
 
 static int upload_tables(const TableImage& img, void* dst, hipStream_t s) {
   if (img.data.empty()) return ORTH_OK;
+  // a captured copy would read its staging buffer at replay, after later
+  // calls have refilled it: calls with tables refuse a capturing stream
+  // (this is their first enqueue, so nothing is left half-captured)
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  ORTH_HIP(hipStreamIsCapturing(s, &cap));
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(ORTH_EUNSUPPORTED, "the call cannot be captured into a HIP graph: its descriptor tables are "
+                                   "copied from staging buffers that later calls reuse");
   std::lock_guard<std::mutex> lk(g_smu);
   const size_t total = img.data.size();
   // the smallest idle buffer that fits

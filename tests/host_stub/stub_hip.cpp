@@ -219,6 +219,10 @@ hipError_t hipStreamGetDevice(hipStream_t, hipDevice_t* d) {
   *d = 0;
   return hipSuccess;
 }
+hipError_t hipStreamIsCapturing(hipStream_t, hipStreamCaptureStatus* c) {
+  *c = hipStreamCaptureStatusNone;
+  return hipSuccess;
+}
 hipError_t hipGetDevice(int* d) {
   *d = 0;
   return hipSuccess;

@@ -263,6 +263,27 @@ def test_empty_batch():
     orth.orth_orthogonalize_batched([], [], 5)
 
 
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
+def test_calls_refuse_stream_capture():
+    """Calls that copy descriptor tables refuse a capturing stream before
+    enqueuing anything (a captured copy would read a staging buffer that
+    later calls refill); the stream works normally afterwards."""
+    st = stored(110, [(300, 200), (40, 20)])
+    ins = [to_dev(a) for a in st]
+    outs = [torch.empty(t.shape, device=DEV) for t in ins]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with pytest.raises(orth.OrthError) as e:
+        with torch.cuda.graph(g):
+            orth.orth_orthogonalize_batched(ins, outs, 5)
+    assert e.value.code == orth.ORTH_EUNSUPPORTED and "captured" in str(e.value)
+    torch.cuda.synchronize()
+    got, status = gpu_orthogonalize(st, 5)
+    assert np.all(status == 0)
+    for s, o in zip(oracle_inputs(st), got):
+        assert checks.relative_difference(to_f64(o), bjorck.bjorck(s, 5)) <= REL_F32
+
+
 @pytest.mark.parametrize("shape", [(16, 8), (300, 200)])
 def test_zero_and_nonfinite(shape):
     z = np.zeros(shape, dtype=np.float32)
