@@ -378,3 +378,54 @@ def test_imagenet_spectral_full_size():
         ref, v, _ = spectral.bjorck_spectral(x, v0, w.iters, 1)
         assert checks.relative_difference(to_f64(outs[i]), ref) <= BF16_REL, i
         assert np.max(np.abs(un[offs[i]:offs[i + 1]] - v)) <= 1e-5, i
+
+
+def test_imagenet_spectral_vjp_full_size():
+    """The backward pass through spectral pre-scaling (one power step from
+    warmed cached vectors, held constant) of all 89 factors of the
+    ImageNet-like stack in one call: sampled factors of every size class
+    against the oracle, the 2048-wide ones through the scale invariance of
+    the parametrization (<W, dL/dW> = 0), and the VJP from a saving forward
+    equal to the recomputing one bit for bit."""
+    from oracle import spectral
+    w = wl.WORKLOADS["imagenet_backbone25"]
+    shapes = w.matrix_shapes()
+    ins = [to_dev(wl.stored_matrix(w, i, *s)) for i, s in enumerate(shapes)]
+    outs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in ins]
+    rng = np.random.default_rng(12)
+    u = torch.from_numpy(np.concatenate([rng.standard_normal(min(s)).astype(np.float32) for s in shapes])).to(DEV)
+    orth.orth_orthogonalize_batched(ins, outs, 0, compute="bf16", prescale="spectral", power_iters=5, u=u)
+    torch.cuda.synchronize()
+    warm = u.cpu().numpy().copy()
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(13)
+    gouts = [torch.randn(s, generator=gen, device=DEV) for s in shapes]
+    gins = [torch.empty_like(t) for t in ins]
+    status = torch.full((len(ins),), -1, dtype=torch.int32, device=DEV)
+    opts = dict(compute="bf16", prescale="spectral", power_iters=1, u=u)
+    ws = orth.orth_orthogonalize_vjp_batched(ins, gouts, gins, w.iters, status=status, **opts)
+    torch.cuda.synchronize()
+    print("[imagenet spectral vjp] done", flush=True)
+    assert np.all(status.cpu().numpy() == 0)
+    assert np.array_equal(u.cpu().numpy(), warm), "the vector-Jacobian product must not write the cached vectors"
+    # the training pattern: a saving forward (which advances the vectors) and
+    # the VJP from what it kept
+    orth.orth_orthogonalize_save_batched(ins, outs, w.iters, workspace=ws, **opts)
+    gsaved = [torch.empty_like(t) for t in ins]
+    orth.orth_orthogonalize_vjp_batched(ins, gouts, gsaved, w.iters, workspace=ws, saved=True, **opts)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(gsaved, gins))
+    del gsaved, ws
+    offs = np.cumsum([0] + [min(s) for s in shapes])
+    for i in (1, 21, 40, 61, 80):
+        print(f"[imagenet spectral vjp] factor {i} {shapes[i]}", flush=True)
+        x = wl.as_f64(wl.stored_matrix(w, i, *shapes[i]))
+        v0 = warm[offs[i]:offs[i + 1]].astype(np.float64)
+        ref = spectral.bjorck_spectral_vjp(x, v0, to_f64(gouts[i]), w.iters, 1)
+        bound = 6e-2 if shapes[i][0] == shapes[i][1] else 1e-2
+        assert checks.relative_difference(to_f64(gins[i]), ref) <= bound, i
+    for i in (84, 87, 88):
+        wf, gf = to_f64(ins[i]), to_f64(gins[i])
+        assert bool(np.isfinite(gf).all()), i
+        assert abs(float(np.sum(wf * gf))) <= 2e-2 * np.linalg.norm(wf) * np.linalg.norm(gf), i
+
