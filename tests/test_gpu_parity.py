@@ -364,7 +364,11 @@ def test_output_holding_the_iterate(compute, shape, iters):
 
 COMPOSE_GEOMS = [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (128, 512, 2, 2, 1, 1), (32, 32, 3, 1, 1, 4),
                  (32, 32, 3, 1, 2, 1), (8, 8, 1, 1, 1, 1), (6, 6, 5, 2, 3, 3), (24, 16, 4, 2, 1, 2),
-                 (4, 6, 3, 1, 1, 1), (100, 70, 3, 1, 1, 1)]
+                 (4, 6, 3, 1, 1, 1), (100, 70, 3, 1, 1, 1),
+                 # a 3-channel stem and head (rank-1 projectors on 3 channels), k = 7,
+                 # even k with stride, dilation with groups, k = s with groups
+                 (3, 64, 3, 1, 1, 1), (64, 3, 3, 1, 1, 1), (64, 64, 7, 1, 1, 1), (32, 64, 4, 2, 1, 1),
+                 (48, 48, 3, 1, 2, 3), (16, 32, 2, 2, 1, 2), (12, 12, 5, 1, 2, 2)]
 
 
 def oracle_factors(geom, seed, iters=40):

@@ -208,7 +208,8 @@ def test_conv_vjp_parity_batched():
             assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= REL_F32, geom
 
 
-@pytest.mark.parametrize("geom", [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (6, 6, 5, 2, 3, 3)])
+@pytest.mark.parametrize("geom", [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (6, 6, 5, 2, 3, 3),
+                                  (3, 64, 3, 1, 1, 1), (32, 64, 4, 2, 1, 1), (12, 12, 5, 1, 2, 2)])
 def test_conv_vjp_parity_single(geom):
     rko, proj, dk = conv_factors(geom, 400)
     L = conv_vjp_gpu([(geom, rko, proj, dk)])[0]
