@@ -45,7 +45,9 @@ def test_status_strings(L):
 
 GEOMS = [(16, 16, 3, 1, 1, 1), (64, 128, 3, 2, 1, 1), (128, 512, 2, 2, 1, 1), (256, 256, 3, 1, 1, 4),
          (256, 256, 3, 1, 2, 1), (8, 8, 1, 1, 1, 1), (6, 6, 5, 2, 3, 3), (4, 4, 1, 2, 1, 1),
-         (4, 4, 3, 2, 2, 1), (4, 4, 3, 1, 1, 3), (0, 4, 3, 1, 1, 1), (2, 4, 3, 1, 1, 2), (4, 4, 3, 1, 0, 1)]
+         (4, 4, 3, 2, 2, 1), (4, 4, 3, 1, 1, 3), (0, 4, 3, 1, 1, 1), (2, 4, 3, 1, 1, 2), (4, 4, 3, 1, 0, 1),
+         (3, 64, 3, 1, 1, 1), (64, 3, 3, 1, 1, 1), (64, 64, 7, 1, 1, 1), (32, 64, 4, 2, 1, 1), (48, 48, 3, 1, 2, 3),
+         (16, 32, 2, 2, 1, 2), (12, 12, 5, 1, 2, 2), (16, 16, 3, 1, 1, 16), (8, 8, 3, 2, 1, 8)]
 
 
 @pytest.mark.parametrize("geom", GEOMS)
