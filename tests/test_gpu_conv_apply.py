@@ -26,6 +26,8 @@ GEOMS = [  # (cin, cout, k, s, d, g), H
     ((4, 4, 5, 1, 3, 1), 4), ((8, 8, 3, 2, 5, 2), 4),
     # 128 x 128 tiles with ragged rows both ways (200 and 130 output rows)
     ((130, 200, 3, 1, 1, 1), 6),
+    # a 3-channel stem and head, k = 7 (no halo path), even k with stride
+    ((3, 64, 3, 1, 1, 1), 16), ((64, 3, 3, 1, 1, 1), 16), ((16, 16, 7, 1, 1, 1), 11), ((32, 64, 4, 2, 1, 1), 12),
 ]
 
 
@@ -80,7 +82,8 @@ def aoc_kernel_gpu(geom, seed):
 
 
 @pytest.mark.parametrize("geom,hw", [((16, 16, 3, 1, 1, 1), 16), ((64, 128, 3, 2, 1, 1), 16),
-                                     ((32, 32, 3, 1, 1, 4), 12), ((24, 48, 4, 2, 1, 2), 8)])
+                                     ((32, 32, 3, 1, 1, 4), 12), ((24, 48, 4, 2, 1, 2), 8),
+                                     ((64, 3, 3, 1, 1, 1), 16), ((16, 16, 7, 1, 1, 1), 11)])
 def test_transposed_aoc_is_isometry(geom, hw):
     """cout/g <= c s^2: the AOC conv has orthonormal rows, so its transpose
     (learnable upsampling) preserves norms and the forward conv undoes it."""
