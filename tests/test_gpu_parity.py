@@ -93,6 +93,23 @@ def test_beta_and_no_prescale(beta):
         assert checks.relative_difference(to_f64(o), ref) <= REL_F32
 
 
+@pytest.mark.parametrize("beta,tile", [(0.25, 0), (0.25, 256), (0.5, 128)])
+def test_bf16_beta_and_no_prescale(beta, tile):
+    """bf16 products with beta < 1/2 and without pre-scaling (the caller's
+    scale is the iterate's start), on both tile classes and the fused
+    small-matrix kernel."""
+    shapes = [(40, 20), (256, 128), (1024, 1024), (1100, 1030)]
+    st = stored(113, shapes)
+    pre = [(x / np.linalg.norm(x)).astype(np.float32) for x in oracle_inputs(st)]
+    outs, status = gpu_orthogonalize(pre, 12, compute="bf16", beta=beta, prescale="none", tile=tile)
+    assert np.all(status == 0)
+    for p, o, shape in zip(pre, outs, shapes):
+        ref = bjorck.bjorck(p.astype(np.float64), 12, beta=beta, prescale="none")
+        got = to_f64(o)
+        assert checks.relative_difference(got, ref) <= BF16_REL, shape
+        assert checks.tile_relative_differences(got, ref, 256).max() <= BF16_REL, shape
+
+
 BF16_SHAPES = [(256, 128), (128, 256), (384, 200), (1024, 512), (2048, 1000), (1000, 2048), (1024, 1024),
                (1100, 1030), (64, 32), (32, 32)]
 
