@@ -107,6 +107,23 @@ def test_vjp_bf16_mixed_batch(tile):
         assert rel <= bound, (shape, rel)
 
 
+@pytest.mark.parametrize("beta,prescale,tile", [(0.25, "frobenius", 0), (0.5, "none", 256)])
+def test_vjp_bf16_beta_and_no_prescale(beta, prescale, tile):
+    """bf16 products with beta < 1/2, and without pre-scaling (inputs inside
+    the basin), both tile classes and the small bucket."""
+    shapes = [(128, 64), (256, 128), (512, 512), (1100, 1030)]
+    st = stored(207, shapes)
+    if prescale == "none":
+        st = [(s / np.linalg.norm(s.astype(np.float64), 2) * 0.9).astype(np.float32) for s in st]
+    gouts = upstream(208, shapes)
+    gis, status = run_vjp(st, gouts, 12, compute="bf16", beta=beta, prescale=prescale, tile=tile)
+    assert np.all(status == 0)
+    for s, g, o, shape in zip(st, gouts, gis, shapes):
+        ref = bjorck_grad.bjorck_vjp(s.astype(np.float64), g.astype(np.float64), 12, beta, prescale)
+        bound = REL_BF16_SQUARE if shape[0] == shape[1] else REL_BF16_RECT
+        assert checks.relative_difference(to_f64(o), ref) <= bound, shape
+
+
 def test_vjp_scale_invariance_property():
     """With Frobenius pre-scaling the gradient is orthogonal to W (any size)."""
     shapes = [(384, 200), (200, 384), (2048, 1024)]
