@@ -1,7 +1,7 @@
 // Exact-cover checks of the tiled launches' work lists (tile_order.h), run on
 // the CPU: every upper tile (i <= j) of every matrix appears exactly once in
-// a Gram list, every tile once in an update list, and the XCD reordering is
-// a permutation.  Prints "ok <n>" per case and "FAIL ..." otherwise.
+// a Gram list (bf16, and the fp32 grouped upper list), every tile once in an
+// update list, and the XCD reordering is a permutation.  Prints "ok <n>" per case and "FAIL ..." otherwise.
 #include <cstdio>
 #include <map>
 #include <random>
@@ -47,6 +47,20 @@ void check_update(int mat, int tm, int tn, int c) {
   std::printf("ok %d\n", c);
 }
 
+// the fp32 Gram list: grouped tiles of the upper triangle
+void check_grouped_upper(int tn, int gm, int c) {
+  std::vector<orth::TileItem> out;
+  orth::grouped_tiles(5, tn, tn, gm, true, out);
+  std::map<std::pair<int, int>, int> seen;
+  for (const auto& t : out) {
+    if (t.mat != 5 || t.ti > t.tj || t.tj >= tn || t.ti < 0) return fail("grouped upper tile out of range", c);
+    ++seen[{t.ti, t.tj}];
+  }
+  if (out.size() != (size_t)tn * (tn + 1) / 2 || seen.size() != out.size())
+    return fail("grouped upper tile missing or repeated", c);
+  std::printf("ok %d\n", c);
+}
+
 void check_xcd(size_t n, int c) {
   std::vector<int> v(n);
   for (size_t i = 0; i < n; ++i) v[i] = (int)i;
@@ -82,6 +96,7 @@ int main() {
     check_gram(m, 1 + (int)(rng() % 5), ++c);
     check_update((int)(rng() % 9), 1 + (int)(rng() % 24), 1 + (int)(rng() % 24), ++c);
     check_xcd(rng() % 300, ++c);
+    check_grouped_upper(1 + (int)(rng() % 40), 1 + (int)(rng() % 6), ++c);
   }
   check_update(3, 16, 16, ++c);
   check_update(0, 1, 1, ++c);
