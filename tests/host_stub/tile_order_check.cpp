@@ -1,7 +1,8 @@
 // Exact-cover checks of the tiled launches' work lists (tile_order.h), run on
 // the CPU: every upper tile (i <= j) of every matrix appears exactly once in
 // a Gram list (bf16, and the fp32 grouped upper list), every tile once in an
-// update list, and the XCD reordering is a permutation.  Prints "ok <n>" per case and "FAIL ..." otherwise.
+// update list, and the XCD reordering is a permutation.  Prints "ok <n>" per
+// case and "FAIL ..." otherwise.
 #include <cstdio>
 #include <map>
 #include <random>
