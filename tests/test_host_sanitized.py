@@ -137,21 +137,23 @@ def test_stub_checks_catch_planted_violations(which, message):
     assert "STUB VIOLATION: " + message in r.stderr, r.stderr[-2000:]
 
 
-def build_tile_order_check():
+def build_tile_order_check(planted=False):
     """The exact-cover checks of the work-list orders (tile_order.h), built
-    for the CPU with the same sanitizers (once per source state)."""
+    for the CPU with the same sanitizers (once per source state); planted:
+    with a duplicated tile that the checks must catch."""
     srcs = [os.path.join(CSRC, f) for f in ("tile_order.h", "internal.h")] + \
         [os.path.join(ROOT, "include", "orth.h"), os.path.join(STUB, "tile_order_check.cpp")]
     h = hashlib.sha256()
     for f in srcs:
         h.update(open(f, "rb").read())
-    exe = os.path.join(BUILD, f"tile_order_check_{h.hexdigest()[:16]}")
+    exe = os.path.join(BUILD, f"tile_order_check_{'planted_' if planted else ''}{h.hexdigest()[:16]}")
     if os.path.exists(exe):
         return exe
     os.makedirs(BUILD, exist_ok=True)
     r = subprocess.run([HIPCC, "-x", "hip", "--offload-host-only", "-O1", "-g", "-std=c++17", *SAN,
-                        "-Wno-unused-command-line-argument", os.path.join(STUB, "tile_order_check.cpp"),
-                        "-o", exe + ".tmp"], capture_output=True, text=True)
+                        *(["-DPLANT_MISTAKE"] if planted else []), "-Wno-unused-command-line-argument",
+                        os.path.join(STUB, "tile_order_check.cpp"), "-o", exe + ".tmp"],
+                       capture_output=True, text=True)
     assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
     os.replace(exe + ".tmp", exe)
     return exe
@@ -168,4 +170,12 @@ def test_work_lists_cover_every_tile_once():
                        env=dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1"))
     assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
     assert "failures 0" in r.stdout and "FAIL" not in r.stdout
+
+
+@pytest.mark.slow
+def test_work_list_checks_catch_a_duplicated_tile():
+    exe = build_tile_order_check(planted=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=300,
+                       env=dict(os.environ, ASAN_OPTIONS="detect_leaks=0"))
+    assert r.returncode != 0 and "FAIL" in r.stdout and "Gram tile missing or repeated" in r.stdout
 
