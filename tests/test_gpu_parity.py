@@ -142,7 +142,7 @@ def test_bf16_two_tile_classes_and_timing_span():
     calls of their own, the oracle's result on a sampled large matrix, and
     a timing span (the union of the launches' intervals) between the longer
     class's kernel time and the sum of both."""
-    shapes = [(2048, 2048)] * 4 + [(512, 256), (256, 512), (384, 384), (1000, 130)] * 2
+    shapes = [(2048, 2048)] * 4 + [(512, 256), (256, 512), (384, 384), (1000, 130)] * 2 + [(32, 32), (64, 48)] * 3
     st = stored(109, shapes, dtype="bf16")
     ins = [to_dev(a) for a in st]
     iters = 6
@@ -155,10 +155,15 @@ def test_bf16_two_tile_classes_and_timing_span():
     t256, n256 = orth.orth_timing_read("bjorck_bf16_256")
     t128, n128 = orth.orth_timing_read("bjorck_bf16_128")
     span, n = orth.orth_timing_span("bjorck_bf16_")
+    tsmall, nsmall = orth.orth_timing_read("bjorck_small")
+    span_all, n_all = orth.orth_timing_span("bjorck_")
     orth.orth_timing_enable(False)
     orth.orth_timing_reset()
     assert n256 == n128 == 2 * iters and n == n256 + n128
     assert max(t256, t128) * 0.999 <= span <= (t256 + t128) * 1.001
+    # the small matrices' kernels run on side streams beside the tiled ones
+    assert nsmall >= 1 and n_all == n + nsmall
+    assert span * 0.999 <= span_all <= (span + tsmall) * 1.001
     print("[bf16 two classes] classes apart", flush=True)
     for part in ([0, 1, 2, 3], list(range(4, len(shapes)))):
         outs = [torch.empty(ins[i].shape, device=DEV) for i in part]
