@@ -176,6 +176,27 @@ def test_bf16_two_tile_classes_and_timing_span():
     assert checks.tile_relative_differences(to_f64(both[3]), ref, 256).max() <= BF16_REL
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2, 3, 4])
+def test_random_ragged_batches(seed):
+    """Seeded random batches of ragged shapes (1 to 1100 rows and columns,
+    tall and wide, every size class) through both product precisions,
+    against the oracle whole and per 256-block."""
+    rng = np.random.default_rng(900 + seed)
+    shapes = [(int(rng.integers(1, 1101)), int(rng.integers(1, 1101))) for _ in range(6)] + \
+             [(int(rng.integers(1, 129)), int(rng.integers(1, 65))) for _ in range(4)]
+    print(f"[random batch {seed}] {shapes}", flush=True)
+    for compute, dtype, bound in (("f32", "f32", REL_F32), ("bf16", "bf16", BF16_REL)):
+        st = stored(950 + seed, shapes, dtype=dtype)
+        outs, status = gpu_orthogonalize(st, 8, compute=compute)
+        assert np.all(status == 0)
+        for s, o, shape in zip(oracle_inputs(st), outs, shapes):
+            ref = bjorck.bjorck(s, 8)
+            got = to_f64(o)
+            assert checks.relative_difference(got, ref) <= bound, (compute, shape)
+            if compute == "bf16" and min(shape) > 1:
+                assert checks.tile_relative_differences(got, ref, 256).max() <= bound, (compute, shape)
+
+
 # K-loop lengths of the bf16 tile kernel: with 64-deep k-steps, a Gram tile
 # runs Mp / 64 k-steps and an update tile tj * T / 64 (stored-tile part)
 # plus (Np - tj * T) / 64 (the rest) for tile size T, always even; the loop
