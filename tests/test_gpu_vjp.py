@@ -124,6 +124,23 @@ def test_vjp_bf16_beta_and_no_prescale(beta, prescale, tile):
         assert checks.relative_difference(to_f64(o), ref) <= bound, shape
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_vjp_random_ragged_batches(seed):
+    """Seeded random ragged batches (1 to 600 rows and columns, tall and
+    wide, fused and tiled) through the fp32 vector-Jacobian product."""
+    rng = np.random.default_rng(700 + seed)
+    shapes = [(int(rng.integers(1, 601)), int(rng.integers(1, 601))) for _ in range(5)] + \
+             [(int(rng.integers(1, 129)), int(rng.integers(1, 65))) for _ in range(3)]
+    print(f"[vjp random batch {seed}] {shapes}", flush=True)
+    st = stored(710 + seed, shapes)
+    gouts = upstream(720 + seed, shapes)
+    gis, status = run_vjp(st, gouts, 6)
+    assert np.all(status == 0)
+    for s, g, o, shape in zip(st, gouts, gis, shapes):
+        ref = bjorck_grad.bjorck_vjp(wl.as_f64(s), g.astype(np.float64), 6)
+        assert checks.relative_difference(to_f64(o), ref) <= REL_F32, shape
+
+
 def test_vjp_scale_invariance_property():
     """With Frobenius pre-scaling the gradient is orthogonal to W (any size)."""
     shapes = [(384, 200), (200, 384), (2048, 1024)]
