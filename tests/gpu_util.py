@@ -34,3 +34,22 @@ def gpu_orthogonalize(stored_list, iters, compute="f32", out_dtype=torch.float32
 
 def oracle_inputs(stored_list):
     return [wl.as_f64(s) for s in stored_list]
+
+
+def random_geometries(seed, count, shapes_of):
+    """Seeded random convolution geometries (cin, cout, k, stride, dilation,
+    groups): k up to 5, stride up to 2, dilation up to 3, up to 4 groups and
+    ragged channel counts; those that shapes_of (a parameter-shape rule that
+    raises on an invalid geometry) refuses are drawn again."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        g = int(rng.choice([1, 1, 2, 3, 4]))
+        geom = (g * int(rng.integers(2, 17)), g * int(rng.integers(1, 17)), int(rng.integers(1, 6)),
+                int(rng.integers(1, 3)), int(rng.integers(1, 4)), g)
+        try:
+            shapes_of(*geom)
+        except ValueError:
+            continue
+        out.append(geom)
+    return out

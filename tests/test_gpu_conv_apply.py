@@ -12,7 +12,7 @@ import torch
 from oracle import aoc, bjorck, checks, conv
 from paper_2601_13776_amd import orth
 
-from gpu_util import DEV, to_f64
+from gpu_util import DEV, random_geometries, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -46,6 +46,26 @@ def test_forward_and_transposed_parity(geom, hw):
     ref = conv.conv_circular(kern.astype(np.float64), x.astype(np.float64), s, d, g)
     assert checks.relative_difference(to_f64(y), ref) <= REL
     yy = rand((3, cout, hw // s, hw // s), 3)
+    z = orth.orth_conv_apply(kt, geom, torch.from_numpy(yy).to(DEV), transposed=True)
+    ref_t = conv.conv_circular_adjoint(kern.astype(np.float64), yy.astype(np.float64), (hw, hw), s, d, g)
+    assert checks.relative_difference(to_f64(z), ref_t) <= REL
+
+
+@pytest.mark.parametrize("case", range(10))
+def test_random_geometries_parity(case):
+    """Seeded random geometries (groups, stride, dilation, k up to 5, ragged
+    channel counts) on random grid sizes from one stride period up, batch 2."""
+    geom = random_geometries(79, 10, aoc.param_shapes)[case]
+    cin, cout, k, s, d, g = geom
+    hw = s * int(np.random.default_rng(case).integers(1, 8))
+    print(f"[conv apply random] {geom} hw={hw}", flush=True)
+    kern = rand((cout, cin // g, k, k), 10 + case)
+    x = rand((2, cin, hw, hw), 20 + case)
+    kt = torch.from_numpy(kern).to(DEV)
+    y = orth.orth_conv_apply(kt, geom, torch.from_numpy(x).to(DEV))
+    assert checks.relative_difference(to_f64(y), conv.conv_circular(kern.astype(np.float64), x.astype(np.float64),
+                                                                    s, d, g)) <= REL
+    yy = rand((2, cout, hw // s, hw // s), 30 + case)
     z = orth.orth_conv_apply(kt, geom, torch.from_numpy(yy).to(DEV), transposed=True)
     ref_t = conv.conv_circular_adjoint(kern.astype(np.float64), yy.astype(np.float64), (hw, hw), s, d, g)
     assert checks.relative_difference(to_f64(z), ref_t) <= REL

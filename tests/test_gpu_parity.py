@@ -22,7 +22,7 @@ from oracle import aoc, bjorck, checks, conv
 from paper_2601_13776_amd import orth
 from paper_2601_13776_amd import workloads as wl
 
-from gpu_util import DEV, gpu_orthogonalize, oracle_inputs, to_dev, to_f64
+from gpu_util import DEV, gpu_orthogonalize, oracle_inputs, random_geometries, to_dev, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -438,6 +438,24 @@ def test_compose_parity(geom):
     torch.cuda.synchronize()
     ref = aoc.aoc_kernel(rko.astype(np.float64), None if proj is None else proj.astype(np.float64), *geom)
     assert checks.relative_difference(to_f64(kern), ref) <= REL_F32
+
+
+def test_compose_random_geometries_batched():
+    """Twelve seeded random geometries (groups, stride, dilation, k up to 5,
+    ragged channel counts) composed in one batched call."""
+    geoms = random_geometries(77, 12, aoc.param_shapes)
+    print(f"[compose random] {geoms}", flush=True)
+    layers, refs = [], []
+    for i, geom in enumerate(geoms):
+        cin, cout, k, s, d, g = geom
+        rko, proj = oracle_factors(geom, 300 + i)
+        kern = torch.empty(cout, cin // g, k, k, device=DEV)
+        layers.append(dict(geom=geom, rko=to_dev(rko), proj=to_dev(proj) if proj is not None else None, kernel=kern))
+        refs.append(aoc.aoc_kernel(rko.astype(np.float64), None if proj is None else proj.astype(np.float64), *geom))
+    orth.orth_build_conv_kernels_batched(layers)
+    torch.cuda.synchronize()
+    for L, ref, geom in zip(layers, refs, geoms):
+        assert checks.relative_difference(to_f64(L["kernel"]), ref) <= REL_F32, geom
 
 
 def test_compose_batched_bf16_storage():

@@ -22,7 +22,7 @@ from oracle import bjorck_grad, checks
 from paper_2601_13776_amd import orth
 from paper_2601_13776_amd import workloads as wl
 
-from gpu_util import DEV, to_dev, to_f64
+from gpu_util import DEV, random_geometries, to_dev, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -252,6 +252,22 @@ def test_conv_vjp_parity_single(geom):
     assert checks.relative_difference(to_f64(L["grad_rko"]), ref_r) <= REL_F32
     if proj is not None:
         assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= REL_F32
+
+
+def test_conv_vjp_random_geometries_batched():
+    """Twelve seeded random geometries (groups, stride, dilation, k up to 5,
+    ragged channel counts) in one batched call."""
+    geoms = random_geometries(78, 12, aoc.param_shapes)
+    print(f"[conv vjp random] {geoms}", flush=True)
+    items = [(geom, *conv_factors(geom, 500 + i)) for i, geom in enumerate(geoms)]
+    layers = conv_vjp_gpu(items)
+    for (geom, rko, proj, dk), L in zip(items, layers):
+        ref_r, ref_p = aoc_grad.aoc_kernel_vjp(rko.astype(np.float64),
+                                               None if proj is None else proj.astype(np.float64), *geom,
+                                               dk.astype(np.float64))
+        assert checks.relative_difference(to_f64(L["grad_rko"]), ref_r) <= REL_F32, geom
+        if proj is not None:
+            assert checks.relative_difference(to_f64(L["grad_proj"]), ref_p) <= REL_F32, geom
 
 
 def test_conv_vjp_bf16_storage():
