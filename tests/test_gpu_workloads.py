@@ -377,6 +377,7 @@ def test_imagenet_spectral_full_size():
         v0 = warm[offs[i]:offs[i + 1]].astype(np.float64)
         ref, v, _ = spectral.bjorck_spectral(x, v0, w.iters, 1)
         assert checks.relative_difference(to_f64(outs[i]), ref) <= BF16_REL, i
+        assert checks.tile_relative_differences(to_f64(outs[i]), ref, 256).max() <= TILE_REL_BF16, i
         assert np.max(np.abs(un[offs[i]:offs[i + 1]] - v)) <= 1e-5, i
 
 
@@ -424,6 +425,7 @@ def test_imagenet_spectral_vjp_full_size():
         ref = spectral.bjorck_spectral_vjp(x, v0, to_f64(gouts[i]), w.iters, 1)
         bound = 6e-2 if shapes[i][0] == shapes[i][1] else 1e-2
         assert checks.relative_difference(to_f64(gins[i]), ref) <= bound, i
+        assert checks.tile_relative_differences(to_f64(gins[i]), ref, 256).max() <= bound, i
     for i in (84, 87, 88):
         wf, gf = to_f64(ins[i]), to_f64(gins[i])
         assert bool(np.isfinite(gf).all()), i
