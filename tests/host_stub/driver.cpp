@@ -13,11 +13,18 @@
 //   selftest <which>   (a planted violation of the stand-ins' checks: must abort)
 // `expect` is the orth_status the call must return (for the workspace query
 // and the call); data buffers are fake device allocations of the right size.
+// With an argument N > 1 the driver reads all commands first and runs them
+// in N threads at once (every thread all commands, on buffers of its own,
+// selftests skipped), printing only failures and a summary: the library's
+// shared state (plan cache, staging pool, per-thread side streams and
+// errors) under concurrent callers, for ThreadSanitizer.
+#include <atomic>
 #include <cstdio>
 #include <cstdlib>
 #include <iostream>
 #include <sstream>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/orth.h"
@@ -26,11 +33,12 @@ extern "C" {
 void* stub_dev_alloc(size_t bytes);
 void stub_reset(void);
 long stub_launches(void);
+long stub_launches_total(void);
 void stub_selftest(int which);
 }
 
 namespace {
-int g_fail = 0;
+std::atomic<int> g_fail{0};
 
 void check(int rc, int expect, int line, const char* what) {
   if (rc != expect) {
@@ -151,32 +159,51 @@ void run_conv(std::istringstream& in, const std::string& kind, int line) {
     }
   }
 }
+
+// one command line; returns false for a blank line or a comment
+bool run_line(const std::string& text, int line, bool threaded) {
+  std::istringstream in(text);
+  std::string kind;
+  if (!(in >> kind) || kind[0] == '#') return false;
+  if (kind == "ortho" || kind == "save" || kind == "vjp")
+    run_ortho(in, kind, line);
+  else if (kind == "conv" || kind == "convvjp" || kind == "convsave")
+    run_conv(in, kind, line);
+  else if (kind == "selftest") {
+    int which = 0;
+    in >> which;
+    if (!threaded) stub_selftest(which);
+  } else {
+    std::printf("FAIL line %d: unknown command %s\n", line, kind.c_str());
+    ++g_fail;
+  }
+  return true;
+}
 }  // namespace
 
-int main() {
-  std::string text;
-  int line = 0, done = 0;
-  while (std::getline(std::cin, text)) {
-    ++line;
-    std::istringstream in(text);
-    std::string kind;
-    if (!(in >> kind) || kind[0] == '#') continue;
+int main(int argc, char** argv) {
+  const int threads = argc > 1 ? std::atoi(argv[1]) : 1;
+  std::vector<std::string> lines;
+  for (std::string text; std::getline(std::cin, text);) lines.push_back(text);
+  if (threads > 1) {
+    std::atomic<int> done{0};
+    std::vector<std::thread> pool;
+    for (int t = 0; t < threads; ++t)
+      pool.emplace_back([&] {
+        for (size_t i = 0; i < lines.size(); ++i) done += run_line(lines[i], (int)i + 1, true);
+      });
+    for (auto& th : pool) th.join();
+    std::printf("threads %d commands %d failures %d launches %ld\n", threads, done.load(), g_fail.load(),
+                stub_launches_total());
+    return g_fail ? 1 : 0;
+  }
+  int done = 0;
+  for (size_t i = 0; i < lines.size(); ++i) {
     const int before = g_fail;
-    if (kind == "ortho" || kind == "save" || kind == "vjp")
-      run_ortho(in, kind, line);
-    else if (kind == "conv" || kind == "convvjp" || kind == "convsave")
-      run_conv(in, kind, line);
-    else if (kind == "selftest") {
-      int which = 0;
-      in >> which;
-      stub_selftest(which);
-    } else {
-      std::printf("FAIL line %d: unknown command %s\n", line, kind.c_str());
-      ++g_fail;
-    }
-    if (g_fail == before) std::printf("ok %d\n", line);
+    if (!run_line(lines[i], (int)i + 1, false)) continue;
+    if (g_fail == before) std::printf("ok %d\n", (int)i + 1);
     ++done;
   }
-  std::printf("commands %d failures %d launches %ld\n", done, g_fail, stub_launches());
+  std::printf("commands %d failures %d launches %ld\n", done, g_fail.load(), stub_launches_total());
   return g_fail ? 1 : 0;
 }

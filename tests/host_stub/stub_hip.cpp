@@ -10,8 +10,9 @@
 // sanitizer checks the whole source), and the written byte ranges are kept.
 // Every launcher then checks that the descriptor tables it is handed lie
 // inside registered device memory and were written by a copy since the last
-// stub_reset() — i.e. that a call uploads every table byte its launches
-// read.  A violation prints its kind and aborts.
+// stub_reset() on the same thread — i.e. that a call uploads every table
+// byte its launches read.  A violation prints its kind and aborts.  The
+// stand-ins are safe to call from several threads at once.
 #include <sys/mman.h>
 
 #include <cstdio>
@@ -25,11 +26,20 @@
 
 #include "../../paper_2601_13776_amd/csrc/internal.h"
 
+// log2 of the reserved "device" address space (32 TiB by default; the
+// ThreadSanitizer build takes less, to fit its application ranges)
+#ifndef STUB_ARENA_BITS
+#define STUB_ARENA_BITS 45
+#endif
+
 namespace {
 std::mutex g_mu;
 std::map<uintptr_t, uintptr_t> g_dev;       // registered device ranges [begin, end)
-std::map<uintptr_t, uintptr_t> g_written;   // written ranges since the last reset, merged
+// written ranges since the calling thread's last reset, merged: a call's
+// copies and launches all happen on the thread that made the call
+thread_local std::map<uintptr_t, uintptr_t> g_written;
 long g_launches = 0;
+thread_local long t_launches = 0;           // launches of the calling thread
 long g_copies = 0;
 unsigned char* g_arena = nullptr;           // reserved PROT_NONE address space
 size_t g_arena_size = 0, g_arena_used = 0;
@@ -85,9 +95,17 @@ void table(const T* p, long n, const char* where) {
   if (!covered(a, bytes)) violation("table not uploaded by this call", where, a, bytes);
 }
 
+#ifdef PLANT_RACE
+long g_racy = 0;   // a counter every thread bumps without the lock: a planted race
+#endif
+
 hipError_t launched() {
+#ifdef PLANT_RACE
+  ++g_racy;
+#endif
   std::lock_guard<std::mutex> lk(g_mu);
   ++g_launches;
+  ++t_launches;
   return hipSuccess;
 }
 }  // namespace
@@ -99,7 +117,7 @@ extern "C" {
 void* stub_dev_alloc(size_t bytes) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_arena) {
-    g_arena_size = (size_t)1 << 45;   // 32 TiB of address space, nothing committed
+    g_arena_size = (size_t)1 << STUB_ARENA_BITS;   // address space only, nothing committed
     void* p = mmap(nullptr, g_arena_size, PROT_NONE, MAP_PRIVATE | MAP_ANONYMOUS | MAP_NORESERVE, -1, 0);
     if (p == MAP_FAILED) {
       std::fprintf(stderr, "stub: cannot reserve device address space\n");
@@ -124,7 +142,9 @@ void stub_reset(void) {
   g_written.clear();
 }
 
-long stub_launches(void) {
+long stub_launches(void) { return t_launches; }
+
+long stub_launches_total(void) {
   std::lock_guard<std::mutex> lk(g_mu);
   return g_launches;
 }

@@ -3,7 +3,8 @@ descriptor uploads, plan cache) built for the CPU with AddressSanitizer and
 UndefinedBehaviorSanitizer, its HIP runtime calls and kernel launches
 replaced by checking stand-ins (tests/host_stub/stub_hip.cpp), and driven
 through every batched entry point for all five workloads, their spectral
-and saving variants and the error paths (tests/host_stub/driver.cpp).
+and saving variants and the error paths (tests/host_stub/driver.cpp), from
+one thread and from four at once (then also under ThreadSanitizer).
 
 The stand-ins check that every copy lands in the call's device buffers and
 that every table a launch reads lies in the workspace and was uploaded by
@@ -33,19 +34,28 @@ SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined
        "-Xarch_host", "-fno-sanitize-recover=undefined"]
 
 
-def build_driver():
+# ThreadSanitizer instead (it cannot be combined with AddressSanitizer); its
+# application address ranges hold a 1 TiB stand-in device space, not 32 TiB
+TSAN = ["-Xarch_host", "-fsanitize=thread", "-DSTUB_ARENA_BITS=40"]
+
+
+def build_driver(thread=False, planted=False):
     """Compile (once per source state) the sanitized host code, the stand-ins
-    and the driver; returns the driver's path."""
+    and the driver; returns the driver's path.  thread: built with
+    ThreadSanitizer instead of AddressSanitizer and UndefinedBehaviorSanitizer;
+    planted: with a data race planted in the stand-ins."""
     h = hashlib.sha256()
     for f in SOURCES:
         h.update(open(f, "rb").read())
-    tag = h.hexdigest()[:16]
+    tag = h.hexdigest()[:16] + ("_tsan" if thread else "") + ("_race" if planted else "")
     exe = os.path.join(BUILD, f"driver_{tag}")
     if os.path.exists(exe):
         return exe
     os.makedirs(BUILD, exist_ok=True)
-    hip = [HIPCC, "-x", "hip", "--offload-host-only", "-O1", "-g", "-std=c++17", "-fPIC", *SAN,
-           "-Wno-unused-command-line-argument"]
+    hip = [HIPCC, "-x", "hip", "--offload-host-only", "-O1", "-g", "-std=c++17", "-fPIC", *(TSAN if thread else SAN),
+           *(["-DPLANT_RACE"] if planted else []), "-Wno-unused-command-line-argument"]
+    host_san = ["-fsanitize=thread"] if thread else ["-fsanitize=address", "-fsanitize=undefined",
+                                                     "-fno-sanitize-recover=undefined"]
     objs = []
     procs = []
     for src, obj in ((os.path.join(CSRC, "host.hip"), "host.o"), (os.path.join(STUB, "stub_hip.cpp"), "stub.o")):
@@ -53,14 +63,13 @@ def build_driver():
         procs.append(subprocess.Popen(hip + ["-c", src, "-o", out], stdout=subprocess.PIPE, stderr=subprocess.STDOUT))
         objs.append(out)
     drv = os.path.join(BUILD, f"{tag}_driver.o")
-    procs.append(subprocess.Popen([CLANG, "-O1", "-g", "-std=c++17", "-fsanitize=address", "-fsanitize=undefined",
-                                   "-fno-sanitize-recover=undefined", "-c", os.path.join(STUB, "driver.cpp"),
+    procs.append(subprocess.Popen([CLANG, "-O1", "-g", "-std=c++17", *host_san, "-c", os.path.join(STUB, "driver.cpp"),
                                    "-o", drv], stdout=subprocess.PIPE, stderr=subprocess.STDOUT))
     objs.append(drv)
     for p in procs:
         out, _ = p.communicate()
         assert p.returncode == 0, out.decode()[-3000:]
-    r = subprocess.run([CLANG, "-fsanitize=address", "-fsanitize=undefined", *objs, "-o", exe + ".tmp", "-lpthread"],
+    r = subprocess.run([CLANG, *host_san[:2 if not thread else 1], *objs, "-o", exe + ".tmp", "-lpthread"],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-3000:]
     os.replace(exe + ".tmp", exe)
@@ -122,6 +131,33 @@ def test_host_code_under_sanitizers():
     assert "failures 0" in r.stdout, tail
     n_cmds = sum(1 for l in workload_spec().splitlines() if l and not l.startswith("#"))
     assert r.stdout.count("\nok ") + r.stdout.startswith("ok ") == n_cmds, tail
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("thread", [False, True], ids=["asan-ubsan", "tsan"])
+def test_host_code_from_four_threads(thread):
+    """Every command of the workload spec from four threads at once, each on
+    buffers of its own: the shared plan cache (evicting under concurrent
+    users), the staging pool, the per-thread side streams and last errors;
+    AddressSanitizer sees a plan or buffer freed under a user, and
+    ThreadSanitizer any data race."""
+    exe = build_driver(thread=thread)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1:halt_on_error=1",
+               UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1", TSAN_OPTIONS="halt_on_error=1")
+    r = subprocess.run([exe, "4"], input=workload_spec(), capture_output=True, text=True, env=env, timeout=900)
+    tail = (r.stdout[-3000:] + "\n" + r.stderr[-6000:])
+    assert r.returncode == 0, tail
+    n_cmds = sum(1 for l in workload_spec().splitlines() if l and not l.startswith("#"))
+    assert f"threads 4 commands {4 * n_cmds} failures 0" in r.stdout, tail
+    assert "WARNING: ThreadSanitizer" not in r.stderr, tail
+
+
+@pytest.mark.slow
+def test_thread_sanitizer_catches_a_planted_race():
+    exe = build_driver(thread=True, planted=True)
+    r = subprocess.run([exe, "4"], input=workload_spec(), capture_output=True, text=True, timeout=900,
+                       env=dict(os.environ, TSAN_OPTIONS="halt_on_error=1"))
+    assert r.returncode != 0 and "WARNING: ThreadSanitizer: data race" in r.stderr, r.stderr[-2000:]
 
 
 @pytest.mark.slow
