@@ -504,7 +504,8 @@ int32_t orth_version(void);
 
 /*
  * Per-kernel timing with HIP events recorded around every launch on the
- * launch stream (off by default; process-wide; not for concurrent callers).
+ * launch stream (off by default; process-wide: the launches of every thread
+ * and stream count together, each timed by two events on its own stream).
  * orth_timing_read synchronizes the recorded events and returns the total
  * milliseconds and launch count of the named kernel since the last reset.
  * orth_timing_span returns the wall-clock milliseconds covered by the

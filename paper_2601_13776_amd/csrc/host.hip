@@ -4,6 +4,7 @@
 // enqueues anything; the library allocates no device memory.
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <climits>
 #include <cstdarg>
 #include <cstdlib>
@@ -70,10 +71,11 @@ void log_line(const char* fmt, ...) {
 namespace {
 struct TimingRec {
   std::string name;
+  hipStream_t stream;   // the launch's stream: its end event pairs with the start on the same stream
   hipEvent_t a, b;
 };
 std::mutex g_tmu;
-bool g_timing = false;
+std::atomic<bool> g_timing{false};
 std::vector<TimingRec> g_pending;
 std::vector<hipEvent_t> g_event_pool;
 std::map<std::string, std::pair<double, int64_t>> g_totals;
@@ -114,22 +116,38 @@ hipEvent_t pool_event() {
   return e;
 }
 
+// the first failure of the last drain (for the error message)
+std::string g_drain_err;
+
 int drain_timing_locked() {
   int rc = ORTH_OK;
+  g_drain_err.clear();
+  auto failed = [&](const char* what, const std::string& name, hipError_t e) {
+    if (rc == ORTH_OK) g_drain_err = std::string(what) + " of " + name + ": " + hipGetErrorString(e);
+    rc = ORTH_EHIP;
+  };
   for (auto& r : g_pending) {
     float ms = 0.f, at = 0.f;
-    if (r.a && r.b && hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+    hipError_t e = r.a && r.b ? hipEventSynchronize(r.b) : hipErrorInvalidValue;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e == hipSuccess) {
       auto& t = g_totals[r.name];
       t.first += ms;
       t.second += 1;
-      // events of every stream share the device's clock
+      // events of every stream share the device's clock; a launch on
+      // another stream may start before the reference event
       if (!g_ref) g_ref = r.a;
-      if (hipEventElapsedTime(&at, g_ref, r.a) == hipSuccess)
+      e = hipEventElapsedTime(&at, g_ref, r.a);
+      if (e != hipSuccess && hipEventElapsedTime(&at, r.a, g_ref) == hipSuccess) {
+        at = -at;
+        e = hipSuccess;
+      }
+      if (e == hipSuccess)
         g_spans[r.name].push_back({(double)at, (double)at + ms});
       else
-        rc = ORTH_EHIP;
+        failed("start relative to the reference event", r.name, e);
     } else {
-      rc = ORTH_EHIP;
+      failed("launch events", r.name, e);
     }
     if (r.a && r.a != g_ref) g_event_pool.push_back(r.a);
     if (r.b) g_event_pool.push_back(r.b);
@@ -137,6 +155,8 @@ int drain_timing_locked() {
   g_pending.clear();
   return rc;
 }
+
+int drain_failed(int rc) { return fail(rc, ("timing events: " + g_drain_err).c_str()); }
 }  // namespace
 
 void timing_begin(const char* name, hipStream_t s) {
@@ -144,7 +164,7 @@ void timing_begin(const char* name, hipStream_t s) {
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   if (!timed_locked(name)) return;
-  TimingRec r{name, pool_event(), nullptr};
+  TimingRec r{name, s, pool_event(), nullptr};
   // a failed record leaves the pair incomplete, which the read reports
   if (r.a && hipEventRecord(r.a, s) != hipSuccess) {
     g_event_pool.push_back(r.a);
@@ -166,7 +186,7 @@ void timing_end(const char* name, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_tmu);
   if (!timed_locked(name)) return;
   for (auto it = g_pending.rbegin(); it != g_pending.rend(); ++it) {
-    if (it->b == nullptr && it->name == name) {
+    if (it->b == nullptr && it->stream == s && it->name == name) {
       it->b = pool_event();
       if (it->b && hipEventRecord(it->b, s) != hipSuccess) {
         g_event_pool.push_back(it->b);
@@ -2983,7 +3003,7 @@ int orth_timing_reset(void) {
   g_spans.clear();
   if (g_ref) g_event_pool.push_back(g_ref);
   g_ref = nullptr;
-  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+  return rc ? drain_failed(rc) : ORTH_OK;
 }
 
 int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launches) {
@@ -2993,7 +3013,7 @@ int orth_timing_read(const char* kernel_name, double* total_ms, int64_t* launche
   auto it = g_totals.find(kernel_name);
   *total_ms = it == g_totals.end() ? 0.0 : it->second.first;
   *launches = it == g_totals.end() ? 0 : it->second.second;
-  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+  return rc ? drain_failed(rc) : ORTH_OK;
 }
 
 int orth_timing_filter(const char* prefixes) {
@@ -3028,13 +3048,14 @@ int orth_timing_span(const char* prefixes, double* covered_ms, int64_t* launches
   if (!iv.empty()) covered += hi - lo;
   *covered_ms = covered;
   *launches = (int64_t)iv.size();
-  return rc ? fail(rc, "event synchronization failed") : ORTH_OK;
+  return rc ? drain_failed(rc) : ORTH_OK;
 }
 
 int orth_timing_names(char* buf, size_t buf_bytes) {
   if (!buf || buf_bytes == 0) return fail(ORTH_EINVAL, "NULL buffer");
   std::lock_guard<std::mutex> lk(g_tmu);
-  drain_timing_locked();
+  const int rc = drain_timing_locked();
+  if (rc) return drain_failed(rc);
   std::string all;
   for (auto& kv : g_totals) {
     if (!all.empty()) all += ";";

@@ -79,3 +79,55 @@ def test_concurrent_callers_match_single_calls():
         for r in range(reps):
             for i, (a, b) in enumerate(zip(got[r], ref)):
                 assert torch.equal(a, b), (job[0], r, i)
+
+
+def test_timing_from_concurrent_callers():
+    """Per-kernel timing with the callers on four threads and streams: the
+    same launches counted as when the calls run one after another, every
+    event pair complete (each launch's end pairs with its start on its own
+    stream), and the covered span no longer than the summed durations."""
+    data = [inputs(job) for job in JOBS]
+    torch.cuda.synchronize()
+
+    def counts():
+        names = orth.orth_timing_names()
+        return {n: orth.orth_timing_read(n) for n in names}
+
+    orth.orth_timing_reset()
+    orth.orth_timing_enable(True)
+    try:
+        for job, d in zip(JOBS, data):
+            run(job, *d)
+        torch.cuda.synchronize()
+        alone = counts()
+        orth.orth_timing_reset()
+        errors = []
+        start = threading.Barrier(len(JOBS))
+
+        def worker(k):
+            try:
+                stream = torch.cuda.Stream(device=DEV)
+                with torch.cuda.stream(stream):
+                    start.wait()
+                    run(JOBS[k], *data[k])
+                stream.synchronize()
+            except Exception as e:
+                errors.append((JOBS[k][0], repr(e)))
+
+        threads = [threading.Thread(target=worker, args=(k,)) for k in range(len(JOBS))]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join(timeout=120)
+        assert not any(t.is_alive() for t in threads) and not errors, errors
+        torch.cuda.synchronize()
+        together = counts()
+        prefixes = sorted({n.split("_")[0] for n in together})
+        span_ms, span_n = orth.orth_timing_span(*prefixes)
+    finally:
+        orth.orth_timing_enable(False)
+        orth.orth_timing_reset()
+    assert {n: c[1] for n, c in together.items()} == {n: c[1] for n, c in alone.items()}
+    assert all(c[0] > 0 for c in together.values())
+    assert span_n == sum(c[1] for c in together.values())
+    assert 0 < span_ms <= sum(c[0] for c in together.values()) * (1 + 1e-6)
