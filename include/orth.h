@@ -40,6 +40,9 @@
  *   conversions to bfloat16 round to nearest, ties to even.
  * - orth_last_error() returns a thread-local message for the last failing
  *   call of the calling thread.
+ * - Several host threads may call at once (the plan cache and the staging
+ *   pool are shared under locks); calls whose work may overlap on the GPU
+ *   need workspaces and outputs of their own.
  */
 #ifndef ORTH_H_
 #define ORTH_H_
