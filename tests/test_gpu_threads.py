@@ -1,7 +1,8 @@
-"""Calls from several host threads at once, each thread on a stream of its
-own, so that the library's shared host state (plan cache, pinned staging
-pool, per-thread side streams and last errors) serves concurrent callers:
-every result must be bit-identical to the same call made alone."""
+"""Calls from several host threads at once (orthogonalization, its VJP and
+the kernel composition), each thread on a stream of its own, so that the
+library's shared host state (plan cache, pinned staging pool, per-thread
+side streams and last errors) serves concurrent callers: every result must
+be bit-identical to the same call made alone."""
 
 import threading
 
@@ -21,11 +22,24 @@ JOBS = [
     ("f32 mixed", 32, "f32", [(512, 256), (256, 256), (33, 17), (130, 64), (700, 300)], "f32", 10, "fwd"),
     ("bf16 small", 33, "bf16", [(32, 32)] * 200 + [(128, 64)] * 20, "bf16", 15, "fwd"),
     ("bf16 vjp", 34, "bf16", [(512, 512), (1024, 512), (64, 64), (200, 130)], "bf16", 8, "vjp"),
+    # (cin, cout, k, stride, dilation, groups) of explicit kernels composed from given factors
+    ("composition", 35, "f32",
+     [(64, 64, 3, 1, 1, 1), (128, 256, 3, 2, 1, 1), (32, 32, 3, 1, 2, 4), (16, 32, 2, 2, 1, 2)], "f32", 0, "conv"),
 ]
 
 
 def inputs(job):
     name, seed, dt, shapes = job[:4]
+    if job[6] == "conv":
+        gen = torch.Generator(device=DEV)
+        gen.manual_seed(seed)
+        layers = []
+        for geom in shapes:
+            rr, rc, npj, pr, pc = orth.orth_aoc_param_shapes(*geom)
+            g = geom[5]
+            layers.append(dict(geom=geom, rko=torch.randn(g, rr, rc, generator=gen, device=DEV),
+                               proj=torch.randn(g, npj, pr, pc, generator=gen, device=DEV) if npj else None))
+        return layers, None
     w = wl.Workload("threads", seed, dt, 0, ())
     ins = [to_dev(wl.stored_matrix(w, i, r, c)) for i, (r, c) in enumerate(shapes)]
     gen = torch.Generator(device=DEV)
@@ -37,7 +51,13 @@ def inputs(job):
 def run(job, ins, gouts):
     """One call of the job on the current stream; returns its outputs."""
     compute, iters, kind = job[4:]
-    if kind == "fwd":
+    if kind == "conv":
+        outs = []
+        for L in ins:
+            cin, cout, k, _, _, g = L["geom"]
+            outs.append(torch.empty(cout, cin // g, k, k, device=DEV))
+        orth.orth_build_conv_kernels_batched([dict(L, kernel=o) for L, o in zip(ins, outs)])
+    elif kind == "fwd":
         outs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in ins]
         orth.orth_orthogonalize_batched(ins, outs, iters, compute=compute)
     else:
