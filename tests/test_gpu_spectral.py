@@ -61,6 +61,24 @@ def test_spectral_f32_mixed_batch(q, iters):
         assert np.max(np.abs(u1 - v)) <= U_ABS, shape
 
 
+@pytest.mark.parametrize("seed,q", [(0, 1), (1, 3)])
+def test_spectral_random_ragged_batches(seed, q):
+    """Seeded random ragged batches (1 to 600 rows and columns, tall and
+    wide, fused and tiled) with 1 and 3 power steps, fp32 products."""
+    rng = np.random.default_rng(800 + seed)
+    shapes = [(int(rng.integers(1, 601)), int(rng.integers(1, 601))) for _ in range(5)] + \
+             [(int(rng.integers(1, 129)), int(rng.integers(1, 65))) for _ in range(3)]
+    print(f"[spectral random batch {seed}] q={q} {shapes}", flush=True)
+    st = stored(810 + seed, shapes)
+    us = cached(820 + seed, shapes)
+    outs, u_new, status = run(st, us, 8, q)
+    assert np.all(status == 0)
+    for s, u0, o, u1, shape in zip(st, us, outs, u_new, shapes):
+        ref, v, _ = spectral.bjorck_spectral(s.astype(np.float64), u0.astype(np.float64), 8, q)
+        assert checks.relative_difference(to_f64(o), ref) <= REL_F32, shape
+        assert np.max(np.abs(u1 - v)) <= U_ABS, shape
+
+
 def test_spectral_bf16_batch():
     shapes = [(128, 64), (256, 128), (300, 700), (1024, 512), (512, 512), (2048, 1024)]
     st = stored(703, shapes, "bf16")
